@@ -1,0 +1,29 @@
+"""Shared test set-up: the gpu marker, and an in-tree build of the oracle when
+(and only when) it is not built yet."""
+import os
+import sys
+
+import pytest
+
+REPO = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+if REPO not in sys.path:
+    sys.path.insert(0, REPO)
+TESTS = os.path.dirname(os.path.abspath(__file__))
+if TESTS not in sys.path:
+    sys.path.insert(0, TESTS)
+
+
+def pytest_configure(config):
+    config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU")
+
+
+def pytest_sessionstart(session):
+    import oracle
+    if not os.path.exists(oracle.LIB):
+        oracle.build()
+
+
+@pytest.fixture(scope="session")
+def orc():
+    import oracle
+    return oracle.default()

@@ -1,0 +1,355 @@
+"""Pins of the CPU oracle: checks against what the paper and the mathematics
+fix, not against the oracle itself.
+
+Each pin takes an oracle.Oracle and raises AssertionError on a mismatch.  The
+same pins run against the real oracle (all must pass) and against builds
+with a planted mistake (at least one must fail for each).
+
+Sources of truth used here:
+  * hand-worked blocks under tests/golden (Sec. 3.2 Eq. 3-4, Sec. 4.3 Eq. 9-12);
+  * the E2M1 magnitudes {0, 0.5, 1, 1.5, 2, 3, 4, 6} (Sec. 3.2.2 format);
+  * brute force: nearest grid point by exhaustive distance comparison, block
+    exponent by counting, fp64 matrix products with numpy of values decoded
+    here from the literal table;
+  * invariants of the method (zero residual on grid values, power-of-two
+    equivariance, idempotence, negation symmetry, monotone improvement, the
+    half-error bound of the second stage);
+  * closed forms for the SwiGLU intermediate and bf16 rounding.
+"""
+import math
+import os
+
+import numpy as np
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+E2M1 = (0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0)
+
+
+# ---------------------------------------------------------------- helpers
+def read_golden(name):
+    d = {}
+    with open(os.path.join(GOLDEN, name)) as f:
+        for line in f:
+            line = line.split("#", 1)[0].strip()
+            if not line:
+                continue
+            k, v = line.split(":", 1)
+            d[k.strip()] = v.split()
+    return d
+
+
+def padded_floats(vals, n=32):
+    a = [float(v) for v in vals]
+    return np.array(a + [0.0] * (n - len(a)), dtype=np.float64)
+
+
+def padded_bytes(vals, n=16):
+    a = [int(v, 16) for v in vals]
+    return np.array(a + [0] * (n - len(a)), dtype=np.uint8)
+
+
+def decode_codes(codes, scales):
+    """Independent decode: literal table, nibble 2j low, scale 2^(s-127)."""
+    codes = np.asarray(codes, np.uint8)
+    rows, K = codes.shape[0], codes.shape[1] * 2
+    nib = np.empty((rows, K), np.int64)
+    nib[:, 0::2] = codes & 0x0F
+    nib[:, 1::2] = codes >> 4
+    mag = np.array(E2M1)[nib & 7]
+    val = np.where(nib & 8, -mag, mag)
+    sc = np.repeat(np.asarray(scales, np.float64) - 127.0, 32, axis=1)
+    return val * np.exp2(sc)
+
+
+def brute_code(y):
+    """Nearest E2M1 magnitude by exhaustive comparison, ties to the even
+    index, values beyond 6 saturate; the sign bit follows y's sign."""
+    a = min(abs(y), 6.0)
+    cands = sorted(range(8), key=lambda i: (abs(a - E2M1[i]), i % 2))
+    return (8 if math.copysign(1.0, y) < 0 else 0) | cands[0]
+
+
+def brute_exponent(amax):
+    """Smallest e in [-127, 127] with amax < 8 * 2^e (the E2M1 range
+    [0, 8) of x / 2^e before saturation), found by counting."""
+    e = -127
+    while e < 127 and amax >= 8.0 * 2.0 ** e:
+        e += 1
+    return e
+
+
+def brute_block(x):
+    """Quantize one block by brute force; returns (codes, scale byte)."""
+    e = brute_exponent(max(abs(v) for v in x))
+    return [brute_code(v / 2.0 ** e) for v in x], e + 127
+
+
+def pack(codes):
+    return bytes(codes[2 * j] | (codes[2 * j + 1] << 4) for j in range(len(codes) // 2))
+
+
+def bf16_ulp(v):
+    if v == 0:
+        return 2.0 ** -133
+    return 2.0 ** (math.floor(math.log2(abs(v))) - 7)
+
+
+# ---------------------------------------------------------------- pins
+def pin_e2m1_table(o):
+    """The 16 code values are the E2M1 magnitudes with the sign bit."""
+    for c in range(16):
+        want = E2M1[c & 7] * (-1.0 if c & 8 else 1.0)
+        got = o.e2m1_value(c)
+        assert got == want and math.copysign(1, got) == math.copysign(1, want), (c, got)
+
+
+def pin_encode_boundaries(o):
+    """Every grid point, every midpoint and one ulp either side of each, both
+    signs, plus values beyond saturation, against brute force."""
+    ys = set(E2M1)
+    for a, b in zip(E2M1, E2M1[1:]):
+        mid = (a + b) / 2
+        ys.update([mid, math.nextafter(mid, 0), math.nextafter(mid, 10)])
+        ys.update([float(np.nextafter(np.float32(mid), np.float32(0))),
+                   float(np.nextafter(np.float32(mid), np.float32(10)))])
+    ys.update([6.5, 7.0, 7.99, 1e-30, 0.0])
+    for y in sorted(ys):
+        for s in (1.0, -1.0):
+            v = s * y
+            assert o.e2m1_encode(v) == brute_code(v), (v, o.e2m1_encode(v), brute_code(v))
+
+
+def pin_block_exponent(o):
+    """e = floor(log2 amax) - 2 by construction amax = f * 2^j, against
+    counting, including both clamps and zero."""
+    assert o.block_exponent(0.0) == -127
+    for j in range(-149, 128):
+        for f in (1.0, 1.5, 1.9999999):
+            amax = f * 2.0 ** j
+            want = max(-127, min(127, j - 2))
+            assert o.block_exponent(amax) == want == brute_exponent(amax), (amax, j)
+
+
+def _check_golden_block(o, name):
+    g = read_golden(name)
+    x = padded_floats(g["x"])
+    if "x" in g and len(g["x"]) == 1 and g["x"][0] in ("0", "-0"):
+        x = np.full(32, float(g["x"][0]))
+    qc, qs, rc, rs = o.quantize(x[None, :])
+    assert qs[0, 0] == int(g["q_scale"][0], 16), (name, "q_scale", hex(qs[0, 0]))
+    assert bytes(qc[0]) == bytes(padded_bytes(g["q_codes"])), (name, "q_codes", qc[0])
+    assert rs[0, 0] == int(g["r_scale"][0], 16), (name, "r_scale", hex(rs[0, 0]))
+    assert bytes(rc[0]) == bytes(padded_bytes(g["r_codes"])), (name, "r_codes", rc[0])
+    recon = o.dequant(qc, qs) + o.dequant(rc, rs)
+    want = padded_floats(g["recon"]) if len(g["recon"]) > 1 else np.zeros(32)
+    assert np.array_equal(recon[0], want), (name, recon[0])
+
+
+def pin_golden_h1(o):
+    _check_golden_block(o, "h1_mixed_block.txt")
+
+
+def pin_golden_h2(o):
+    _check_golden_block(o, "h2_outlier_block.txt")
+
+
+def pin_golden_h3(o):
+    _check_golden_block(o, "h3_representable_block.txt")
+
+
+def pin_golden_h4(o):
+    _check_golden_block(o, "h4_zero_blocks.txt")
+    _check_golden_block(o, "h4_negative_zero_block.txt")
+
+
+def pin_golden_h5_identity_gemm(o):
+    g = read_golden("h5_identity_weight.txt")
+    x = padded_floats(g["x"])[None, :]
+    qc, qs, rc, rs = o.quantize(x)
+    wc, ws, _, _ = o.quantize(np.eye(32), residual=False)
+    assert np.all(ws == int(g["w_scale"][0], 16))
+    z, _ = o.gemm(qc, qs, rc, rs, wc, ws)
+    assert np.array_equal(z[0], padded_floats(g["z_rfq"])), z[0]
+    z0, _ = o.gemm(qc, qs, None, None, wc, ws)
+    assert np.array_equal(z0[0], padded_floats(g["z_plain"])), z0[0]
+
+
+def _random_blocks(seed, n=400):
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((n, 32))
+    x *= np.exp2(rng.integers(-20, 20, (n, 1)))
+    x[::7, rng.integers(0, 32)] *= 60.0                    # outliers
+    x[::11] = np.round(x[::11] * 4) / 4                     # coarse values
+    x[::13, ::3] = 0.0                                      # zeros
+    return x.astype(np.float32).astype(np.float64)
+
+
+def pin_brute_force_blocks(o):
+    """Random blocks (fp32 values) quantized by brute force in pure Python."""
+    x = _random_blocks(1, 300)
+    qc, qs, rc, rs = o.quantize(x)
+    for i in range(x.shape[0]):
+        codes, sb = brute_block(list(x[i]))
+        assert qs[i, 0] == sb, (i, qs[i, 0], sb)
+        assert bytes(qc[i]) == pack(codes), i
+        deq = [E2M1[c & 7] * (-1 if c & 8 else 1) * 2.0 ** (sb - 127) for c in codes]
+        res = [a - b for a, b in zip(x[i], deq)]
+        rcodes, rsb = brute_block(res)
+        assert rs[i, 0] == rsb, (i, rs[i, 0], rsb)
+        assert bytes(rc[i]) == pack(rcodes), i
+
+
+def pin_dequant_independent(o):
+    """Oracle dequant equals the literal-table decode written here."""
+    x = _random_blocks(2, 200).reshape(50, 128)
+    qc, qs, rc, rs = o.quantize(x)
+    assert np.array_equal(o.dequant(qc, qs), decode_codes(qc, qs))
+    assert np.array_equal(o.dequant(rc, rs), decode_codes(rc, rs))
+
+
+def pin_zero_residual_on_grid(o):
+    """I1: blocks made of grid values times 2^e, with the block maximum 4 or 6,
+    reproduce exactly and leave an all-zero residual."""
+    rng = np.random.default_rng(3)
+    for t in range(200):
+        e = int(rng.integers(-100, 100))
+        mags = rng.choice(E2M1, 32)
+        mags[rng.integers(0, 32)] = rng.choice([4.0, 6.0])
+        x = (mags * rng.choice([-1.0, 1.0], 32) * 2.0 ** e)[None, :]
+        qc, qs, rc, rs = o.quantize(x)
+        assert qs[0, 0] == e + 127
+        assert np.array_equal(o.dequant(qc, qs), x)
+        assert rs[0, 0] == 0 and not rc.any()
+
+
+def pin_power_of_two_equivariance(o):
+    """I2: scaling a block by 2^j shifts both scale bytes by j and keeps every
+    code (no clamp in range)."""
+    x = _random_blocks(4, 200)
+    qc, qs, rc, rs = o.quantize(x)
+    ok = (qs.astype(int) > 40) & (qs.astype(int) < 200) & (rs.astype(int) > 40) & (rs.astype(int) < 200)
+    for j in (-7, -1, 1, 13):
+        qc2, qs2, rc2, rs2 = o.quantize(x * 2.0 ** j)
+        sel = ok[:, 0]
+        assert np.array_equal(qc2[sel], qc[sel]) and np.array_equal(rc2[sel], rc[sel])
+        assert np.array_equal(qs2[sel].astype(int), qs[sel].astype(int) + j)
+        assert np.array_equal(rs2[sel].astype(int), rs[sel].astype(int) + j)
+
+
+def pin_idempotence(o):
+    """I3: quantizing the dequantized code gives the same code back, and its
+    residual is zero."""
+    x = _random_blocks(5, 300)
+    qc, qs, _, _ = o.quantize(x)
+    d = o.dequant(qc, qs)
+    qc2, qs2, rc2, rs2 = o.quantize(d)
+    assert np.array_equal(qc2, qc) and np.array_equal(qs2, qs)
+    assert not rc2.any()
+
+
+def pin_negation(o):
+    """I4: deq Q(-x) = -deq Q(x) for both stages."""
+    x = _random_blocks(6, 300)
+    a = o.quantize(x)
+    b = o.quantize(-x)
+    assert np.array_equal(o.dequant(b[0], b[1]), -o.dequant(a[0], a[1]))
+    assert np.array_equal(o.dequant(b[2], b[3]), -o.dequant(a[2], a[3]))
+
+
+def pin_residual_improves(o):
+    """I5 and I6: the two-stage error never exceeds the one-stage error, and
+    per block it is at most half of the largest one-stage error (blocks whose
+    residual scale is not clamped)."""
+    x = _random_blocks(7, 400)
+    qc, qs, rc, rs = o.quantize(x)
+    q = o.dequant(qc, qs)
+    r = o.dequant(rc, rs)
+    e1 = np.abs(x - q)
+    e2 = np.abs(x - (q + r))
+    assert np.all(e2 <= e1)
+    unclamped = rs[:, 0] > 0
+    assert np.all(e2.max(axis=1)[unclamped] <= 0.5 * e1.max(axis=1)[unclamped])
+    # and the residual is exactly x - deq(q)
+    assert np.array_equal(o.residual(x), x - q)
+
+
+def pin_gemm_bruteforce(o):
+    """Eq. 11 on small shapes against numpy fp64 products of values decoded
+    here; also the phi = 0 product and linearity in the residual term."""
+    rng = np.random.default_rng(8)
+    for (M, N, K) in ((3, 5, 32), (7, 9, 96), (16, 16, 256)):
+        x = rng.standard_normal((M, K))
+        x[:, rng.integers(0, K)] *= 40
+        w = rng.normal(0, 0.02, (N, K))
+        qc, qs, rc, rs = o.quantize(x)
+        wc, ws, _, _ = o.quantize(w, residual=False)
+        dq, dr, dw = decode_codes(qc, qs), decode_codes(rc, rs), decode_codes(wc, ws)
+        z, bound = o.gemm(qc, qs, rc, rs, wc, ws)
+        want = dq @ dw.T + dr @ dw.T
+        assert np.all(np.abs(z - want) <= 1e-12 * bound + 1e-300), (M, N, K)
+        assert np.allclose(bound, np.abs(dq) @ np.abs(dw).T + np.abs(dr) @ np.abs(dw).T,
+                           rtol=1e-12, atol=0)
+        z0, _ = o.gemm(qc, qs, None, None, wc, ws)
+        assert np.all(np.abs(z0 - dq @ dw.T) <= 1e-12 * bound + 1e-300)
+        zs, bs = o.gemm_sampled(qc, qs, rc, rs, wc, ws, [0, M - 1, M // 2], [N - 1, 0, N // 2])
+        assert np.array_equal(zs, z[[0, M - 1, M // 2], [N - 1, 0, N // 2]])
+
+
+def pin_rfq_beats_mxfp4(o):
+    """On outlier-bearing activations the RFQ product is closer to the exact
+    product than plain MXFP4 (the accuracy claim of Sec. 4.3)."""
+    rng = np.random.default_rng(9)
+    x = rng.standard_normal((32, 256))
+    x[:, rng.choice(256, 4, replace=False)] *= 50
+    w = rng.normal(0, 0.02, (64, 256))
+    qc, qs, rc, rs = o.quantize(x)
+    wc, ws, _, _ = o.quantize(w, residual=False)
+    exact = x @ decode_codes(wc, ws).T
+    z1, _ = o.gemm(qc, qs, rc, rs, wc, ws)
+    z0, _ = o.gemm(qc, qs, None, None, wc, ws)
+    e_rfq = np.linalg.norm(z1 - exact)
+    e_mx = np.linalg.norm(z0 - exact)
+    assert e_rfq < 0.25 * e_mx, (e_rfq, e_mx)
+
+
+def pin_round_bf16(o):
+    """bf16 rounding: ties to even, above-tie rounds up, subnormal grid 2^-133,
+    overflow to infinity."""
+    cases = [
+        (1.0 + 2.0 ** -8, 1.0),
+        (1.0 + 3 * 2.0 ** -8, 1.0 + 2.0 ** -6),
+        (1.0 + 2.0 ** -8 + 2.0 ** -30, 1.0 + 2.0 ** -7),
+        (-(1.0 + 2.0 ** -8 + 2.0 ** -30), -(1.0 + 2.0 ** -7)),
+        (1.5 * 2.0 ** -133, 2.0 ** -132),
+        (0.5 * 2.0 ** -133, 0.0),
+        (3.0, 3.0),
+        ((2.0 - 2.0 ** -7) * 2.0 ** 127, (2.0 - 2.0 ** -7) * 2.0 ** 127),
+        ((2.0 - 2.0 ** -9) * 2.0 ** 127, math.inf),
+        (0.1, 0.10009765625),
+    ]
+    for v, want in cases:
+        assert o.round_bf16(v) == want, (v, o.round_bf16(v), want)
+
+
+def pin_swiglu_closed_forms(o):
+    """silu(0) = 0; silu(g) - silu(-g) = g; u = 0 gives 0; large g gives g*u;
+    every output is a bf16 value within half a bf16 ulp of the exact one."""
+    g = np.array([0.0, 1.0, -1.0, 2.5, -2.5, 30.0, -30.0, 0.125, 3.0])
+    u = np.array([1.0, 1.0, 1.0, 1.0, 1.0, 2.0, 2.0, 0.0, 1.0])
+    h = o.swiglu(g, u)
+    assert h[0] == 0.0 and h[7] == 0.0
+    assert h[5] == 60.0 and abs(h[6]) < 1e-10
+    s1 = 1.0 / (1.0 + math.exp(-1.0))
+    exact = [0, s1, -(1 - s1), 2.5 / (1 + math.exp(-2.5)), -2.5 / (1 + math.exp(2.5))]
+    for i, e in enumerate(exact):
+        assert abs(h[i] - e) <= 0.5 * bf16_ulp(e), (i, h[i], e)
+    # h(1) - h(-1) = 1 up to the two roundings
+    assert abs((h[1] - h[2]) - 1.0) <= bf16_ulp(1.0)
+    # outputs are bf16 values
+    for v in h:
+        if v != 0:
+            m, p = math.frexp(v)
+            assert (m * 2 ** 8) == int(m * 2 ** 8), v
+
+
+ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -1,0 +1,31 @@
+"""The oracle against its pins (CPU only), and proof that the pins catch
+plausible mistakes planted in the oracle."""
+import pytest
+
+import oracle
+import oracle_pins
+
+# Planted mistakes compiled into oracle variants (see ORACLE_PLANT in
+# oracle/rfq_oracle.c): 1 Eq. 3 without the -2 offset, 2 offset off by one,
+# 3 ties away from zero, 4 sign of zero dropped, 5 nibble order swapped,
+# 6 residual taken of x instead of x - q, 7 weight scaled by the activation
+# scale, 8 residual term dropped from the product, 9 bf16 truncation,
+# 10 sign error in silu, 11 weight index shifted by one.
+PLANTS = list(range(1, 12))
+
+
+@pytest.mark.parametrize("pin", oracle_pins.ALL_PINS, ids=lambda f: f.__name__)
+def test_oracle_pin(orc, pin):
+    pin(orc)
+
+
+@pytest.mark.parametrize("plant", PLANTS)
+def test_planted_mistake_is_caught(plant, tmp_path):
+    bad = oracle.variant(["-DORACLE_PLANT=%d" % plant], "plant%d" % plant)
+    failed = []
+    for pin in oracle_pins.ALL_PINS:
+        try:
+            pin(bad)
+        except AssertionError:
+            failed.append(pin.__name__)
+    assert failed, "no pin caught planted mistake %d" % plant
