@@ -1,0 +1,253 @@
+"""Benchmark of the RFQ forward path on one MI355X.
+
+One step = the whole hot path over one batch of the Qwen3-VL-like up-projection
+(X 4096x4096 bf16 with 0.5% outlier channels x50, W 4096x12288 fp32 master):
+  1. rfq_quantize_weight  W[N][K] fp32 -> MXFP4 codes + scales
+  2. rfq_quantize_act     X[M][K] bf16 -> primary + residual MXFP4
+  3. rfq_gemm             Z = (deq q + deq r) deq(w)^T, bf16 out
+Inputs are resident in HBM before the timed region; three input sets are
+rotated so that no step finds its inputs in the 256 MB last-level cache.
+
+value = executed FP4 flops of the step (4*M*N*K: the primary and the residual
+contraction) / step time.  The per-kernel durations come from HIP events
+recorded on the launch stream around every kernel of the timed steps; the
+roofline object reports the dominant kernel (the product) against the dense
+MXFP4 matrix-core peak.  The oracle (plain C) is timed on a bounded sample of
+the same step on the host cores.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+REPO = os.path.dirname(os.path.abspath(__file__))
+if REPO not in sys.path:
+    sys.path.insert(0, REPO)
+
+PEAK_FP4_TFLOPS = 10100.0     # MI355X dense MXFP4 matrix cores
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+N_SETS = 3
+METRIC = "RFQ-MXFP4 GEMM TFLOP/s + quantizer GB/s (Qwen3-VL-like 4096×4096×12288)"
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-rows", type=int, default=8,
+                   help="activation rows in the oracle's sample of the step")
+    return p.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: the RFQ path is data parallel over "
+              "tokens and this build runs and reports a single MI355X "
+              "(got --gpus %d)." % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2608_26581_amd as rfq
+    from paper_2608_26581_amd import workloads as wl
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    wk = wl.WORKLOADS["qwen"]
+    M, K = wk.M, wk.K
+    N = wk.weights[0][2]
+
+    # ---- inputs: N_SETS independent draws, resident on the device
+    xs, ws, outs = [], [], []
+    for s in range(N_SETS):
+        d = wl.generate(wk, seed=s)
+        xs.append(torch.from_numpy(d["x_bf16"].view(np.int16)).to(dev).view(torch.bfloat16))
+        ws.append(torch.from_numpy(d["w"]).to(dev))
+        del d
+    for s in range(N_SETS):
+        outs.append({
+            "wc": torch.empty((N, K // 2), dtype=torch.uint8, device=dev),
+            "ws": torch.empty((N, K // 32), dtype=torch.uint8, device=dev),
+            "q": [torch.empty((M, K // 2), dtype=torch.uint8, device=dev),
+                  torch.empty((M, K // 32), dtype=torch.uint8, device=dev),
+                  torch.empty((M, K // 2), dtype=torch.uint8, device=dev),
+                  torch.empty((M, K // 32), dtype=torch.uint8, device=dev)],
+            "z": torch.empty((M, N), dtype=torch.bfloat16, device=dev),
+        })
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+
+    def step(i, ev=None):
+        s = i % N_SETS
+        o = outs[s]
+        if ev is not None:
+            ev[0].record(stream)
+        rfq.rfq_quantize_weight(ws[s], out=(o["wc"], o["ws"]), stream=stream)
+        if ev is not None:
+            ev[1].record(stream)
+        rfq.rfq_quantize_act(xs[s], out=o["q"], stream=stream)
+        if ev is not None:
+            ev[2].record(stream)
+        rfq.rfq_gemm(*o["q"], o["wc"], o["ws"], out=o["z"], stream=stream)
+        if ev is not None:
+            ev[3].record(stream)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for i in range(args.steps):
+        step(i, evs[i])
+    t1.record(stream)
+    torch.cuda.synchronize()
+    total_ms = t0.elapsed_time(t1)
+    ms_step = total_ms / args.steps
+    wq_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    xq_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    gm_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+
+    exec_flops = 4.0 * M * N * K
+    value = exec_flops / (ms_step * 1e-3) / 1e12
+    gemm_tflops = exec_flops / (gm_ms * 1e-3) / 1e12
+    xq_bytes = M * K * 2 + 2 * (M * K // 2 + M * K // 32)
+    wq_bytes = N * K * 4 + N * K // 2 + N * K // 32
+    xq_gbs = xq_bytes / (xq_ms * 1e-3) / 1e9
+    wq_gbs = wq_bytes / (wq_ms * 1e-3) / 1e9
+
+    # ---- quantizer alone on the 8192x4096 bf16 workload (pure bandwidth)
+    qk = wl.WORKLOADS["quant"]
+    qx = []
+    for s in range(N_SETS):
+        d = wl.generate(qk, seed=100 + s)
+        qx.append(torch.from_numpy(d["x_bf16"].view(np.int16)).to(dev).view(torch.bfloat16))
+        del d
+    qo = [torch.empty((qk.M, qk.K // 2), dtype=torch.uint8, device=dev),
+          torch.empty((qk.M, qk.K // 32), dtype=torch.uint8, device=dev),
+          torch.empty((qk.M, qk.K // 2), dtype=torch.uint8, device=dev),
+          torch.empty((qk.M, qk.K // 32), dtype=torch.uint8, device=dev)]
+    for i in range(5):
+        rfq.rfq_quantize_act(qx[i % N_SETS], out=qo, stream=stream)
+    qreps = 50
+    qe = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(qreps)]
+    torch.cuda.synchronize()
+    for i in range(qreps):
+        qe[i][0].record(stream)
+        rfq.rfq_quantize_act(qx[i % N_SETS], out=qo, stream=stream)
+        qe[i][1].record(stream)
+    torch.cuda.synchronize()
+    q_ms = float(np.mean([a.elapsed_time(b) for a, b in qe]))
+    q_bytes = qk.M * qk.K * 2 + 2 * (qk.M * qk.K // 2 + qk.M * qk.K // 32)
+    quant_gbs = q_bytes / (q_ms * 1e-3) / 1e9
+
+    # ---- plain copy of 1 GiB as the achievable-bandwidth calibration
+    src = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    c0 = torch.cuda.Event(enable_timing=True)
+    c1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    c0.record(stream)
+    for _ in range(10):
+        dst.copy_(src)
+    c1.record(stream)
+    torch.cuda.synchronize()
+    copy_gbs = 2 * src.numel() * 4 * 10 / (c0.elapsed_time(c1) * 1e-3) / 1e9
+    del src, dst
+
+    result = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp4-e2m1 (fp32 accumulate)",
+        "data": "synthetic",
+        "config": {
+            "workload": "Qwen3-VL-like MLP up-projection: X 4096x4096 bf16 N(0,1) with 0.5% "
+                        "outlier channels x50, W 4096x12288 N(0,0.02) fp32 master; step = "
+                        "weight quantize + RFQ activation quantize + RFQ GEMM (phi=1), bf16 Z",
+            "M": M, "K": K, "N": N, "phi": 1, "z_dtype": "bf16", "input_sets": N_SETS,
+        },
+        "components": {
+            "rfq_gemm": {"ms": round(gm_ms, 5), "exec_tflops": round(gemm_tflops, 1),
+                         "effective_tflops": round(gemm_tflops / 2, 1)},
+            "quantize_act": {"ms": round(xq_ms, 5), "gbs": round(xq_gbs, 1),
+                             "bytes": xq_bytes},
+            "quantize_weight": {"ms": round(wq_ms, 5), "gbs": round(wq_gbs, 1),
+                                "bytes": wq_bytes},
+            "quantizer_8192x4096_bf16": {"ms": round(q_ms, 5), "gbs": round(quant_gbs, 1),
+                                         "frac_hbm": round(quant_gbs / PEAK_HBM_GBS, 4),
+                                         "bytes": q_bytes},
+            "copy_1GiB_gbs": round(copy_gbs, 1),
+        },
+        "roofline": {
+            "kernel": "rfq_gemm_kernel",
+            "bound": "mfma",
+            "achieved": round(gemm_tflops, 1),
+            "peak": PEAK_FP4_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(gemm_tflops / PEAK_FP4_TFLOPS, 4),
+            "traffic": None,
+        },
+    }
+    del xs, ws, outs, qx, qo
+    torch.cuda.empty_cache()
+
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(wk, args.cpu_rows)
+    print(json.dumps(result), flush=True)
+
+
+def cpu_baseline(wk, rows):
+    """The oracle, as it stands, on a bounded sample of one step: the whole
+    weight quantization plus `rows` activation rows through the activation
+    quantizer and the product (all N outputs).  Scaled to a full step as
+    t_w + (M / rows) * (t_x + t_gemm)."""
+    import oracle
+    from paper_2608_26581_amd import workloads as wl
+    o = oracle.default()
+    d = wl.generate(wk, seed=0)
+    M, K = d["x"].shape
+    N = d["w"].shape[0]
+    t = time.perf_counter()
+    wc, wsc, _, _ = o.quantize(d["w"], residual=False)
+    t_w = time.perf_counter() - t
+    t = time.perf_counter()
+    q = o.quantize(d["x"][:rows])
+    t_x = time.perf_counter() - t
+    t = time.perf_counter()
+    o.gemm(*q, wc, wsc)
+    t_g = time.perf_counter() - t
+    t_step = t_w + (M / rows) * (t_x + t_g)
+    return {
+        "value": round(4.0 * M * N * K / t_step / 1e12, 6),
+        "unit": "TFLOP/s",
+        "cores": o.num_threads(),
+        "kind": "oracle",
+        "sample": "full weight quantization (%dx%d) + %d activation rows through the RFQ "
+                  "quantizer and the fp64 product against all %d outputs; scaled to the "
+                  "%d-row step (t_w=%.2fs t_x=%.3fs t_gemm=%.2fs)" % (N, K, rows, N, M, t_w,
+                                                                      t_x, t_g),
+    }
+
+
+if __name__ == "__main__":
+    main()

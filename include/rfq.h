@@ -1,0 +1,145 @@
+/*
+ * rfq.h -- C ABI of librfq: Residual Fallback Quantization (RFQ) with MXFP4
+ * codes on AMD Instinct MI355X (gfx950).
+ *
+ * The library computes the data-parallel forward path of RFQ (Sec. 4.3 of the
+ * paper): an MX activation quantizer that emits a primary MXFP4 code and an
+ * MXFP4 code of the residual the primary code lost (Eq. 8-10), and a
+ * block-scaled FP4 product that contracts both codes against MXFP4 weights
+ * (Eq. 11, Algorithm 1).
+ *
+ * Number format (Sec. 3.2, Eq. 3-4, element format of Sec. 3.2.2):
+ *   - a block is 32 consecutive elements of one row along K (the reduction
+ *     dimension); K must be a multiple of 32;
+ *   - one E8M0 scale byte per block, value 2^(byte - 127); the block exponent
+ *     is floor(log2 amax) - 2 clamped to [-127, 127], an all-zero block gets
+ *     byte 0x00;
+ *   - one 4-bit E2M1 code per element, sign<<3 | magnitude index, magnitudes
+ *     {0, 0.5, 1, 1.5, 2, 3, 4, 6}; round to nearest, ties to even,
+ *     saturating at +-6; the sign of an element that rounds to zero is kept;
+ *   - codes are packed two per byte, element 2j in the low nibble of byte j;
+ *   - layouts: codes[rows][K/2] bytes and scales[rows][K/32] bytes, both
+ *     row-major and dense.
+ *
+ * Conventions shared by every call:
+ *   - Ownership: the caller allocates and owns every buffer.  All data
+ *     pointers are device pointers (HIP device memory of the current device).
+ *     The library never allocates, frees or retains a pointer after return.
+ *   - Asynchrony: every compute call is enqueued on hip_stream (a hipStream_t
+ *     passed as void*; NULL selects the null stream) and returns before the
+ *     work completes.  The caller synchronizes.
+ *   - Errors: every call returns an rfq_status.  Arguments are validated on
+ *     the host before any HIP call is made, so argument errors are reported
+ *     without touching the device.  RFQ_ERR_DEVICE means the current device
+ *     is not a gfx950 GPU; RFQ_ERR_LAUNCH means a HIP launch failed.  Faults
+ *     inside kernels surface at the caller's next synchronization, as in HIP.
+ *   - Empty work: rows == 0 (or N == 0 for the product) is a valid no-op;
+ *     the pointers of such a call are not read and may be NULL.
+ *   - Thread safety: calls may be issued from several host threads; calls on
+ *     one stream execute in issue order.
+ */
+#ifndef RFQ_H
+#define RFQ_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    RFQ_OK = 0,
+    RFQ_ERR_NULL = 1,    /* a required pointer is NULL, or an optional pair is half given */
+    RFQ_ERR_SHAPE = 2,   /* negative size, K < 32 or K not a multiple of 32 */
+    RFQ_ERR_DTYPE = 3,   /* unknown rfq_dtype value */
+    RFQ_ERR_ALIGN = 4,   /* a pointer violates the alignment stated for it */
+    RFQ_ERR_DEVICE = 5,  /* no current HIP device, or it is not gfx950 */
+    RFQ_ERR_LAUNCH = 6   /* a kernel launch failed */
+} rfq_status;
+
+typedef enum {
+    RFQ_F32 = 0,   /* IEEE binary32 */
+    RFQ_BF16 = 1   /* bfloat16 (upper half of a binary32) */
+} rfq_dtype;
+
+/*
+ * RFQ activation quantizer: primary code Q(X) (Eq. 8) and, when r_codes and
+ * r_scales are given, the residual DeltaX = X - deq(Q(X)) (Eq. 9) quantized
+ * with its own block scales (Eq. 10).  The residual is formed in registers
+ * and never written to memory.
+ *   x        [M][K] row-major, element type x_dtype; 16-byte aligned.
+ *   q_codes  [M][K/2] bytes, 16-byte aligned.    q_scales [M][K/32] bytes.
+ *   r_codes  [M][K/2] bytes, 16-byte aligned, or NULL.
+ *   r_scales [M][K/32] bytes, or NULL.  Both residual pointers are NULL
+ *            (plain MXFP4) or both non-NULL.
+ * Non-finite inputs are outside the contract (results unspecified).
+ */
+rfq_status rfq_quantize_act(const void *x, rfq_dtype x_dtype, int64_t M, int64_t K,
+                            uint8_t *q_codes, uint8_t *q_scales,
+                            uint8_t *r_codes, uint8_t *r_scales,
+                            void *hip_stream);
+
+/*
+ * Weight quantizer Q(Y) (Eq. 8), primary code only.  The weight is given as
+ * W[N][K] (the transpose of the paper's Y, K contiguous), blocks along K.
+ *   w        [N][K] row-major, element type w_dtype; 16-byte aligned.
+ *   w_codes  [N][K/2] bytes, 16-byte aligned.    w_scales [N][K/32] bytes.
+ */
+rfq_status rfq_quantize_weight(const void *w, rfq_dtype w_dtype, int64_t N, int64_t K,
+                               uint8_t *w_codes, uint8_t *w_scales,
+                               void *hip_stream);
+
+/*
+ * RFQ product, Eq. (11) / Algorithm 1:
+ *   Z[m][n] = sum_k deq(q)[m][k] * deq(w)[n][k]  +  sum_k deq(r)[m][k] * deq(w)[n][k]
+ * with every block of the residual taken (fallback indicator phi = 1), or
+ * without the second sum (phi = 0, plain MXFP4) when r_codes and r_scales are
+ * both NULL.  Products of codes are exact; accumulation is in fp32 in an
+ * unspecified order.  The output is fp32, or bf16 rounded to nearest even.
+ *   q_codes, r_codes, w_codes: 16-byte aligned, layouts as above.
+ *   z        [M][N] row-major, z_dtype; 16-byte aligned.
+ */
+rfq_status rfq_gemm(const uint8_t *q_codes, const uint8_t *q_scales,
+                    const uint8_t *r_codes, const uint8_t *r_scales,
+                    const uint8_t *w_codes, const uint8_t *w_scales,
+                    int64_t M, int64_t N, int64_t K,
+                    void *z, rfq_dtype z_dtype, void *hip_stream);
+
+/*
+ * Dequantization, one term of Eq. (12): out[r][k] = value(code) * 2^(scale-127),
+ * exact in fp32 (scale byte 0xFF gives NaN).
+ *   codes [rows][K/2] 16-byte aligned; scales [rows][K/32]; out [rows][K]
+ *   fp32, 16-byte aligned.
+ */
+rfq_status rfq_dequant(const uint8_t *codes, const uint8_t *scales, int64_t rows,
+                       int64_t K, float *out, void *hip_stream);
+
+/*
+ * SwiGLU intermediate of a gated MLP followed by the RFQ quantizer: h =
+ * bf16(silu(g) * u) with silu(g) = g / (1 + exp(-g)) in fp32 arithmetic,
+ * then Q(h) and Q(h - deq Q(h)) exactly as rfq_quantize_act on bf16 input.
+ * This chains two RFQ products (gate/up, then down) without a bf16 round trip
+ * of h through memory.
+ *   g, u     [M][Nh] row-major, element type dt; 16-byte aligned.  Nh is
+ *            the K of the following product (multiple of 32).
+ *   q_codes, q_scales, r_codes, r_scales: as rfq_quantize_act with K = Nh (residual pair optional).
+ *   h_out    [M][Nh] bf16, 16-byte aligned, or NULL; when given, h is also
+ *            written (for inspection).
+ */
+rfq_status rfq_swiglu_quantize_act(const void *g, const void *u, rfq_dtype dt,
+                                   int64_t M, int64_t Nh,
+                                   uint8_t *q_codes, uint8_t *q_scales,
+                                   uint8_t *r_codes, uint8_t *r_scales,
+                                   void *h_out, void *hip_stream);
+
+/* Static, never-NULL description of a status code. */
+const char *rfq_status_str(rfq_status s);
+
+/* Version of this interface; changes whenever a signature or layout changes. */
+int rfq_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RFQ_H */

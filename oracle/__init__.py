@@ -47,6 +47,8 @@ def _load(path=LIB):
                                         ctypes.POINTER(ctypes.c_int64), I64, D, D]
     lib.oracle_swiglu.argtypes = [D, D, I64, D]
     lib.oracle_residual.argtypes = [D, I64, I64, D]
+    lib.oracle_num_threads.argtypes = []
+    lib.oracle_num_threads.restype = ctypes.c_int
     for f in ("oracle_rfq_quantize", "oracle_dequant", "oracle_gemm",
               "oracle_gemm_sampled", "oracle_swiglu", "oracle_residual"):
         getattr(lib, f).restype = None
@@ -78,6 +80,9 @@ class Oracle:
         if a is None:
             return None
         return a.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8))
+
+    def num_threads(self):
+        return int(self.h.oracle_num_threads())
 
     def e2m1_value(self, code):
         return self.h.oracle_e2m1_value(int(code))

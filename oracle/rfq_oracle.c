@@ -39,6 +39,9 @@
  * (value 2^(byte-127)).
  */
 #include <math.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 #include <stdint.h>
 #include <stddef.h>
 #include <string.h>
@@ -351,4 +354,14 @@ void oracle_residual(const double *x, int64_t rows, int64_t K, double *res)
                 res[m * K + b * ORACLE_BLOCK + i] = xb[i] - deq[i];
         }
     }
+}
+
+/* Number of threads the parallel loops above use (1 without OpenMP). */
+int oracle_num_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
 }

@@ -1,0 +1,9 @@
+"""RFQ (Residual Fallback Quantization) with MXFP4 codes on MI355X (gfx950).
+
+The compute path is librfq.so (HIP kernels behind the C ABI in include/rfq.h);
+this package holds its Python binding and the seeded synthetic workloads.
+"""
+from .rfq import (  # noqa: F401
+    EXPORTS, LIB_PATH, RfqError, load, rfq_abi_version, rfq_dequant, rfq_gemm,
+    rfq_quantize_act, rfq_quantize_weight, rfq_status_str, rfq_swiglu_quantize_act,
+)

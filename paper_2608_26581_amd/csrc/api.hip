@@ -1,0 +1,160 @@
+// C ABI of librfq: host-side argument validation and kernel dispatch.
+// Every check that can be made on the host runs before the first HIP call,
+// so argument errors are reported without touching a device.  Order: dtype,
+// shape, empty work (a no-op whose pointers are not read and may be NULL),
+// pointers, alignment, device.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <atomic>
+
+#include "rfq.h"
+#include "rfq_internal.h"
+
+namespace {
+
+constexpr int kAbiVersion = 1;
+constexpr int kMaxDevices = 64;
+
+// Per-device result of the architecture check: 0 unknown, 1 gfx950, 2 other.
+std::atomic<int> g_arch_state[kMaxDevices];
+
+bool aligned(const void *p, uintptr_t a) {
+  return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0;
+}
+
+bool valid_dtype(rfq_dtype d) { return d == RFQ_F32 || d == RFQ_BF16; }
+
+rfq_status check_k(int64_t rows, int64_t K) {
+  if (rows < 0 || K < 32 || (K % 32) != 0) return RFQ_ERR_SHAPE;
+  return RFQ_OK;
+}
+
+// Confirms that the current device is a gfx950 GPU (cached per device).
+rfq_status check_device() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return RFQ_ERR_DEVICE;
+  if (dev >= kMaxDevices) return RFQ_ERR_DEVICE;
+  int st = g_arch_state[dev].load(std::memory_order_acquire);
+  if (st == 0) {
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return RFQ_ERR_DEVICE;
+    st = strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : 2;
+    g_arch_state[dev].store(st, std::memory_order_release);
+  }
+  return st == 1 ? RFQ_OK : RFQ_ERR_DEVICE;
+}
+
+rfq_status launched(hipError_t e) { return e == hipSuccess ? RFQ_OK : RFQ_ERR_LAUNCH; }
+
+}  // namespace
+
+extern "C" {
+
+rfq_status rfq_quantize_act(const void *x, rfq_dtype x_dtype, int64_t M, int64_t K,
+                            uint8_t *q_codes, uint8_t *q_scales,
+                            uint8_t *r_codes, uint8_t *r_scales,
+                            void *hip_stream) {
+  if (!valid_dtype(x_dtype)) return RFQ_ERR_DTYPE;
+  rfq_status s = check_k(M, K);
+  if (s != RFQ_OK) return s;
+  if (M == 0) return RFQ_OK;
+  if (!x || !q_codes || !q_scales) return RFQ_ERR_NULL;
+  if ((r_codes == nullptr) != (r_scales == nullptr)) return RFQ_ERR_NULL;
+  if (!aligned(x, 16) || !aligned(q_codes, 16) || (r_codes && !aligned(r_codes, 16)))
+    return RFQ_ERR_ALIGN;
+  if ((s = check_device()) != RFQ_OK) return s;
+  return launched(rfq::launch_quantize(x, x_dtype == RFQ_BF16, M * K, q_codes, q_scales,
+                                       r_codes, r_scales,
+                                       static_cast<hipStream_t>(hip_stream)));
+}
+
+rfq_status rfq_quantize_weight(const void *w, rfq_dtype w_dtype, int64_t N, int64_t K,
+                               uint8_t *w_codes, uint8_t *w_scales,
+                               void *hip_stream) {
+  if (!valid_dtype(w_dtype)) return RFQ_ERR_DTYPE;
+  rfq_status s = check_k(N, K);
+  if (s != RFQ_OK) return s;
+  if (N == 0) return RFQ_OK;
+  if (!w || !w_codes || !w_scales) return RFQ_ERR_NULL;
+  if (!aligned(w, 16) || !aligned(w_codes, 16)) return RFQ_ERR_ALIGN;
+  if ((s = check_device()) != RFQ_OK) return s;
+  return launched(rfq::launch_quantize(w, w_dtype == RFQ_BF16, N * K, w_codes, w_scales,
+                                       nullptr, nullptr,
+                                       static_cast<hipStream_t>(hip_stream)));
+}
+
+rfq_status rfq_gemm(const uint8_t *q_codes, const uint8_t *q_scales,
+                    const uint8_t *r_codes, const uint8_t *r_scales,
+                    const uint8_t *w_codes, const uint8_t *w_scales,
+                    int64_t M, int64_t N, int64_t K,
+                    void *z, rfq_dtype z_dtype, void *hip_stream) {
+  if (!valid_dtype(z_dtype)) return RFQ_ERR_DTYPE;
+  rfq_status s = check_k(M, K);
+  if (s != RFQ_OK) return s;
+  if (N < 0) return RFQ_ERR_SHAPE;
+  if (M > INT32_MAX || N > INT32_MAX) return RFQ_ERR_SHAPE;
+  // Output tiles are at least 64 x 64 and their count must fit one grid axis.
+  if (((M + 63) / 64) * ((N + 63) / 64) > INT32_MAX) return RFQ_ERR_SHAPE;
+  if (M == 0 || N == 0) return RFQ_OK;
+  if (!q_codes || !q_scales || !w_codes || !w_scales || !z) return RFQ_ERR_NULL;
+  if ((r_codes == nullptr) != (r_scales == nullptr)) return RFQ_ERR_NULL;
+  if (!aligned(q_codes, 16) || !aligned(w_codes, 16) || (r_codes && !aligned(r_codes, 16)) ||
+      !aligned(z, 16))
+    return RFQ_ERR_ALIGN;
+  if ((s = check_device()) != RFQ_OK) return s;
+  return launched(rfq::launch_gemm(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales,
+                                   M, N, K, z, z_dtype == RFQ_BF16,
+                                   static_cast<hipStream_t>(hip_stream)));
+}
+
+rfq_status rfq_dequant(const uint8_t *codes, const uint8_t *scales, int64_t rows,
+                       int64_t K, float *out, void *hip_stream) {
+  rfq_status s = check_k(rows, K);
+  if (s != RFQ_OK) return s;
+  if (rows == 0) return RFQ_OK;
+  if (!codes || !scales || !out) return RFQ_ERR_NULL;
+  if (!aligned(codes, 16) || !aligned(out, 16)) return RFQ_ERR_ALIGN;
+  if ((s = check_device()) != RFQ_OK) return s;
+  return launched(rfq::launch_dequant(codes, scales, rows * K, out,
+                                      static_cast<hipStream_t>(hip_stream)));
+}
+
+rfq_status rfq_swiglu_quantize_act(const void *g, const void *u, rfq_dtype dt,
+                                   int64_t M, int64_t Nh,
+                                   uint8_t *q_codes, uint8_t *q_scales,
+                                   uint8_t *r_codes, uint8_t *r_scales,
+                                   void *h_out, void *hip_stream) {
+  if (!valid_dtype(dt)) return RFQ_ERR_DTYPE;
+  rfq_status s = check_k(M, Nh);
+  if (s != RFQ_OK) return s;
+  if (M == 0) return RFQ_OK;
+  if (!g || !u || !q_codes || !q_scales) return RFQ_ERR_NULL;
+  if ((r_codes == nullptr) != (r_scales == nullptr)) return RFQ_ERR_NULL;
+  if (!aligned(g, 16) || !aligned(u, 16) || !aligned(q_codes, 16) ||
+      (r_codes && !aligned(r_codes, 16)) || (h_out && !aligned(h_out, 16)))
+    return RFQ_ERR_ALIGN;
+  if ((s = check_device()) != RFQ_OK) return s;
+  return launched(rfq::launch_swiglu_quantize(g, u, dt == RFQ_BF16, M * Nh, q_codes, q_scales,
+                                              r_codes, r_scales,
+                                              static_cast<uint16_t *>(h_out),
+                                              static_cast<hipStream_t>(hip_stream)));
+}
+
+const char *rfq_status_str(rfq_status s) {
+  switch (s) {
+    case RFQ_OK: return "ok";
+    case RFQ_ERR_NULL: return "null pointer (or half of an optional pair)";
+    case RFQ_ERR_SHAPE: return "bad shape (negative size, or K not a positive multiple of 32)";
+    case RFQ_ERR_DTYPE: return "unknown dtype";
+    case RFQ_ERR_ALIGN: return "misaligned pointer";
+    case RFQ_ERR_DEVICE: return "no gfx950 device current";
+    case RFQ_ERR_LAUNCH: return "kernel launch failed";
+  }
+  return "unknown status";
+}
+
+int rfq_abi_version(void) { return kAbiVersion; }
+
+}  // extern "C"

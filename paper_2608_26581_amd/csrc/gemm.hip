@@ -1,0 +1,311 @@
+// RFQ product on the gfx950 block-scaled FP4 matrix cores (Eq. 11,
+// Algorithm 1 with the fallback indicator phi = 1, or phi = 0 without the
+// residual operand):
+//
+//   Z[m][n] = sum_k q[m][k] w[n][k] * Sq[m][k/32] Sw[n][k/32]
+//           + sum_k r[m][k] w[n][k] * Sr[m][k/32] Sw[n][k/32]
+//
+// Instruction: v_mfma_scale_f32_16x16x128_f8f6f4 with both operands in E2M1
+// (format code 4).  Lane l of a 16x16x128 operand holds row (l mod 16) and 32
+// consecutive K values (one MX block, 16 bytes, element 2j in the low nibble of
+// byte j) and supplies that block's E8M0 scale in a byte of its scale VGPR
+// selected by op_sel.  The weight fragment is the A operand and the
+// activation fragment the B operand, so the 16x16 fp32 result in lane l holds
+// Z[m = l mod 16][n = 4*(l/16) .. +3]: four consecutive outputs of one row.
+//
+// Because the contraction order inside one instruction is irrelevant, the K
+// values given to the four lane groups may be permuted as long as weights and
+// activations use the same permutation: in a stage of 256 K values (8 blocks),
+// lane group g takes blocks 2g (first instruction) and 2g+1 (second), so its
+// two scale bytes are adjacent and one 16-bit LDS read serves both.
+//
+// Data flow per workgroup (output tile BM x BN, 4 waves as 2 x 2, each wave a
+// (BM/2) x (BN/2) sub-tile): each stage copies 128 code bytes per row of the
+// q, r and w tiles plus 8 scale bytes per row from global memory into LDS
+// (double buffered; the next stage's global loads are in flight while the
+// current stage is multiplied).  The residual contraction reuses every
+// weight fragment read from LDS: per weight fragment two MFMAs are issued,
+// one against q and one against r.  16-byte chunks are XOR-swizzled by row
+// inside LDS so that the 16 rows read by one fragment hit distinct banks.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <atomic>
+#include <type_traits>
+
+#include "rfq_internal.h"
+
+namespace rfq {
+namespace {
+
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+constexpr int kStageK = 256;                 // K values per stage
+constexpr int kRowBytes = kStageK / 2;       // code bytes per row per stage
+constexpr int kRowChunks = kRowBytes / 16;   // 16-byte chunks per row
+constexpr int kRowScales = kStageK / 32;     // scale bytes per row per stage
+constexpr int kFmtFp4 = 4;                   // E2M1 operand format code
+
+template <int BM, int BN, bool RES>
+struct Smem {
+  static constexpr int kRows = (RES ? 2 : 1) * BM + BN;   // q, r, w rows
+  static constexpr int kDataBytes = kRows * kRowBytes;
+  static constexpr int kScaleBytes = kRows * kRowScales;
+  static constexpr int kStageBytes = kDataBytes + kScaleBytes;
+  static constexpr int kBytes = 2 * kStageBytes;
+};
+
+__device__ __forceinline__ int swz(int row, int chunk) {
+  return row * kRowBytes + 16 * (chunk ^ (row & 7));
+}
+
+// bf16 round to nearest even of a finite fp32 value.
+__device__ __forceinline__ uint32_t bf16_rne(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+template <int BM, int BN, bool RES, bool ZBF16>
+__global__ __launch_bounds__(256) void rfq_gemm_kernel(
+    const uint8_t *__restrict__ qc, const uint8_t *__restrict__ qs,
+    const uint8_t *__restrict__ rc, const uint8_t *__restrict__ rs,
+    const uint8_t *__restrict__ wc, const uint8_t *__restrict__ ws,
+    int64_t M, int64_t N, int64_t K, void *__restrict__ z) {
+  constexpr int kThreads = 256;
+  constexpr int TM = BM / 2, TN = BN / 2;     // wave sub-tile
+  constexpr int FM = TM / 16, FN = TN / 16;   // 16x16 fragments per wave
+  using S = Smem<BM, BN, RES>;
+  constexpr int kRows = S::kRows;
+  constexpr int kChunksPerStage = kRows * kRowChunks;
+  static_assert(kChunksPerStage % kThreads == 0, "chunk split");
+  constexpr int kLoads = kChunksPerStage / kThreads;
+  constexpr int kScaleLoads = (kRows + kThreads - 1) / kThreads;
+
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+
+  // ---- tile order: consecutive tiles on one XCD, grouped by 8 tile rows.
+  const int ntm = (int)((M + BM - 1) / BM), ntn = (int)((N + BN - 1) / BN);
+  const int ntiles = ntm * ntn;
+  int t = blockIdx.x;
+  if ((ntiles & 7) == 0) t = (t & 7) * (ntiles >> 3) + (t >> 3);
+  constexpr int GM = 8;
+  const int group = t / (GM * ntn);
+  const int first_m = group * GM;
+  const int gsize = min(ntm - first_m, GM);
+  const int in_group = t - group * GM * ntn;
+  const int tm = first_m + in_group % gsize;
+  const int tn = in_group / gsize;
+  const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int64_t kbytes = K / 2, kblocks = K / 32;
+  const int nstages = (int)((K + kStageK - 1) / kStageK);
+  const bool fast_scales =
+      (kblocks % kRowScales) == 0 &&
+      ((reinterpret_cast<uintptr_t>(qs) | reinterpret_cast<uintptr_t>(rs) |
+        reinterpret_cast<uintptr_t>(ws)) & 7) == 0;
+
+  // Row r of the stage tile: [0, BM) q, [BM, 2BM) r (RES), then BN rows of w.
+  constexpr int kWRow0 = (RES ? 2 : 1) * BM;
+  auto src_codes = [&](int r) { return r >= kWRow0 ? wc : (RES && r >= BM ? rc : qc); };
+  auto src_scales = [&](int r) { return r >= kWRow0 ? ws : (RES && r >= BM ? rs : qs); };
+  auto src_row = [&](int r) -> int64_t {
+    return r >= kWRow0 ? n0 + (r - kWRow0) : m0 + (RES && r >= BM ? r - BM : r);
+  };
+  auto src_limit = [&](int r) -> int64_t { return r >= kWRow0 ? N : M; };
+
+  uint4 pref[kLoads];
+  uint2 spref[kScaleLoads];
+
+  auto load_stage = [&](int st) {
+    const int64_t kb0 = (int64_t)st * kRowBytes;   // byte offset in a row
+#pragma unroll
+    for (int i = 0; i < kLoads; ++i) {
+      const int c = tid + i * kThreads;
+      const int r = c / kRowChunks, ch = c % kRowChunks;
+      const int64_t grow = src_row(r);
+      const int64_t kb = kb0 + 16 * ch;
+      if (grow < src_limit(r) && kb < kbytes)
+        pref[i] = *reinterpret_cast<const uint4 *>(src_codes(r) + grow * kbytes + kb);
+      else
+        pref[i] = make_uint4(0, 0, 0, 0);
+    }
+    const int64_t sb0 = (int64_t)st * kRowScales;
+#pragma unroll
+    for (int i = 0; i < kScaleLoads; ++i) {
+      const int r = tid + i * kThreads;
+      uint2 v = make_uint2(0, 0);
+      if (r < kRows) {
+        const int64_t grow = src_row(r);
+        if (grow < src_limit(r)) {
+          const uint8_t *p = src_scales(r) + grow * kblocks + sb0;
+          if (fast_scales) {
+            v = *reinterpret_cast<const uint2 *>(p);
+          } else {
+            uint32_t lo = 0, hi = 0;
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+              if (sb0 + b < kblocks) lo |= (uint32_t)p[b] << (8 * b);
+              if (sb0 + 4 + b < kblocks) hi |= (uint32_t)p[4 + b] << (8 * b);
+            }
+            v = make_uint2(lo, hi);
+          }
+        }
+      }
+      spref[i] = v;
+    }
+  };
+
+  auto store_stage = [&](int buf) {
+    uint8_t *base = smem + buf * S::kStageBytes;
+#pragma unroll
+    for (int i = 0; i < kLoads; ++i) {
+      const int c = tid + i * kThreads;
+      const int r = c / kRowChunks, ch = c % kRowChunks;
+      *reinterpret_cast<uint4 *>(base + swz(r, ch)) = pref[i];
+    }
+#pragma unroll
+    for (int i = 0; i < kScaleLoads; ++i) {
+      const int r = tid + i * kThreads;
+      if (r < kRows)
+        *reinterpret_cast<uint2 *>(base + S::kDataBytes + r * kRowScales) = spref[i];
+    }
+  };
+
+  v4f acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+
+  const int frow = lane & 15, g = lane >> 4;
+
+  // One instruction step: blocks 2g+SUB of the stage for every lane group.
+  auto mma_step = [&](const uint8_t *base, auto sub_tag) {
+    constexpr int SUB = decltype(sub_tag)::value;
+    const uint8_t *sc = base + S::kDataBytes;
+    v8i wf[FN];
+    int wsc[FN];
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int r = (RES ? 2 : 1) * BM + wn * TN + 16 * j + frow;
+      const uint4 d = *reinterpret_cast<const uint4 *>(base + swz(r, 2 * g + SUB));
+      wf[j] = v8i{(int)d.x, (int)d.y, (int)d.z, (int)d.w, 0, 0, 0, 0};
+      wsc[j] = *reinterpret_cast<const uint16_t *>(sc + r * kRowScales + 2 * g);
+    }
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int r = wm * TM + 16 * i + frow;
+      const uint4 d = *reinterpret_cast<const uint4 *>(base + swz(r, 2 * g + SUB));
+      const v8i af = v8i{(int)d.x, (int)d.y, (int)d.z, (int)d.w, 0, 0, 0, 0};
+      const int asc = *reinterpret_cast<const uint16_t *>(sc + r * kRowScales + 2 * g);
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(
+            wf[j], af, acc[i][j], kFmtFp4, kFmtFp4, SUB, wsc[j], SUB, asc);
+      if constexpr (RES) {
+        const int rr = BM + r;
+        const uint4 e = *reinterpret_cast<const uint4 *>(base + swz(rr, 2 * g + SUB));
+        const v8i rf = v8i{(int)e.x, (int)e.y, (int)e.z, (int)e.w, 0, 0, 0, 0};
+        const int rsc = *reinterpret_cast<const uint16_t *>(sc + rr * kRowScales + 2 * g);
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(
+              wf[j], rf, acc[i][j], kFmtFp4, kFmtFp4, SUB, wsc[j], SUB, rsc);
+      }
+    }
+  };
+
+  load_stage(0);
+  store_stage(0);
+  __syncthreads();
+  for (int st = 0; st < nstages; ++st) {
+    const bool more = st + 1 < nstages;
+    if (more) load_stage(st + 1);
+    const uint8_t *base = smem + (st & 1) * S::kStageBytes;
+    mma_step(base, std::integral_constant<int, 0>{});
+    mma_step(base, std::integral_constant<int, 1>{});
+    if (more) store_stage((st + 1) & 1);
+    __syncthreads();
+  }
+
+  // ---- epilogue: lane holds Z[m][n .. n+3] for every fragment pair.
+  const bool vec_ok = (N & 3) == 0;
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    const int64_t m = m0 + wm * TM + 16 * i + frow;
+    if (m >= M) continue;
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int64_t n = n0 + wn * TN + 16 * j + 4 * g;
+      const v4f a = acc[i][j];
+      if constexpr (ZBF16) {
+        uint16_t *zp = reinterpret_cast<uint16_t *>(z) + m * N + n;
+        if (vec_ok && n + 3 < N) {
+          uint2 w;
+          w.x = bf16_rne(a[0]) | (bf16_rne(a[1]) << 16);
+          w.y = bf16_rne(a[2]) | (bf16_rne(a[3]) << 16);
+          *reinterpret_cast<uint2 *>(zp) = w;
+        } else {
+#pragma unroll
+          for (int v = 0; v < 4; ++v)
+            if (n + v < N) zp[v] = (uint16_t)bf16_rne(a[v]);
+        }
+      } else {
+        float *zp = reinterpret_cast<float *>(z) + m * N + n;
+        if (vec_ok && n + 3 < N) {
+          *reinterpret_cast<float4 *>(zp) = make_float4(a[0], a[1], a[2], a[3]);
+        } else {
+#pragma unroll
+          for (int v = 0; v < 4; ++v)
+            if (n + v < N) zp[v] = a[v];
+        }
+      }
+    }
+  }
+}
+
+template <int BM, int BN, bool RES, bool ZBF16>
+hipError_t launch_tile(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc,
+                       const uint8_t *rs, const uint8_t *wc, const uint8_t *ws,
+                       int64_t M, int64_t N, int64_t K, void *z,
+                       hipStream_t stream) {
+  using S = Smem<BM, BN, RES>;
+  auto kern = rfq_gemm_kernel<BM, BN, RES, ZBF16>;
+  // The dynamic-LDS limit is an attribute of the kernel function; setting it
+  // twice from racing threads is harmless.
+  static std::atomic<bool> attr_done{false};
+  if (!attr_done.load(std::memory_order_acquire)) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       S::kBytes);
+    if (e != hipSuccess) return e;
+    attr_done.store(true, std::memory_order_release);
+  }
+  const int64_t ntiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+  kern<<<dim3((unsigned)ntiles), dim3(256), S::kBytes, stream>>>(qc, qs, rc, rs, wc, ws, M, N, K, z);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_gemm(const uint8_t *q_codes, const uint8_t *q_scales,
+                       const uint8_t *r_codes, const uint8_t *r_scales,
+                       const uint8_t *w_codes, const uint8_t *w_scales,
+                       int64_t M, int64_t N, int64_t K, void *z, bool z_bf16,
+                       hipStream_t stream) {
+  constexpr int BM = 128, BN = 128;
+  if (r_codes) {
+    if (z_bf16)
+      return launch_tile<BM, BN, true, true>(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K, z, stream);
+    return launch_tile<BM, BN, true, false>(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K, z, stream);
+  }
+  if (z_bf16)
+    return launch_tile<BM, BN, false, true>(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K, z, stream);
+  return launch_tile<BM, BN, false, false>(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K, z, stream);
+}
+
+}  // namespace rfq

@@ -1,0 +1,279 @@
+// Streaming MXFP4 kernels for gfx950: the RFQ activation quantizer (primary
+// code, Eq. 8, plus the quantized residual, Eq. 9-10), the weight quantizer,
+// the fused SwiGLU + quantizer and dequantization (Eq. 12).
+//
+// Work decomposition: the tensor is treated as a flat array (K is a multiple
+// of 32, so no MX block straddles a row and the scale index of a block is its
+// flat block index).  One thread owns 8 consecutive elements; the four lanes
+// of a DPP quad own one 32-element block, so the block maximum takes two
+// quad-permute steps and no LDS.  Each thread issues U independent 16-byte
+// loads before any arithmetic to keep enough bytes in flight for HBM.
+//
+// Element conversion uses the gfx950 scaled FP4 conversions: the convert to
+// FP4 divides by the scale 2^(byte-127), rounds to nearest-even, saturates at
+// +-6 and keeps the sign of zero; the convert from FP4 multiplies by the scale
+// exactly.  The residual x - deq(q) is exact in fp32 (a nonzero E2M1 rounding
+// lies within a factor of two of x), so it is formed in registers only.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "rfq_internal.h"
+
+namespace rfq {
+namespace {
+
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kThreads = 256;
+constexpr int kUnroll = 4;
+
+// Maximum over the four lanes of a quad (DPP quad_perm 1,0,3,2 then 2,3,0,1).
+__device__ __forceinline__ float quad_max(float v) {
+  float o = __int_as_float(
+      __builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
+  v = fmaxf(v, o);
+  o = __int_as_float(
+      __builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));
+  return fmaxf(v, o);
+}
+
+// E8M0 byte of a block whose largest magnitude is amax (Eq. 3 with the OCP
+// offset): floor(log2 amax) - 2 + 127 is the biased exponent field minus 2;
+// blocks with amax < 2^-125 (zero and subnormal included) clamp to byte 0.
+__device__ __forceinline__ uint32_t scale_byte(float amax) {
+  const uint32_t e = __float_as_uint(amax) >> 23;
+  return e > 2u ? e - 2u : 0u;
+}
+
+// Scale operand of the scaled conversions: a float whose exponent field is
+// the E8M0 byte.
+__device__ __forceinline__ float scale_operand(uint32_t byte) {
+  return __uint_as_float(byte << 23);
+}
+
+__device__ __forceinline__ uint32_t encode8(const float (&v)[8], float s) {
+  uint32_t c = 0;
+  c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, v[0], v[1], s, 0);
+  c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, v[2], v[3], s, 1);
+  c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, v[4], v[5], s, 2);
+  c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, v[6], v[7], s, 3);
+  return c;
+}
+
+__device__ __forceinline__ void decode8(uint32_t c, float s, float (&d)[8]) {
+  f32x2 p0 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(c, s, 0);
+  f32x2 p1 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(c, s, 1);
+  f32x2 p2 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(c, s, 2);
+  f32x2 p3 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(c, s, 3);
+  d[0] = p0[0]; d[1] = p0[1]; d[2] = p1[0]; d[3] = p1[1];
+  d[4] = p2[0]; d[5] = p2[1]; d[6] = p3[0]; d[7] = p3[1];
+}
+
+__device__ __forceinline__ float absmax8(const float (&v)[8]) {
+  float a = fmaxf(fabsf(v[0]), fabsf(v[1]));
+  a = fmaxf(a, fmaxf(fabsf(v[2]), fabsf(v[3])));
+  a = fmaxf(a, fmaxf(fabsf(v[4]), fabsf(v[5])));
+  return fmaxf(a, fmaxf(fabsf(v[6]), fabsf(v[7])));
+}
+
+__device__ __forceinline__ void unpack_bf16x8(const uint4 &w, float (&v)[8]) {
+  v[0] = __uint_as_float(w.x << 16); v[1] = __uint_as_float(w.x & 0xFFFF0000u);
+  v[2] = __uint_as_float(w.y << 16); v[3] = __uint_as_float(w.y & 0xFFFF0000u);
+  v[4] = __uint_as_float(w.z << 16); v[5] = __uint_as_float(w.z & 0xFFFF0000u);
+  v[6] = __uint_as_float(w.w << 16); v[7] = __uint_as_float(w.w & 0xFFFF0000u);
+}
+
+// Quantize the 8 values a thread owns: primary code and scale byte and, with
+// RES, the residual code and scale byte.  All four quad lanes must call it.
+template <bool RES>
+__device__ __forceinline__ void quantize8(const float (&v)[8], uint32_t &qc,
+                                          uint32_t &qb, uint32_t &rc,
+                                          uint32_t &rb) {
+  qb = scale_byte(quad_max(absmax8(v)));
+  const float qs = scale_operand(qb);
+  qc = encode8(v, qs);
+  if constexpr (RES) {
+    float d[8], r[8];
+    decode8(qc, qs, d);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) r[i] = v[i] - d[i];
+    rb = scale_byte(quad_max(absmax8(r)));
+    rc = encode8(r, scale_operand(rb));
+  }
+}
+
+template <bool BF16_IN>
+__device__ __forceinline__ void load8(const void *__restrict__ x, int64_t chunk,
+                                      float (&v)[8]) {
+  if constexpr (BF16_IN) {
+    const uint4 w = reinterpret_cast<const uint4 *>(x)[chunk];
+    unpack_bf16x8(w, v);
+  } else {
+    const float4 *p = reinterpret_cast<const float4 *>(x) + 2 * chunk;
+    const float4 a = p[0];
+    const float4 b = p[1];
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+  }
+}
+
+template <bool BF16_IN, bool RES>
+__global__ __launch_bounds__(kThreads) void quantize_kernel(
+    const void *__restrict__ x, int64_t nchunks, uint32_t *__restrict__ q_codes,
+    uint8_t *__restrict__ q_scales, uint32_t *__restrict__ r_codes,
+    uint8_t *__restrict__ r_scales) {
+  const int64_t base = (int64_t)blockIdx.x * (kThreads * kUnroll) + threadIdx.x;
+  float v[kUnroll][8];
+#pragma unroll
+  for (int u = 0; u < kUnroll; ++u) {
+    // Lanes past the end load the last chunk (never out of bounds) and skip
+    // their stores; nchunks is a multiple of 4, so quads stay whole.
+    const int64_t ch = base + u * kThreads;
+    load8<BF16_IN>(x, ch < nchunks ? ch : nchunks - 1, v[u]);
+  }
+  const bool leader = (threadIdx.x & 3) == 0;
+#pragma unroll
+  for (int u = 0; u < kUnroll; ++u) {
+    const int64_t ch = base + u * kThreads;
+    uint32_t qc, qb, rc = 0, rb = 0;
+    quantize8<RES>(v[u], qc, qb, rc, rb);
+    if (ch < nchunks) {
+      __builtin_nontemporal_store(qc, q_codes + ch);
+      if (leader) q_scales[ch >> 2] = (uint8_t)qb;
+      if constexpr (RES) {
+        __builtin_nontemporal_store(rc, r_codes + ch);
+        if (leader) r_scales[ch >> 2] = (uint8_t)rb;
+      }
+    }
+  }
+}
+
+// bf16 round to nearest even of a finite fp32 value, returned as the bf16
+// value widened back to fp32 (low 16 bits zero).
+__device__ __forceinline__ uint32_t bf16_rne_bits(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u + 0x7FFFu + ((u >> 16) & 1u)) & 0xFFFF0000u;
+}
+
+template <bool BF16_IN, bool RES>
+__global__ __launch_bounds__(kThreads) void swiglu_quantize_kernel(
+    const void *__restrict__ g, const void *__restrict__ u, int64_t nchunks,
+    uint32_t *__restrict__ q_codes, uint8_t *__restrict__ q_scales,
+    uint32_t *__restrict__ r_codes, uint8_t *__restrict__ r_scales,
+    uint4 *__restrict__ h_out) {
+  const int64_t base = (int64_t)blockIdx.x * (kThreads * kUnroll) + threadIdx.x;
+  float gv[kUnroll][8], uv[kUnroll][8];
+#pragma unroll
+  for (int i = 0; i < kUnroll; ++i) {
+    const int64_t ch = base + i * kThreads;
+    const int64_t c = ch < nchunks ? ch : nchunks - 1;
+    load8<BF16_IN>(g, c, gv[i]);
+    load8<BF16_IN>(u, c, uv[i]);
+  }
+  const bool leader = (threadIdx.x & 3) == 0;
+#pragma unroll
+  for (int i = 0; i < kUnroll; ++i) {
+    const int64_t ch = base + i * kThreads;
+    float h[8];
+    uint32_t hb[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float gj = gv[i][j];
+      const float silu = gj * __builtin_amdgcn_rcpf(1.0f + __expf(-gj));
+      hb[j] = bf16_rne_bits(silu * uv[i][j]);
+      h[j] = __uint_as_float(hb[j]);
+    }
+    uint32_t qc, qb, rc = 0, rb = 0;
+    quantize8<RES>(h, qc, qb, rc, rb);
+    if (ch < nchunks) {
+      __builtin_nontemporal_store(qc, q_codes + ch);
+      if (leader) q_scales[ch >> 2] = (uint8_t)qb;
+      if constexpr (RES) {
+        __builtin_nontemporal_store(rc, r_codes + ch);
+        if (leader) r_scales[ch >> 2] = (uint8_t)rb;
+      }
+      if (h_out) {
+        uint4 w;
+        w.x = (hb[0] >> 16) | hb[1];
+        w.y = (hb[2] >> 16) | hb[3];
+        w.z = (hb[4] >> 16) | hb[5];
+        w.w = (hb[6] >> 16) | hb[7];
+        h_out[ch] = w;
+      }
+    }
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void dequant_kernel(
+    const uint32_t *__restrict__ codes, const uint8_t *__restrict__ scales,
+    int64_t nchunks, float4 *__restrict__ out) {
+  const int64_t ch = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (ch >= nchunks) return;
+  float d[8];
+  decode8(codes[ch], scale_operand(scales[ch >> 2]), d);
+  out[2 * ch] = make_float4(d[0], d[1], d[2], d[3]);
+  out[2 * ch + 1] = make_float4(d[4], d[5], d[6], d[7]);
+}
+
+inline unsigned grid_for(int64_t nchunks, int64_t per_block) {
+  return (unsigned)((nchunks + per_block - 1) / per_block);
+}
+
+}  // namespace
+
+hipError_t launch_quantize(const void *x, bool bf16_in, int64_t nelem,
+                           uint8_t *q_codes, uint8_t *q_scales,
+                           uint8_t *r_codes, uint8_t *r_scales,
+                           hipStream_t stream) {
+  const int64_t nchunks = nelem / kChunk;
+  const dim3 grid(grid_for(nchunks, kThreads * kUnroll)), block(kThreads);
+  uint32_t *qc = reinterpret_cast<uint32_t *>(q_codes);
+  uint32_t *rc = reinterpret_cast<uint32_t *>(r_codes);
+  if (bf16_in) {
+    if (r_codes)
+      quantize_kernel<true, true><<<grid, block, 0, stream>>>(x, nchunks, qc, q_scales, rc, r_scales);
+    else
+      quantize_kernel<true, false><<<grid, block, 0, stream>>>(x, nchunks, qc, q_scales, rc, r_scales);
+  } else {
+    if (r_codes)
+      quantize_kernel<false, true><<<grid, block, 0, stream>>>(x, nchunks, qc, q_scales, rc, r_scales);
+    else
+      quantize_kernel<false, false><<<grid, block, 0, stream>>>(x, nchunks, qc, q_scales, rc, r_scales);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_swiglu_quantize(const void *g, const void *u, bool bf16_in,
+                                  int64_t nelem, uint8_t *q_codes,
+                                  uint8_t *q_scales, uint8_t *r_codes,
+                                  uint8_t *r_scales, uint16_t *h_out,
+                                  hipStream_t stream) {
+  const int64_t nchunks = nelem / kChunk;
+  const dim3 grid(grid_for(nchunks, kThreads * kUnroll)), block(kThreads);
+  uint32_t *qc = reinterpret_cast<uint32_t *>(q_codes);
+  uint32_t *rc = reinterpret_cast<uint32_t *>(r_codes);
+  uint4 *h = reinterpret_cast<uint4 *>(h_out);
+  if (bf16_in) {
+    if (r_codes)
+      swiglu_quantize_kernel<true, true><<<grid, block, 0, stream>>>(g, u, nchunks, qc, q_scales, rc, r_scales, h);
+    else
+      swiglu_quantize_kernel<true, false><<<grid, block, 0, stream>>>(g, u, nchunks, qc, q_scales, rc, r_scales, h);
+  } else {
+    if (r_codes)
+      swiglu_quantize_kernel<false, true><<<grid, block, 0, stream>>>(g, u, nchunks, qc, q_scales, rc, r_scales, h);
+    else
+      swiglu_quantize_kernel<false, false><<<grid, block, 0, stream>>>(g, u, nchunks, qc, q_scales, rc, r_scales, h);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_dequant(const uint8_t *codes, const uint8_t *scales,
+                          int64_t nelem, float *out, hipStream_t stream) {
+  const int64_t nchunks = nelem / kChunk;
+  dequant_kernel<<<grid_for(nchunks, kThreads), kThreads, 0, stream>>>(
+      reinterpret_cast<const uint32_t *>(codes), scales, nchunks,
+      reinterpret_cast<float4 *>(out));
+  return hipGetLastError();
+}
+
+}  // namespace rfq

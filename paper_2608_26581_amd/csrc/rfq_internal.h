@@ -1,0 +1,39 @@
+// Internal declarations shared by the translation units of librfq (host side).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rfq {
+
+// Elements handled by one thread of the streaming kernels (a quarter block).
+constexpr int kChunk = 8;
+// MX block length along K.
+constexpr int kBlock = 32;
+
+// Streaming quantizer: nelem elements (multiple of 32) of bf16 or fp32 input
+// in flat row-major order.  r_codes == nullptr selects the primary code only.
+hipError_t launch_quantize(const void *x, bool bf16_in, int64_t nelem,
+                           uint8_t *q_codes, uint8_t *q_scales,
+                           uint8_t *r_codes, uint8_t *r_scales,
+                           hipStream_t stream);
+
+// h = bf16(silu(g) * u) followed by the quantizer above.
+hipError_t launch_swiglu_quantize(const void *g, const void *u, bool bf16_in,
+                                  int64_t nelem, uint8_t *q_codes,
+                                  uint8_t *q_scales, uint8_t *r_codes,
+                                  uint8_t *r_scales, uint16_t *h_out,
+                                  hipStream_t stream);
+
+// codes/scales -> fp32, nelem a multiple of 32.
+hipError_t launch_dequant(const uint8_t *codes, const uint8_t *scales,
+                          int64_t nelem, float *out, hipStream_t stream);
+
+// RFQ product (r_codes == nullptr: primary contraction only).
+hipError_t launch_gemm(const uint8_t *q_codes, const uint8_t *q_scales,
+                       const uint8_t *r_codes, const uint8_t *r_scales,
+                       const uint8_t *w_codes, const uint8_t *w_scales,
+                       int64_t M, int64_t N, int64_t K, void *z, bool z_bf16,
+                       hipStream_t stream);
+
+}  // namespace rfq

@@ -1,0 +1,181 @@
+"""Thin Python binding of librfq (C ABI declared in include/rfq.h).
+
+Argument marshalling only: every step of the RFQ path runs in the HIP
+kernels of librfq.so.  torch supplies device memory and the current HIP
+stream.  There is no fallback of any kind: if the library is missing, or a
+call fails, an exception is raised.
+
+Each function carries the name of the C entry point it calls.  Tensors must be
+contiguous device tensors on the current device; outputs are allocated when
+not passed in.
+"""
+import ctypes
+import os
+
+import torch
+
+_PKG_DIR = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG_DIR, "librfq.so")
+
+RFQ_F32 = 0
+RFQ_BF16 = 1
+
+_STATUS_NAMES = {
+    0: "RFQ_OK", 1: "RFQ_ERR_NULL", 2: "RFQ_ERR_SHAPE", 3: "RFQ_ERR_DTYPE",
+    4: "RFQ_ERR_ALIGN", 5: "RFQ_ERR_DEVICE", 6: "RFQ_ERR_LAUNCH",
+}
+
+# Every symbol declared in include/rfq.h.
+EXPORTS = (
+    "rfq_quantize_act", "rfq_quantize_weight", "rfq_gemm", "rfq_dequant",
+    "rfq_swiglu_quantize_act", "rfq_status_str", "rfq_abi_version",
+)
+
+_lib = None
+
+
+class RfqError(RuntimeError):
+    """A librfq call returned a status other than RFQ_OK."""
+
+    def __init__(self, func, status):
+        self.status = status
+        super().__init__("%s failed: %s (%s)" % (
+            func, _STATUS_NAMES.get(status, status), rfq_status_str(status)))
+
+
+def load():
+    """Loads librfq.so once; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(
+            "librfq.so is not built (expected at %s); run __graft_entry__.build()" % LIB_PATH)
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I64, I32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
+    lib.rfq_quantize_act.argtypes = [P, I32, I64, I64, P, P, P, P, P]
+    lib.rfq_quantize_weight.argtypes = [P, I32, I64, I64, P, P, P]
+    lib.rfq_gemm.argtypes = [P, P, P, P, P, P, I64, I64, I64, P, I32, P]
+    lib.rfq_dequant.argtypes = [P, P, I64, I64, P, P]
+    lib.rfq_swiglu_quantize_act.argtypes = [P, P, I32, I64, I64, P, P, P, P, P, P]
+    for f in ("rfq_quantize_act", "rfq_quantize_weight", "rfq_gemm", "rfq_dequant",
+              "rfq_swiglu_quantize_act"):
+        getattr(lib, f).restype = I32
+    lib.rfq_status_str.argtypes = [I32]
+    lib.rfq_status_str.restype = ctypes.c_char_p
+    lib.rfq_abi_version.argtypes = []
+    lib.rfq_abi_version.restype = I32
+    _lib = lib
+    return lib
+
+
+def rfq_status_str(status):
+    return load().rfq_status_str(int(status)).decode()
+
+
+def rfq_abi_version():
+    return int(load().rfq_abi_version())
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _check(func, status):
+    if status != 0:
+        raise RfqError(func, status)
+
+
+def _dtype_code(t):
+    if t.dtype == torch.bfloat16:
+        return RFQ_BF16
+    if t.dtype == torch.float32:
+        return RFQ_F32
+    raise TypeError("unsupported dtype %s (bf16 or fp32)" % t.dtype)
+
+
+def _need(t, name):
+    if not t.is_cuda or not t.is_contiguous():
+        raise ValueError("%s must be a contiguous device tensor" % name)
+
+
+def _codes_out(rows, K, device):
+    return (torch.empty((rows, K // 2), dtype=torch.uint8, device=device),
+            torch.empty((rows, K // 32), dtype=torch.uint8, device=device))
+
+
+def rfq_quantize_act(x, residual=True, out=None, stream=None):
+    """X[M][K] -> (q_codes, q_scales, r_codes, r_scales); r_* are None when
+    residual is False.  out may supply the four (or two) output tensors."""
+    _need(x, "x")
+    M, K = x.shape
+    if out is None:
+        qc, qs = _codes_out(M, K, x.device)
+        rc, rs = _codes_out(M, K, x.device) if residual else (None, None)
+    else:
+        qc, qs, rc, rs = out
+    st = load().rfq_quantize_act(_ptr(x), _dtype_code(x), M, K, _ptr(qc), _ptr(qs),
+                                 _ptr(rc), _ptr(rs), _stream(stream))
+    _check("rfq_quantize_act", st)
+    return qc, qs, rc, rs
+
+
+def rfq_quantize_weight(w, out=None, stream=None):
+    """W[N][K] -> (w_codes, w_scales)."""
+    _need(w, "w")
+    N, K = w.shape
+    wc, ws = _codes_out(N, K, w.device) if out is None else out
+    st = load().rfq_quantize_weight(_ptr(w), _dtype_code(w), N, K, _ptr(wc), _ptr(ws),
+                                    _stream(stream))
+    _check("rfq_quantize_weight", st)
+    return wc, ws
+
+
+def rfq_gemm(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales,
+             out_dtype=torch.float32, out=None, stream=None):
+    """Z[M][N] = (deq q + deq r) deq(w)^T; r_* None gives plain MXFP4."""
+    M = q_codes.shape[0]
+    K = q_codes.shape[1] * 2
+    N = w_codes.shape[0]
+    if w_codes.shape[1] * 2 != K:
+        raise ValueError("K mismatch between activation and weight codes")
+    z = out if out is not None else torch.empty((M, N), dtype=out_dtype, device=q_codes.device)
+    st = load().rfq_gemm(_ptr(q_codes), _ptr(q_scales), _ptr(r_codes), _ptr(r_scales),
+                         _ptr(w_codes), _ptr(w_scales), M, N, K, _ptr(z), _dtype_code(z),
+                         _stream(stream))
+    _check("rfq_gemm", st)
+    return z
+
+
+def rfq_dequant(codes, scales, out=None, stream=None):
+    """codes[rows][K/2], scales[rows][K/32] -> fp32 [rows][K]."""
+    rows, K = codes.shape[0], codes.shape[1] * 2
+    o = out if out is not None else torch.empty((rows, K), dtype=torch.float32, device=codes.device)
+    st = load().rfq_dequant(_ptr(codes), _ptr(scales), rows, K, _ptr(o), _stream(stream))
+    _check("rfq_dequant", st)
+    return o
+
+
+def rfq_swiglu_quantize_act(g, u, residual=True, return_h=False, out=None, stream=None):
+    """h = bf16(silu(g) * u) -> RFQ codes; returns (qc, qs, rc, rs, h or None)."""
+    _need(g, "g")
+    _need(u, "u")
+    if g.shape != u.shape or g.dtype != u.dtype:
+        raise ValueError("g and u must have the same shape and dtype")
+    M, Nh = g.shape
+    if out is None:
+        qc, qs = _codes_out(M, Nh, g.device)
+        rc, rs = _codes_out(M, Nh, g.device) if residual else (None, None)
+    else:
+        qc, qs, rc, rs = out
+    h = torch.empty((M, Nh), dtype=torch.bfloat16, device=g.device) if return_h else None
+    st = load().rfq_swiglu_quantize_act(_ptr(g), _ptr(u), _dtype_code(g), M, Nh, _ptr(qc),
+                                        _ptr(qs), _ptr(rc), _ptr(rs), _ptr(h), _stream(stream))
+    _check("rfq_swiglu_quantize_act", st)
+    return qc, qs, rc, rs, h

@@ -1,5 +1,5 @@
-"""Shared test set-up: the gpu marker, and an in-tree build of the oracle when
-(and only when) it is not built yet."""
+"""Shared test set-up: the gpu marker, and in-tree builds of the oracle and of
+librfq when (and only when) nothing is built yet."""
 import os
 import sys
 
@@ -21,6 +21,9 @@ def pytest_sessionstart(session):
     import oracle
     if not os.path.exists(oracle.LIB):
         oracle.build()
+    from paper_2608_26581_amd import build as rfq_build
+    if not os.path.exists(rfq_build.LIB_PATH):
+        rfq_build.build()
 
 
 @pytest.fixture(scope="session")

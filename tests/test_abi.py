@@ -1,0 +1,150 @@
+"""C-ABI contract of librfq, checked on the CPU: the library loads, exports
+every symbol include/rfq.h declares, and rejects bad arguments on the host
+before any HIP call.  No call here reaches a kernel launch."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2608_26581_amd as rfq
+from paper_2608_26581_amd import rfq as binding
+
+REPO = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(REPO, "include", "rfq.h")
+
+OK, ENULL, ESHAPE, EDTYPE, EALIGN, EDEVICE, ELAUNCH = range(7)
+A = 0x10000          # a fake, 16-byte aligned address: never dereferenced here
+MIS = 0x10008        # misaligned by 8
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(rfq_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    assert declared_functions() == sorted(binding.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(rfq.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_binding_names_match_the_c_names():
+    for name in declared_functions():
+        assert callable(getattr(rfq, name)), name
+
+
+def test_version_and_status_strings():
+    assert rfq.rfq_abi_version() == 1
+    seen = set()
+    for s in range(7):
+        txt = rfq.rfq_status_str(s)
+        assert txt and txt not in seen
+        seen.add(txt)
+    assert rfq.rfq_status_str(99) == "unknown status"
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    monkeypatch.setattr(binding, "_lib", None)
+    monkeypatch.setattr(binding, "LIB_PATH", str(tmp_path / "nope.so"))
+    with pytest.raises(RuntimeError, match="not built"):
+        binding.load()
+
+
+def _lib():
+    return binding.load()
+
+
+def test_quantize_act_validation():
+    q = _lib().rfq_quantize_act
+    assert q(None, 1, 4, 64, A, A, A, A, None) == ENULL
+    assert q(A, 1, 4, 64, None, A, A, A, None) == ENULL
+    assert q(A, 1, 4, 64, A, None, A, A, None) == ENULL
+    assert q(A, 1, 4, 64, A, A, A, None, None) == ENULL      # half residual pair
+    assert q(A, 1, 4, 64, A, A, None, A, None) == ENULL
+    assert q(A, 2, 4, 64, A, A, A, A, None) == EDTYPE
+    assert q(A, -1, 4, 64, A, A, A, A, None) == EDTYPE
+    assert q(A, 1, -1, 64, A, A, A, A, None) == ESHAPE
+    assert q(A, 1, 4, 48, A, A, A, A, None) == ESHAPE
+    assert q(A, 1, 4, 0, A, A, A, A, None) == ESHAPE
+    assert q(A, 1, 4, 16, A, A, A, A, None) == ESHAPE
+    assert q(MIS, 1, 4, 64, A, A, A, A, None) == EALIGN
+    assert q(A, 1, 4, 64, MIS, A, A, A, None) == EALIGN
+    assert q(A, 1, 4, 64, A, A, MIS, A, None) == EALIGN
+    assert q(A, 1, 0, 64, A, A, A, A, None) == OK              # empty: no-op
+    assert q(None, 1, 0, 64, None, None, None, None, None) == OK
+    assert q(A, 0, 0, 64, A, A, None, None, None) == OK
+
+
+def test_quantize_weight_validation():
+    q = _lib().rfq_quantize_weight
+    assert q(None, 0, 4, 64, A, A, None) == ENULL
+    assert q(A, 0, 4, 64, None, A, None) == ENULL
+    assert q(A, 5, 4, 64, A, A, None) == EDTYPE
+    assert q(A, 0, 4, 33, A, A, None) == ESHAPE
+    assert q(A, 0, -2, 64, A, A, None) == ESHAPE
+    assert q(MIS, 0, 4, 64, A, A, None) == EALIGN
+    assert q(A, 0, 0, 64, A, A, None) == OK
+
+
+def test_gemm_validation():
+    g = _lib().rfq_gemm
+    args = [A, A, A, A, A, A, 8, 8, 64, A, 0, None]
+
+    def call(**kw):
+        a = list(args)
+        for k, v in kw.items():
+            a[int(k[1:])] = v
+        return g(*a)
+
+    assert call(a0=None) == ENULL
+    assert call(a1=None) == ENULL
+    assert call(a4=None) == ENULL
+    assert call(a5=None) == ENULL
+    assert call(a9=None) == ENULL
+    assert call(a2=None) == ENULL                     # half residual pair
+    assert call(a3=None) == ENULL
+    assert call(a10=3) == EDTYPE
+    assert call(a8=40) == ESHAPE
+    assert call(a8=0) == ESHAPE
+    assert call(a6=-1) == ESHAPE
+    assert call(a7=-1) == ESHAPE
+    assert call(a6=1 << 40) == ESHAPE
+    assert call(a0=MIS) == EALIGN
+    assert call(a4=MIS) == EALIGN
+    assert call(a2=MIS) == EALIGN
+    assert call(a9=MIS) == EALIGN
+    assert call(a6=0) == OK
+    assert call(a7=0) == OK
+    assert call(a2=None, a3=None, a6=0) == OK         # plain MXFP4, empty
+    assert call(a0=None, a1=None, a2=None, a3=None, a9=None, a6=0) == OK
+    assert call(a4=None, a5=None, a9=None, a7=0) == OK
+
+
+def test_dequant_and_swiglu_validation():
+    d = _lib().rfq_dequant
+    assert d(None, A, 4, 64, A, None) == ENULL
+    assert d(A, A, 4, 63, A, None) == ESHAPE
+    assert d(A, A, 4, 64, MIS, None) == EALIGN
+    assert d(A, A, 0, 64, A, None) == OK
+    s = _lib().rfq_swiglu_quantize_act
+    assert s(A, None, 1, 4, 64, A, A, A, A, None, None) == ENULL
+    assert s(A, A, 1, 4, 64, A, A, A, None, None, None) == ENULL
+    assert s(A, A, 9, 4, 64, A, A, A, A, None, None) == EDTYPE
+    assert s(A, A, 1, 4, 100, A, A, A, A, None, None) == ESHAPE
+    assert s(A, MIS, 1, 4, 64, A, A, A, A, None, None) == EALIGN
+    assert s(A, A, 1, 4, 64, A, A, A, A, MIS, None) == EALIGN
+    assert s(A, A, 1, 0, 64, A, A, A, A, None, None) == OK
+
+
+def test_valid_arguments_without_a_gpu_report_device_error():
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present; fake pointers must not reach a launch")
+    assert _lib().rfq_quantize_act(A, 1, 4, 64, A, A, A, A, None) == EDEVICE
+    assert _lib().rfq_gemm(A, A, A, A, A, A, 8, 8, 64, A, 0, None) == EDEVICE

@@ -1,0 +1,318 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Quantizer codes and scales: bit-exact.  Dequantization: exact.  RFQ product:
+within the tolerance derived in gpu_util.  The small cases span several
+tiles and ragged tails; the full-size cases use the shapes of the synthetic
+workloads, with every output checked for the quantizers and sampled outputs
+(plus whole rows) for the products.
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2608_26581_amd as rfq
+from paper_2608_26581_amd import workloads as wl
+from gpu_util import (assert_gemm_close, dev, dev_bf16, host, host_bf16_as_f32,
+                      x_device)
+from oracle_pins import padded_floats, padded_bytes, read_golden
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+def _quant_both(o, data, residual=True, rows=None):
+    """GPU and oracle quantization of a workload's activations."""
+    x = x_device(data)
+    g = [None if t is None else host(t) for t in rfq.rfq_quantize_act(x, residual=residual)]
+    torch.cuda.synchronize()
+    xr = data["x"] if rows is None else data["x"][rows]
+    if rows is not None:
+        g = [None if a is None else a[rows] for a in g]
+    r = o.quantize(xr, residual=residual)
+    return g, r
+
+
+def _assert_codes_equal(g, r, what):
+    names = ("q_codes", "q_scales", "r_codes", "r_scales")
+    for n, a, b in zip(names, g, r):
+        if b is None:
+            assert a is None
+            continue
+        if not np.array_equal(a, b):
+            i = np.argwhere(a != b)[0]
+            raise AssertionError("%s %s differ at %s: gpu %#x oracle %#x" %
+                                 (what, n, tuple(i), a[tuple(i)], b[tuple(i)]))
+
+
+# ----------------------------------------------------------------- golden
+@pytest.mark.parametrize("name", ["h1_mixed_block.txt", "h2_outlier_block.txt",
+                                  "h3_representable_block.txt", "h4_zero_blocks.txt",
+                                  "h4_negative_zero_block.txt"])
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_golden_blocks(name, dtype):
+    g = read_golden(name)
+    x = padded_floats(g["x"])
+    if len(g["x"]) == 1:
+        x = np.full(32, float(g["x"][0]))
+    xt = torch.tensor(x, dtype=torch.float32).reshape(1, 32).to(dtype).cuda()
+    qc, qs, rc, rs = [host(t) for t in rfq.rfq_quantize_act(xt)]
+    assert qs[0, 0] == int(g["q_scale"][0], 16)
+    assert bytes(qc[0]) == bytes(padded_bytes(g["q_codes"]))
+    assert rs[0, 0] == int(g["r_scale"][0], 16)
+    assert bytes(rc[0]) == bytes(padded_bytes(g["r_codes"]))
+
+
+def test_golden_identity_gemm():
+    g = read_golden("h5_identity_weight.txt")
+    x = torch.tensor(padded_floats(g["x"]), dtype=torch.float32).reshape(1, 32).cuda()
+    q = rfq.rfq_quantize_act(x)
+    w = rfq.rfq_quantize_weight(torch.eye(32, dtype=torch.float32).cuda())
+    assert np.all(host(w[1]) == int(g["w_scale"][0], 16))
+    z = host(rfq.rfq_gemm(*q, *w))
+    assert np.array_equal(z[0], padded_floats(g["z_rfq"]).astype(np.float32))
+    z0 = host(rfq.rfq_gemm(q[0], q[1], None, None, *w))
+    assert np.array_equal(z0[0], padded_floats(g["z_plain"]).astype(np.float32))
+
+
+# -------------------------------------------------------------- quantizer
+QUANT_SMALL = [
+    ("tiny", None, None),             # 64 x 256 fp32, full size
+    ("quant", 300, 4096),             # ragged row count
+    ("qwen", 7, 96),                  # odd number of blocks per row
+    ("wan", 129, 5120),
+    ("quant", 1, 32),                 # single block
+]
+
+
+@pytest.mark.parametrize("name,M,K", QUANT_SMALL)
+@pytest.mark.parametrize("residual", [True, False])
+def test_quantize_small(orc, name, M, K, residual):
+    w = wl.WORKLOADS[name]
+    if M is not None:
+        w = w.scaled(M=M, K=K, weights=())
+    data = wl.generate(w, seed=11)
+    _say("quantize %s M=%d K=%d residual=%s" % (name, w.M, w.K, residual))
+    g, r = _quant_both(orc, data, residual)
+    _assert_codes_equal(g, r, name)
+
+
+@pytest.mark.parametrize("name", ["quant", "qwen", "wan"])
+def test_quantize_full_size(orc, name):
+    data = wl.generate(wl.WORKLOADS[name], seed=0)
+    M = data["x"].shape[0]
+    rows = None if M <= 8192 else np.arange(0, M, 8)      # wan: every 8th row
+    _say("quantize full %s %s" % (name, data["x"].shape))
+    g, r = _quant_both(orc, data, True, rows)
+    _assert_codes_equal(g, r, name)
+
+
+def test_quantize_weight_full_size(orc):
+    data = wl.generate(wl.WORKLOADS["qwen"], seed=0)
+    w = data["w"]
+    _say("quantize weight %s" % (w.shape,))
+    wc, ws = [host(t) for t in rfq.rfq_quantize_weight(dev(w))]
+    rows = np.arange(0, w.shape[0], 3)
+    oc, os_, _, _ = orc.quantize(w[rows], residual=False)
+    _assert_codes_equal((wc[rows], ws[rows]), (oc, os_), "weight")
+
+
+def test_quantize_special_values(orc):
+    """Subnormal, huge and mixed-sign blocks, fp32 and bf16."""
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal((16, 128)).astype(np.float32)
+    x[0] = 0.0
+    x[1] = -0.0
+    x[2, :32] = np.float32(1e-39)                          # subnormal block
+    x[2, 32:64] = rng.standard_normal(32).astype(np.float32) * np.float32(1e-40)
+    x[3, :32] = np.float32(3e38)
+    x[3, 32:64] = rng.standard_normal(32).astype(np.float32) * np.float32(1e37)
+    x[4] *= np.float32(2.0 ** -120)
+    x[5] *= np.float32(2.0 ** 120)
+    x[6, 5] = 6.0e4
+    for arr in (x, wl.bf16_bits_to_f32(wl.f32_to_bf16_bits(x))):
+        for dt in (torch.float32, torch.bfloat16):
+            if dt == torch.bfloat16 and arr is x:
+                continue
+            xt = torch.from_numpy(arr).cuda().to(dt)
+            g = [host(t) for t in rfq.rfq_quantize_act(xt)]
+            _assert_codes_equal(g, orc.quantize(arr.astype(np.float64)), "special %s" % dt)
+
+
+def test_power_of_two_equivariance():
+    """Metamorphic: scaling X by 2^j keeps every code and shifts every scale
+    byte by j; the product scales by exactly 2^j (no oracle involved)."""
+    data = wl.generate(wl.WORKLOADS["qwen"].scaled(M=256, K=1024,
+                                                  weights=(("w", 1024, 384),)), seed=3)
+    x = dev(data["x"])
+    w = rfq.rfq_quantize_weight(dev(data["w"]))
+    base = rfq.rfq_quantize_act(x)
+    z = host(rfq.rfq_gemm(*base, *w))
+    for j in (-5, 3):
+        sc = rfq.rfq_quantize_act(x * 2.0 ** j)
+        assert torch.equal(sc[0], base[0]) and torch.equal(sc[2], base[2])
+        assert torch.equal(sc[1].int(), base[1].int() + j)
+        assert torch.equal(sc[3].int(), base[3].int() + j)
+        zj = host(rfq.rfq_gemm(*sc, *w))
+        assert np.array_equal(zj, z * np.float32(2.0 ** j))
+
+
+def test_determinism():
+    data = wl.generate(wl.WORKLOADS["qwen"].scaled(M=512, K=2048,
+                                                  weights=(("w", 2048, 1024),)), seed=4)
+    x = x_device(data)
+    w = rfq.rfq_quantize_weight(dev(data["w"]))
+    a = rfq.rfq_quantize_act(x)
+    b = rfq.rfq_quantize_act(x)
+    for s, t in zip(a, b):
+        assert torch.equal(s, t)
+    assert torch.equal(rfq.rfq_gemm(*a, *w), rfq.rfq_gemm(*b, *w))
+
+
+# ---------------------------------------------------------------- dequant
+def test_dequant_exact(orc):
+    data = wl.generate(wl.WORKLOADS["qwen"].scaled(M=130, K=2080, weights=()), seed=6)
+    q = rfq.rfq_quantize_act(x_device(data))
+    for c, s in ((q[0], q[1]), (q[2], q[3])):
+        d = host(rfq.rfq_dequant(c, s)).astype(np.float64)
+        assert np.array_equal(d, orc.dequant(host(c), host(s)))
+
+
+def test_dequant_all_codes_and_scales(orc):
+    codes = np.arange(256, dtype=np.uint8).reshape(16, 16)
+    scales = np.array([[0], [1], [2], [60], [120], [126], [127], [128], [129], [130],
+                       [200], [250], [252], [253], [254], [127]], np.uint8)
+    d = host(rfq.rfq_dequant(dev(codes), dev(scales))).astype(np.float64)
+    assert np.array_equal(d, orc.dequant(codes, scales))
+
+
+# ---------------------------------------------------------------- product
+GEMM_SMALL = [
+    ("tiny", 64, 256, 256),
+    ("qwen", 200, 328, 1056),       # ragged M and N, K not a multiple of 256
+    ("qwen", 129, 257, 512),
+    ("wan", 256, 384, 5120),
+    ("qwen", 1, 1, 32),
+    ("qwen", 3, 130, 96),
+]
+
+
+def _gemm_case(name, M, N, K, seed):
+    w = wl.WORKLOADS[name]
+    w = w.scaled(M=M, K=K, weights=(("w", K, N),))
+    return wl.generate(w, seed=seed)
+
+
+@pytest.mark.parametrize("name,M,N,K", GEMM_SMALL)
+@pytest.mark.parametrize("residual", [True, False])
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
+def test_gemm_small(orc, name, M, N, K, residual, out_dtype):
+    data = _gemm_case(name, M, N, K, seed=M + N + K)
+    _say("gemm %s M=%d N=%d K=%d residual=%s out=%s" % (name, M, N, K, residual, out_dtype))
+    q = rfq.rfq_quantize_act(x_device(data), residual=residual)
+    w = rfq.rfq_quantize_weight(dev(data["w"]))
+    z = rfq.rfq_gemm(*q, *w, out_dtype=out_dtype)
+    zh = host(z) if out_dtype == torch.float32 else host_bf16_as_f32(z)
+    hq = [None if t is None else host(t) for t in q]
+    zr, bound = orc.gemm(*hq, host(w[0]), host(w[1]))
+    assert_gemm_close(zh, zr, bound, out_dtype == torch.bfloat16, "gemm %s" % name)
+
+
+@pytest.mark.parametrize("name", ["qwen", "wan"])
+def test_gemm_full_size_sampled(orc, name):
+    data = wl.generate(wl.WORKLOADS[name], seed=0)
+    M, K = data["x"].shape
+    N = data["w"].shape[0]
+    _say("gemm full %s M=%d N=%d K=%d" % (name, M, N, K))
+    q = rfq.rfq_quantize_act(x_device(data))
+    w = rfq.rfq_quantize_weight(dev(data["w"]))
+    z32 = host(rfq.rfq_gemm(*q, *w))
+    zbf = host_bf16_as_f32(rfq.rfq_gemm(*q, *w, out_dtype=torch.bfloat16))
+    hq = [host(t) for t in q]
+    hw = [host(t) for t in w]
+    rng = np.random.default_rng(1)
+    rows = np.concatenate([rng.integers(0, M, 4000), np.repeat([0, M - 1], N)])
+    cols = np.concatenate([rng.integers(0, N, 4000), np.tile(np.arange(N), 2)])
+    zr, bound = orc.gemm_sampled(*hq, *hw, rows, cols)
+    assert_gemm_close(z32[rows, cols], zr, bound, False, "full fp32")
+    assert_gemm_close(zbf[rows, cols], zr, bound, True, "full bf16")
+
+
+def test_gemm_identity_weight_matches_dequant():
+    """I7 on GPU outputs: with W = I the product returns deq(q) + deq(r)
+    (exact here because the sum of the two fp32 terms is exact)."""
+    g = read_golden("h1_mixed_block.txt")
+    x = torch.tensor(np.tile(padded_floats(g["x"]), (40, 4)), dtype=torch.float32).cuda()
+    q = rfq.rfq_quantize_act(x)
+    w = rfq.rfq_quantize_weight(torch.eye(128, dtype=torch.float32).cuda())
+    z = rfq.rfq_gemm(*q, *w)
+    assert torch.equal(z, rfq.rfq_dequant(q[0], q[1]) + rfq.rfq_dequant(q[2], q[3]))
+
+
+# ---------------------------------------------------------------- SwiGLU
+@pytest.mark.parametrize("M,Nh", [(3, 96), (64, 12288), (257, 640)])
+def test_swiglu_quantize(orc, M, Nh):
+    rng = np.random.default_rng(M * Nh)
+    gb = wl.f32_to_bf16_bits((rng.standard_normal((M, Nh)) * 2).astype(np.float32))
+    ub = wl.f32_to_bf16_bits(rng.standard_normal((M, Nh)).astype(np.float32))
+    g, u = dev_bf16(gb), dev_bf16(ub)
+    qc, qs, rc, rs, h = rfq.rfq_swiglu_quantize_act(g, u, return_h=True)
+    hg = host_bf16_as_f32(h).astype(np.float64)
+    href = orc.swiglu(wl.bf16_bits_to_f32(gb), wl.bf16_bits_to_f32(ub))
+    ulp = np.exp2(np.floor(np.log2(np.maximum(np.abs(href), 2.0 ** -126))) - 7)
+    assert np.all(np.abs(hg - href) <= ulp)
+    _assert_codes_equal([host(t) for t in (qc, qs, rc, rs)], orc.quantize(hg), "swiglu")
+
+
+def test_swiglu_mlp_block_stagewise(orc):
+    """The chained MLP block at reduced width: quantize -> gate/up product ->
+    SwiGLU + quantize -> down product, each stage against the oracle on the
+    GPU's own input to that stage."""
+    w = wl.WORKLOADS["swiglu"].scaled(M=192, K=512, weights=(
+        ("w_gate", 512, 640), ("w_up", 512, 640), ("w_down", 640, 512)))
+    data = wl.generate(w, seed=2)
+    q = rfq.rfq_quantize_act(x_device(data))
+    wgu = rfq.rfq_quantize_weight(dev(np.concatenate([data["w_gate"], data["w_up"]], 0)))
+    gu = rfq.rfq_gemm(*q, *wgu, out_dtype=torch.bfloat16)
+    gu_h = host_bf16_as_f32(gu)
+    zr, bound = orc.gemm(*[host(t) for t in q], host(wgu[0]), host(wgu[1]))
+    assert_gemm_close(gu_h, zr, bound, True, "gate/up")
+    gate, up = gu[:, :640].contiguous(), gu[:, 640:].contiguous()
+    hq = rfq.rfq_swiglu_quantize_act(gate, up, return_h=True)
+    hg = host_bf16_as_f32(hq[4]).astype(np.float64)
+    href = orc.swiglu(gu_h[:, :640], gu_h[:, 640:])
+    ulp = np.exp2(np.floor(np.log2(np.maximum(np.abs(href), 2.0 ** -126))) - 7)
+    assert np.all(np.abs(hg - href) <= ulp)
+    _assert_codes_equal([host(t) for t in hq[:4]], orc.quantize(hg), "h")
+    wd = rfq.rfq_quantize_weight(dev(data["w_down"]))
+    z = host(rfq.rfq_gemm(*hq[:4], *wd))
+    zr, bound = orc.gemm(*[host(t) for t in hq[:4]], host(wd[0]), host(wd[1]))
+    assert_gemm_close(z, zr, bound, False, "down")
+
+
+# ---------------------------------------------------------------- edges
+def test_empty_inputs_are_noops():
+    x = torch.empty((0, 64), dtype=torch.bfloat16, device="cuda")
+    q = rfq.rfq_quantize_act(x)
+    assert q[0].shape == (0, 32)
+    w = rfq.rfq_quantize_weight(torch.randn(16, 64, device="cuda"))
+    z = rfq.rfq_gemm(*q, *w)
+    assert z.shape == (0, 16)
+    w0 = rfq.rfq_quantize_weight(torch.empty((0, 64), device="cuda"))
+    q1 = rfq.rfq_quantize_act(torch.randn(4, 64, device="cuda"))
+    assert rfq.rfq_gemm(*q1, *w0).shape == (4, 0)
+    torch.cuda.synchronize()
+
+
+def test_stream_argument_is_honoured(orc):
+    data = _gemm_case("qwen", 256, 256, 512, seed=9)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        q = rfq.rfq_quantize_act(x_device(data), stream=s)
+        w = rfq.rfq_quantize_weight(dev(data["w"]), stream=s)
+        z = rfq.rfq_gemm(*q, *w, stream=s)
+    s.synchronize()
+    zr, bound = orc.gemm(*[host(t) for t in q], host(w[0]), host(w[1]))
+    assert_gemm_close(host(z), zr, bound, False, "stream")
