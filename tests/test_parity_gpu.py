@@ -185,7 +185,10 @@ def test_dequant_all_codes_and_scales(orc):
     scales = np.array([[0], [1], [2], [60], [120], [126], [127], [128], [129], [130],
                        [200], [250], [252], [253], [254], [127]], np.uint8)
     d = host(rfq.rfq_dequant(dev(codes), dev(scales))).astype(np.float64)
-    assert np.array_equal(d, orc.dequant(codes, scales))
+    # fp32 output: values beyond the fp32 range (6 * 2^127) become infinite.
+    with np.errstate(over="ignore"):
+        want = orc.dequant(codes, scales).astype(np.float32).astype(np.float64)
+    assert np.array_equal(d, want)
 
 
 # ---------------------------------------------------------------- product
