@@ -199,7 +199,7 @@ def main():
             "copy_1GiB_gbs": round(copy_gbs, 1),
         },
         "roofline": {
-            "kernel": "rfq_gemm_kernel",
+            "kernel": "rfq_gemm_large_kernel",
             "bound": "mfma",
             "achieved": round(gemm_tflops, 1),
             "peak": PEAK_FP4_TFLOPS,

@@ -29,11 +29,21 @@ hipError_t launch_swiglu_quantize(const void *g, const void *u, bool bf16_in,
 hipError_t launch_dequant(const uint8_t *codes, const uint8_t *scales,
                           int64_t nelem, float *out, hipStream_t stream);
 
-// RFQ product (r_codes == nullptr: primary contraction only).
+// RFQ product (r_codes == nullptr: primary contraction only).  Picks the
+// large-tile kernel when gemm_large_applies(), else the general one.
 hipError_t launch_gemm(const uint8_t *q_codes, const uint8_t *q_scales,
                        const uint8_t *r_codes, const uint8_t *r_scales,
                        const uint8_t *w_codes, const uint8_t *w_scales,
                        int64_t M, int64_t N, int64_t K, void *z, bool z_bf16,
                        hipStream_t stream);
+
+// Large-tile product: K a multiple of 128 and 4-byte aligned scale tensors.
+bool gemm_large_applies(const uint8_t *q_scales, const uint8_t *r_scales,
+                        const uint8_t *w_scales, int64_t K);
+hipError_t launch_gemm_large(const uint8_t *q_codes, const uint8_t *q_scales,
+                             const uint8_t *r_codes, const uint8_t *r_scales,
+                             const uint8_t *w_codes, const uint8_t *w_scales,
+                             int64_t M, int64_t N, int64_t K, void *z, bool z_bf16,
+                             hipStream_t stream);
 
 }  // namespace rfq
