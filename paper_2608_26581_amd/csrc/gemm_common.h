@@ -8,6 +8,10 @@ namespace rfq {
 
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v4f __attribute__((ext_vector_type(4)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+// Native 16-byte vector (HIP's uint4 is a struct that copies through memcpy,
+// which keeps staging arrays out of registers).
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kFmtFp4 = 4;   // E2M1 operand format code of the scaled MFMA
 

@@ -37,9 +37,10 @@ hipError_t launch_gemm(const uint8_t *q_codes, const uint8_t *q_scales,
                        int64_t M, int64_t N, int64_t K, void *z, bool z_bf16,
                        hipStream_t stream);
 
-// Large-tile product: K a multiple of 128 and 4-byte aligned scale tensors.
+// Large-tile product: K a multiple of 128, 4-byte aligned scale tensors and
+// code tensors below 4 GiB.
 bool gemm_large_applies(const uint8_t *q_scales, const uint8_t *r_scales,
-                        const uint8_t *w_scales, int64_t K);
+                        const uint8_t *w_scales, int64_t M, int64_t N, int64_t K);
 hipError_t launch_gemm_large(const uint8_t *q_codes, const uint8_t *q_scales,
                              const uint8_t *r_codes, const uint8_t *r_scales,
                              const uint8_t *w_codes, const uint8_t *w_scales,
