@@ -53,6 +53,7 @@ constexpr int kTM = 128, kTN = 128;          // wave sub-tile
 constexpr int kFM = kTM / 32, kFN = kTN / 32;   // 32x32 fragments
 constexpr int kStageK = 128;
 constexpr int kRowBytes = kStageK / 2;       // 64 code bytes per row per stage
+constexpr int kPF = 2;                       // stages of global loads in flight
 
 template <bool RES>
 struct Layout {
@@ -61,7 +62,7 @@ struct Layout {
   static constexpr int kDataBytes = kRows * kRowBytes;
   static constexpr int kScaleBytes = kRows * 4;
   static constexpr int kStageBytes = kDataBytes + kScaleBytes;
-  static constexpr int kBytes = 2 * kStageBytes;
+  static constexpr int kBytes = 3 * kStageBytes;
   static constexpr int kWRow = (kOps - 1) * 256;           // first weight row
   static constexpr int kLoads = kRows * 4 / kThreads;      // 16-byte chunks per thread
   static constexpr int kScaleLoads = kRows / kThreads;     // one row of scales each
@@ -99,6 +100,20 @@ struct Scales {
   int w[kFN], q[kFM], r[RES ? kFM : 1];
 };
 
+// Scheduling pattern for one region: NM MFMAs with ND LDS instructions and
+// NV global loads spread evenly between them.
+template <int NM, int ND, int NV, int I = 0>
+__device__ __forceinline__ void interleave() {
+  if constexpr (I < NM) {
+    constexpr int nd = (ND * (I + 1)) / NM - (ND * I) / NM;
+    constexpr int nv = (NV * (I + 1)) / NM - (NV * I) / NM;
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);          // one MFMA
+    if constexpr (nd > 0) __builtin_amdgcn_sched_group_barrier(0x080, nd, 0);   // LDS
+    if constexpr (nv > 0) __builtin_amdgcn_sched_group_barrier(0x020, nv, 0);   // loads
+    interleave<NM, ND, NV, I + 1>();
+  }
+}
+
 template <bool RES, bool ZBF16>
 __global__ __launch_bounds__(kThreads) void rfq_gemm_large_kernel(
     const uint8_t *__restrict__ qc, const uint8_t *__restrict__ qs,
@@ -118,71 +133,69 @@ __global__ __launch_bounds__(kThreads) void rfq_gemm_large_kernel(
   const int64_t kbytes = K / 2, kblocks = K / 32;
   const int nstages = (int)(K / kStageK);
 
-  // ---- fixed per-thread sources of the staged chunks, as 32-bit byte
-  // offsets from the operand base (the caller guarantees every code and scale
-  // tensor is smaller than 4 GiB).  Chunk u of this thread is chunk
-  // tid + 256 u of the stage tile: buffer row (tid / 4 + 64 u), chunk
-  // (tid mod 4); rows [256 o, 256 o + 256) belong to operand o (q, r, w), so
-  // u / 4 is the operand.
-  uint32_t src[L::kLoads];
-#pragma unroll
-  for (int u = 0; u < L::kLoads; ++u) {
-    const bool is_w = u / 4 == L::kOps - 1;
-    const int rl = tid / 4 + 64 * (u % 4);
-    const int64_t grow = min((is_w ? n0 : m0) + rl, (is_w ? N : M) - 1);
-    src[u] = (uint32_t)(grow * kbytes + 16 * (tid & 3));
-  }
-  // Scale row tid + 256 v of the stage tile (operand v), 4 bytes per stage.
-  uint32_t ssrc[L::kScaleLoads];
-#pragma unroll
-  for (int v = 0; v < L::kScaleLoads; ++v) {
-    const bool is_w = v == L::kOps - 1;
-    const int64_t grow = min((is_w ? n0 : m0) + tid, (is_w ? N : M) - 1);
-    ssrc[v] = (uint32_t)(grow * kblocks);
-  }
+  // ---- staged chunks.  Chunk u of this thread is chunk tid + 256 u of the
+  // stage tile: buffer row (tid / 4 + 64 u), chunk (tid mod 4); rows
+  // [256 o, 256 o + 256) belong to operand o (q, r, w), so u / 4 is the
+  // operand.  Source rows are clamped to the tensor (32-bit byte offsets: the
+  // caller guarantees every code and scale tensor is below 4 GiB).
+  const int trow = tid / 4, tcol = 16 * (tid & 3);
   auto codes_of = [&](int o) { return o == L::kOps - 1 ? wc : (o == 0 ? qc : rc); };
   auto scales_of = [&](int o) { return o == L::kOps - 1 ? ws : (o == 0 ? qs : rs); };
+  auto row_of = [&](int o, int rl) -> uint32_t {
+    const bool is_w = o == L::kOps - 1;
+    return (uint32_t)min((is_w ? n0 : m0) + rl, (is_w ? N : M) - 1);
+  };
 
-  u32x4 pref[L::kLoads];
-  uint32_t spref[L::kScaleLoads];
-  auto load_stage = [&](int st) {
+  // Register prefetch sets: stage s lives in set s mod kPF until it is
+  // written to LDS; kPF stages of loads are in flight behind the one being
+  // multiplied.
+  struct Stage {
+    u32x4 d[L::kLoads];
+    uint32_t s[L::kScaleLoads];
+  };
+  Stage pf[kPF];
+  auto load_stage = [&](Stage &g, int st) {
 #pragma unroll
     for (int u = 0; u < L::kLoads; ++u)
-      pref[u] = *reinterpret_cast<const u32x4 *>(codes_of(u / 4) + src[u] +
-                                                 (uint32_t)st * kRowBytes);
+      g.d[u] = *reinterpret_cast<const u32x4 *>(
+          codes_of(u / 4) + row_of(u / 4, trow + 64 * (u % 4)) * (uint32_t)kbytes + tcol +
+          (uint32_t)st * kRowBytes);
 #pragma unroll
     for (int v = 0; v < L::kScaleLoads; ++v)
-      spref[v] = *reinterpret_cast<const uint32_t *>(scales_of(v) + ssrc[v] + 4u * st);
+      g.s[v] = *reinterpret_cast<const uint32_t *>(
+          scales_of(v) + row_of(v, tid) * (uint32_t)kblocks + 4u * st);
   };
-  auto store_stage = [&](int buf) {
+  auto store_stage = [&](const Stage &g, int buf) {
     uint8_t *b = smem + buf * L::kStageBytes;
 #pragma unroll
     for (int u = 0; u < L::kLoads; ++u)
-      *reinterpret_cast<u32x4 *>(b + chunk_off(tid / 4 + 64 * u, tid & 3)) = pref[u];
+      *reinterpret_cast<u32x4 *>(b + chunk_off(trow + 64 * u, tid & 3)) = g.d[u];
 #pragma unroll
     for (int v = 0; v < L::kScaleLoads; ++v)
-      *reinterpret_cast<uint32_t *>(b + L::kDataBytes + 4 * (tid + kThreads * v)) = spref[v];
+      *reinterpret_cast<uint32_t *>(b + L::kDataBytes + 4 * (tid + kThreads * v)) = g.s[v];
   };
 
   const int frow = lane & 31, h = lane >> 5;
   // Buffer rows of this wave's fragments.
   auto wrow = [&](int j) { return L::kWRow + wn * kTN + 32 * j + frow; };
   auto qrow = [&](int i) { return wm * kTM + 32 * i + frow; };
+  auto lds = [&](int buf) { return smem + buf * L::kStageBytes; };
 
-  auto read_frags = [&](int buf, int s, Frags<RES> &f) {
-    const uint8_t *b = smem + buf * L::kStageBytes;
+  // Weight chunks of one k-step, and the q / r chunks of one fragment row.
+  struct WFrag { u32x4 w[kFN]; };
+  struct AFrag { u32x4 q, r; };
+  auto read_w = [&](int buf, int s, WFrag &f) {
 #pragma unroll
     for (int j = 0; j < kFN; ++j)
-      f.w[j] = *reinterpret_cast<const u32x4 *>(b + chunk_off(wrow(j), 2 * h + s));
-#pragma unroll
-    for (int i = 0; i < kFM; ++i) {
-      f.q[i] = *reinterpret_cast<const u32x4 *>(b + chunk_off(qrow(i), 2 * h + s));
-      if constexpr (RES)
-        f.r[i] = *reinterpret_cast<const u32x4 *>(b + chunk_off(256 + qrow(i), 2 * h + s));
-    }
+      f.w[j] = *reinterpret_cast<const u32x4 *>(lds(buf) + chunk_off(wrow(j), 2 * h + s));
+  };
+  auto read_a = [&](int buf, int s, int i, AFrag &f) {
+    f.q = *reinterpret_cast<const u32x4 *>(lds(buf) + chunk_off(qrow(i), 2 * h + s));
+    if constexpr (RES)
+      f.r = *reinterpret_cast<const u32x4 *>(lds(buf) + chunk_off(256 + qrow(i), 2 * h + s));
   };
   auto read_scales = [&](int buf, Scales<RES> &sc) {
-    const uint8_t *b = smem + buf * L::kStageBytes + L::kDataBytes + 2 * h;
+    const uint8_t *b = lds(buf) + L::kDataBytes + 2 * h;
 #pragma unroll
     for (int j = 0; j < kFN; ++j) sc.w[j] = *reinterpret_cast<const uint16_t *>(b + 4 * wrow(j));
 #pragma unroll
@@ -198,66 +211,110 @@ __global__ __launch_bounds__(kThreads) void rfq_gemm_large_kernel(
 #pragma unroll
     for (int j = 0; j < kFN; ++j) acc[i][j] = v16f{};
 
-  // MFMAs of one k-step, rows i in [i0, i1).
-  auto mma = [&](const Frags<RES> &f, const Scales<RES> &sc, auto s_tag, int i0, int i1) {
+  // MFMAs of fragment row i of one k-step.
+  auto mma_row = [&](const WFrag &w, const AFrag &a, const Scales<RES> &sc, int i, auto s_tag) {
     constexpr int S = decltype(s_tag)::value;
 #pragma unroll
-    for (int i = 0; i < kFM; ++i) {
-      if (i < i0 || i >= i1) continue;
-#pragma unroll
-      for (int j = 0; j < kFN; ++j) {
+    for (int j = 0; j < kFN; ++j) {
+      acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+          as_v8i(w.w[j]), as_v8i(a.q), acc[i][j], kFmtFp4, kFmtFp4, S, sc.w[j], S, sc.q[i]);
+      if constexpr (RES)
         acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-            as_v8i(f.w[j]), as_v8i(f.q[i]), acc[i][j], kFmtFp4, kFmtFp4, S, sc.w[j], S, sc.q[i]);
-        if constexpr (RES)
-          acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-              as_v8i(f.w[j]), as_v8i(f.r[i]), acc[i][j], kFmtFp4, kFmtFp4, S, sc.w[j], S, sc.r[i]);
-      }
+            as_v8i(w.w[j]), as_v8i(a.r), acc[i][j], kFmtFp4, kFmtFp4, S, sc.w[j], S, sc.r[i]);
     }
   };
   using S0 = std::integral_constant<int, 0>;
   using S1 = std::integral_constant<int, 1>;
 
-  Frags<RES> f0, f1;
-  Scales<RES> sc;
-
-  load_stage(0);
-  store_stage(0);
+  // ---- prologue: stage 0 into LDS buffer 0, stages 1 .. kPF in flight.
+  load_stage(pf[0], 0);
+  store_stage(pf[0], 0);
+#pragma unroll
+  for (int p = 1; p <= kPF; ++p) load_stage(pf[p % kPF], min(p, nstages - 1));
+  asm volatile("" ::: "memory");
   __syncthreads();
-  read_frags(0, 0, f0);
+  WFrag w0, w1;
+  AFrag a0, a1;
+  Scales<RES> sc;
+  read_w(0, 0, w0);
   read_scales(0, sc);
+  read_a(0, 0, 0, a0);
 
-  // The memory clobbers pin the global loads, LDS writes and LDS reads to
-  // their places in the pipeline (the compiler would otherwise sink the
-  // global loads next to their LDS writes); the MFMAs are free to move
-  // within the regions delimited by the scheduling barriers.
-  for (int st = 0; st + 1 < nstages; ++st) {
-    const int buf = st & 1;
-    load_stage(st + 1);
-    asm volatile("" ::: "memory");
-    // k-step 0 on f0 while k-step 1 is read into f1.
-    read_frags(buf, 1, f1);
-    mma(f0, sc, S0{}, 0, kFM);
+  // One stage = 4 fragment rows x 2 k-steps of MFMAs.  LDS buffers rotate
+  // over 3 so that the buffer written during stage st (for st+1) was last
+  // read before the barrier of stage st-1.  Every other instruction of the
+  // stage is spread between the MFMAs so that no burst of memory
+  // instructions stalls the single wave of the SIMD:
+  //   k0 row 0-1 : LDS writes of stage st+1      | read A(k0, 1), A(k0, 2)
+  //   k0 row 2-3 : global loads of st+1+kPF       | read A(k0, 3), W(k1), A(k1, 0)
+  //   k1 row 0-1 :                                | read A(k1, 1), A(k1, 2)
+  //   barrier (every wave's LDS writes of stage st+1 are done)
+  //   k1 row 2-3 :                                | read A(k1, 3), next W(k0),
+  //                                                 scales and A(k0, 0)
+  // Rolling A fragments: row i+1 is read while row i is multiplied.
+  constexpr int kRowMfma = RES ? 8 : 4;
+  auto region_end = [&]() {
     __builtin_amdgcn_sched_barrier(0);
     asm volatile("" ::: "memory");
-    // k-step 1 on f1; it overlaps the hand-over of the next stage: LDS write
-    // of the prefetched stage, one barrier, reads of the next k-step 0.
-    mma(f1, sc, S1{}, 0, kFM / 2);
-    store_stage(buf ^ 1);
+  };
+  auto stage = [&](int st, Stage &next_set, auto handover_tag) {
+    constexpr bool HANDOVER = decltype(handover_tag)::value;
+    const int buf = st % 3, nbuf = (st + 1) % 3;
+    constexpr int kW = HANDOVER ? L::kLoads + L::kScaleLoads : 0;   // LDS writes / loads
+    constexpr int kAR = RES ? 2 : 1;                                 // reads per A row
+
+    if constexpr (HANDOVER) store_stage(next_set, nbuf);
+    read_a(buf, 0, 1, a1);
+    mma_row(w0, a0, sc, 0, S0{});
+    read_a(buf, 0, 2, a0);
+    mma_row(w0, a1, sc, 1, S0{});
+    interleave<2 * kRowMfma, kW + 2 * kAR, 0>();
+    region_end();
+
+    if constexpr (HANDOVER) load_stage(next_set, min(st + 1 + kPF, nstages - 1));
+    read_a(buf, 0, 3, a1);
+    read_w(buf, 1, w1);
+    mma_row(w0, a0, sc, 2, S0{});
+    read_a(buf, 1, 0, a0);
+    mma_row(w0, a1, sc, 3, S0{});
+    interleave<2 * kRowMfma, 2 * kAR + kFN, kW>();
+    region_end();
+
+    read_a(buf, 1, 1, a1);
+    mma_row(w1, a0, sc, 0, S1{});
+    read_a(buf, 1, 2, a0);
+    mma_row(w1, a1, sc, 1, S1{});
+    interleave<2 * kRowMfma, 2 * kAR, 0>();
+    region_end();
     __syncthreads();
-    read_frags(buf ^ 1, 0, f0);
-    Scales<RES> scn;
-    read_scales(buf ^ 1, scn);
-    mma(f1, sc, S1{}, kFM / 2, kFM);
+
+    read_a(buf, 1, 3, a1);
+    Scales<RES> scn = sc;
+    if constexpr (HANDOVER) {
+      read_w(nbuf, 0, w0);
+      read_scales(nbuf, scn);
+    }
+    mma_row(w1, a0, sc, 2, S1{});
+    if constexpr (HANDOVER) read_a(nbuf, 0, 0, a0);
+    mma_row(w1, a1, sc, 3, S1{});
+    interleave<2 * kRowMfma, HANDOVER ? 2 * kAR + kFN + kFM * (RES ? 2 : 1) + kFN : kAR, 0>();
+    region_end();
     sc = scn;
-    __builtin_amdgcn_sched_barrier(0);
-    asm volatile("" ::: "memory");
+  };
+  using HO = std::integral_constant<bool, true>;
+  using NoHO = std::integral_constant<bool, false>;
+
+  // Stages 0 .. nstages-2 hand over to the next stage; stage st writes set
+  // (st+1) mod kPF, so unrolling by kPF keeps every set index static.
+  int st = 0;
+  for (; st + kPF <= nstages - 1; st += kPF) {
+#pragma unroll
+    for (int p = 0; p < kPF; ++p) stage(st + p, pf[(p + 1) % kPF], HO{});
   }
-  {
-    const int buf = (nstages - 1) & 1;
-    read_frags(buf, 1, f1);
-    mma(f0, sc, S0{}, 0, kFM);
-    mma(f1, sc, S1{}, 0, kFM);
-  }
+#pragma unroll
+  for (int p = 0; p < kPF; ++p)
+    if (st + p < nstages - 1) stage(st + p, pf[(p + 1) % kPF], HO{});
+  stage(nstages - 1, pf[0], NoHO{});
   __syncthreads();
 
   // ---- epilogue: per pass (i, jp) a wave owns 32 rows x 64 columns.
