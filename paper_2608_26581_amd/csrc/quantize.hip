@@ -6,8 +6,14 @@
 // of 32, so no MX block straddles a row and the scale index of a block is its
 // flat block index).  One thread owns 8 consecutive elements; the four lanes
 // of a DPP quad own one 32-element block, so the block maximum takes two
-// quad-permute steps and no LDS.  Each thread issues U independent 16-byte
-// loads before any arithmetic to keep enough bytes in flight for HBM.
+// quad-permute steps and no LDS.  A wave owns a span of 64 consecutive blocks
+// and walks it in 4 steps; in step u the 16-lane row r holds blocks
+// 16r + 4u .. 16r + 4u + 3, so every load of a row is 256 contiguous bytes
+// and, after the steps, the row's 16 scale bytes are contiguous: two DPP
+// row shifts gather a step's 4 bytes into the row's first lane, which then
+// writes all 16 with one store (64 bytes per wave).  All loads are issued
+// before any arithmetic, and loads and stores are non-temporal (the data is
+// touched once).
 //
 // Element conversion uses the gfx950 scaled FP4 conversions: the convert to
 // FP4 divides by the scale 2^(byte-127), rounds to nearest-even, saturates at
@@ -25,7 +31,7 @@ namespace {
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kThreads = 256;
-constexpr int kUnroll = 4;
+constexpr int kUnroll = 4;   // steps per wave span of 64 blocks (4 blocks per row)
 
 // Maximum over the four lanes of a quad (DPP quad_perm 1,0,3,2 then 2,3,0,1).
 __device__ __forceinline__ float quad_max(float v) {
@@ -76,13 +82,6 @@ __device__ __forceinline__ float absmax8(const float (&v)[8]) {
   return fmaxf(a, fmaxf(fabsf(v[6]), fabsf(v[7])));
 }
 
-__device__ __forceinline__ void unpack_bf16x8(const uint4 &w, float (&v)[8]) {
-  v[0] = __uint_as_float(w.x << 16); v[1] = __uint_as_float(w.x & 0xFFFF0000u);
-  v[2] = __uint_as_float(w.y << 16); v[3] = __uint_as_float(w.y & 0xFFFF0000u);
-  v[4] = __uint_as_float(w.z << 16); v[5] = __uint_as_float(w.z & 0xFFFF0000u);
-  v[6] = __uint_as_float(w.w << 16); v[7] = __uint_as_float(w.w & 0xFFFF0000u);
-}
-
 // Quantize the 8 values a thread owns: primary code and scale byte and, with
 // RES, the residual code and scale byte.  All four quad lanes must call it.
 template <bool RES>
@@ -102,18 +101,66 @@ __device__ __forceinline__ void quantize8(const float (&v)[8], uint32_t &qc,
   }
 }
 
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+static_assert(kUnroll == 4, "a wave span is 16 rows of 4 steps");
+
 template <bool BF16_IN>
 __device__ __forceinline__ void load8(const void *__restrict__ x, int64_t chunk,
                                       float (&v)[8]) {
   if constexpr (BF16_IN) {
-    const uint4 w = reinterpret_cast<const uint4 *>(x)[chunk];
-    unpack_bf16x8(w, v);
+    const u32x4 w = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(x) + chunk);
+    v[0] = __uint_as_float(w.x << 16); v[1] = __uint_as_float(w.x & 0xFFFF0000u);
+    v[2] = __uint_as_float(w.y << 16); v[3] = __uint_as_float(w.y & 0xFFFF0000u);
+    v[4] = __uint_as_float(w.z << 16); v[5] = __uint_as_float(w.z & 0xFFFF0000u);
+    v[6] = __uint_as_float(w.w << 16); v[7] = __uint_as_float(w.w & 0xFFFF0000u);
   } else {
-    const float4 *p = reinterpret_cast<const float4 *>(x) + 2 * chunk;
-    const float4 a = p[0];
-    const float4 b = p[1];
-    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
-    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+    const u32x4 *p = reinterpret_cast<const u32x4 *>(x) + 2 * chunk;
+    const u32x4 a = __builtin_nontemporal_load(p);
+    const u32x4 b = __builtin_nontemporal_load(p + 1);
+    v[0] = __uint_as_float(a.x); v[1] = __uint_as_float(a.y);
+    v[2] = __uint_as_float(a.z); v[3] = __uint_as_float(a.w);
+    v[4] = __uint_as_float(b.x); v[5] = __uint_as_float(b.y);
+    v[6] = __uint_as_float(b.z); v[7] = __uint_as_float(b.w);
+  }
+}
+
+// Chunk (8 elements) of lane `lane` in step u of a wave span of 64 blocks:
+// block 16r + 4u + q, elements 8j .. 8j+7 of it (lane = 16r + 4q + j).
+__device__ __forceinline__ int span_chunk(int lane, int u) {
+  return 4 * (16 * (lane >> 4) + 4 * u + ((lane >> 2) & 3)) + (lane & 3);
+}
+
+// Collects the scale bytes of the four quads of a 16-lane row into the
+// row's first lane (byte q from quad q).
+__device__ __forceinline__ uint32_t gather_row4(uint32_t b) {
+  const uint32_t t = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)b, 0x104, 0xF, 0xF, false);
+  const uint32_t v = b | (t << 8);                                  // row_shl:4
+  const uint32_t t2 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x108, 0xF, 0xF, false);
+  return v | (t2 << 16);                                            // row_shl:8
+}
+
+// Writes the scale bytes of a wave span: sw[u] holds, in the first lane of
+// row r, the bytes of blocks 16r + 4u .. +3.  Full spans with an aligned
+// tensor use one 16-byte store per row; otherwise each quad leader writes its
+// own byte (bytes[u] in every lane of the quad).
+__device__ __forceinline__ void store_span_scales(uint8_t *__restrict__ scales,
+                                                  int64_t span_block0, int64_t nblocks,
+                                                  int lane, const uint32_t (&sw)[4],
+                                                  const uint32_t (&bytes)[4]) {
+  const bool full = span_block0 + 64 <= nblocks &&
+                    (reinterpret_cast<uintptr_t>(scales) & 15) == 0;
+  if (full) {
+    if ((lane & 15) == 0) {
+      u32x4 w = {sw[0], sw[1], sw[2], sw[3]};
+      __builtin_nontemporal_store(
+          w, reinterpret_cast<u32x4 *>(scales + span_block0 + (lane & 48)));
+    }
+  } else if ((lane & 3) == 0) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int64_t b = span_block0 + 16 * (lane >> 4) + 4 * u + ((lane >> 2) & 3);
+      if (b < nblocks) scales[b] = (uint8_t)bytes[u];
+    }
   }
 }
 
@@ -122,30 +169,36 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
     const void *__restrict__ x, int64_t nchunks, uint32_t *__restrict__ q_codes,
     uint8_t *__restrict__ q_scales, uint32_t *__restrict__ r_codes,
     uint8_t *__restrict__ r_scales) {
-  const int64_t base = (int64_t)blockIdx.x * (kThreads * kUnroll) + threadIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int64_t span0 = ((int64_t)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6)) * 256;
   float v[kUnroll][8];
 #pragma unroll
   for (int u = 0; u < kUnroll; ++u) {
     // Lanes past the end load the last chunk (never out of bounds) and skip
     // their stores; nchunks is a multiple of 4, so quads stay whole.
-    const int64_t ch = base + u * kThreads;
+    const int64_t ch = span0 + span_chunk(lane, u);
     load8<BF16_IN>(x, ch < nchunks ? ch : nchunks - 1, v[u]);
   }
-  const bool leader = (threadIdx.x & 3) == 0;
+  uint32_t qsw[kUnroll], rsw[kUnroll], qbytes[kUnroll], rbytes[kUnroll];
 #pragma unroll
   for (int u = 0; u < kUnroll; ++u) {
-    const int64_t ch = base + u * kThreads;
+    const int64_t ch = span0 + span_chunk(lane, u);
     uint32_t qc, qb, rc = 0, rb = 0;
     quantize8<RES>(v[u], qc, qb, rc, rb);
+    qbytes[u] = qb;
+    qsw[u] = gather_row4(qb);
+    if constexpr (RES) {
+      rbytes[u] = rb;
+      rsw[u] = gather_row4(rb);
+    }
     if (ch < nchunks) {
       __builtin_nontemporal_store(qc, q_codes + ch);
-      if (leader) q_scales[ch >> 2] = (uint8_t)qb;
-      if constexpr (RES) {
-        __builtin_nontemporal_store(rc, r_codes + ch);
-        if (leader) r_scales[ch >> 2] = (uint8_t)rb;
-      }
+      if constexpr (RES) __builtin_nontemporal_store(rc, r_codes + ch);
     }
   }
+  const int64_t nblocks = nchunks >> 2;
+  store_span_scales(q_scales, span0 >> 2, nblocks, lane, qsw, qbytes);
+  if constexpr (RES) store_span_scales(r_scales, span0 >> 2, nblocks, lane, rsw, rbytes);
 }
 
 // bf16 round to nearest even of a finite fp32 value, returned as the bf16
@@ -160,20 +213,21 @@ __global__ __launch_bounds__(kThreads) void swiglu_quantize_kernel(
     const void *__restrict__ g, const void *__restrict__ u, int64_t nchunks,
     uint32_t *__restrict__ q_codes, uint8_t *__restrict__ q_scales,
     uint32_t *__restrict__ r_codes, uint8_t *__restrict__ r_scales,
-    uint4 *__restrict__ h_out) {
-  const int64_t base = (int64_t)blockIdx.x * (kThreads * kUnroll) + threadIdx.x;
+    u32x4 *__restrict__ h_out) {
+  const int lane = threadIdx.x & 63;
+  const int64_t span0 = ((int64_t)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6)) * 256;
   float gv[kUnroll][8], uv[kUnroll][8];
 #pragma unroll
   for (int i = 0; i < kUnroll; ++i) {
-    const int64_t ch = base + i * kThreads;
+    const int64_t ch = span0 + span_chunk(lane, i);
     const int64_t c = ch < nchunks ? ch : nchunks - 1;
     load8<BF16_IN>(g, c, gv[i]);
     load8<BF16_IN>(u, c, uv[i]);
   }
-  const bool leader = (threadIdx.x & 3) == 0;
+  uint32_t qsw[kUnroll], rsw[kUnroll], qbytes[kUnroll], rbytes[kUnroll];
 #pragma unroll
   for (int i = 0; i < kUnroll; ++i) {
-    const int64_t ch = base + i * kThreads;
+    const int64_t ch = span0 + span_chunk(lane, i);
     float h[8];
     uint32_t hb[8];
 #pragma unroll
@@ -185,15 +239,17 @@ __global__ __launch_bounds__(kThreads) void swiglu_quantize_kernel(
     }
     uint32_t qc, qb, rc = 0, rb = 0;
     quantize8<RES>(h, qc, qb, rc, rb);
+    qbytes[i] = qb;
+    qsw[i] = gather_row4(qb);
+    if constexpr (RES) {
+      rbytes[i] = rb;
+      rsw[i] = gather_row4(rb);
+    }
     if (ch < nchunks) {
       __builtin_nontemporal_store(qc, q_codes + ch);
-      if (leader) q_scales[ch >> 2] = (uint8_t)qb;
-      if constexpr (RES) {
-        __builtin_nontemporal_store(rc, r_codes + ch);
-        if (leader) r_scales[ch >> 2] = (uint8_t)rb;
-      }
+      if constexpr (RES) __builtin_nontemporal_store(rc, r_codes + ch);
       if (h_out) {
-        uint4 w;
+        u32x4 w;
         w.x = (hb[0] >> 16) | hb[1];
         w.y = (hb[2] >> 16) | hb[3];
         w.z = (hb[4] >> 16) | hb[5];
@@ -202,6 +258,9 @@ __global__ __launch_bounds__(kThreads) void swiglu_quantize_kernel(
       }
     }
   }
+  const int64_t nblocks = nchunks >> 2;
+  store_span_scales(q_scales, span0 >> 2, nblocks, lane, qsw, qbytes);
+  if constexpr (RES) store_span_scales(r_scales, span0 >> 2, nblocks, lane, rsw, rbytes);
 }
 
 __global__ __launch_bounds__(kThreads) void dequant_kernel(
@@ -252,7 +311,7 @@ hipError_t launch_swiglu_quantize(const void *g, const void *u, bool bf16_in,
   const dim3 grid(grid_for(nchunks, kThreads * kUnroll)), block(kThreads);
   uint32_t *qc = reinterpret_cast<uint32_t *>(q_codes);
   uint32_t *rc = reinterpret_cast<uint32_t *>(r_codes);
-  uint4 *h = reinterpret_cast<uint4 *>(h_out);
+  u32x4 *h = reinterpret_cast<u32x4 *>(h_out);
   if (bf16_in) {
     if (r_codes)
       swiglu_quantize_kernel<true, true><<<grid, block, 0, stream>>>(g, u, nchunks, qc, q_scales, rc, r_scales, h);
