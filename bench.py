@@ -42,6 +42,8 @@ def parse():
     p.add_argument("--steps", type=int, default=50)
     p.add_argument("--warmup", type=int, default=10)
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-extras", action="store_true",
+                   help="skip the secondary workloads and the accuracy diagnostics")
     p.add_argument("--cpu-rows", type=int, default=8,
                    help="activation rows in the oracle's sample of the step")
     return p.parse_args()
@@ -213,12 +215,134 @@ def main():
             "traffic": None,
         },
     }
+    if not args.no_extras:
+        result["components"].update(secondary(torch, rfq, wl, xs[0], ws[0], stream))
+        result["accuracy"] = accuracy(torch, rfq, xs[0], ws[0])
     del xs, ws, outs, qx, qo
     torch.cuda.empty_cache()
 
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wk, args.cpu_rows)
     print(json.dumps(result), flush=True)
+
+
+def _per_launch_ms(torch, stream, fn, reps):
+    """Mean time of `reps` back-to-back launches between one pair of events."""
+    for i in range(2):
+        fn(i)
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for i in range(reps):
+        fn(i)
+    b.record(stream)
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / reps
+
+
+def secondary(torch, rfq, wl, x, w, stream):
+    """Rates reported beside the headline step: the product without the
+    residual (plain MXFP4), the bf16 matrix product of the same shape
+    (hipBLASLt through torch), the product on the Wan2.2-DiT-like shape, and
+    the chained SwiGLU MLP block (quantize -> gate and up products ->
+    SwiGLU + quantize -> down product, weights quantized beforehand)."""
+    out = {}
+    M, K = x.shape
+    N = w.shape[0]
+    q = rfq.rfq_quantize_act(x)
+    wq = rfq.rfq_quantize_weight(w)
+    z = torch.empty((M, N), dtype=torch.bfloat16, device=x.device)
+    ms = _per_launch_ms(torch, stream, lambda i: rfq.rfq_gemm(
+        q[0], q[1], None, None, *wq, out=z, stream=stream), 20)
+    out["rfq_gemm_plain_mxfp4"] = {"ms": round(ms, 5),
+                                   "exec_tflops": round(2.0 * M * N * K / ms / 1e9, 1)}
+    wt = w.to(torch.bfloat16).t().contiguous()
+    ms = _per_launch_ms(torch, stream, lambda i: torch.matmul(x, wt, out=z), 20)
+    out["bf16_matmul"] = {"ms": round(ms, 5), "tflops": round(2.0 * M * N * K / ms / 1e9, 1)}
+    del q, wq, z, wt
+
+    # Wan2.2-DiT-like product: X 32768x5120, W 5120x13824.
+    d = wl.generate(wl.WORKLOADS["wan"], seed=0)
+    xw = torch.from_numpy(d["x_bf16"].view(np.int16)).to(x.device).view(torch.bfloat16)
+    ww = torch.from_numpy(d["w"]).to(x.device)
+    del d
+    Mw, Kw = xw.shape
+    Nw = ww.shape[0]
+    q = rfq.rfq_quantize_act(xw)
+    wq = rfq.rfq_quantize_weight(ww)
+    del xw, ww
+    z = torch.empty((Mw, Nw), dtype=torch.bfloat16, device=x.device)
+    ms = _per_launch_ms(torch, stream, lambda i: rfq.rfq_gemm(*q, *wq, out=z, stream=stream), 5)
+    out["rfq_gemm_wan_32768x5120x13824"] = {
+        "ms": round(ms, 5), "exec_tflops": round(4.0 * Mw * Nw * Kw / ms / 1e9, 1)}
+    del q, wq, z
+    torch.cuda.empty_cache()
+
+    # SwiGLU MLP block on the Qwen3-VL-like activations.
+    d = wl.generate(wl.WORKLOADS["swiglu"], seed=0)
+    dev = x.device
+    xs = torch.from_numpy(d["x_bf16"].view(np.int16)).to(dev).view(torch.bfloat16)
+    wg = rfq.rfq_quantize_weight(torch.from_numpy(d["w_gate"]).to(dev))
+    wu = rfq.rfq_quantize_weight(torch.from_numpy(d["w_up"]).to(dev))
+    wd = rfq.rfq_quantize_weight(torch.from_numpy(d["w_down"]).to(dev))
+    del d
+    Ms, Ks = xs.shape
+    Nh = wg[0].shape[0]
+    q = [torch.empty((Ms, Ks // 2), dtype=torch.uint8, device=dev),
+         torch.empty((Ms, Ks // 32), dtype=torch.uint8, device=dev),
+         torch.empty((Ms, Ks // 2), dtype=torch.uint8, device=dev),
+         torch.empty((Ms, Ks // 32), dtype=torch.uint8, device=dev)]
+    g = torch.empty((Ms, Nh), dtype=torch.bfloat16, device=dev)
+    u = torch.empty_like(g)
+    h = [torch.empty((Ms, Nh // 2), dtype=torch.uint8, device=dev),
+         torch.empty((Ms, Nh // 32), dtype=torch.uint8, device=dev),
+         torch.empty((Ms, Nh // 2), dtype=torch.uint8, device=dev),
+         torch.empty((Ms, Nh // 32), dtype=torch.uint8, device=dev)]
+    y = torch.empty((Ms, Ks), dtype=torch.bfloat16, device=dev)
+
+    def block(i):
+        rfq.rfq_quantize_act(xs, out=q, stream=stream)
+        rfq.rfq_gemm(*q, *wg, out=g, stream=stream)
+        rfq.rfq_gemm(*q, *wu, out=u, stream=stream)
+        rfq.rfq_swiglu_quantize_act(g, u, out=h, stream=stream)
+        rfq.rfq_gemm(*h, *wd, out=y, stream=stream)
+
+    ms = _per_launch_ms(torch, stream, block, 10)
+    flops = 4.0 * Ms * Ks * Nh * 3
+    out["swiglu_mlp_block_4096x4096x12288"] = {
+        "ms": round(ms, 5), "exec_tflops": round(flops / ms / 1e9, 1),
+        "stages": "quantize X; RFQ gate and up products (N=12288 each); SwiGLU + RFQ "
+                  "quantize (K=12288); RFQ down product; bf16 outputs"}
+    return out
+
+
+def accuracy(torch, rfq, x, w, nrows=64):
+    """Relative Frobenius errors against the fp64 product of the unquantized
+    activations (bf16 values) and the fp32 master weights, on `nrows` rows
+    spread over the batch: bf16 matrix product, plain MXFP4, RFQ, and the
+    weight-only floor X deq(Q(W))."""
+    M = x.shape[0]
+    rows = torch.arange(0, M, max(M // nrows, 1), device=x.device)[:nrows]
+    x64 = x[rows].double()
+    zt = x64 @ w.double().t()
+    nt = torch.linalg.norm(zt)
+
+    def rel(z):
+        return float(torch.linalg.norm(z[rows].double() - zt) / nt)
+
+    q = rfq.rfq_quantize_act(x)
+    wq = rfq.rfq_quantize_weight(w)
+    wt = w.to(torch.bfloat16).t().contiguous()
+    out = {
+        "bf16_matmul": rel(torch.matmul(x, wt)),
+        "plain_mxfp4": rel(rfq.rfq_gemm(q[0], q[1], None, None, *wq)),
+        "rfq": rel(rfq.rfq_gemm(*q, *wq)),
+    }
+    wdq = rfq.rfq_dequant(*wq).double()
+    out["weight_only_floor"] = float(torch.linalg.norm(x64 @ wdq.t() - zt) / nt)
+    out["rows"] = int(rows.numel())
+    return {k: (round(v, 6) if isinstance(v, float) else v) for k, v in out.items()}
 
 
 def cpu_baseline(wk, rows):
@@ -246,12 +370,24 @@ def cpu_baseline(wk, rows):
         "value": round(4.0 * M * N * K / t_step / 1e12, 6),
         "unit": "TFLOP/s",
         "cores": o.num_threads(),
+        "cpu": _cpu_model(),
         "kind": "oracle",
         "sample": "full weight quantization (%dx%d) + %d activation rows through the RFQ "
                   "quantizer and the fp64 product against all %d outputs; scaled to the "
                   "%d-row step (t_w=%.2fs t_x=%.3fs t_gemm=%.2fs)" % (N, K, rows, N, M, t_w,
                                                                       t_x, t_g),
     }
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 if __name__ == "__main__":

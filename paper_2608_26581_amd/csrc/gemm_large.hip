@@ -68,6 +68,10 @@ struct Layout {
   static constexpr int kScaleLoads = kRows / kThreads;     // one row of scales each
 };
 
+// Scale bytes are fetched 16 per row (kGroup stages) at a time: a 4-byte
+// fetch per row and stage would cost a whole L2 request for 4 useful bytes.
+constexpr int kGroup = 4;
+
 // Byte offset of 16-byte chunk c of buffer row r.
 __device__ __forceinline__ int chunk_off(int r, int c) {
   return r * kRowBytes + 16 * (c ^ ((r >> 1) & 3));
@@ -136,43 +140,63 @@ __global__ __launch_bounds__(kThreads) void rfq_gemm_large_kernel(
   // ---- staged chunks.  Chunk u of this thread is chunk tid + 256 u of the
   // stage tile: buffer row (tid / 4 + 64 u), chunk (tid mod 4); rows
   // [256 o, 256 o + 256) belong to operand o (q, r, w), so u / 4 is the
-  // operand.  Source rows are clamped to the tensor (32-bit byte offsets: the
-  // caller guarantees every code and scale tensor is below 4 GiB).
+  // operand.  Loads go through buffer descriptors (base and size in scalar
+  // registers, a 32-bit offset per load; the caller guarantees every code and
+  // scale tensor is below 4 GiB).  Source rows are clamped to the tensor.
   const int trow = tid / 4, tcol = 16 * (tid & 3);
-  auto codes_of = [&](int o) { return o == L::kOps - 1 ? wc : (o == 0 ? qc : rc); };
-  auto scales_of = [&](int o) { return o == L::kOps - 1 ? ws : (o == 0 ? qs : rs); };
-  auto row_of = [&](int o, int rl) -> uint32_t {
-    const bool is_w = o == L::kOps - 1;
-    return (uint32_t)min((is_w ? n0 : m0) + rl, (is_w ? N : M) - 1);
+  auto rsrc = [](const uint8_t *p, int64_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t *>(p), (short)0, (int)bytes,
+                                             0x00020000);
   };
+  const __amdgpu_buffer_rsrc_t c_rsrc[3] = {
+      rsrc(qc, M * kbytes), rsrc(RES ? rc : qc, M * kbytes), rsrc(wc, N * kbytes)};
+  const __amdgpu_buffer_rsrc_t s_rsrc[3] = {
+      rsrc(qs, M * kblocks), rsrc(RES ? rs : qs, M * kblocks), rsrc(ws, N * kblocks)};
+  auto crsrc = [&](int o) { return c_rsrc[o == L::kOps - 1 ? 2 : o]; };
+  auto srsrc = [&](int o) { return s_rsrc[o == L::kOps - 1 ? 2 : o]; };
+  // Row byte offsets of this thread's chunks (activation rows serve q and r).
+  uint32_t a_off[4], w_off[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    a_off[u] = (uint32_t)min(m0 + trow + 64 * u, M - 1) * (uint32_t)kbytes + tcol;
+    w_off[u] = (uint32_t)min(n0 + trow + 64 * u, N - 1) * (uint32_t)kbytes + tcol;
+  }
+  const uint32_t as_off = (uint32_t)min(m0 + tid, M - 1) * (uint32_t)kblocks;
+  const uint32_t ws_off = (uint32_t)min(n0 + tid, N - 1) * (uint32_t)kblocks;
 
   // Register prefetch sets: stage s lives in set s mod kPF until it is
   // written to LDS; kPF stages of loads are in flight behind the one being
-  // multiplied.
+  // multiplied.  The scale bytes of kGroup stages (16 per row, this thread's
+  // row of each operand) live in `grp`.
   struct Stage {
     u32x4 d[L::kLoads];
-    uint32_t s[L::kScaleLoads];
   };
   Stage pf[kPF];
+  u32x4 grp[L::kScaleLoads];
   auto load_stage = [&](Stage &g, int st) {
 #pragma unroll
-    for (int u = 0; u < L::kLoads; ++u)
-      g.d[u] = *reinterpret_cast<const u32x4 *>(
-          codes_of(u / 4) + row_of(u / 4, trow + 64 * (u % 4)) * (uint32_t)kbytes + tcol +
-          (uint32_t)st * kRowBytes);
+    for (int u = 0; u < L::kLoads; ++u) {
+      const int o = u / 4;
+      const uint32_t off = (o == L::kOps - 1 ? w_off : a_off)[u % 4];
+      g.d[u] = __builtin_amdgcn_raw_buffer_load_b128(crsrc(o), off, st * kRowBytes, 0);
+    }
+  };
+  auto load_group = [&](int gi) {
 #pragma unroll
     for (int v = 0; v < L::kScaleLoads; ++v)
-      g.s[v] = *reinterpret_cast<const uint32_t *>(
-          scales_of(v) + row_of(v, tid) * (uint32_t)kblocks + 4u * st);
+      grp[v] = __builtin_amdgcn_raw_buffer_load_b128(
+          srsrc(v), v == L::kOps - 1 ? ws_off : as_off, 16 * gi, 0);
   };
-  auto store_stage = [&](const Stage &g, int buf) {
+  // Writes a register stage and word `word` of the scale group to LDS.
+  auto store_stage = [&](const Stage &g, int buf, auto word_tag) {
+    constexpr int W = decltype(word_tag)::value;
     uint8_t *b = smem + buf * L::kStageBytes;
 #pragma unroll
     for (int u = 0; u < L::kLoads; ++u)
       *reinterpret_cast<u32x4 *>(b + chunk_off(trow + 64 * u, tid & 3)) = g.d[u];
 #pragma unroll
     for (int v = 0; v < L::kScaleLoads; ++v)
-      *reinterpret_cast<uint32_t *>(b + L::kDataBytes + 4 * (tid + kThreads * v)) = g.s[v];
+      *reinterpret_cast<uint32_t *>(b + L::kDataBytes + 4 * (tid + kThreads * v)) = grp[v][W];
   };
 
   const int frow = lane & 31, h = lane >> 5;
@@ -226,11 +250,18 @@ __global__ __launch_bounds__(kThreads) void rfq_gemm_large_kernel(
   using S0 = std::integral_constant<int, 0>;
   using S1 = std::integral_constant<int, 1>;
 
+  using W0 = std::integral_constant<int, 0>;
   // ---- prologue: stage 0 into LDS buffer 0, stages 1 .. kPF in flight.
+  load_group(0);
   load_stage(pf[0], 0);
-  store_stage(pf[0], 0);
+  store_stage(pf[0], 0, W0{});
+  // Issued stage by stage, in order, so that the wait before each LDS write
+  // of the loop can leave the later stages in flight.
 #pragma unroll
-  for (int p = 1; p <= kPF; ++p) load_stage(pf[p % kPF], min(p, nstages - 1));
+  for (int p = 1; p <= kPF; ++p) {
+    load_stage(pf[p % kPF], min(p, nstages - 1));
+    __builtin_amdgcn_sched_barrier(0);
+  }
   asm volatile("" ::: "memory");
   __syncthreads();
   WFrag w0, w1;
@@ -257,13 +288,19 @@ __global__ __launch_bounds__(kThreads) void rfq_gemm_large_kernel(
     __builtin_amdgcn_sched_barrier(0);
     asm volatile("" ::: "memory");
   };
-  auto stage = [&](int st, Stage &next_set, auto handover_tag) {
+  // Stage st writes stage st+1 (scale word (st+1) mod kGroup) to LDS; when
+  // that is the last word of its group, the next group is fetched before
+  // the stage's data loads, so that waiting for it never waits for them.
+  auto stage = [&](int st, Stage &next_set, auto handover_tag, auto word_tag,
+                   auto reload_tag) {
     constexpr bool HANDOVER = decltype(handover_tag)::value;
+    constexpr bool RELOAD = decltype(reload_tag)::value;
     const int buf = st % 3, nbuf = (st + 1) % 3;
-    constexpr int kW = HANDOVER ? L::kLoads + L::kScaleLoads : 0;   // LDS writes / loads
+    constexpr int kW = HANDOVER ? L::kLoads + L::kScaleLoads : 0;   // LDS writes
+    constexpr int kV = (HANDOVER ? L::kLoads : 0) + (RELOAD ? L::kScaleLoads : 0);   // loads
     constexpr int kAR = RES ? 2 : 1;                                 // reads per A row
 
-    if constexpr (HANDOVER) store_stage(next_set, nbuf);
+    if constexpr (HANDOVER) store_stage(next_set, nbuf, word_tag);
     read_a(buf, 0, 1, a1);
     mma_row(w0, a0, sc, 0, S0{});
     read_a(buf, 0, 2, a0);
@@ -271,13 +308,14 @@ __global__ __launch_bounds__(kThreads) void rfq_gemm_large_kernel(
     interleave<2 * kRowMfma, kW + 2 * kAR, 0>();
     region_end();
 
+    if constexpr (RELOAD) load_group((st + 2) / kGroup);
     if constexpr (HANDOVER) load_stage(next_set, min(st + 1 + kPF, nstages - 1));
     read_a(buf, 0, 3, a1);
     read_w(buf, 1, w1);
     mma_row(w0, a0, sc, 2, S0{});
     read_a(buf, 1, 0, a0);
     mma_row(w0, a1, sc, 3, S0{});
-    interleave<2 * kRowMfma, 2 * kAR + kFN, kW>();
+    interleave<2 * kRowMfma, 2 * kAR + kFN, kV>();
     region_end();
 
     read_a(buf, 1, 1, a1);
@@ -303,18 +341,28 @@ __global__ __launch_bounds__(kThreads) void rfq_gemm_large_kernel(
   };
   using HO = std::integral_constant<bool, true>;
   using NoHO = std::integral_constant<bool, false>;
+  using Rl = std::integral_constant<bool, true>;
+  using NoRl = std::integral_constant<bool, false>;
+  using W1 = std::integral_constant<int, 1>;
+  using W2 = std::integral_constant<int, 2>;
+  using W3 = std::integral_constant<int, 3>;
+  static_assert(kGroup == 4 && kPF == 2, "the unrolled loop below assumes these");
 
-  // Stages 0 .. nstages-2 hand over to the next stage; stage st writes set
-  // (st+1) mod kPF, so unrolling by kPF keeps every set index static.
+  // nstages is a multiple of kGroup.  Stage st writes set (st+1) mod kPF and
+  // scale word (st+1) mod kGroup, so unrolling by kGroup keeps both static.
   int st = 0;
-  for (; st + kPF <= nstages - 1; st += kPF) {
-#pragma unroll
-    for (int p = 0; p < kPF; ++p) stage(st + p, pf[(p + 1) % kPF], HO{});
+  for (; st < nstages - kGroup; st += kGroup) {
+    stage(st + 0, pf[1], HO{}, W1{}, NoRl{});
+    stage(st + 1, pf[0], HO{}, W2{}, NoRl{});
+    stage(st + 2, pf[1], HO{}, W3{}, Rl{});
+    stage(st + 3, pf[0], HO{}, W0{}, NoRl{});
   }
-#pragma unroll
-  for (int p = 0; p < kPF; ++p)
-    if (st + p < nstages - 1) stage(st + p, pf[(p + 1) % kPF], HO{});
-  stage(nstages - 1, pf[0], NoHO{});
+  // The last group.  (Its stages are written as conditional: unconditional
+  // straight-line copies make the register allocator spill.)
+  if (st + 0 < nstages - 1) stage(st + 0, pf[1], HO{}, W1{}, NoRl{});
+  if (st + 1 < nstages - 1) stage(st + 1, pf[0], HO{}, W2{}, NoRl{});
+  if (st + 2 < nstages - 1) stage(st + 2, pf[1], HO{}, W3{}, NoRl{});
+  stage(nstages - 1, pf[0], NoHO{}, W0{}, NoRl{});
   __syncthreads();
 
   // ---- epilogue: per pass (i, jp) a wave owns 32 rows x 64 columns.
@@ -404,7 +452,8 @@ bool gemm_large_applies(const uint8_t *q_scales, const uint8_t *r_scales,
                       reinterpret_cast<uintptr_t>(w_scales);
   // Byte offsets inside an operand are 32-bit.
   const int64_t limit = int64_t(1) << 32;
-  return (K % kStageK) == 0 && (a & 3) == 0 && M * (K / 2) < limit && N * (K / 2) < limit;
+  return (K % (kStageK * kGroup)) == 0 && (a & 15) == 0 && M * (K / 2) < limit &&
+         N * (K / 2) < limit;
 }
 
 hipError_t launch_gemm_large(const uint8_t *q_codes, const uint8_t *q_scales,

@@ -196,7 +196,9 @@ GEMM_SMALL = [
     ("tiny", 64, 256, 256),
     ("qwen", 200, 328, 1056),       # ragged M and N, K not a multiple of 256
     ("qwen", 129, 257, 512),
+    ("qwen", 513, 769, 2048),       # several 256-wide tiles, ragged both ways
     ("wan", 256, 384, 5120),
+    ("qwen", 70, 300, 640),         # K a multiple of 128 but not of 512
     ("qwen", 1, 1, 32),
     ("qwen", 3, 130, 96),
 ]
