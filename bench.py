@@ -122,6 +122,8 @@ def main():
     gm_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
 
     exec_flops = 4.0 * M * N * K
+    # Operand and result bytes of one product: q, r and w codes and scales, bf16 Z.
+    gemm_bytes = 2 * (M * K // 2 + M * K // 32) + (N * K // 2 + N * K // 32) + 2 * M * N
     value = exec_flops / (ms_step * 1e-3) / 1e12
     gemm_tflops = exec_flops / (gm_ms * 1e-3) / 1e12
     xq_bytes = M * K * 2 + 2 * (M * K // 2 + M * K // 32)
@@ -213,8 +215,13 @@ def main():
             "unit": "TFLOP/s",
             "frac": round(gemm_tflops / PEAK_FP4_TFLOPS, 4),
             "traffic": None,
+            "algorithmic_bytes": gemm_bytes,
         },
     }
+    rec = recorded_traffic()
+    if rec is not None:
+        result["roofline"]["traffic"] = rec["read_bytes"] + rec["write_bytes"]
+        result["roofline"]["traffic_read_write"] = [rec["read_bytes"], rec["write_bytes"]]
     if not args.no_extras:
         result["components"].update(secondary(torch, rfq, wl, xs[0], ws[0], stream))
         result["accuracy"] = accuracy(torch, rfq, xs[0], ws[0])
@@ -224,6 +231,34 @@ def main():
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wk, args.cpu_rows)
     print(json.dumps(result), flush=True)
+
+
+TRAFFIC_RECORD = os.path.join(REPO, "profiles", "rfq_gemm_large_qwen_hbm_counters.md")
+
+
+def recorded_traffic(path=TRAFFIC_RECORD):
+    """HBM bytes per launch of the product, from the FETCH_SIZE / WRITE_SIZE
+    counter passes summarised in `path` (calibrated against a plain copy).
+    The record names the sources it was measured on with their SHA-256; if
+    any of them has changed since, the figure no longer describes this
+    kernel and None is returned."""
+    import hashlib
+    try:
+        with open(path) as f:
+            lines = [ln for ln in f if ln.startswith("<!-- traffic-record ")]
+    except OSError:
+        return None
+    if not lines:
+        return None
+    rec = json.loads(lines[0][len("<!-- traffic-record "):].rsplit("-->", 1)[0])
+    for rel, digest in rec["sources"].items():
+        try:
+            with open(os.path.join(REPO, rel), "rb") as f:
+                if hashlib.sha256(f.read()).hexdigest() != digest:
+                    return None
+        except OSError:
+            return None
+    return rec
 
 
 def _per_launch_ms(torch, stream, fn, reps):

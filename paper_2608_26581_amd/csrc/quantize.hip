@@ -12,8 +12,9 @@
 // and, after the steps, the row's 16 scale bytes are contiguous: two DPP
 // row shifts gather a step's 4 bytes into the row's first lane, which then
 // writes all 16 with one store (64 bytes per wave).  All loads are issued
-// before any arithmetic, and loads and stores are non-temporal (the data is
-// touched once).
+// before any arithmetic.  bf16 inputs are read non-temporally; stores are
+// plain (measured: non-temporal stores of these partial lines cost about a
+// fifth more write traffic, and non-temporal fp32 loads were slower).
 //
 // Element conversion uses the gfx950 scaled FP4 conversions: the convert to
 // FP4 divides by the scale 2^(byte-127), rounds to nearest-even, saturates at
@@ -115,8 +116,8 @@ __device__ __forceinline__ void load8(const void *__restrict__ x, int64_t chunk,
     v[6] = __uint_as_float(w.w << 16); v[7] = __uint_as_float(w.w & 0xFFFF0000u);
   } else {
     const u32x4 *p = reinterpret_cast<const u32x4 *>(x) + 2 * chunk;
-    const u32x4 a = __builtin_nontemporal_load(p);
-    const u32x4 b = __builtin_nontemporal_load(p + 1);
+    const u32x4 a = p[0];
+    const u32x4 b = p[1];
     v[0] = __uint_as_float(a.x); v[1] = __uint_as_float(a.y);
     v[2] = __uint_as_float(a.z); v[3] = __uint_as_float(a.w);
     v[4] = __uint_as_float(b.x); v[5] = __uint_as_float(b.y);
@@ -152,8 +153,7 @@ __device__ __forceinline__ void store_span_scales(uint8_t *__restrict__ scales,
   if (full) {
     if ((lane & 15) == 0) {
       u32x4 w = {sw[0], sw[1], sw[2], sw[3]};
-      __builtin_nontemporal_store(
-          w, reinterpret_cast<u32x4 *>(scales + span_block0 + (lane & 48)));
+      *reinterpret_cast<u32x4 *>(scales + span_block0 + (lane & 48)) = w;
     }
   } else if ((lane & 3) == 0) {
 #pragma unroll
@@ -192,8 +192,8 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
       rsw[u] = gather_row4(rb);
     }
     if (ch < nchunks) {
-      __builtin_nontemporal_store(qc, q_codes + ch);
-      if constexpr (RES) __builtin_nontemporal_store(rc, r_codes + ch);
+      q_codes[ch] = qc;
+      if constexpr (RES) r_codes[ch] = rc;
     }
   }
   const int64_t nblocks = nchunks >> 2;
@@ -246,8 +246,8 @@ __global__ __launch_bounds__(kThreads) void swiglu_quantize_kernel(
       rsw[i] = gather_row4(rb);
     }
     if (ch < nchunks) {
-      __builtin_nontemporal_store(qc, q_codes + ch);
-      if constexpr (RES) __builtin_nontemporal_store(rc, r_codes + ch);
+      q_codes[ch] = qc;
+      if constexpr (RES) r_codes[ch] = rc;
       if (h_out) {
         u32x4 w;
         w.x = (hb[0] >> 16) | hb[1];
