@@ -295,6 +295,19 @@ def secondary(torch, rfq, wl, x, w, stream):
     wt = w.to(torch.bfloat16).t().contiguous()
     ms = _per_launch_ms(torch, stream, lambda i: torch.matmul(x, wt, out=z), 20)
     out["bf16_matmul"] = {"ms": round(ms, 5), "tflops": round(2.0 * M * N * K / ms / 1e9, 1)}
+    # The vendor's block-scaled FP4 product (hipBLASLt through torch) on the
+    # same primary codes: one plain MXFP4 contraction.
+    try:
+        a4 = q[0].view(torch.float4_e2m1fn_x2)
+        b4 = wq[0].view(torch.float4_e2m1fn_x2).t()
+        sa = q[1].view(torch.float8_e8m0fnu)
+        sb = wq[1].view(torch.float8_e8m0fnu)
+        ms = _per_launch_ms(torch, stream, lambda i: torch._scaled_mm(
+            a4, b4, sa, sb, out_dtype=torch.bfloat16), 20)
+        out["hipblaslt_mxfp4_scaled_mm"] = {
+            "ms": round(ms, 5), "exec_tflops": round(2.0 * M * N * K / ms / 1e9, 1)}
+    except (AttributeError, RuntimeError, ValueError, NotImplementedError) as e:
+        out["hipblaslt_mxfp4_scaled_mm"] = {"unavailable": str(e)[:120]}
     del q, wq, z, wt
 
     # Wan2.2-DiT-like product: X 32768x5120, W 5120x13824.

@@ -297,6 +297,36 @@ def test_swiglu_mlp_block_stagewise(orc):
     assert_gemm_close(z, zr, bound, False, "down")
 
 
+def test_plain_mxfp4_agrees_with_hipblaslt(orc):
+    """Independent cross-check of the MXFP4 encoding (nibble order, E8M0
+    scales, block layout): the vendor's block-scaled FP4 product on the very
+    same codes and scales agrees with the oracle to within one bf16 ulp of
+    its output (its own accumulation and rounding are not ours: observed up
+    to one ulp off), far below what a wrong nibble order or scale would
+    give."""
+    if not hasattr(torch, "float4_e2m1fn_x2"):
+        pytest.skip("this torch has no FP4 dtype")
+    w = wl.WORKLOADS["qwen"].scaled(M=256, K=1024, weights=(("w", 1024, 512),))
+    data = wl.generate(w, seed=1)
+    q = rfq.rfq_quantize_act(x_device(data))
+    wq = rfq.rfq_quantize_weight(dev(data["w"]))
+    try:
+        zv = torch._scaled_mm(q[0].view(torch.float4_e2m1fn_x2),
+                              wq[0].view(torch.float4_e2m1fn_x2).t(),
+                              q[1].view(torch.float8_e8m0fnu), wq[1].view(torch.float8_e8m0fnu),
+                              out_dtype=torch.bfloat16)
+    except (RuntimeError, ValueError, NotImplementedError) as e:
+        pytest.skip("block-scaled FP4 product unavailable: %s" % e)
+    z = host(rfq.rfq_gemm(q[0], q[1], None, None, *wq))
+    zr, bound = orc.gemm(host(q[0]), host(q[1]), None, None, host(wq[0]), host(wq[1]))
+    assert_gemm_close(z, zr, bound, False, "phi=0")
+    zv = host_bf16_as_f32(zv).astype(np.float64)
+    err = np.abs(zv - zr)
+    tol = 2.0 ** -10 * bound + 2.0 ** -7 * np.abs(zr)
+    assert np.all(err <= tol), "vendor: %d outputs differ by more than one bf16 ulp" % int(
+        (err > tol).sum())
+
+
 # ---------------------------------------------------------------- edges
 def test_empty_inputs_are_noops():
     x = torch.empty((0, 64), dtype=torch.bfloat16, device="cuda")
