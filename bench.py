@@ -362,6 +362,21 @@ def secondary(torch, rfq, wl, x, w, stream):
         "ms": round(ms, 5), "exec_tflops": round(flops / ms / 1e9, 1),
         "stages": "quantize X; RFQ gate and up products (N=12288 each); SwiGLU + RFQ "
                   "quantize (K=12288); RFQ down product; bf16 outputs"}
+
+    # The same block with SwiGLU + quantization fused into the gate/up product.
+    wgu = (rfq.interleave_gate_up(wg[0], wu[0]), rfq.interleave_gate_up(wg[1], wu[1]))
+    del g, u
+
+    def fused(i):
+        rfq.rfq_quantize_act(xs, out=q, stream=stream)
+        rfq.rfq_gemm_swiglu_quantize(*q, *wgu, out=h, stream=stream)
+        rfq.rfq_gemm(*h, *wd, out=y, stream=stream)
+
+    ms = _per_launch_ms(torch, stream, fused, 10)
+    out["swiglu_mlp_block_fused_4096x4096x12288"] = {
+        "ms": round(ms, 5), "exec_tflops": round(flops / ms / 1e9, 1),
+        "stages": "quantize X; RFQ gate/up product (N=24576) with SwiGLU + RFQ quantize "
+                  "in its epilogue; RFQ down product; bf16 output"}
     return out
 
 
@@ -414,16 +429,32 @@ def cpu_baseline(wk, rows):
     o.gemm(*q, wc, wsc)
     t_g = time.perf_counter() - t
     t_step = t_w + (M / rows) * (t_x + t_g)
+    # The same with one thread, on a smaller sample: 1/16 of the weight rows
+    # and one activation row.
+    cores = o.num_threads()
+    o.set_num_threads(1)
+    wrows = max(N // 16, 1)
+    t = time.perf_counter()
+    o.quantize(d["w"][:wrows], residual=False)
+    t_w1 = (time.perf_counter() - t) * (N / wrows)
+    t = time.perf_counter()
+    q1 = o.quantize(d["x"][:1])
+    o.gemm(*q1, wc, wsc)
+    t_r1 = time.perf_counter() - t
+    o.set_num_threads(cores)
+    t_step1 = t_w1 + M * t_r1
     return {
         "value": round(4.0 * M * N * K / t_step / 1e12, 6),
         "unit": "TFLOP/s",
-        "cores": o.num_threads(),
+        "cores": cores,
+        "single_thread_value": round(4.0 * M * N * K / t_step1 / 1e12, 7),
         "cpu": _cpu_model(),
         "kind": "oracle",
         "sample": "full weight quantization (%dx%d) + %d activation rows through the RFQ "
                   "quantizer and the fp64 product against all %d outputs; scaled to the "
-                  "%d-row step (t_w=%.2fs t_x=%.3fs t_gemm=%.2fs)" % (N, K, rows, N, M, t_w,
-                                                                      t_x, t_g),
+                  "%d-row step (t_w=%.2fs t_x=%.3fs t_gemm=%.2fs); single_thread_value: 1/%d "
+                  "of the weight rows and 1 activation row on one thread, scaled the same "
+                  "way" % (N, K, rows, N, M, t_w, t_x, t_g, N // wrows),
     }
 
 

@@ -132,6 +132,39 @@ rfq_status rfq_swiglu_quantize_act(const void *g, const void *u, rfq_dtype dt,
                                    uint8_t *r_codes, uint8_t *r_scales,
                                    void *h_out, void *hip_stream);
 
+/*
+ * Gate/up product of a gated MLP with the SwiGLU intermediate and its RFQ
+ * quantization fused into the product's epilogue: Z = RFQ product (Eq. 11)
+ * of the activation codes with interleaved gate/up weights, then, per row and
+ * per 32 hidden units, g and u are the bf16 roundings of Z's gate and up
+ * columns, h = bf16(silu(g) * u) as in rfq_swiglu_quantize_act, and Q(h),
+ * Q(h - deq Q(h)) (Eq. 8-10) are written.  Neither Z nor g and u reach
+ * memory.  The codes are bit-identical to rfq_gemm with bf16 Z (gate and up
+ * columns) followed by rfq_swiglu_quantize_act.
+ *   q_codes, q_scales, r_codes, r_scales: activation codes as for rfq_gemm
+ *            ([M][K/2], [M][K/32]; residual pair optional, NULL gives phi = 0).
+ *   wgu_codes [2 Nh][K/2], wgu_scales [2 Nh][K/32]: quantized weights whose
+ *            rows are gate and up rows interleaved in groups of 32: rows
+ *            64 j .. 64 j + 31 are gate rows 32 j .., rows 64 j + 32 ..
+ *            64 j + 63 are up rows 32 j .. (weights are quantized row by row,
+ *            so interleaving the fp32 weights or their codes is the same).
+ *   M, Nh, K: Nh a multiple of 32 (it is the K of the down product); K a
+ *            multiple of 512; every code tensor below 4 GiB.
+ *   hq_codes [M][Nh/2], hq_scales [M][Nh/32], hr_codes, hr_scales: codes of
+ *            h as rfq_quantize_act with K = Nh (residual pair optional).
+ *   h_out    [M][Nh] bf16, or NULL; when given, h is also written.
+ * Alignment: all code tensors, the activation and weight scale tensors and
+ * h_out 16-byte aligned.  Errors: RFQ_ERR_SHAPE for the shape conditions
+ * above, otherwise as rfq_gemm.  Asynchronous on hip_stream.
+ */
+rfq_status rfq_gemm_swiglu_quantize(const uint8_t *q_codes, const uint8_t *q_scales,
+                                    const uint8_t *r_codes, const uint8_t *r_scales,
+                                    const uint8_t *wgu_codes, const uint8_t *wgu_scales,
+                                    int64_t M, int64_t Nh, int64_t K,
+                                    uint8_t *hq_codes, uint8_t *hq_scales,
+                                    uint8_t *hr_codes, uint8_t *hr_scales,
+                                    void *h_out, void *hip_stream);
+
 /* Static, never-NULL description of a status code. */
 const char *rfq_status_str(rfq_status s);
 

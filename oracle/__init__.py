@@ -49,6 +49,8 @@ def _load(path=LIB):
     lib.oracle_residual.argtypes = [D, I64, I64, D]
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = ctypes.c_int
+    lib.oracle_set_num_threads.argtypes = [ctypes.c_int]
+    lib.oracle_set_num_threads.restype = None
     for f in ("oracle_rfq_quantize", "oracle_dequant", "oracle_gemm",
               "oracle_gemm_sampled", "oracle_swiglu", "oracle_residual"):
         getattr(lib, f).restype = None
@@ -83,6 +85,9 @@ class Oracle:
 
     def num_threads(self):
         return int(self.h.oracle_num_threads())
+
+    def set_num_threads(self, n):
+        self.h.oracle_set_num_threads(int(n))
 
     def e2m1_value(self, code):
         return self.h.oracle_e2m1_value(int(code))

@@ -365,3 +365,14 @@ int oracle_num_threads(void)
     return 1;
 #endif
 }
+
+/* Sets the number of threads of later parallel loops (for timing the oracle
+ * single-threaded); no effect without OpenMP. */
+void oracle_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}

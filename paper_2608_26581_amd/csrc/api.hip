@@ -142,6 +142,37 @@ rfq_status rfq_swiglu_quantize_act(const void *g, const void *u, rfq_dtype dt,
                                               static_cast<hipStream_t>(hip_stream)));
 }
 
+rfq_status rfq_gemm_swiglu_quantize(const uint8_t *q_codes, const uint8_t *q_scales,
+                                    const uint8_t *r_codes, const uint8_t *r_scales,
+                                    const uint8_t *wgu_codes, const uint8_t *wgu_scales,
+                                    int64_t M, int64_t Nh, int64_t K,
+                                    uint8_t *hq_codes, uint8_t *hq_scales,
+                                    uint8_t *hr_codes, uint8_t *hr_scales,
+                                    void *h_out, void *hip_stream) {
+  rfq_status s = check_k(M, K);
+  if (s != RFQ_OK) return s;
+  if (Nh < 0 || (Nh % 32) != 0 || (K % 512) != 0) return RFQ_ERR_SHAPE;
+  if (M > INT32_MAX || 2 * Nh > INT32_MAX) return RFQ_ERR_SHAPE;
+  // Byte offsets inside each code tensor are 32-bit.
+  const int64_t limit = int64_t(1) << 32;
+  if (M * (K / 2) >= limit || 2 * Nh * (K / 2) >= limit) return RFQ_ERR_SHAPE;
+  if (M == 0 || Nh == 0) return RFQ_OK;
+  if (!q_codes || !q_scales || !wgu_codes || !wgu_scales || !hq_codes || !hq_scales)
+    return RFQ_ERR_NULL;
+  if ((r_codes == nullptr) != (r_scales == nullptr)) return RFQ_ERR_NULL;
+  if ((hr_codes == nullptr) != (hr_scales == nullptr)) return RFQ_ERR_NULL;
+  if (!aligned(q_codes, 16) || !aligned(q_scales, 16) || !aligned(wgu_codes, 16) ||
+      !aligned(wgu_scales, 16) || (r_codes && (!aligned(r_codes, 16) || !aligned(r_scales, 16))) ||
+      !aligned(hq_codes, 16) || (hr_codes && !aligned(hr_codes, 16)) ||
+      (h_out && !aligned(h_out, 16)))
+    return RFQ_ERR_ALIGN;
+  if ((s = check_device()) != RFQ_OK) return s;
+  return launched(rfq::launch_gemm_swiglu(q_codes, q_scales, r_codes, r_scales, wgu_codes,
+                                          wgu_scales, M, Nh, K, hq_codes, hq_scales, hr_codes,
+                                          hr_scales, static_cast<uint16_t *>(h_out),
+                                          static_cast<hipStream_t>(hip_stream)));
+}
+
 const char *rfq_status_str(rfq_status s) {
   switch (s) {
     case RFQ_OK: return "ok";

@@ -37,7 +37,13 @@
 // read hit distinct banks.
 //
 // Epilogue: each wave stages its results through LDS (padded rows) and
-// writes Z with 16-byte stores covering whole row segments.
+// writes Z with 16-byte stores covering whole row segments.  The SwiGLU
+// epilogue instead takes the product of interleaved gate/up weights (32-row
+// groups: gate rows 32g.., then up rows 32g..), so that columns 64g..64g+31
+// of Z are g and 64g+32..64g+63 are u for the same 32 hidden units: it rounds
+// both to bf16 as a bf16 Z would be, forms h = bf16(silu(g) u) and quantizes
+// each 32-wide block of h (primary and residual, Eq. 8-10) from registers,
+// with the same arithmetic as the standalone SwiGLU quantizer.
 //
 // Rows past M or N are clamped to the last row for loading (their results
 // are never stored), so no load leaves its tensor.
@@ -48,6 +54,7 @@
 #include <type_traits>
 
 #include "gemm_common.h"
+#include "mx_device.h"
 #include "rfq_internal.h"
 
 namespace rfq {
@@ -96,6 +103,14 @@ struct Epi {
   static constexpr int kChunksPerRow = 64 * kElem / 16;
 };
 
+// Outputs of the SwiGLU epilogue: codes and scales of h [M][nh] (residual
+// pair optional) and, when h is not null, h itself in bf16.
+struct SwigluOut {
+  uint8_t *qc, *qs, *rc, *rs;
+  uint16_t *h;
+  int64_t nh;
+};
+
 // Scale pairs of one stage (both k-steps) for the wave's fragments.
 template <bool RES>
 struct Scales {
@@ -125,12 +140,99 @@ __device__ __forceinline__ void reads_first() {
   if constexpr (N > 0) __builtin_amdgcn_sched_group_barrier(kDsRead, N, 0);
 }
 
-template <bool RES, bool ZBF16>
+// SwiGLU epilogue of one wave.  Fragment pair p of fragment row i holds g
+// (fragment 2p) and u (fragment 2p+1) of h block (n_base + 64 p) / 64 for
+// row m_base + 32 i.  Lane l has 16 of the block's 32 values, positions
+// 8a + 4(l/32) + v for accumulator element 4a + v; the other 16 are in lane
+// l ^ 32.  The block maximum and the 16-bit code pieces are exchanged with
+// that lane; the lower lane stores the primary codes, the upper the residual.
+template <bool HRES>
+__device__ __forceinline__ void swiglu_epilogue(const v16f (&acc)[kFM][kFN], const SwigluOut &so,
+                                                int64_t M, int64_t m_base, int64_t n_base,
+                                                int h) {
+  const int64_t nblk = so.nh / 32;
+#pragma unroll
+  for (int i = 0; i < kFM; ++i) {
+#pragma unroll
+    for (int p = 0; p < kFN / 2; ++p) {
+      const v16f &ag = acc[i][2 * p], &au = acc[i][2 * p + 1];
+      const int64_t m = m_base + 32 * i;
+      const int64_t blk = (n_base + 64 * p) / 64;
+      float hv[16];
+      uint32_t hbits[16];
+      float am = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        hbits[e] = swiglu_bits(__uint_as_float(bf16_rne_bits(ag[e])),
+                               __uint_as_float(bf16_rne_bits(au[e])));
+        hv[e] = __uint_as_float(hbits[e]);
+        am = fmaxf(am, fabsf(hv[e]));
+      }
+      am = fmaxf(am, __shfl_xor(am, 32));
+      const uint32_t qb = scale_byte(am);
+      const float qsc = scale_operand(qb);
+      uint32_t qp[4], rp[4] = {0, 0, 0, 0}, rb = 0;
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+        qp[a] = encode4(hv[4 * a], hv[4 * a + 1], hv[4 * a + 2], hv[4 * a + 3], qsc);
+      if constexpr (HRES) {
+        float r[16], ram = 0.0f;
+#pragma unroll
+        for (int a = 0; a < 4; ++a) {
+          float d[4];
+          decode4(qp[a], qsc, d);
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            r[4 * a + v] = hv[4 * a + v] - d[v];
+            ram = fmaxf(ram, fabsf(r[4 * a + v]));
+          }
+        }
+        ram = fmaxf(ram, __shfl_xor(ram, 32));
+        rb = scale_byte(ram);
+        const float rsc = scale_operand(rb);
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+          rp[a] = encode4(r[4 * a], r[4 * a + 1], r[4 * a + 2], r[4 * a + 3], rsc);
+      }
+      // Bytes 4a, 4a+1 of the block come from the lower lane, 4a+2, 4a+3
+      // from the upper: each lane sends the pieces its partner stores.
+      const uint32_t s01 = h ? (qp[0] | qp[1] << 16) : (rp[0] | rp[1] << 16);
+      const uint32_t s23 = h ? (qp[2] | qp[3] << 16) : (rp[2] | rp[3] << 16);
+      const uint32_t g01 = __shfl_xor(s01, 32), g23 = __shfl_xor(s23, 32);
+      if (m < M && blk < nblk) {
+        const int64_t off = m * (so.nh / 2) + 16 * blk;
+        if (h == 0) {
+          const u32x4 w = {qp[0] | (g01 << 16), qp[1] | (g01 & 0xFFFF0000u),
+                           qp[2] | (g23 << 16), qp[3] | (g23 & 0xFFFF0000u)};
+          *reinterpret_cast<u32x4 *>(so.qc + off) = w;
+          so.qs[m * nblk + blk] = (uint8_t)qb;
+        } else if constexpr (HRES) {
+          const u32x4 w = {(g01 & 0xFFFFu) | (rp[0] << 16), (g01 >> 16) | (rp[1] << 16),
+                           (g23 & 0xFFFFu) | (rp[2] << 16), (g23 >> 16) | (rp[3] << 16)};
+          *reinterpret_cast<u32x4 *>(so.rc + off) = w;
+          so.rs[m * nblk + blk] = (uint8_t)rb;
+        }
+        if (so.h) {
+          uint16_t *hp = so.h + m * so.nh + 32 * blk + 4 * h;
+#pragma unroll
+          for (int a = 0; a < 4; ++a) {
+            uint2 w;
+            w.x = (hbits[4 * a] >> 16) | (hbits[4 * a + 1] & 0xFFFF0000u);
+            w.y = (hbits[4 * a + 2] >> 16) | (hbits[4 * a + 3] & 0xFFFF0000u);
+            *reinterpret_cast<uint2 *>(hp + 8 * a) = w;
+          }
+        }
+      }
+    }
+  }
+}
+
+template <bool RES, bool ZBF16, bool SWIGLU = false, bool HRES = false>
 __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
     const uint8_t *__restrict__ qc, const uint8_t *__restrict__ qs,
     const uint8_t *__restrict__ rc, const uint8_t *__restrict__ rs,
     const uint8_t *__restrict__ wc, const uint8_t *__restrict__ ws,
-    int64_t M, int64_t N, int64_t K, void *__restrict__ z) {
+    int64_t M, int64_t N, int64_t K, void *__restrict__ z, SwigluOut so) {
   using L = Layout<RES>;
   extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
 
@@ -337,6 +439,11 @@ __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
   if (st + 2 < nstages - 1) stage(st + 2, HO{}, W3{}, NoRl{});
   stage(nstages - 1, NoHO{}, W0{}, NoRl{});
 
+  if constexpr (SWIGLU) {
+    swiglu_epilogue<HRES>(acc, so, M, m0 + wm * kTM + frow, n0 + wn * kTN, h);
+    return;
+  }
+
   // ---- epilogue: per pass (i, jp) a wave owns 32 rows x 64 columns.
   using E = Epi<ZBF16>;
   uint8_t *ep = smem + wave * E::kWaveBytes;
@@ -394,13 +501,14 @@ __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
   }
 }
 
-template <bool RES, bool ZBF16>
+template <bool RES, bool ZBF16, bool SWIGLU = false, bool HRES = false>
 hipError_t launch(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc,
                   const uint8_t *rs, const uint8_t *wc, const uint8_t *ws,
-                  int64_t M, int64_t N, int64_t K, void *z, hipStream_t stream) {
+                  int64_t M, int64_t N, int64_t K, void *z, hipStream_t stream,
+                  const SwigluOut &so = SwigluOut{}) {
   using L = Layout<RES>;
   static_assert(4 * Epi<ZBF16>::kWaveBytes <= L::kBytes, "epilogue staging fits");
-  auto kern = rfq_gemm_large_kernel<RES, ZBF16>;
+  auto kern = rfq_gemm_large_kernel<RES, ZBF16, SWIGLU, HRES>;
   static std::atomic<bool> attr_done{false};
   if (!attr_done.load(std::memory_order_acquire)) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
@@ -410,7 +518,7 @@ hipError_t launch(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc,
   }
   const int64_t ntiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
   kern<<<dim3((unsigned)ntiles), dim3(kThreads), L::kBytes, stream>>>(qc, qs, rc, rs, wc, ws,
-                                                                       M, N, K, z);
+                                                                       M, N, K, z, so);
   return hipGetLastError();
 }
 
@@ -440,6 +548,28 @@ hipError_t launch_gemm_large(const uint8_t *q_codes, const uint8_t *q_scales,
   if (z_bf16)
     return launch<false, true>(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K, z, stream);
   return launch<false, false>(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K, z, stream);
+}
+
+hipError_t launch_gemm_swiglu(const uint8_t *q_codes, const uint8_t *q_scales,
+                              const uint8_t *r_codes, const uint8_t *r_scales,
+                              const uint8_t *wgu_codes, const uint8_t *wgu_scales,
+                              int64_t M, int64_t Nh, int64_t K, uint8_t *hq_codes,
+                              uint8_t *hq_scales, uint8_t *hr_codes, uint8_t *hr_scales,
+                              uint16_t *h_out, hipStream_t stream) {
+  const SwigluOut so{hq_codes, hq_scales, hr_codes, hr_scales, h_out, Nh};
+  const int64_t N = 2 * Nh;
+  if (r_codes) {
+    if (hr_codes)
+      return launch<true, true, true, true>(q_codes, q_scales, r_codes, r_scales, wgu_codes,
+                                            wgu_scales, M, N, K, nullptr, stream, so);
+    return launch<true, true, true, false>(q_codes, q_scales, r_codes, r_scales, wgu_codes,
+                                           wgu_scales, M, N, K, nullptr, stream, so);
+  }
+  if (hr_codes)
+    return launch<false, true, true, true>(q_codes, q_scales, r_codes, r_scales, wgu_codes,
+                                           wgu_scales, M, N, K, nullptr, stream, so);
+  return launch<false, true, true, false>(q_codes, q_scales, r_codes, r_scales, wgu_codes,
+                                          wgu_scales, M, N, K, nullptr, stream, so);
 }
 
 }  // namespace rfq

@@ -16,20 +16,18 @@
 // plain (measured: non-temporal stores of these partial lines cost about a
 // fifth more write traffic, and non-temporal fp32 loads were slower).
 //
-// Element conversion uses the gfx950 scaled FP4 conversions: the convert to
-// FP4 divides by the scale 2^(byte-127), rounds to nearest-even, saturates at
-// +-6 and keeps the sign of zero; the convert from FP4 multiplies by the scale
-// exactly.  The residual x - deq(q) is exact in fp32 (a nonzero E2M1 rounding
-// lies within a factor of two of x), so it is formed in registers only.
+// Element arithmetic (scale byte, scaled FP4 conversions, SwiGLU) comes from
+// mx_device.h.  The residual x - deq(q) is exact in fp32 (a nonzero E2M1
+// rounding lies within a factor of two of x), so it is formed in registers
+// only.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "mx_device.h"
 #include "rfq_internal.h"
 
 namespace rfq {
 namespace {
-
-typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kThreads = 256;
 constexpr int kUnroll = 4;   // steps per wave span of 64 blocks (4 blocks per row)
@@ -42,38 +40,6 @@ __device__ __forceinline__ float quad_max(float v) {
   o = __int_as_float(
       __builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));
   return fmaxf(v, o);
-}
-
-// E8M0 byte of a block whose largest magnitude is amax (Eq. 3 with the OCP
-// offset): floor(log2 amax) - 2 + 127 is the biased exponent field minus 2;
-// blocks with amax < 2^-125 (zero and subnormal included) clamp to byte 0.
-__device__ __forceinline__ uint32_t scale_byte(float amax) {
-  const uint32_t e = __float_as_uint(amax) >> 23;
-  return e > 2u ? e - 2u : 0u;
-}
-
-// Scale operand of the scaled conversions: a float whose exponent field is
-// the E8M0 byte.
-__device__ __forceinline__ float scale_operand(uint32_t byte) {
-  return __uint_as_float(byte << 23);
-}
-
-__device__ __forceinline__ uint32_t encode8(const float (&v)[8], float s) {
-  uint32_t c = 0;
-  c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, v[0], v[1], s, 0);
-  c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, v[2], v[3], s, 1);
-  c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, v[4], v[5], s, 2);
-  c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, v[6], v[7], s, 3);
-  return c;
-}
-
-__device__ __forceinline__ void decode8(uint32_t c, float s, float (&d)[8]) {
-  f32x2 p0 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(c, s, 0);
-  f32x2 p1 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(c, s, 1);
-  f32x2 p2 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(c, s, 2);
-  f32x2 p3 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(c, s, 3);
-  d[0] = p0[0]; d[1] = p0[1]; d[2] = p1[0]; d[3] = p1[1];
-  d[4] = p2[0]; d[5] = p2[1]; d[6] = p3[0]; d[7] = p3[1];
 }
 
 __device__ __forceinline__ float absmax8(const float (&v)[8]) {
@@ -201,13 +167,6 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
   if constexpr (RES) store_span_scales(r_scales, span0 >> 2, nblocks, lane, rsw, rbytes);
 }
 
-// bf16 round to nearest even of a finite fp32 value, returned as the bf16
-// value widened back to fp32 (low 16 bits zero).
-__device__ __forceinline__ uint32_t bf16_rne_bits(float f) {
-  const uint32_t u = __float_as_uint(f);
-  return (u + 0x7FFFu + ((u >> 16) & 1u)) & 0xFFFF0000u;
-}
-
 template <bool BF16_IN, bool RES>
 __global__ __launch_bounds__(kThreads) void swiglu_quantize_kernel(
     const void *__restrict__ g, const void *__restrict__ u, int64_t nchunks,
@@ -232,9 +191,7 @@ __global__ __launch_bounds__(kThreads) void swiglu_quantize_kernel(
     uint32_t hb[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      const float gj = gv[i][j];
-      const float silu = gj * __builtin_amdgcn_rcpf(1.0f + __expf(-gj));
-      hb[j] = bf16_rne_bits(silu * uv[i][j]);
+      hb[j] = swiglu_bits(gv[i][j], uv[i][j]);
       h[j] = __uint_as_float(hb[j]);
     }
     uint32_t qc, qb, rc = 0, rb = 0;

@@ -37,7 +37,7 @@ hipError_t launch_gemm(const uint8_t *q_codes, const uint8_t *q_scales,
                        int64_t M, int64_t N, int64_t K, void *z, bool z_bf16,
                        hipStream_t stream);
 
-// Large-tile product: K a multiple of 128, 4-byte aligned scale tensors and
+// Large-tile product: K a multiple of 512, 16-byte aligned scale tensors and
 // code tensors below 4 GiB.
 bool gemm_large_applies(const uint8_t *q_scales, const uint8_t *r_scales,
                         const uint8_t *w_scales, int64_t M, int64_t N, int64_t K);
@@ -46,5 +46,15 @@ hipError_t launch_gemm_large(const uint8_t *q_codes, const uint8_t *q_scales,
                              const uint8_t *w_codes, const uint8_t *w_scales,
                              int64_t M, int64_t N, int64_t K, void *z, bool z_bf16,
                              hipStream_t stream);
+
+// Gate/up product of interleaved weights [2 Nh][K] with the SwiGLU + RFQ
+// quantizer in its epilogue (large-tile conditions must hold); writes the
+// codes of h [M][Nh] (hr_codes == nullptr: primary only) and optionally h.
+hipError_t launch_gemm_swiglu(const uint8_t *q_codes, const uint8_t *q_scales,
+                              const uint8_t *r_codes, const uint8_t *r_scales,
+                              const uint8_t *wgu_codes, const uint8_t *wgu_scales,
+                              int64_t M, int64_t Nh, int64_t K, uint8_t *hq_codes,
+                              uint8_t *hq_scales, uint8_t *hr_codes, uint8_t *hr_scales,
+                              uint16_t *h_out, hipStream_t stream);
 
 }  // namespace rfq

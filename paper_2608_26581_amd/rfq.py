@@ -28,7 +28,8 @@ _STATUS_NAMES = {
 # Every symbol declared in include/rfq.h.
 EXPORTS = (
     "rfq_quantize_act", "rfq_quantize_weight", "rfq_gemm", "rfq_dequant",
-    "rfq_swiglu_quantize_act", "rfq_status_str", "rfq_abi_version",
+    "rfq_swiglu_quantize_act", "rfq_gemm_swiglu_quantize", "rfq_status_str",
+    "rfq_abi_version",
 )
 
 _lib = None
@@ -58,8 +59,9 @@ def load():
     lib.rfq_gemm.argtypes = [P, P, P, P, P, P, I64, I64, I64, P, I32, P]
     lib.rfq_dequant.argtypes = [P, P, I64, I64, P, P]
     lib.rfq_swiglu_quantize_act.argtypes = [P, P, I32, I64, I64, P, P, P, P, P, P]
+    lib.rfq_gemm_swiglu_quantize.argtypes = [P, P, P, P, P, P, I64, I64, I64, P, P, P, P, P, P]
     for f in ("rfq_quantize_act", "rfq_quantize_weight", "rfq_gemm", "rfq_dequant",
-              "rfq_swiglu_quantize_act"):
+              "rfq_swiglu_quantize_act", "rfq_gemm_swiglu_quantize"):
         getattr(lib, f).restype = I32
     lib.rfq_status_str.argtypes = [I32]
     lib.rfq_status_str.restype = ctypes.c_char_p
@@ -179,3 +181,42 @@ def rfq_swiglu_quantize_act(g, u, residual=True, return_h=False, out=None, strea
                                         _ptr(qs), _ptr(rc), _ptr(rs), _ptr(h), _stream(stream))
     _check("rfq_swiglu_quantize_act", st)
     return qc, qs, rc, rs, h
+
+
+def rfq_gemm_swiglu_quantize(q_codes, q_scales, r_codes, r_scales, wgu_codes, wgu_scales,
+                             residual=True, return_h=False, out=None, stream=None):
+    """Gate/up product with SwiGLU + RFQ quantization of h in its epilogue.
+    wgu_* are the quantized interleaved gate/up weights [2 Nh][K]
+    (interleave_gate_up).  Returns (hq_codes, hq_scales, hr_codes, hr_scales,
+    h or None); hr_* are None when residual is False."""
+    M = q_codes.shape[0]
+    K = q_codes.shape[1] * 2
+    Nh = wgu_codes.shape[0] // 2
+    if wgu_codes.shape[1] * 2 != K:
+        raise ValueError("K mismatch between activation and weight codes")
+    if out is None:
+        hqc, hqs = _codes_out(M, Nh, q_codes.device)
+        hrc, hrs = _codes_out(M, Nh, q_codes.device) if residual else (None, None)
+    else:
+        hqc, hqs, hrc, hrs = out
+    h = (torch.empty((M, Nh), dtype=torch.bfloat16, device=q_codes.device)
+         if return_h else None)
+    st = load().rfq_gemm_swiglu_quantize(
+        _ptr(q_codes), _ptr(q_scales), _ptr(r_codes), _ptr(r_scales), _ptr(wgu_codes),
+        _ptr(wgu_scales), M, Nh, K, _ptr(hqc), _ptr(hqs), _ptr(hrc), _ptr(hrs), _ptr(h),
+        _stream(stream))
+    _check("rfq_gemm_swiglu_quantize", st)
+    return hqc, hqs, hrc, hrs, h
+
+
+def interleave_gate_up(gate, up):
+    """Rows of gate [Nh][...] and up [Nh][...] interleaved in groups of 32
+    (the weight layout rfq_gemm_swiglu_quantize takes).  Works on fp32
+    weights and, equivalently, on their codes or scales, since weights are
+    quantized row by row.  A one-off layout step, not part of the path."""
+    if gate.shape != up.shape or gate.shape[0] % 32:
+        raise ValueError("gate and up must have the same shape, rows a multiple of 32")
+    nh = gate.shape[0]
+    g = gate.reshape(nh // 32, 32, *gate.shape[1:])
+    u = up.reshape(nh // 32, 32, *up.shape[1:])
+    return torch.stack((g, u), dim=1).reshape(2 * nh, *gate.shape[1:]).contiguous()

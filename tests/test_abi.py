@@ -142,6 +142,36 @@ def test_dequant_and_swiglu_validation():
     assert s(A, A, 1, 0, 64, A, A, A, A, None, None) == OK
 
 
+def test_gemm_swiglu_validation():
+    f = _lib().rfq_gemm_swiglu_quantize
+    #       q  qs r  rs w  ws  M   Nh   K    hq hs hr hrs h
+    ok = (A, A, A, A, A, A, 64, 128, 512, A, A, A, A, None, None)
+
+    def call(**kw):
+        args = list(ok)
+        names = ["q", "qs", "r", "rs", "w", "ws", "M", "Nh", "K", "hq", "hs", "hr", "hrs",
+                 "h", "st"]
+        for k, v in kw.items():
+            args[names.index(k)] = v
+        return f(*args)
+
+    assert call(K=480) == ESHAPE             # not a multiple of 32
+    assert call(K=256) == ESHAPE             # multiple of 32, not of 512
+    assert call(Nh=100) == ESHAPE            # hidden width not a multiple of 32
+    assert call(Nh=-32) == ESHAPE
+    assert call(M=-1) == ESHAPE
+    assert call(M=0) == OK and call(Nh=0) == OK
+    assert call(M=1 << 23, K=1024) == ESHAPE     # activation codes of 4 GiB
+    assert call(q=None) == ENULL
+    assert call(hq=None) == ENULL
+    assert call(r=None) == ENULL             # half of the residual input pair
+    assert call(hrs=None) == ENULL           # half of the residual output pair
+    assert call(qs=MIS) == EALIGN            # scale tensors must be 16-byte aligned
+    assert call(ws=MIS) == EALIGN
+    assert call(hq=MIS) == EALIGN
+    assert call(h=MIS) == EALIGN
+
+
 def test_valid_arguments_without_a_gpu_report_device_error():
     import torch
     if torch.cuda.is_available():

@@ -327,6 +327,59 @@ def test_plain_mxfp4_agrees_with_hipblaslt(orc):
         (err > tol).sum())
 
 
+# --------------------------------------------------- fused SwiGLU epilogue
+def _fused_and_unfused(data, K, Nh, res_in, res_out):
+    """The chained path (gate and up products with bf16 Z, then the SwiGLU
+    quantizer) and the fused one on the same codes."""
+    q = rfq.rfq_quantize_act(x_device(data), residual=res_in)
+    wg = rfq.rfq_quantize_weight(dev(data["w_gate"]))
+    wu = rfq.rfq_quantize_weight(dev(data["w_up"]))
+    g = rfq.rfq_gemm(*q, *wg, out_dtype=torch.bfloat16)
+    u = rfq.rfq_gemm(*q, *wu, out_dtype=torch.bfloat16)
+    ref = rfq.rfq_swiglu_quantize_act(g, u, residual=res_out, return_h=True)
+    wgu = (rfq.interleave_gate_up(wg[0], wu[0]), rfq.interleave_gate_up(wg[1], wu[1]))
+    got = rfq.rfq_gemm_swiglu_quantize(*q, *wgu, residual=res_out, return_h=True)
+    return got, ref
+
+
+FUSED = [(200, 640, 512), (64, 96, 1024), (300, 1280, 1536), (1, 32, 512)]
+
+
+@pytest.mark.parametrize("M,Nh,K", FUSED)
+@pytest.mark.parametrize("res_in,res_out", [(True, True), (False, True), (True, False)])
+def test_gemm_swiglu_fused_matches_chained(M, Nh, K, res_in, res_out):
+    """The fused epilogue is bit-identical to the chained path (whose stages
+    are pinned to the oracle in test_swiglu_mlp_block_stagewise): codes,
+    scales and h."""
+    w = wl.WORKLOADS["swiglu"].scaled(M=M, K=K, weights=(
+        ("w_gate", K, Nh), ("w_up", K, Nh), ("w_down", Nh, K)))
+    data = wl.generate(w, seed=8)
+    _say("fused swiglu M=%d Nh=%d K=%d res_in=%s res_out=%s" % (M, Nh, K, res_in, res_out))
+    got, ref = _fused_and_unfused(data, K, Nh, res_in, res_out)
+    for n, a, b in zip(("hq_codes", "hq_scales", "hr_codes", "hr_scales", "h"), got, ref):
+        if b is None:
+            assert a is None
+            continue
+        assert torch.equal(a, b), n
+
+
+def test_gemm_swiglu_fused_full_size_and_down_product(orc):
+    """Config-5 shape: fused gate/up epilogue equals the chained path bit for
+    bit; the down product on the fused codes is checked against the oracle
+    on sampled rows."""
+    data = wl.generate(wl.WORKLOADS["swiglu"], seed=0)
+    _say("fused swiglu full size")
+    got, ref = _fused_and_unfused(data, 4096, 12288, True, True)
+    for n, a, b in zip(("hq_codes", "hq_scales", "hr_codes", "hr_scales", "h"), got, ref):
+        assert torch.equal(a, b), n
+    wd = rfq.rfq_quantize_weight(dev(data["w_down"]))
+    z = host(rfq.rfq_gemm(*got[:4], *wd))
+    rows = np.arange(0, 4096, 97)
+    hq = [host(t)[rows] for t in got[:4]]
+    zr, bound = orc.gemm(*hq, host(wd[0]), host(wd[1]))
+    assert_gemm_close(z[rows], zr, bound, False, "down on fused codes")
+
+
 # ---------------------------------------------------------------- edges
 def test_empty_inputs_are_noops():
     x = torch.empty((0, 64), dtype=torch.bfloat16, device="cuda")
