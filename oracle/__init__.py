@@ -42,6 +42,8 @@ def _load(path=LIB):
     lib.oracle_rfq_quantize.argtypes = [D, I64, I64, U8, U8, U8, U8]
     lib.oracle_dequant.argtypes = [U8, U8, I64, I64, D]
     lib.oracle_gemm.argtypes = [U8, U8, U8, U8, U8, U8, I64, I64, I64, D, D]
+    lib.oracle_gemm_phi.argtypes = [U8, U8, U8, U8, U8, U8, U8, I64, I64, I64, D, D]
+    lib.oracle_fallback_map.argtypes = [U8, U8, I64, I64, ctypes.c_int, ctypes.c_int, U8]
     lib.oracle_gemm_sampled.argtypes = [U8, U8, U8, U8, U8, U8, I64,
                                         ctypes.POINTER(ctypes.c_int64),
                                         ctypes.POINTER(ctypes.c_int64), I64, D, D]
@@ -51,7 +53,8 @@ def _load(path=LIB):
     lib.oracle_num_threads.restype = ctypes.c_int
     lib.oracle_set_num_threads.argtypes = [ctypes.c_int]
     lib.oracle_set_num_threads.restype = None
-    for f in ("oracle_rfq_quantize", "oracle_dequant", "oracle_gemm",
+    for f in ("oracle_rfq_quantize", "oracle_dequant", "oracle_gemm", "oracle_gemm_phi",
+              "oracle_fallback_map",
               "oracle_gemm_sampled", "oracle_swiglu", "oracle_residual"):
         getattr(lib, f).restype = None
     return lib
@@ -138,6 +141,27 @@ class Oracle:
         b = np.empty((M, N), np.float64)
         self.h.oracle_gemm(*[self._u8(a) for a in arrs], M, N, K, self._d(z), self._d(b))
         return z, b
+
+    def gemm_phi(self, qc, qs, rc, rs, wc, ws, phi):
+        """Z and bound with the phi map phi[ceil(M/64)][ceil(K/256)]."""
+        arrs = [np.ascontiguousarray(a, np.uint8) if a is not None else None
+                for a in (qc, qs, rc, rs, wc, ws, phi)]
+        M, K, N = arrs[0].shape[0], arrs[0].shape[1] * 2, arrs[4].shape[0]
+        z = np.empty((M, N), np.float64)
+        b = np.empty((M, N), np.float64)
+        self.h.oracle_gemm_phi(*[self._u8(a) for a in arrs], M, N, K, self._d(z), self._d(b))
+        return z, b
+
+    def fallback_map(self, rc, qs, rule, threshold=0):
+        """phi[ceil(M/64)][ceil(K/256)] by rule 0 (nonzero residual codes) or
+        rule 1 (a primary scale byte >= threshold)."""
+        qs = np.ascontiguousarray(qs, np.uint8)
+        M, K = qs.shape[0], qs.shape[1] * 32
+        rc = np.ascontiguousarray(rc if rc is not None else np.zeros((M, K // 2)), np.uint8)
+        phi = np.empty(((M + 63) // 64, (K + 255) // 256), np.uint8)
+        self.h.oracle_fallback_map(self._u8(rc), self._u8(qs), M, K, int(rule), int(threshold),
+                                   self._u8(phi))
+        return phi
 
     def gemm_sampled(self, qc, qs, rc, rs, wc, ws, rows, cols):
         arrs = [np.ascontiguousarray(a, np.uint8) if a is not None else None

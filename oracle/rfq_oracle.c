@@ -22,8 +22,14 @@
  *   - Residual DeltaX = X - Xtilde, Sec. 4.3 Eq. (9), and its quantization
  *     with the same quantizer, Eq. (10), with its own block scale.
  *   - The RFQ product, Sec. 4.3 Eq. (11) / Algorithm 1, with the fallback
- *     indicator phi fixed to 1 (every block carries a residual) or 0 (plain
- *     MXFP4).
+ *     indicator phi fixed to 1 (every block carries a residual), 0 (plain
+ *     MXFP4), or given per activation tile of ORACLE_PHI_ROWS rows by
+ *     ORACLE_PHI_K reduction columns (Algorithm 1 takes phi(p, r) as an input
+ *     over blocks of P_s x R_s; these are the tile sizes of this build).
+ *   - Two rules that produce such a phi map (the paper states none): phi = 1
+ *     where a tile's residual codes are not all zero (the residual term of
+ *     the other tiles is exactly zero), or where a tile holds a primary scale
+ *     byte at least a threshold (a large block maximum marks an outlier).
  *   - Dequantization X ~ Xtilde + phi * Xhat, Sec. 4.3 Eq. (12).
  *   - SwiGLU intermediate h = bf16(silu(g) * u) for the MLP workload (not
  *     from the paper; used to chain two RFQ products).
@@ -47,6 +53,12 @@
 #include <string.h>
 
 #define ORACLE_BLOCK 32
+#define ORACLE_PHI_ROWS 64
+#if ORACLE_PLANT == 12
+#define ORACLE_PHI_K 128        /* planted: phi tile width halved */
+#else
+#define ORACLE_PHI_K 256
+#endif
 
 #ifndef ORACLE_PLANT
 #define ORACLE_PLANT 0
@@ -233,9 +245,10 @@ void oracle_dequant(const uint8_t *codes, const uint8_t *scales, int64_t rows,
  * fp32 evaluation may make). */
 static void gemm_one(const uint8_t *qc, const uint8_t *qs,
                      const uint8_t *rc, const uint8_t *rs,
-                     const uint8_t *wc, const uint8_t *ws,
+                     const uint8_t *wc, const uint8_t *ws, const uint8_t *phi,
                      int64_t K, int64_t m, int64_t n, double *z, double *bound)
 {
+    int64_t phi_cols = (K + ORACLE_PHI_K - 1) / ORACLE_PHI_K;
     int64_t nb = K / ORACLE_BLOCK;
     double zq = 0.0, zr = 0.0, bsum = 0.0;
     int64_t k;
@@ -256,7 +269,7 @@ static void gemm_one(const uint8_t *qc, const uint8_t *qs,
                          (int)qs[m * nb + b] - 127);
         zq += q * w;
         bsum += fabs(q * w);
-        if (rc) {
+        if (rc && (!phi || phi[(m / ORACLE_PHI_ROWS) * phi_cols + k / ORACLE_PHI_K])) {
             double r = ldexp(oracle_e2m1_value(get_nibble(rc + m * (K / 2), k)),
                              (int)rs[m * nb + b] - 127);
             zr += r * w;
@@ -270,20 +283,65 @@ static void gemm_one(const uint8_t *qc, const uint8_t *qs,
     *bound = bsum;
 }
 
-/* Full RFQ product Z[M][N] (phi = 1; phi = 0 when rc is NULL), weights
- * stored [N][K] with blocks along K. */
-void oracle_gemm(const uint8_t *qc, const uint8_t *qs,
-                 const uint8_t *rc, const uint8_t *rs,
-                 const uint8_t *wc, const uint8_t *ws,
-                 int64_t M, int64_t N, int64_t K, double *z, double *bound)
+/* Full RFQ product Z[M][N] with a phi map phi[ceil(M/64)][ceil(K/256)]
+ * (nonzero: the tile's residual term is included; NULL: phi = 1; rc NULL:
+ * phi = 0), weights stored [N][K] with blocks along K.  The bound covers the
+ * terms included. */
+void oracle_gemm_phi(const uint8_t *qc, const uint8_t *qs,
+                     const uint8_t *rc, const uint8_t *rs,
+                     const uint8_t *wc, const uint8_t *ws, const uint8_t *phi,
+                     int64_t M, int64_t N, int64_t K, double *z, double *bound)
 {
     int64_t m;
 #pragma omp parallel for schedule(dynamic, 1)
     for (m = 0; m < M; ++m) {
         int64_t n;
         for (n = 0; n < N; ++n)
-            gemm_one(qc, qs, rc, rs, wc, ws, K, m, n, z + m * N + n,
+            gemm_one(qc, qs, rc, rs, wc, ws, phi, K, m, n, z + m * N + n,
                      bound + m * N + n);
+    }
+}
+
+/* Full RFQ product with phi = 1 (phi = 0 when rc is NULL). */
+void oracle_gemm(const uint8_t *qc, const uint8_t *qs,
+                 const uint8_t *rc, const uint8_t *rs,
+                 const uint8_t *wc, const uint8_t *ws,
+                 int64_t M, int64_t N, int64_t K, double *z, double *bound)
+{
+    oracle_gemm_phi(qc, qs, rc, rs, wc, ws, NULL, M, N, K, z, bound);
+}
+
+/* phi map [ceil(M/64)][ceil(K/256)] by one of two rules (the paper gives
+ * none): rule 0 sets phi where some residual code of the tile has a nonzero
+ * magnitude, rule 1 where some primary scale byte of the tile is at least
+ * threshold. */
+void oracle_fallback_map(const uint8_t *rc, const uint8_t *qs, int64_t M, int64_t K,
+                         int rule, int threshold, uint8_t *phi)
+{
+    int64_t nb = K / ORACLE_BLOCK;
+    int64_t pr = (M + ORACLE_PHI_ROWS - 1) / ORACLE_PHI_ROWS;
+    int64_t pc = (K + ORACLE_PHI_K - 1) / ORACLE_PHI_K;
+    int64_t t;
+#pragma omp parallel for schedule(static)
+    for (t = 0; t < pr * pc; ++t) {
+        int64_t p = t / pc, c = t % pc, m, k;
+        int on = 0;
+        for (m = p * ORACLE_PHI_ROWS; m < M && m < (p + 1) * ORACLE_PHI_ROWS; ++m) {
+            for (k = c * ORACLE_PHI_K; k < K && k < (c + 1) * ORACLE_PHI_K; ++k) {
+                if (rule == 0) {
+                    if ((get_nibble(rc + m * (K / 2), k) & 7) != 0)
+                        on = 1;
+                } else {
+#if ORACLE_PLANT == 13
+                    if ((int)qs[m * nb + k / ORACLE_BLOCK] > threshold)   /* planted: > */
+#else
+                    if ((int)qs[m * nb + k / ORACLE_BLOCK] >= threshold)
+#endif
+                        on = 1;
+                }
+            }
+        }
+        phi[t] = (uint8_t)on;
     }
 }
 
@@ -297,7 +355,7 @@ void oracle_gemm_sampled(const uint8_t *qc, const uint8_t *qs,
     int64_t i;
 #pragma omp parallel for schedule(static)
     for (i = 0; i < count; ++i)
-        gemm_one(qc, qs, rc, rs, wc, ws, K, rows[i], cols[i], z + i, bound + i);
+        gemm_one(qc, qs, rc, rs, wc, ws, NULL, K, rows[i], cols[i], z + i, bound + i);
 }
 
 /* Round a double to the nearest bfloat16 value (8 significant bits, the

@@ -352,4 +352,74 @@ def pin_swiglu_closed_forms(o):
             assert (m * 2 ** 8) == int(m * 2 ** 8), v
 
 
+def pin_gemm_phi_tiles(o):
+    """Eq. 11 with a phi map (Algorithm 1's phi(p, r) over tiles of 64 rows
+    by 256 reduction columns): brute force from values decoded here, for
+    random maps on shapes with ragged tiles; phi = 1 and phi = 0 reduce to the
+    RFQ and the plain products."""
+    rng = np.random.default_rng(12)
+    for (M, N, K) in ((130, 6, 544), (64, 3, 256), (7, 5, 96)):
+        x = rng.standard_normal((M, K))
+        x[:, rng.integers(0, K, 3)] *= 30
+        w = rng.normal(0, 0.02, (N, K))
+        qc, qs, rc, rs = o.quantize(x)
+        wc, ws, _, _ = o.quantize(w, residual=False)
+        dq, dr, dw = decode_codes(qc, qs), decode_codes(rc, rs), decode_codes(wc, ws)
+        pr, pc = (M + 63) // 64, (K + 255) // 256
+        for trial in range(4):
+            phi = rng.integers(0, 2, (pr, pc)).astype(np.uint8)
+            if trial == 0:
+                phi[:] = 1
+            if trial == 1:
+                phi[:] = 0
+            mask = np.zeros((M, K))
+            for m in range(M):
+                for k in range(K):
+                    mask[m, k] = phi[m // 64, k // 256]
+            z, bound = o.gemm_phi(qc, qs, rc, rs, wc, ws, phi)
+            want = dq @ dw.T + (dr * mask) @ dw.T
+            assert np.all(np.abs(z - want) <= 1e-12 * bound + 1e-300), (M, N, K, trial)
+            if trial == 0:
+                assert np.array_equal(z, o.gemm(qc, qs, rc, rs, wc, ws)[0])
+            if trial == 1:
+                assert np.array_equal(z, o.gemm(qc, qs, None, None, wc, ws)[0])
+
+
+def pin_fallback_map_rules(o):
+    """The two phi rules by brute force over tiles: rule 0 marks tiles with a
+    residual code of nonzero magnitude, rule 1 tiles with a primary scale
+    byte at least the threshold; on grid-valued rows the residual is zero, so
+    rule 0 leaves their tiles off, and phi from rule 0 gives exactly the
+    phi = 1 product."""
+    rng = np.random.default_rng(13)
+    M, K = 150, 800
+    x = rng.standard_normal((M, K))
+    # Rows 64..127 hold E2M1 grid values only: their residual is exactly zero.
+    grid = np.array([0, 0.5, 1, 1.5, 2, 3, 4, 6])
+    x[64:128] = rng.choice(grid, (64, K)) * rng.choice([-1, 1], (64, K))
+    x[:64, 700] *= 100
+    x[128:, 700] *= 100
+    qc, qs, rc, rs = o.quantize(x)
+    top00 = int(qs[:64, :8].max())          # a threshold met with equality by tile (0, 0)
+    for rule, thr in ((0, 0), (1, int(np.median(qs)) + 3), (1, top00), (1, 255), (1, 0)):
+        phi = o.fallback_map(rc, qs, rule, thr)
+        assert phi.shape == ((M + 63) // 64, (K + 255) // 256)
+        for p in range(phi.shape[0]):
+            for c in range(phi.shape[1]):
+                rows = slice(64 * p, min(64 * p + 64, M))
+                if rule == 0:
+                    nib = np.stack([rc[rows] & 15, rc[rows] >> 4], -1).reshape(
+                        rc[rows].shape[0], K)[:, 256 * c:256 * c + 256]
+                    want = bool(np.any(nib & 7))
+                else:
+                    want = bool(np.any(qs[rows, 8 * c:8 * c + 8] >= thr))
+                assert phi[p, c] == want, (rule, thr, p, c)
+    phi = o.fallback_map(rc, qs, 0)
+    assert not phi[1].any() and phi[0].all()
+    w = rng.normal(0, 0.02, (4, K))
+    wc, ws, _, _ = o.quantize(w, residual=False)
+    assert np.array_equal(o.gemm_phi(qc, qs, rc, rs, wc, ws, phi)[0],
+                          o.gemm(qc, qs, rc, rs, wc, ws)[0])
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

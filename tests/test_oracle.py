@@ -10,8 +10,9 @@ import oracle_pins
 # 3 ties away from zero, 4 sign of zero dropped, 5 nibble order swapped,
 # 6 residual taken of x instead of x - q, 7 weight scaled by the activation
 # scale, 8 residual term dropped from the product, 9 bf16 truncation,
-# 10 sign error in silu, 11 weight index shifted by one.
-PLANTS = list(range(1, 12))
+# 10 sign error in silu, 11 weight index shifted by one, 12 phi tile width
+# halved, 13 strict comparison in the scale-threshold phi rule.
+PLANTS = list(range(1, 14))
 
 
 @pytest.mark.parametrize("pin", oracle_pins.ALL_PINS, ids=lambda f: f.__name__)
