@@ -33,6 +33,7 @@ PEAK_FP4_TFLOPS = 10100.0     # MI355X dense MXFP4 matrix cores
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 N_SETS = 3
 Q_SETS = 6
+PHI_MARGIN = 4                # scale-threshold phi: median primary scale byte + 4
 METRIC = "RFQ-MXFP4 GEMM TFLOP/s + quantizer GB/s (Qwen3-VL-like 4096×4096×12288)"
 
 
@@ -308,7 +309,18 @@ def secondary(torch, rfq, wl, x, w, stream):
             "ms": round(ms, 5), "exec_tflops": round(2.0 * M * N * K / ms / 1e9, 1)}
     except (AttributeError, RuntimeError, ValueError, NotImplementedError) as e:
         out["hipblaslt_mxfp4_scaled_mm"] = {"unavailable": str(e)[:120]}
-    del q, wq, z, wt
+    # Fallback indicator by the scale-threshold rule (phi = 1 on tiles holding
+    # a primary scale byte >= the median + PHI_MARGIN): residual MFMAs only
+    # where outliers are.
+    thr = int(q[1].float().median().item()) + PHI_MARGIN
+    phi = rfq.rfq_fallback_map(None, q[1], rfq.RFQ_PHI_SCALE_AT_LEAST, thr)
+    ms = _per_launch_ms(torch, stream, lambda i: rfq.rfq_gemm_phi(
+        *q, *wq, phi, out=z, stream=stream), 20)
+    on = float(phi.float().mean().item())
+    out["rfq_gemm_phi_scale_threshold"] = {
+        "ms": round(ms, 5), "threshold_byte": thr, "tiles_on": round(on, 4),
+        "exec_tflops": round((2.0 + 2.0 * on) * M * N * K / ms / 1e9, 1)}
+    del q, wq, z, wt, phi
 
     # Wan2.2-DiT-like product: X 32768x5120, W 5120x13824.
     d = wl.generate(wl.WORKLOADS["wan"], seed=0)
@@ -402,6 +414,9 @@ def accuracy(torch, rfq, x, w, nrows=64):
         "plain_mxfp4": rel(rfq.rfq_gemm(q[0], q[1], None, None, *wq)),
         "rfq": rel(rfq.rfq_gemm(*q, *wq)),
     }
+    thr = int(q[1].float().median().item()) + PHI_MARGIN
+    phi = rfq.rfq_fallback_map(None, q[1], rfq.RFQ_PHI_SCALE_AT_LEAST, thr)
+    out["rfq_phi_scale_threshold"] = rel(rfq.rfq_gemm_phi(*q, *wq, phi))
     wdq = rfq.rfq_dequant(*wq).double()
     out["weight_only_floor"] = float(torch.linalg.norm(x64 @ wdq.t() - zt) / nt)
     out["rows"] = int(rows.numel())

@@ -62,6 +62,13 @@ typedef enum {
     RFQ_BF16 = 1   /* bfloat16 (upper half of a binary32) */
 } rfq_dtype;
 
+/* Rules that build a fallback-indicator map (the paper defines phi(p, r) as
+ * an input of Algorithm 1 but gives no rule; these two are this library's). */
+typedef enum {
+    RFQ_PHI_RESIDUAL_NONZERO = 0,   /* phi = 1 where a residual code of the tile is nonzero */
+    RFQ_PHI_SCALE_AT_LEAST = 1      /* phi = 1 where a primary scale byte of the tile >= threshold */
+} rfq_phi_rule;
+
 /*
  * RFQ activation quantizer: primary code Q(X) (Eq. 8) and, when r_codes and
  * r_scales are given, the residual DeltaX = X - deq(Q(X)) (Eq. 9) quantized
@@ -131,6 +138,42 @@ rfq_status rfq_swiglu_quantize_act(const void *g, const void *u, rfq_dtype dt,
                                    uint8_t *q_codes, uint8_t *q_scales,
                                    uint8_t *r_codes, uint8_t *r_scales,
                                    void *h_out, void *hip_stream);
+
+/*
+ * RFQ product with the fallback indicator of Algorithm 1 / Eq. (11) given as
+ * a map: Z = sum_r Xq Yq + sum_r phi(p, r) Xr Yq, where phi(p, r) is one byte
+ * per activation tile of 64 rows (p = m / 64) by 256 reduction columns
+ * (r = k / 256); a nonzero byte includes the tile's residual term.  Tiles
+ * with phi = 0 skip the residual matrix-core work.
+ *   phi      [ceil(M/64)][ceil(K/256)] bytes, device memory, any alignment.
+ *            NULL means phi = 1 everywhere (then, and when r_codes is NULL,
+ *            the call is exactly rfq_gemm).
+ *   Other arguments, layouts and errors as rfq_gemm; with a map, K must not
+ *   exceed 2^20 (RFQ_ERR_SHAPE).
+ */
+rfq_status rfq_gemm_phi(const uint8_t *q_codes, const uint8_t *q_scales,
+                        const uint8_t *r_codes, const uint8_t *r_scales,
+                        const uint8_t *w_codes, const uint8_t *w_scales, const uint8_t *phi,
+                        int64_t M, int64_t N, int64_t K, void *z, rfq_dtype z_dtype,
+                        void *hip_stream);
+
+/*
+ * Builds a fallback-indicator map for rfq_gemm_phi over the same tiles
+ * (64 rows by 256 reduction columns; ragged edge tiles cover what exists).
+ *   rule RFQ_PHI_RESIDUAL_NONZERO: phi = 1 where some residual code of the
+ *        tile has a nonzero magnitude; the other tiles' residual terms are
+ *        exactly zero, so the product equals phi = 1 (up to the sign of a zero
+ *        output).  Reads r_codes [M][K/2] (16-byte aligned); q_scales unused.
+ *   rule RFQ_PHI_SCALE_AT_LEAST: phi = 1 where some primary scale byte of the
+ *        tile is >= threshold (a large block maximum marks an outlier);
+ *        reads q_scales [M][K/32]; r_codes unused.
+ *   phi  [ceil(M/64)][ceil(K/256)] bytes (0 or 1), written.
+ * Errors: RFQ_ERR_SHAPE for an unknown rule or the K conditions of
+ * rfq_quantize_act; RFQ_ERR_NULL for a missing input the rule reads or phi.
+ */
+rfq_status rfq_fallback_map(const uint8_t *r_codes, const uint8_t *q_scales, int64_t M,
+                            int64_t K, int rule, int threshold, uint8_t *phi,
+                            void *hip_stream);
 
 /*
  * Gate/up product of a gated MLP with the SwiGLU intermediate and its RFQ

@@ -142,6 +142,45 @@ rfq_status rfq_swiglu_quantize_act(const void *g, const void *u, rfq_dtype dt,
                                               static_cast<hipStream_t>(hip_stream)));
 }
 
+rfq_status rfq_gemm_phi(const uint8_t *q_codes, const uint8_t *q_scales,
+                        const uint8_t *r_codes, const uint8_t *r_scales,
+                        const uint8_t *w_codes, const uint8_t *w_scales, const uint8_t *phi,
+                        int64_t M, int64_t N, int64_t K, void *z, rfq_dtype z_dtype,
+                        void *hip_stream) {
+  if (!phi || !r_codes)
+    return rfq_gemm(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K, z,
+                    z_dtype, hip_stream);
+  if (!valid_dtype(z_dtype)) return RFQ_ERR_DTYPE;
+  rfq_status s = check_k(M, K);
+  if (s != RFQ_OK) return s;
+  if (N < 0 || K > (int64_t(1) << 20)) return RFQ_ERR_SHAPE;
+  if (M > INT32_MAX || N > INT32_MAX) return RFQ_ERR_SHAPE;
+  if (((M + 63) / 64) * ((N + 63) / 64) > INT32_MAX) return RFQ_ERR_SHAPE;
+  if (M == 0 || N == 0) return RFQ_OK;
+  if (!q_codes || !q_scales || !r_scales || !w_codes || !w_scales || !z) return RFQ_ERR_NULL;
+  if (!aligned(q_codes, 16) || !aligned(w_codes, 16) || !aligned(r_codes, 16) ||
+      !aligned(z, 16))
+    return RFQ_ERR_ALIGN;
+  if ((s = check_device()) != RFQ_OK) return s;
+  return launched(rfq::launch_gemm_phi(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales,
+                                       phi, M, N, K, z, z_dtype == RFQ_BF16,
+                                       static_cast<hipStream_t>(hip_stream)));
+}
+
+rfq_status rfq_fallback_map(const uint8_t *r_codes, const uint8_t *q_scales, int64_t M,
+                            int64_t K, int rule, int threshold, uint8_t *phi,
+                            void *hip_stream) {
+  rfq_status s = check_k(M, K);
+  if (s != RFQ_OK) return s;
+  if (rule != RFQ_PHI_RESIDUAL_NONZERO && rule != RFQ_PHI_SCALE_AT_LEAST) return RFQ_ERR_SHAPE;
+  if (M == 0) return RFQ_OK;
+  if (!phi || (rule == RFQ_PHI_RESIDUAL_NONZERO ? !r_codes : !q_scales)) return RFQ_ERR_NULL;
+  if (rule == RFQ_PHI_RESIDUAL_NONZERO && !aligned(r_codes, 16)) return RFQ_ERR_ALIGN;
+  if ((s = check_device()) != RFQ_OK) return s;
+  return launched(rfq::launch_fallback_map(r_codes, q_scales, M, K, rule, threshold, phi,
+                                           static_cast<hipStream_t>(hip_stream)));
+}
+
 rfq_status rfq_gemm_swiglu_quantize(const uint8_t *q_codes, const uint8_t *q_scales,
                                     const uint8_t *r_codes, const uint8_t *r_scales,
                                     const uint8_t *wgu_codes, const uint8_t *wgu_scales,

@@ -66,12 +66,18 @@ __device__ __forceinline__ uint32_t bf16_rne(float f) {
   return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
 }
 
-template <int BM, int BN, bool RES, bool ZBF16>
+// Fallback-indicator map: one byte per tile of 64 activation rows (a wave's
+// rows) by 256 reduction columns (a stage).
+constexpr int kPhiRows = 64;
+constexpr int kPhiMapMaxBytes = 2 * ((1 << 20) / kStageK);   // two rows, K up to 2^20
+
+template <int BM, int BN, bool RES, bool ZBF16, bool PHI = false>
 __global__ __launch_bounds__(256) void rfq_gemm_kernel(
     const uint8_t *__restrict__ qc, const uint8_t *__restrict__ qs,
     const uint8_t *__restrict__ rc, const uint8_t *__restrict__ rs,
     const uint8_t *__restrict__ wc, const uint8_t *__restrict__ ws,
-    int64_t M, int64_t N, int64_t K, void *__restrict__ z) {
+    int64_t M, int64_t N, int64_t K, void *__restrict__ z,
+    const uint8_t *__restrict__ phi) {
   constexpr int kThreads = 256;
   constexpr int TM = BM / 2, TN = BN / 2;     // wave sub-tile
   constexpr int FM = TM / 16, FN = TN / 16;   // 16x16 fragments per wave
@@ -183,8 +189,23 @@ __global__ __launch_bounds__(256) void rfq_gemm_kernel(
 
   const int frow = lane & 15, g = lane >> 4;
 
-  // One instruction step: blocks 2g+SUB of the stage for every lane group.
-  auto mma_step = [&](const uint8_t *base, auto sub_tag) {
+  static_assert(!PHI || BM == 2 * kPhiRows, "a wave's rows are one indicator row");
+  // The indicator rows of this workgroup's two wave rows, behind the stage
+  // buffers in LDS (published by the barrier after the first stage store).
+  const int pcols = nstages;
+  uint8_t *phi_lds = smem + S::kBytes;
+  if constexpr (PHI) {
+    const int64_t prow0 = m0 / kPhiRows, prows = (M + kPhiRows - 1) / kPhiRows;
+    for (int i = tid; i < 2 * pcols; i += kThreads) {
+      const int64_t pr = prow0 + i / pcols;
+      phi_lds[i] = pr < prows ? phi[pr * pcols + i % pcols] : (uint8_t)0;
+    }
+  }
+  const int wm_u = __builtin_amdgcn_readfirstlane(wm);
+
+  // One instruction step: blocks 2g+SUB of the stage for every lane group;
+  // `res_on` (wave-uniform) switches the residual MFMAs of the stage.
+  auto mma_step = [&](const uint8_t *base, auto sub_tag, bool res_on) {
     constexpr int SUB = decltype(sub_tag)::value;
     const uint8_t *sc = base + S::kDataBytes;
     v8i wf[FN];
@@ -206,7 +227,7 @@ __global__ __launch_bounds__(256) void rfq_gemm_kernel(
       for (int j = 0; j < FN; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(
             wf[j], af, acc[i][j], kFmtFp4, kFmtFp4, SUB, wsc[j], SUB, asc);
-      if constexpr (RES) {
+      if (RES && res_on) {
         const int rr = BM + r;
         const uint4 e = *reinterpret_cast<const uint4 *>(base + swz(rr, 2 * g + SUB));
         const v8i rf = v8i{(int)e.x, (int)e.y, (int)e.z, (int)e.w, 0, 0, 0, 0};
@@ -226,8 +247,10 @@ __global__ __launch_bounds__(256) void rfq_gemm_kernel(
     const bool more = st + 1 < nstages;
     if (more) load_stage(st + 1);
     const uint8_t *base = smem + (st & 1) * S::kStageBytes;
-    mma_step(base, std::integral_constant<int, 0>{});
-    mma_step(base, std::integral_constant<int, 1>{});
+    const bool res_on =
+        !PHI || __builtin_amdgcn_readfirstlane((int)phi_lds[wm_u * pcols + st]) != 0;
+    mma_step(base, std::integral_constant<int, 0>{}, res_on);
+    mma_step(base, std::integral_constant<int, 1>{}, res_on);
     if (more) store_stage((st + 1) & 1);
     __syncthreads();
   }
@@ -268,25 +291,28 @@ __global__ __launch_bounds__(256) void rfq_gemm_kernel(
   }
 }
 
-template <int BM, int BN, bool RES, bool ZBF16>
+template <int BM, int BN, bool RES, bool ZBF16, bool PHI = false>
 hipError_t launch_tile(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc,
                        const uint8_t *rs, const uint8_t *wc, const uint8_t *ws,
                        int64_t M, int64_t N, int64_t K, void *z,
-                       hipStream_t stream) {
+                       hipStream_t stream, const uint8_t *phi = nullptr) {
   using S = Smem<BM, BN, RES>;
-  auto kern = rfq_gemm_kernel<BM, BN, RES, ZBF16>;
+  auto kern = rfq_gemm_kernel<BM, BN, RES, ZBF16, PHI>;
+  constexpr int kMaxBytes = S::kBytes + (PHI ? kPhiMapMaxBytes : 0);
+  const int phi_bytes = PHI ? (int)((2 * ((K + kStageK - 1) / kStageK) + 15) / 16 * 16) : 0;
   // The dynamic-LDS limit is an attribute of the kernel function; setting it
   // twice from racing threads is harmless.
   static std::atomic<bool> attr_done{false};
   if (!attr_done.load(std::memory_order_acquire)) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       S::kBytes);
+                                       kMaxBytes);
     if (e != hipSuccess) return e;
     attr_done.store(true, std::memory_order_release);
   }
   const int64_t ntiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-  kern<<<dim3((unsigned)ntiles), dim3(256), S::kBytes, stream>>>(qc, qs, rc, rs, wc, ws, M, N, K, z);
+  kern<<<dim3((unsigned)ntiles), dim3(256), S::kBytes + phi_bytes, stream>>>(
+      qc, qs, rc, rs, wc, ws, M, N, K, z, phi);
   return hipGetLastError();
 }
 
@@ -309,6 +335,22 @@ hipError_t launch_gemm(const uint8_t *q_codes, const uint8_t *q_scales,
   if (z_bf16)
     return launch_tile<BM, BN, false, true>(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K, z, stream);
   return launch_tile<BM, BN, false, false>(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K, z, stream);
+}
+
+hipError_t launch_gemm_phi(const uint8_t *q_codes, const uint8_t *q_scales,
+                           const uint8_t *r_codes, const uint8_t *r_scales,
+                           const uint8_t *w_codes, const uint8_t *w_scales, const uint8_t *phi,
+                           int64_t M, int64_t N, int64_t K, void *z, bool z_bf16,
+                           hipStream_t stream) {
+  if (gemm_large_applies(q_scales, r_scales, w_scales, M, N, K))
+    return launch_gemm_large_phi(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, phi, M,
+                                 N, K, z, z_bf16, stream);
+  constexpr int BM = 128, BN = 128;
+  if (z_bf16)
+    return launch_tile<BM, BN, true, true, true>(q_codes, q_scales, r_codes, r_scales, w_codes,
+                                                 w_scales, M, N, K, z, stream, phi);
+  return launch_tile<BM, BN, true, false, true>(q_codes, q_scales, r_codes, r_scales, w_codes,
+                                                w_scales, M, N, K, z, stream, phi);
 }
 
 }  // namespace rfq

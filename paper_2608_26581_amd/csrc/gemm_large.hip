@@ -227,12 +227,19 @@ __device__ __forceinline__ void swiglu_epilogue(const v16f (&acc)[kFM][kFN], con
   }
 }
 
-template <bool RES, bool ZBF16, bool SWIGLU = false, bool HRES = false>
+// Fallback-indicator map: one byte per tile of kPhiRows activation rows by
+// kPhiK reduction columns (a wave's rows by two stages).
+constexpr int kPhiRows = 64, kPhiK = 256;
+// LDS reserved for the two map rows of a workgroup (K up to 2^20).
+constexpr int kPhiMapMaxBytes = 2 * ((1 << 20) / kPhiK);
+
+template <bool RES, bool ZBF16, bool SWIGLU = false, bool HRES = false, bool PHI = false>
 __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
     const uint8_t *__restrict__ qc, const uint8_t *__restrict__ qs,
     const uint8_t *__restrict__ rc, const uint8_t *__restrict__ rs,
     const uint8_t *__restrict__ wc, const uint8_t *__restrict__ ws,
-    int64_t M, int64_t N, int64_t K, void *__restrict__ z, SwigluOut so) {
+    int64_t M, int64_t N, int64_t K, void *__restrict__ z, SwigluOut so,
+    const uint8_t *__restrict__ phi) {
   using L = Layout<RES>;
   extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
 
@@ -357,6 +364,18 @@ __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
             as_v8i(w.w[j]), as_v8i(a.r), acc[i][j], kFmtFp4, kFmtFp4, S, sc.w[j], S, sc.r[i]);
     }
   };
+  // The primary (R false) or the residual (R true) MFMAs of fragment row i,
+  // for the fallback-indicator path, which issues them in two groups.
+  auto mma_part = [&](const WFrag &w, const AFrag &a, const Scales<RES> &sc, int i, auto s_tag,
+                      auto r_tag) {
+    constexpr int S = decltype(s_tag)::value;
+    constexpr bool R = decltype(r_tag)::value;
+#pragma unroll
+    for (int j = 0; j < kFN; ++j)
+      acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+          as_v8i(w.w[j]), as_v8i(R ? a.r : a.q), acc[i][j], kFmtFp4, kFmtFp4, S, sc.w[j], S,
+          R ? sc.r[i] : sc.q[i]);
+  };
   using S0 = std::integral_constant<int, 0>;
   using S1 = std::integral_constant<int, 1>;
   using W0 = std::integral_constant<int, 0>;
@@ -368,6 +387,19 @@ __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
   using Rl = std::integral_constant<bool, true>;
   using NoRl = std::integral_constant<bool, false>;
 
+  // The fallback-indicator rows of this workgroup's two waves rows, copied
+  // to LDS behind the stage buffers (the prologue's barrier publishes them).
+  const int pcols = (int)((K + kPhiK - 1) / kPhiK);
+  uint8_t *phi_lds = smem + L::kBytes;
+  if constexpr (PHI) {
+    const int64_t prow0 = m0 / kPhiRows, prows = (M + kPhiRows - 1) / kPhiRows;
+    for (int i = tid; i < 2 * pcols; i += kThreads) {
+      const int64_t pr = prow0 + i / pcols;
+      phi_lds[i] = pr < prows ? phi[pr * pcols + i % pcols] : (uint8_t)0;
+    }
+  }
+  const int wm_u = __builtin_amdgcn_readfirstlane(wm);
+
   // ---- prologue: stage 0 into buffer 0, stage 1 in registers.
   load_group(0);
   load_stage(0);
@@ -377,22 +409,29 @@ __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
   asm volatile("" ::: "memory");
   __syncthreads();
 
-  constexpr int kRowMfma = RES ? 8 : 4;
-  constexpr int kAR = RES ? 2 : 1;
-  constexpr int kSR = kFN + kFM * (RES ? 2 : 1);
   auto region_end = [&]() {
     __builtin_amdgcn_sched_barrier(0);
     asm volatile("" ::: "memory");
   };
+  constexpr int kRowMfma = RES ? 8 : 4;
+  constexpr int kAR = RES ? 2 : 1;
+  constexpr int kSR = kFN + kFM * (RES ? 2 : 1);
+  using Prim = std::integral_constant<bool, false>;
+  using Resi = std::integral_constant<bool, true>;
   // Stage st: multiply buffer st mod 2; write stage st+1 (in registers) to
   // the other buffer, whose previous contents were last read before the
-  // barrier that ended stage st-1; then fetch stage st+2.
+  // barrier that ended stage st-1; then fetch stage st+2.  With a
+  // fallback-indicator map, each k-step issues the primary MFMAs of both
+  // rows (the writes and loads spread between them) and then, where the
+  // wave's indicator `on` is set, the residual MFMAs.
   auto stage = [&](int st, auto handover_tag, auto word_tag, auto reload_tag) {
     constexpr bool HANDOVER = decltype(handover_tag)::value;
     constexpr bool RELOAD = decltype(reload_tag)::value;
     const int buf = st & 1, nbuf = buf ^ 1;
     constexpr int kW = HANDOVER ? L::kLoads + L::kScaleLoads : 0;
     constexpr int kV = (HANDOVER ? L::kLoads : 0) + (RELOAD ? L::kScaleLoads : 0);
+    int on = 1;
+    if constexpr (PHI) on = __builtin_amdgcn_readfirstlane((int)phi_lds[wm_u * pcols + st / 2]);
     WFrag w;
     AFrag a0, a1;
     Scales<RES> sc;
@@ -401,10 +440,22 @@ __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
     read_a(buf, 0, 0, a0);
     read_a(buf, 0, 1, a1);
     if constexpr (HANDOVER) store_stage(nbuf, word_tag);
-    mma_row(w, a0, sc, 0, S0{});
-    mma_row(w, a1, sc, 1, S0{});
-    reads_first<kFN + kSR + 2 * kAR>();
-    spread<2 * kRowMfma, kW, kDsWrite>();
+    if constexpr (PHI) {
+      mma_part(w, a0, sc, 0, S0{}, Prim{});
+      mma_part(w, a1, sc, 1, S0{}, Prim{});
+      reads_first<kFN + kSR + 2 * kAR>();
+      spread<2 * kFN, kW, kDsWrite>();
+      region_end();
+      if (on) {
+        mma_part(w, a0, sc, 0, S0{}, Resi{});
+        mma_part(w, a1, sc, 1, S0{}, Resi{});
+      }
+    } else {
+      mma_row(w, a0, sc, 0, S0{});
+      mma_row(w, a1, sc, 1, S0{});
+      reads_first<kFN + kSR + 2 * kAR>();
+      spread<2 * kRowMfma, kW, kDsWrite>();
+    }
     region_end();
 
     if constexpr (RELOAD) load_group((st + 2) / kGroup);
@@ -414,10 +465,22 @@ __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
     read_w(buf, 1, w1);
     read_a(buf, 1, 0, b0);
     read_a(buf, 1, 1, b1);
-    mma_row(w1, b0, sc, 0, S1{});
-    mma_row(w1, b1, sc, 1, S1{});
-    reads_first<kFN + 2 * kAR>();
-    spread<2 * kRowMfma, kV, kVmemRead>();
+    if constexpr (PHI) {
+      mma_part(w1, b0, sc, 0, S1{}, Prim{});
+      mma_part(w1, b1, sc, 1, S1{}, Prim{});
+      reads_first<kFN + 2 * kAR>();
+      spread<2 * kFN, kV, kVmemRead>();
+      region_end();
+      if (on) {
+        mma_part(w1, b0, sc, 0, S1{}, Resi{});
+        mma_part(w1, b1, sc, 1, S1{}, Resi{});
+      }
+    } else {
+      mma_row(w1, b0, sc, 0, S1{});
+      mma_row(w1, b1, sc, 1, S1{});
+      reads_first<kFN + 2 * kAR>();
+      spread<2 * kRowMfma, kV, kVmemRead>();
+    }
     region_end();
     __syncthreads();
   };
@@ -501,24 +564,27 @@ __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
   }
 }
 
-template <bool RES, bool ZBF16, bool SWIGLU = false, bool HRES = false>
+template <bool RES, bool ZBF16, bool SWIGLU = false, bool HRES = false, bool PHI = false>
 hipError_t launch(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc,
                   const uint8_t *rs, const uint8_t *wc, const uint8_t *ws,
                   int64_t M, int64_t N, int64_t K, void *z, hipStream_t stream,
-                  const SwigluOut &so = SwigluOut{}) {
+                  const SwigluOut &so = SwigluOut{}, const uint8_t *phi = nullptr) {
   using L = Layout<RES>;
   static_assert(4 * Epi<ZBF16>::kWaveBytes <= L::kBytes, "epilogue staging fits");
-  auto kern = rfq_gemm_large_kernel<RES, ZBF16, SWIGLU, HRES>;
+  auto kern = rfq_gemm_large_kernel<RES, ZBF16, SWIGLU, HRES, PHI>;
+  // LDS: the two stage buffers, then (PHI) two rows of the indicator map.
+  constexpr int kMaxBytes = L::kBytes + (PHI ? kPhiMapMaxBytes : 0);
+  const int phi_bytes = PHI ? (int)(((2 * ((K + kPhiK - 1) / kPhiK)) + 15) / 16 * 16) : 0;
   static std::atomic<bool> attr_done{false};
   if (!attr_done.load(std::memory_order_acquire)) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, L::kBytes);
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, kMaxBytes);
     if (e != hipSuccess) return e;
     attr_done.store(true, std::memory_order_release);
   }
   const int64_t ntiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
-  kern<<<dim3((unsigned)ntiles), dim3(kThreads), L::kBytes, stream>>>(qc, qs, rc, rs, wc, ws,
-                                                                       M, N, K, z, so);
+  kern<<<dim3((unsigned)ntiles), dim3(kThreads), L::kBytes + phi_bytes, stream>>>(
+      qc, qs, rc, rs, wc, ws, M, N, K, z, so, phi);
   return hipGetLastError();
 }
 
@@ -548,6 +614,18 @@ hipError_t launch_gemm_large(const uint8_t *q_codes, const uint8_t *q_scales,
   if (z_bf16)
     return launch<false, true>(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K, z, stream);
   return launch<false, false>(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K, z, stream);
+}
+
+hipError_t launch_gemm_large_phi(const uint8_t *q_codes, const uint8_t *q_scales,
+                                 const uint8_t *r_codes, const uint8_t *r_scales,
+                                 const uint8_t *w_codes, const uint8_t *w_scales,
+                                 const uint8_t *phi, int64_t M, int64_t N, int64_t K, void *z,
+                                 bool z_bf16, hipStream_t stream) {
+  if (z_bf16)
+    return launch<true, true, false, false, true>(q_codes, q_scales, r_codes, r_scales, w_codes,
+                                                  w_scales, M, N, K, z, stream, SwigluOut{}, phi);
+  return launch<true, false, false, false, true>(q_codes, q_scales, r_codes, r_scales, w_codes,
+                                                 w_scales, M, N, K, z, stream, SwigluOut{}, phi);
 }
 
 hipError_t launch_gemm_swiglu(const uint8_t *q_codes, const uint8_t *q_scales,

@@ -231,6 +231,40 @@ __global__ __launch_bounds__(kThreads) void dequant_kernel(
   out[2 * ch + 1] = make_float4(d[4], d[5], d[6], d[7]);
 }
 
+// Fallback-indicator map over tiles of 64 rows by 256 reduction columns
+// (one workgroup per tile): rule 0 marks tiles where a residual code has a
+// nonzero magnitude, rule 1 tiles holding a primary scale byte >= threshold.
+__global__ __launch_bounds__(kThreads) void fallback_map_kernel(
+    const uint8_t *__restrict__ r_codes, const uint8_t *__restrict__ q_scales, int64_t M,
+    int64_t K, int rule, int threshold, int pcols, uint8_t *__restrict__ phi) {
+  const int64_t p = blockIdx.x / pcols, c = blockIdx.x % pcols;
+  const int tid = threadIdx.x;
+  const int64_t m = 64 * p + tid / 4;
+  int flag = 0;
+  if (m < M) {
+    if (rule == 0) {
+      const int64_t kb = K / 2;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int64_t b = 128 * c + 32 * (tid & 3) + 16 * h;
+        if (b < kb) {
+          const u32x4 v = *reinterpret_cast<const u32x4 *>(r_codes + m * kb + b);
+          flag |= ((v.x | v.y | v.z | v.w) & 0x77777777u) != 0;
+        }
+      }
+    } else {
+      const int64_t nb = K / 32;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int64_t b = 8 * c + 2 * (tid & 3) + h;
+        if (b < nb) flag |= (int)q_scales[m * nb + b] >= threshold;
+      }
+    }
+  }
+  flag = __syncthreads_or(flag);
+  if (tid == 0) phi[blockIdx.x] = (uint8_t)(flag != 0);
+}
+
 inline unsigned grid_for(int64_t nchunks, int64_t per_block) {
   return (unsigned)((nchunks + per_block - 1) / per_block);
 }
@@ -289,6 +323,16 @@ hipError_t launch_dequant(const uint8_t *codes, const uint8_t *scales,
   dequant_kernel<<<grid_for(nchunks, kThreads), kThreads, 0, stream>>>(
       reinterpret_cast<const uint32_t *>(codes), scales, nchunks,
       reinterpret_cast<float4 *>(out));
+  return hipGetLastError();
+}
+
+hipError_t launch_fallback_map(const uint8_t *r_codes, const uint8_t *q_scales, int64_t M,
+                               int64_t K, int rule, int threshold, uint8_t *phi,
+                               hipStream_t stream) {
+  const int pcols = (int)((K + 255) / 256);
+  const int64_t tiles = ((M + 63) / 64) * pcols;
+  fallback_map_kernel<<<(unsigned)tiles, kThreads, 0, stream>>>(r_codes, q_scales, M, K, rule,
+                                                                 threshold, pcols, phi);
   return hipGetLastError();
 }
 

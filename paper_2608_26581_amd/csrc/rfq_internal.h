@@ -47,6 +47,26 @@ hipError_t launch_gemm_large(const uint8_t *q_codes, const uint8_t *q_scales,
                              int64_t M, int64_t N, int64_t K, void *z, bool z_bf16,
                              hipStream_t stream);
 
+// RFQ product with a fallback-indicator map phi[ceil(M/64)][ceil(K/256)]
+// (residual operand required; K up to 2^20): the residual term of a tile is
+// included where its byte is nonzero.
+hipError_t launch_gemm_phi(const uint8_t *q_codes, const uint8_t *q_scales,
+                           const uint8_t *r_codes, const uint8_t *r_scales,
+                           const uint8_t *w_codes, const uint8_t *w_scales, const uint8_t *phi,
+                           int64_t M, int64_t N, int64_t K, void *z, bool z_bf16,
+                           hipStream_t stream);
+hipError_t launch_gemm_large_phi(const uint8_t *q_codes, const uint8_t *q_scales,
+                                 const uint8_t *r_codes, const uint8_t *r_scales,
+                                 const uint8_t *w_codes, const uint8_t *w_scales,
+                                 const uint8_t *phi, int64_t M, int64_t N, int64_t K, void *z,
+                                 bool z_bf16, hipStream_t stream);
+
+// phi map by rule 0 (residual codes not all zero) or 1 (a primary scale
+// byte >= threshold) over the same tiles.
+hipError_t launch_fallback_map(const uint8_t *r_codes, const uint8_t *q_scales, int64_t M,
+                               int64_t K, int rule, int threshold, uint8_t *phi,
+                               hipStream_t stream);
+
 // Gate/up product of interleaved weights [2 Nh][K] with the SwiGLU + RFQ
 // quantizer in its epilogue (large-tile conditions must hold); writes the
 // codes of h [M][Nh] (hr_codes == nullptr: primary only) and optionally h.

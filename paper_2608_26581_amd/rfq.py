@@ -28,9 +28,12 @@ _STATUS_NAMES = {
 # Every symbol declared in include/rfq.h.
 EXPORTS = (
     "rfq_quantize_act", "rfq_quantize_weight", "rfq_gemm", "rfq_dequant",
-    "rfq_swiglu_quantize_act", "rfq_gemm_swiglu_quantize", "rfq_status_str",
-    "rfq_abi_version",
+    "rfq_swiglu_quantize_act", "rfq_gemm_phi", "rfq_fallback_map", "rfq_gemm_swiglu_quantize",
+    "rfq_status_str", "rfq_abi_version",
 )
+
+RFQ_PHI_RESIDUAL_NONZERO = 0
+RFQ_PHI_SCALE_AT_LEAST = 1
 
 _lib = None
 
@@ -60,8 +63,11 @@ def load():
     lib.rfq_dequant.argtypes = [P, P, I64, I64, P, P]
     lib.rfq_swiglu_quantize_act.argtypes = [P, P, I32, I64, I64, P, P, P, P, P, P]
     lib.rfq_gemm_swiglu_quantize.argtypes = [P, P, P, P, P, P, I64, I64, I64, P, P, P, P, P, P]
+    lib.rfq_gemm_phi.argtypes = [P, P, P, P, P, P, P, I64, I64, I64, P, I32, P]
+    lib.rfq_fallback_map.argtypes = [P, P, I64, I64, I32, I32, P, P]
     for f in ("rfq_quantize_act", "rfq_quantize_weight", "rfq_gemm", "rfq_dequant",
-              "rfq_swiglu_quantize_act", "rfq_gemm_swiglu_quantize"):
+              "rfq_swiglu_quantize_act", "rfq_gemm_swiglu_quantize", "rfq_gemm_phi",
+              "rfq_fallback_map"):
         getattr(lib, f).restype = I32
     lib.rfq_status_str.argtypes = [I32]
     lib.rfq_status_str.restype = ctypes.c_char_p
@@ -153,6 +159,39 @@ def rfq_gemm(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales,
                          _stream(stream))
     _check("rfq_gemm", st)
     return z
+
+
+def rfq_gemm_phi(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, phi,
+                 out_dtype=torch.float32, out=None, stream=None):
+    """RFQ product with a fallback-indicator map phi[ceil(M/64)][ceil(K/256)]
+    (uint8; None: phi = 1)."""
+    M = q_codes.shape[0]
+    K = q_codes.shape[1] * 2
+    N = w_codes.shape[0]
+    if w_codes.shape[1] * 2 != K:
+        raise ValueError("K mismatch between activation and weight codes")
+    if phi is not None and tuple(phi.shape) != ((M + 63) // 64, (K + 255) // 256):
+        raise ValueError("phi must be [ceil(M/64)][ceil(K/256)]")
+    z = out if out is not None else torch.empty((M, N), dtype=out_dtype, device=q_codes.device)
+    st = load().rfq_gemm_phi(_ptr(q_codes), _ptr(q_scales), _ptr(r_codes), _ptr(r_scales),
+                             _ptr(w_codes), _ptr(w_scales), _ptr(phi), M, N, K, _ptr(z),
+                             _dtype_code(z), _stream(stream))
+    _check("rfq_gemm_phi", st)
+    return z
+
+
+def rfq_fallback_map(r_codes, q_scales, rule, threshold=0, out=None, stream=None):
+    """phi[ceil(M/64)][ceil(K/256)] by RFQ_PHI_RESIDUAL_NONZERO (reads r_codes)
+    or RFQ_PHI_SCALE_AT_LEAST (reads q_scales; phi = 1 where a scale byte >=
+    threshold)."""
+    M = q_scales.shape[0]
+    K = q_scales.shape[1] * 32
+    phi = out if out is not None else torch.empty(((M + 63) // 64, (K + 255) // 256),
+                                                  dtype=torch.uint8, device=q_scales.device)
+    st = load().rfq_fallback_map(_ptr(r_codes), _ptr(q_scales), M, K, int(rule), int(threshold),
+                                 _ptr(phi), _stream(stream))
+    _check("rfq_fallback_map", st)
+    return phi
 
 
 def rfq_dequant(codes, scales, out=None, stream=None):

@@ -172,6 +172,28 @@ def test_gemm_swiglu_validation():
     assert call(h=MIS) == EALIGN
 
 
+def test_gemm_phi_and_fallback_map_validation():
+    f = _lib().rfq_gemm_phi
+    #       q  qs r  rs w  ws phi  M  N   K    z  dt st
+    assert f(A, A, A, A, A, A, A, 4, 8, 64, A, 9, None) == EDTYPE
+    assert f(A, A, A, A, A, A, A, 4, 8, 100, A, 0, None) == ESHAPE
+    assert f(A, A, A, A, A, A, A, 4, 8, (1 << 20) + 32, A, 0, None) == ESHAPE
+    assert f(A, A, A, None, A, A, A, 4, 8, 64, A, 0, None) == ENULL
+    assert f(A, A, MIS, A, A, A, A, 4, 8, 64, A, 0, None) == EALIGN
+    assert f(A, A, A, A, A, A, A, 0, 8, 64, A, 0, None) == OK
+    # Without a map (or without the residual) the call is rfq_gemm's.
+    assert f(A, A, A, A, A, A, None, 4, 8, 100, A, 0, None) == ESHAPE
+    m = _lib().rfq_fallback_map
+    #       rc qs  M  K   rule thr phi st
+    assert m(A, A, 4, 64, 2, 0, A, None) == ESHAPE
+    assert m(A, A, 4, 96 + 1, 0, 0, A, None) == ESHAPE
+    assert m(None, A, 4, 64, 0, 0, A, None) == ENULL
+    assert m(A, None, 4, 64, 1, 9, A, None) == ENULL
+    assert m(A, A, 4, 64, 0, 0, None, None) == ENULL
+    assert m(MIS, A, 4, 64, 0, 0, A, None) == EALIGN
+    assert m(A, A, 0, 64, 0, 0, A, None) == OK
+
+
 def test_valid_arguments_without_a_gpu_report_device_error():
     import torch
     if torch.cuda.is_available():

@@ -327,6 +327,75 @@ def test_plain_mxfp4_agrees_with_hipblaslt(orc):
         (err > tol).sum())
 
 
+# ------------------------------------------------- fallback indicator phi
+PHI_SHAPES = [
+    ("qwen", 200, 328, 1024),       # large-tile kernel, ragged M and N
+    ("qwen", 129, 257, 2560),       # large-tile kernel, ragged indicator rows
+    ("qwen", 200, 328, 1056),       # general kernel, K not a multiple of 256
+    ("wan", 64, 96, 640),           # general kernel
+]
+
+
+def _phi_case(name, M, N, K, seed):
+    w = wl.WORKLOADS[name].scaled(M=M, K=K, weights=(("w", K, N),))
+    data = wl.generate(w, seed=seed)
+    q = rfq.rfq_quantize_act(x_device(data))
+    wq = rfq.rfq_quantize_weight(dev(data["w"]))
+    return q, wq
+
+
+@pytest.mark.parametrize("name,M,N,K", PHI_SHAPES)
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
+def test_gemm_phi_random_maps(orc, name, M, N, K, out_dtype):
+    """Eq. 11 with a given phi map against the oracle; phi = 1 and phi = 0
+    give exactly the RFQ and the plain products."""
+    q, wq = _phi_case(name, M, N, K, 21)
+    hq = [host(t) for t in q] + [host(t) for t in wq]
+    rng = np.random.default_rng(M + K)
+    shape = ((M + 63) // 64, (K + 255) // 256)
+    _say("phi %s M=%d N=%d K=%d %s" % (name, M, N, K, out_dtype))
+    for trial in range(3):
+        phi = rng.integers(0, 2, shape).astype(np.uint8)
+        z = rfq.rfq_gemm_phi(*q, *wq, torch.from_numpy(phi).cuda(), out_dtype=out_dtype)
+        zr, bound = orc.gemm_phi(*hq, phi)
+        zg = host_bf16_as_f32(z) if out_dtype == torch.bfloat16 else host(z)
+        assert_gemm_close(zg, zr, bound, out_dtype == torch.bfloat16, "phi trial %d" % trial)
+    ones = torch.ones(shape, dtype=torch.uint8, device="cuda")
+    zeros = torch.zeros(shape, dtype=torch.uint8, device="cuda")
+    assert torch.equal(rfq.rfq_gemm_phi(*q, *wq, ones, out_dtype=out_dtype),
+                       rfq.rfq_gemm(*q, *wq, out_dtype=out_dtype))
+    assert torch.equal(rfq.rfq_gemm_phi(*q, *wq, zeros, out_dtype=out_dtype),
+                       rfq.rfq_gemm(q[0], q[1], None, None, *wq, out_dtype=out_dtype))
+
+
+@pytest.mark.parametrize("M,K", [(150, 800), (64, 4096), (257, 5120)])
+def test_fallback_map_rules(orc, M, K):
+    """Both map rules bit-exact against the oracle; the residual-nonzero map
+    leaves the product unchanged (tiles it switches off carry zero codes)."""
+    rng = np.random.default_rng(K)
+    x = rng.standard_normal((M, K)).astype(np.float32)
+    grid = np.array([0, 0.5, 1, 1.5, 2, 3, 4, 6], np.float32)
+    x[64:128] = rng.choice(grid, x[64:128].shape) * rng.choice(np.float32([-1, 1]),
+                                                                 x[64:128].shape)
+    x[:64, K // 3] *= 80
+    q = rfq.rfq_quantize_act(torch.from_numpy(x).cuda())
+    hq = [host(t) for t in q]
+    _say("fallback map M=%d K=%d" % (M, K))
+    phi0 = rfq.rfq_fallback_map(q[2], q[1], rfq.RFQ_PHI_RESIDUAL_NONZERO)
+    assert np.array_equal(host(phi0), orc.fallback_map(hq[2], hq[1], 0))
+    thr = int(np.median(hq[1])) + 2
+    phi1 = rfq.rfq_fallback_map(None, q[1], rfq.RFQ_PHI_SCALE_AT_LEAST, thr)
+    assert np.array_equal(host(phi1), orc.fallback_map(None, hq[1], 1, thr))
+    if M >= 128:
+        assert not host(phi0)[1].any()
+    w = rng.normal(0, 0.02, (192, K)).astype(np.float32)
+    wq = rfq.rfq_quantize_weight(torch.from_numpy(w).cuda())
+    z1 = rfq.rfq_gemm(*q, *wq)
+    zphi = rfq.rfq_gemm_phi(*q, *wq, phi0)
+    assert torch.equal(zphi.abs(), z1.abs()) and torch.equal(zphi == 0, z1 == 0)
+    assert np.array_equal(host(zphi)[host(zphi) != 0], host(z1)[host(z1) != 0])
+
+
 # --------------------------------------------------- fused SwiGLU epilogue
 def _fused_and_unfused(data, K, Nh, res_in, res_out):
     """The chained path (gate and up products with bf16 Z, then the SwiGLU
