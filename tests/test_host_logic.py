@@ -18,7 +18,7 @@ def test_product_path_does_not_use_the_oracle():
             if f.endswith((".py", ".hip", ".h")):
                 text = open(os.path.join(root, f)).read()
                 # No import, load or call of the oracle (prose may name it).
-                assert not re.search(r"import\s+oracle|from\s+oracle|oracle\.|rfq_oracle|"
+                assert not re.search(r"import\s+oracle|from\s+oracle|oracle\.[A-Za-z_]|rfq_oracle|"
                                      r"oracle_[a-z]", text), os.path.join(root, f)
 
 
