@@ -1,13 +1,16 @@
 // RFQ product, large-tile kernel for K a multiple of 512 (Eq. 11, Algorithm 1
 // with phi = 1; phi = 0 without the residual operand).
 //
-// Output tile 128 x 256 per workgroup of 4 waves (2 x 2, each wave 64 x 128
-// = 2 x 4 fragments of 32 x 32), two workgroups per CU: each SIMD runs one
-// wave of each, so while one waits on LDS, global loads or its barrier the
-// other issues MFMAs (the workgroups' barriers are independent).  With one
-// 256 x 256 workgroup per CU every such wait idled the matrix core; this
-// layout moves a third more operand bytes from L2 per output (measured: 6%
-// faster on 4096 x 4096 x 12288).
+// Output tile 256 x 256 per workgroup of 8 waves (4 x 2, each wave 64 x 128
+// = 2 x 4 fragments of 32 x 32), one workgroup per CU and two waves per SIMD:
+// while one wave waits on LDS or global loads the other issues MFMAs.
+// (Measured on 4096 x 4096 x 12288, bit-identical outputs: 4 waves of
+// 128 x 128 with one wave per SIMD idled the matrix core on every wait; two
+// 4-wave 128 x 256 workgroups per CU were 5-6% faster than that; this layout,
+// which loads a quarter fewer operand bytes per output than the two
+// workgroups, is another 4% faster.  The cost of the global loads lies in the
+// load instructions themselves: pointing them at always-cached data does not
+// change the time.)
 //
 // Instruction: v_mfma_scale_f32_32x32x64_f8f6f4 with E2M1 operands: lane l
 // of an operand holds row (l mod 32) and 32 consecutive K values (one MX
@@ -25,7 +28,7 @@
 // the residual MFMA, which is the residual contraction sharing the weight
 // tile.
 //
-// Pipeline per stage st (two LDS stage buffers, one barrier per stage): the
+// Pipeline per stage st (two LDS stage buffers of 52 KiB, one barrier per stage): the
 // fragments of stage st are read from buffer st mod 2 and multiplied while
 // stage st+1, held in registers, is written to the other buffer (its previous
 // contents were last read before the barrier that ended stage st-1); then
@@ -60,10 +63,12 @@
 namespace rfq {
 namespace {
 
-constexpr int kBM = 128, kBN = 256;
-constexpr int kThreads = 256;                   // 4 waves
+constexpr int kBM = 256, kBN = 256;
+constexpr int kThreads = 512;                   // 8 waves, two per SIMD
 constexpr int kTM = 64, kTN = 128;              // wave sub-tile (2 x 2 waves)
 constexpr int kFM = kTM / 32, kFN = kTN / 32;   // 2 x 4 fragments of 32 x 32
+constexpr int kRPL = kThreads / 4;              // buffer rows per load step (4 chunks a row)
+constexpr int kWaveRows = kBM / kTM;            // waves along M
 constexpr int kStageK = 128;
 constexpr int kRowBytes = kStageK / 2;
 constexpr int kGroup = 4;
@@ -231,7 +236,7 @@ __device__ __forceinline__ void swiglu_epilogue(const v16f (&acc)[kFM][kFN], con
 // kPhiK reduction columns (a wave's rows by two stages).
 constexpr int kPhiRows = 64, kPhiK = 256;
 // LDS reserved for the two map rows of a workgroup (K up to 2^20).
-constexpr int kPhiMapMaxBytes = 2 * ((1 << 20) / kPhiK);
+constexpr int kPhiMapMaxBytes = kWaveRows * ((1 << 20) / kPhiK);
 
 template <bool RES, bool ZBF16, bool SWIGLU = false, bool HRES = false, bool PHI = false>
 __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
@@ -244,7 +249,7 @@ __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
   extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
 
   int tm, tn;
-  tile_coords<8>(blockIdx.x, (int)((M + kBM - 1) / kBM), (int)((N + kBN - 1) / kBN), tm, tn);
+  tile_coords<1024 / kBM>(blockIdx.x, (int)((M + kBM - 1) / kBM), (int)((N + kBN - 1) / kBN), tm, tn);
   const int64_t m0 = (int64_t)tm * kBM, n0 = (int64_t)tn * kBN;
 
   const int tid = threadIdx.x;
@@ -262,16 +267,16 @@ __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
                                cw = rsrc(wc, N * kbytes);
   const __amdgpu_buffer_rsrc_t sq = rsrc(qs, M * kblocks), sr = rsrc(RES ? rs : qs, M * kblocks),
                                sw = rsrc(ws, N * kblocks);
-  // Chunk u of this thread: buffer row trow + 64 u, chunk tid mod 4.
-  // Operand of buffer row block u (64 rows): 0 q, 1 r, 2 w.
-  auto op_of = [](int u) { return u < kBM / 64 ? 0 : (RES && u < 2 * kBM / 64 ? 1 : 2); };
-  uint32_t a_off[2], w_off[4];
+  // Chunk u of this thread: buffer row trow + kRPL u, chunk tid mod 4.
+  // Operand of buffer row block u (kRPL rows): 0 q, 1 r, 2 w.
+  auto op_of = [](int u) { return u * kRPL < kBM ? 0 : (RES && u * kRPL < 2 * kBM ? 1 : 2); };
+  uint32_t a_off[kBM / kRPL], w_off[kBN / kRPL];
 #pragma unroll
-  for (int u = 0; u < 2; ++u)
-    a_off[u] = (uint32_t)min(m0 + trow + 64 * u, M - 1) * (uint32_t)kbytes + tcol;
+  for (int u = 0; u < kBM / kRPL; ++u)
+    a_off[u] = (uint32_t)min(m0 + trow + kRPL * u, M - 1) * (uint32_t)kbytes + tcol;
 #pragma unroll
-  for (int u = 0; u < 4; ++u)
-    w_off[u] = (uint32_t)min(n0 + trow + 64 * u, N - 1) * (uint32_t)kbytes + tcol;
+  for (int u = 0; u < kBN / kRPL; ++u)
+    w_off[u] = (uint32_t)min(n0 + trow + kRPL * u, N - 1) * (uint32_t)kbytes + tcol;
 
   // Scale rows: buffer row min(tid + 256 v, kRows - 1); within a wave all
   // rows belong to one operand.
@@ -296,7 +301,7 @@ __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
 #pragma unroll
     for (int u = 0; u < L::kLoads; ++u) {
       const int o = op_of(u);
-      const uint32_t off = o == 2 ? w_off[u - L::kWRow / 64] : a_off[u % 2];
+      const uint32_t off = o == 2 ? w_off[u - L::kWRow / kRPL] : a_off[u % (kBM / kRPL)];
       pf[u] = __builtin_amdgcn_raw_buffer_load_b128(o == 0 ? cq : (o == 1 ? cr : cw), off,
                                                     st * kRowBytes, 0);
     }
@@ -313,7 +318,7 @@ __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
     uint8_t *b = smem + buf * L::kStageBytes;
 #pragma unroll
     for (int u = 0; u < L::kLoads; ++u)
-      *reinterpret_cast<u32x4 *>(b + chunk_off(trow + 64 * u, tid & 3)) = pf[u];
+      *reinterpret_cast<u32x4 *>(b + chunk_off(trow + kRPL * u, tid & 3)) = pf[u];
 #pragma unroll
     for (int v = 0; v < L::kScaleLoads; ++v)
       *reinterpret_cast<uint32_t *>(b + L::kDataBytes + 4 * sbr(v)) = grp[v][W];
@@ -387,13 +392,13 @@ __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
   using Rl = std::integral_constant<bool, true>;
   using NoRl = std::integral_constant<bool, false>;
 
-  // The fallback-indicator rows of this workgroup's two waves rows, copied
+  // The fallback-indicator rows of this workgroup's wave rows, copied
   // to LDS behind the stage buffers (the prologue's barrier publishes them).
   const int pcols = (int)((K + kPhiK - 1) / kPhiK);
   uint8_t *phi_lds = smem + L::kBytes;
   if constexpr (PHI) {
     const int64_t prow0 = m0 / kPhiRows, prows = (M + kPhiRows - 1) / kPhiRows;
-    for (int i = tid; i < 2 * pcols; i += kThreads) {
+    for (int i = tid; i < kWaveRows * pcols; i += kThreads) {
       const int64_t pr = prow0 + i / pcols;
       phi_lds[i] = pr < prows ? phi[pr * pcols + i % pcols] : (uint8_t)0;
     }
@@ -570,11 +575,11 @@ hipError_t launch(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc,
                   int64_t M, int64_t N, int64_t K, void *z, hipStream_t stream,
                   const SwigluOut &so = SwigluOut{}, const uint8_t *phi = nullptr) {
   using L = Layout<RES>;
-  static_assert(4 * Epi<ZBF16>::kWaveBytes <= L::kBytes, "epilogue staging fits");
+  static_assert((kThreads / 64) * Epi<ZBF16>::kWaveBytes <= L::kBytes, "epilogue staging fits");
   auto kern = rfq_gemm_large_kernel<RES, ZBF16, SWIGLU, HRES, PHI>;
   // LDS: the two stage buffers, then (PHI) two rows of the indicator map.
   constexpr int kMaxBytes = L::kBytes + (PHI ? kPhiMapMaxBytes : 0);
-  const int phi_bytes = PHI ? (int)(((2 * ((K + kPhiK - 1) / kPhiK)) + 15) / 16 * 16) : 0;
+  const int phi_bytes = PHI ? (int)(((kWaveRows * ((K + kPhiK - 1) / kPhiK)) + 15) / 16 * 16) : 0;
   static std::atomic<bool> attr_done{false};
   if (!attr_done.load(std::memory_order_acquire)) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
