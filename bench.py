@@ -9,10 +9,11 @@ Inputs are resident in HBM before the timed region; three input sets are
 rotated so that no step finds its inputs in the 256 MB last-level cache.
 
 value = executed FP4 flops of the step (4*M*N*K: the primary and the residual
-contraction) / step time.  The per-kernel durations come from HIP events
-recorded on the launch stream around every kernel of the timed steps; the
-roofline object reports the dominant kernel (the product) against the dense
-MXFP4 matrix-core peak.  The oracle (plain C) is timed on a bounded sample of
+contraction) / step time.  The product's duration comes from HIP events
+recorded on its launch stream around it in every timed step; the roofline
+object reports it (the dominant kernel) against the dense MXFP4 matrix-core
+peak.  The two quantizers are timed over back-to-back launches after the
+timed region.  The oracle (plain C) is timed on a bounded sample of
 the same step on the host cores.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
@@ -89,25 +90,25 @@ def main():
     stream = torch.cuda.current_stream()
 
     def step(i, ev=None):
+        """One pass of the path; with ev, HIP events bracket the product (the
+        roofline kernel) on its launch stream."""
         s = i % N_SETS
         o = outs[s]
-        if ev is not None:
-            ev[0].record(stream)
         rfq.rfq_quantize_weight(ws[s], out=(o["wc"], o["ws"]), stream=stream)
-        if ev is not None:
-            ev[1].record(stream)
         rfq.rfq_quantize_act(xs[s], out=o["q"], stream=stream)
         if ev is not None:
-            ev[2].record(stream)
+            ev[0].record(stream)
         rfq.rfq_gemm(*o["q"], o["wc"], o["ws"], out=o["z"], stream=stream)
         if ev is not None:
-            ev[3].record(stream)
+            ev[1].record(stream)
 
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
 
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    # Timed region: the K steps, with events only around each product (an
+    # event recorded between two kernels adds a few microseconds of its own).
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -118,9 +119,14 @@ def main():
     torch.cuda.synchronize()
     total_ms = t0.elapsed_time(t1)
     ms_step = total_ms / args.steps
-    wq_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
-    xq_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
-    gm_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+    gm_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+
+    # The two quantizers of the step, each timed over back-to-back launches
+    # on the same rotated inputs (outside the timed region).
+    wq_ms = _per_launch_ms(torch, stream, lambda i: rfq.rfq_quantize_weight(
+        ws[i % N_SETS], out=(outs[i % N_SETS]["wc"], outs[i % N_SETS]["ws"]), stream=stream), 30)
+    xq_ms = _per_launch_ms(torch, stream, lambda i: rfq.rfq_quantize_act(
+        xs[i % N_SETS], out=outs[i % N_SETS]["q"], stream=stream), 30)
 
     exec_flops = 4.0 * M * N * K
     # Operand and result bytes of one product: q, r and w codes and scales, bf16 Z.
