@@ -21,36 +21,6 @@ __device__ __forceinline__ uint32_t bf16_rne(float f) {
   return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
 }
 
-// Stores the four consecutive outputs Z[m][n .. n+3] a lane holds after a
-// 16x16 block-scaled MFMA (weights as the A operand).  Bounds: m < M is the
-// caller's; columns past N are dropped.
-template <bool ZBF16>
-__device__ __forceinline__ void store4(void *__restrict__ z, int64_t m, int64_t n,
-                                       int64_t N, bool vec_ok, const v4f &a) {
-  if constexpr (ZBF16) {
-    uint16_t *zp = reinterpret_cast<uint16_t *>(z) + m * N + n;
-    if (vec_ok && n + 3 < N) {
-      uint2 w;
-      w.x = bf16_rne(a[0]) | (bf16_rne(a[1]) << 16);
-      w.y = bf16_rne(a[2]) | (bf16_rne(a[3]) << 16);
-      *reinterpret_cast<uint2 *>(zp) = w;
-    } else {
-#pragma unroll
-      for (int v = 0; v < 4; ++v)
-        if (n + v < N) zp[v] = (uint16_t)bf16_rne(a[v]);
-    }
-  } else {
-    float *zp = reinterpret_cast<float *>(z) + m * N + n;
-    if (vec_ok && n + 3 < N) {
-      *reinterpret_cast<float4 *>(zp) = make_float4(a[0], a[1], a[2], a[3]);
-    } else {
-#pragma unroll
-      for (int v = 0; v < 4; ++v)
-        if (n + v < N) zp[v] = a[v];
-    }
-  }
-}
-
 // Output-tile order: tiles handed to one XCD (workgroups are dealt to the 8
 // XCDs round robin) are made contiguous, then walked in groups of GM tile
 // rows so that concurrently running tiles share operand rows in that XCD's L2.
