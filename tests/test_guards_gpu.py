@@ -1,0 +1,96 @@
+"""Out-of-bounds writes: every output buffer of every entry point sits between
+guard regions filled with a known byte pattern; after the call the guards must
+be intact.  Ragged shapes exercise the kernels' tail handling on both product
+kernels."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2608_26581_amd as rfq
+from paper_2608_26581_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+GUARD = 4096          # bytes on each side (keeps 16-byte alignment)
+PATTERN = 0xA5
+
+
+class Guarded:
+    """A device tensor of `shape` and `dtype` inside a larger byte buffer."""
+
+    def __init__(self, shape, dtype):
+        n = int(np.prod(shape)) * torch.tensor([], dtype=dtype).element_size()
+        self.n = n
+        self.raw = torch.full((n + 2 * GUARD,), PATTERN, dtype=torch.uint8, device="cuda")
+        self.t = self.raw[GUARD:GUARD + n].view(dtype).view(*shape)
+
+    def check(self, what):
+        torch.cuda.synchronize()
+        head = self.raw[:GUARD].cpu().numpy()
+        tail = self.raw[GUARD + self.n:].cpu().numpy()
+        assert np.all(head == PATTERN), "%s: write before the buffer" % what
+        assert np.all(tail == PATTERN), "%s: write past the buffer" % what
+
+
+def _codes(rows, K):
+    return [Guarded((rows, K // 2), torch.uint8), Guarded((rows, K // 32), torch.uint8)]
+
+
+def _check_all(bufs, what):
+    for i, b in enumerate(bufs):
+        b.check("%s[%d]" % (what, i))
+
+
+@pytest.mark.parametrize("M,N,K", [(131, 97, 512), (131, 97, 96), (1, 1, 1024), (257, 300, 1536)])
+def test_outputs_stay_in_bounds(M, N, K):
+    w = wl.WORKLOADS["qwen"].scaled(M=M, K=K, weights=(("w", K, N),))
+    data = wl.generate(w, seed=31)
+    x = torch.from_numpy(data["x"]).cuda()
+    xb = torch.from_numpy(data["x_bf16"].view(np.int16)).cuda().view(torch.bfloat16)
+    for xin, tag in ((x, "fp32"), (xb, "bf16")):
+        qb = _codes(M, K) + _codes(M, K)
+        rfq.rfq_quantize_act(xin, out=[b.t for b in qb])
+        _check_all(qb, "quantize_act %s" % tag)
+    q = [b.t for b in qb]
+    wb = _codes(N, K)
+    rfq.rfq_quantize_weight(torch.from_numpy(data["w"]).cuda(), out=[b.t for b in wb])
+    _check_all(wb, "quantize_weight")
+    wq = [b.t for b in wb]
+    for dt in (torch.float32, torch.bfloat16):
+        zb = Guarded((M, N), dt)
+        rfq.rfq_gemm(*q, *wq, out=zb.t)
+        zb.check("gemm %s" % dt)
+        zb = Guarded((M, N), dt)
+        rfq.rfq_gemm(q[0], q[1], None, None, *wq, out=zb.t)
+        zb.check("gemm plain %s" % dt)
+    phi_shape = ((M + 63) // 64, (K + 255) // 256)
+    pb = Guarded(phi_shape, torch.uint8)
+    rfq.rfq_fallback_map(None, q[1], rfq.RFQ_PHI_SCALE_AT_LEAST, 128, out=pb.t)
+    pb.check("fallback_map scale")
+    pb2 = Guarded(phi_shape, torch.uint8)
+    rfq.rfq_fallback_map(q[2], q[1], rfq.RFQ_PHI_RESIDUAL_NONZERO, out=pb2.t)
+    pb2.check("fallback_map residual")
+    zb = Guarded((M, N), torch.bfloat16)
+    rfq.rfq_gemm_phi(*q, *wq, pb.t, out=zb.t)
+    zb.check("gemm_phi")
+    db = Guarded((M, K), torch.float32)
+    rfq.rfq_dequant(q[0], q[1], out=db.t)
+    db.check("dequant")
+
+
+@pytest.mark.parametrize("M,Nh,K", [(131, 96, 512), (3, 32, 1024)])
+def test_swiglu_outputs_stay_in_bounds(M, Nh, K):
+    rng = np.random.default_rng(M)
+    g = torch.from_numpy(rng.standard_normal((M, Nh)).astype(np.float32)).cuda()
+    u = torch.from_numpy(rng.standard_normal((M, Nh)).astype(np.float32)).cuda()
+    hb = _codes(M, Nh) + _codes(M, Nh)
+    rfq.rfq_swiglu_quantize_act(g.to(torch.bfloat16), u.to(torch.bfloat16),
+                                out=[b.t for b in hb])
+    _check_all(hb, "swiglu_quantize")
+    x = torch.from_numpy(rng.standard_normal((M, K)).astype(np.float32)).cuda()
+    q = rfq.rfq_quantize_act(x)
+    wgu = rfq.rfq_quantize_weight(torch.from_numpy(
+        rng.normal(0, 0.02, (2 * Nh, K)).astype(np.float32)).cuda())
+    fb = _codes(M, Nh) + _codes(M, Nh)
+    rfq.rfq_gemm_swiglu_quantize(*q, *wgu, out=[b.t for b in fb])
+    _check_all(fb, "gemm_swiglu_quantize")
