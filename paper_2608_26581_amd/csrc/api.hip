@@ -15,7 +15,7 @@
 namespace {
 
 constexpr int kAbiVersion = 1;
-constexpr int kMaxDevices = 64;
+using rfq::kMaxDevices;
 
 // Per-device result of the architecture check: 0 unknown, 1 gfx950, 2 other.
 std::atomic<int> g_arch_state[kMaxDevices];

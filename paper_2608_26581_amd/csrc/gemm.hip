@@ -300,16 +300,11 @@ hipError_t launch_tile(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc,
   auto kern = rfq_gemm_kernel<BM, BN, RES, ZBF16, PHI>;
   constexpr int kMaxBytes = S::kBytes + (PHI ? kPhiMapMaxBytes : 0);
   const int phi_bytes = PHI ? (int)((2 * ((K + kStageK - 1) / kStageK) + 15) / 16 * 16) : 0;
-  // The dynamic-LDS limit is an attribute of the kernel function; setting it
-  // twice from racing threads is harmless.
-  static std::atomic<bool> attr_done{false};
-  if (!attr_done.load(std::memory_order_acquire)) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       kMaxBytes);
-    if (e != hipSuccess) return e;
-    attr_done.store(true, std::memory_order_release);
-  }
+  // The dynamic-LDS limit is an attribute of the kernel function, set once
+  // per device; setting it twice from racing threads is harmless.
+  static std::atomic<bool> attr_done[kMaxDevices];
+  const hipError_t e = set_lds_limit(attr_done, reinterpret_cast<const void *>(kern), kMaxBytes);
+  if (e != hipSuccess) return e;
   const int64_t ntiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
   kern<<<dim3((unsigned)ntiles), dim3(256), S::kBytes + phi_bytes, stream>>>(
       qc, qs, rc, rs, wc, ws, M, N, K, z, phi);

@@ -580,13 +580,9 @@ hipError_t launch(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc,
   // LDS: the two stage buffers, then (PHI) two rows of the indicator map.
   constexpr int kMaxBytes = L::kBytes + (PHI ? kPhiMapMaxBytes : 0);
   const int phi_bytes = PHI ? (int)(((kWaveRows * ((K + kPhiK - 1) / kPhiK)) + 15) / 16 * 16) : 0;
-  static std::atomic<bool> attr_done{false};
-  if (!attr_done.load(std::memory_order_acquire)) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, kMaxBytes);
-    if (e != hipSuccess) return e;
-    attr_done.store(true, std::memory_order_release);
-  }
+  static std::atomic<bool> attr_done[kMaxDevices];
+  const hipError_t e = set_lds_limit(attr_done, reinterpret_cast<const void *>(kern), kMaxBytes);
+  if (e != hipSuccess) return e;
   const int64_t ntiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
   kern<<<dim3((unsigned)ntiles), dim3(kThreads), L::kBytes + phi_bytes, stream>>>(
       qc, qs, rc, rs, wc, ws, M, N, K, z, so, phi);

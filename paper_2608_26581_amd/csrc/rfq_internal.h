@@ -4,7 +4,28 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 namespace rfq {
+
+// Devices the library tracks (the C ABI rejects higher device indices).
+constexpr int kMaxDevices = 64;
+
+// Raises a kernel's dynamic-LDS limit to `bytes` on the current device, once
+// per device (`done` is the caller's per-kernel flag array).
+inline hipError_t set_lds_limit(std::atomic<bool> (&done)[kMaxDevices], const void *kern,
+                                int bytes) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  if (!done[dev].load(std::memory_order_acquire)) {
+    e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    if (e != hipSuccess) return e;
+    done[dev].store(true, std::memory_order_release);
+  }
+  return hipSuccess;
+}
 
 // Elements handled by one thread of the streaming kernels (a quarter block).
 constexpr int kChunk = 8;
