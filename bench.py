@@ -33,7 +33,7 @@ if REPO not in sys.path:
 PEAK_FP4_TFLOPS = 10100.0     # MI355X dense MXFP4 matrix cores
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 N_SETS = 3
-Q_SETS = 6
+Q_SETS = 9                    # 9 x 64 MiB quantizer inputs: over twice the 256 MB last-level cache
 PHI_MARGIN = 4                # scale-threshold phi: median primary scale byte + 4
 METRIC = "RFQ-MXFP4 GEMM TFLOP/s + quantizer GB/s (Qwen3-VL-like 4096×4096×12288)"
 
@@ -140,7 +140,7 @@ def main():
 
     # ---- quantizer alone on the 8192x4096 bf16 workload (pure bandwidth)
     qk = wl.WORKLOADS["quant"]
-    # Six 64 MiB inputs (rows of one draw rotated on the device) so that no
+    # Q_SETS 64 MiB inputs (rows of one draw rotated on the device) so that no
     # launch finds its input in the 256 MB last-level cache.
     d = wl.generate(qk, seed=100)
     x0 = torch.from_numpy(d["x_bf16"].view(np.int16)).to(dev).view(torch.bfloat16)
