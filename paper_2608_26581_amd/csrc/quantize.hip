@@ -2,19 +2,23 @@
 // code, Eq. 8, plus the quantized residual, Eq. 9-10), the weight quantizer,
 // the fused SwiGLU + quantizer and dequantization (Eq. 12).
 //
-// Work decomposition: the tensor is treated as a flat array (K is a multiple
-// of 32, so no MX block straddles a row and the scale index of a block is its
-// flat block index).  One thread owns 8 consecutive elements; the four lanes
-// of a DPP quad own one 32-element block, so the block maximum takes two
-// quad-permute steps and no LDS.  A wave owns a span of 64 consecutive blocks
-// and walks it in 4 steps; in step u the 16-lane row r holds blocks
-// 16r + 4u .. 16r + 4u + 3, so every load of a row is 256 contiguous bytes
-// and, after the steps, the row's 16 scale bytes are contiguous: two DPP
-// row shifts gather a step's 4 bytes into the row's first lane, which then
-// writes all 16 with one store (64 bytes per wave).  All loads are issued
-// before any arithmetic.  bf16 inputs are read non-temporally; stores are
-// plain (measured: non-temporal stores of these partial lines cost about a
-// fifth more write traffic, and non-temporal fp32 loads were slower).
+// Work decomposition of the quantizers: the tensor is treated as a flat array
+// (K is a multiple of 32, so no MX block straddles a row and the scale index
+// of a block is its flat block index).  A wave owns a span of 64 consecutive
+// blocks.  Every load instruction of the wave reads 1 KB of contiguous input,
+// 16 bytes per lane: 8 bf16 elements (4 lanes per block, 4 steps per span) or
+// 4 fp32 elements (8 lanes per block, 8 steps).  The block maximum is a DPP
+// max over the block's lanes.  Each step writes its codes and scale bytes into
+// a wave-private LDS area in the tensor's own order; after the last step each
+// lane reads back the 16 code bytes of one block, so every code store of the
+// wave writes 1 KB of contiguous codes with 16-byte stores, and the 64 scale
+// bytes of a span leave as four 16-byte stores.  Inputs are read
+// non-temporally.  Stores are non-temporal when the whole job moves more bytes
+// than the 256 MB last-level cache holds, and plain otherwise (measured on
+// MI355X: plain stores are slightly faster while everything fits, leaving the
+// codes cached for the product that reads them next; streaming stores are 5-7%
+// faster on larger jobs).  This layout runs 8-10% faster than one that stored
+// 4 code bytes per lane straight from registers (64-byte pieces per store).
 //
 // Element arithmetic (scale byte, scaled FP4 conversions, SwiGLU) comes from
 // mx_device.h.  The residual x - deq(q) is exact in fp32 (a nonzero E2M1
@@ -30,194 +34,183 @@ namespace rfq {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kUnroll = 4;   // steps per wave span of 64 blocks (4 blocks per row)
-
-// Maximum over the four lanes of a quad (DPP quad_perm 1,0,3,2 then 2,3,0,1).
-__device__ __forceinline__ float quad_max(float v) {
-  float o = __int_as_float(
-      __builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
-  v = fmaxf(v, o);
-  o = __int_as_float(
-      __builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));
-  return fmaxf(v, o);
-}
-
-__device__ __forceinline__ float absmax8(const float (&v)[8]) {
-  float a = fmaxf(fabsf(v[0]), fabsf(v[1]));
-  a = fmaxf(a, fmaxf(fabsf(v[2]), fabsf(v[3])));
-  a = fmaxf(a, fmaxf(fabsf(v[4]), fabsf(v[5])));
-  return fmaxf(a, fmaxf(fabsf(v[6]), fabsf(v[7])));
-}
-
-// Quantize the 8 values a thread owns: primary code and scale byte and, with
-// RES, the residual code and scale byte.  All four quad lanes must call it.
-template <bool RES>
-__device__ __forceinline__ void quantize8(const float (&v)[8], uint32_t &qc,
-                                          uint32_t &qb, uint32_t &rc,
-                                          uint32_t &rb) {
-  qb = scale_byte(quad_max(absmax8(v)));
-  const float qs = scale_operand(qb);
-  qc = encode8(v, qs);
-  if constexpr (RES) {
-    float d[8], r[8];
-    decode8(qc, qs, d);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) r[i] = v[i] - d[i];
-    rb = scale_byte(quad_max(absmax8(r)));
-    rc = encode8(r, scale_operand(rb));
-  }
-}
+constexpr int kSpanBlocks = 64;                       // blocks per wave span
+constexpr int kSpanCodeBytes = kSpanBlocks * kBlock / 2;
+constexpr int64_t kLastLevelCacheBytes = int64_t(256) << 20;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-static_assert(kUnroll == 4, "a wave span is 16 rows of 4 steps");
 
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
+// Maximum over aligned groups of G lanes (G = 4: quad_perm 1,0,3,2 and
+// 2,3,0,1; G = 8 adds row_half_mirror, which pairs lane i with 7 - i).
+template <int G>
+__device__ __forceinline__ float group_max(float v) {
+  v = fmaxf(v, dpp_f<0xB1>(v));
+  v = fmaxf(v, dpp_f<0x4E>(v));
+  if constexpr (G == 8) v = fmaxf(v, dpp_f<0x141>(v));
+  return v;
+}
+
+template <int E>
+__device__ __forceinline__ float absmax(const float (&v)[E]) {
+  float a = fabsf(v[0]);
+#pragma unroll
+  for (int i = 1; i < E; ++i) a = fmaxf(a, fabsf(v[i]));
+  return a;
+}
+
+template <int E>
+__device__ __forceinline__ uint32_t encode(const float (&v)[E], float s) {
+  if constexpr (E == 8) return encode8(v, s);
+  else return encode4(v[0], v[1], v[2], v[3], s);
+}
+
+template <int E>
+__device__ __forceinline__ void decode(uint32_t c, float s, float (&d)[E]) {
+  if constexpr (E == 8) decode8(c, s, d);
+  else decode4(c, s, d);
+}
+
+template <bool NT>
+__device__ __forceinline__ void store16(uint8_t *p, const u32x4 &v) {
+  if constexpr (NT) __builtin_nontemporal_store(v, reinterpret_cast<u32x4 *>(p));
+  else *reinterpret_cast<u32x4 *>(p) = v;
+}
+
+// Elements of one 16-byte input unit.
 template <bool BF16_IN>
-__device__ __forceinline__ void load8(const void *__restrict__ x, int64_t chunk,
-                                      float (&v)[8]) {
+__device__ __forceinline__ void unpack(const u32x4 &w, float (&v)[BF16_IN ? 8 : 4]) {
   if constexpr (BF16_IN) {
-    const u32x4 w = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(x) + chunk);
     v[0] = __uint_as_float(w.x << 16); v[1] = __uint_as_float(w.x & 0xFFFF0000u);
     v[2] = __uint_as_float(w.y << 16); v[3] = __uint_as_float(w.y & 0xFFFF0000u);
     v[4] = __uint_as_float(w.z << 16); v[5] = __uint_as_float(w.z & 0xFFFF0000u);
     v[6] = __uint_as_float(w.w << 16); v[7] = __uint_as_float(w.w & 0xFFFF0000u);
   } else {
-    const u32x4 *p = reinterpret_cast<const u32x4 *>(x) + 2 * chunk;
-    const u32x4 a = p[0];
-    const u32x4 b = p[1];
-    v[0] = __uint_as_float(a.x); v[1] = __uint_as_float(a.y);
-    v[2] = __uint_as_float(a.z); v[3] = __uint_as_float(a.w);
-    v[4] = __uint_as_float(b.x); v[5] = __uint_as_float(b.y);
-    v[6] = __uint_as_float(b.z); v[7] = __uint_as_float(b.w);
+    v[0] = __uint_as_float(w.x); v[1] = __uint_as_float(w.y);
+    v[2] = __uint_as_float(w.z); v[3] = __uint_as_float(w.w);
   }
 }
 
-// Chunk (8 elements) of lane `lane` in step u of a wave span of 64 blocks:
-// block 16r + 4u + q, elements 8j .. 8j+7 of it (lane = 16r + 4q + j).
-__device__ __forceinline__ int span_chunk(int lane, int u) {
-  return 4 * (16 * (lane >> 4) + 4 * u + ((lane >> 2) & 3)) + (lane & 3);
-}
+// Wave-private staging of one code stream: the span's codes in tensor order,
+// then its scale bytes.
+struct Stage {
+  uint8_t codes[kSpanCodeBytes];
+  uint8_t scales[kSpanBlocks];
+};
 
-// Collects the scale bytes of the four quads of a 16-lane row into the
-// row's first lane (byte q from quad q).
-__device__ __forceinline__ uint32_t gather_row4(uint32_t b) {
-  const uint32_t t = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)b, 0x104, 0xF, 0xF, false);
-  const uint32_t v = b | (t << 8);                                  // row_shl:4
-  const uint32_t t2 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x108, 0xF, 0xF, false);
-  return v | (t2 << 16);                                            // row_shl:8
-}
-
-// Writes the scale bytes of a wave span: sw[u] holds, in the first lane of
-// row r, the bytes of blocks 16r + 4u .. +3.  Full spans with an aligned
-// tensor use one 16-byte store per row; otherwise each quad leader writes its
-// own byte (bytes[u] in every lane of the quad).
-__device__ __forceinline__ void store_span_scales(uint8_t *__restrict__ scales,
-                                                  int64_t span_block0, int64_t nblocks,
-                                                  int lane, const uint32_t (&sw)[4],
-                                                  const uint32_t (&bytes)[4]) {
-  const bool full = span_block0 + 64 <= nblocks &&
-                    (reinterpret_cast<uintptr_t>(scales) & 15) == 0;
-  if (full) {
-    if ((lane & 15) == 0) {
-      u32x4 w = {sw[0], sw[1], sw[2], sw[3]};
-      *reinterpret_cast<u32x4 *>(scales + span_block0 + (lane & 48)) = w;
-    }
-  } else if ((lane & 3) == 0) {
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int64_t b = span_block0 + 16 * (lane >> 4) + 4 * u + ((lane >> 2) & 3);
-      if (b < nblocks) scales[b] = (uint8_t)bytes[u];
-    }
-  }
-}
-
-template <bool BF16_IN, bool RES>
+// Quantizer kernel (SWIGLU: the input is h = bf16(silu(g) u) of g = x and
+// u = x2, optionally written to h_out).  nblocks = elements / 32.
+template <bool BF16_IN, bool RES, bool NT_STORE, bool SWIGLU>
 __global__ __launch_bounds__(kThreads) void quantize_kernel(
-    const void *__restrict__ x, int64_t nchunks, uint32_t *__restrict__ q_codes,
-    uint8_t *__restrict__ q_scales, uint32_t *__restrict__ r_codes,
-    uint8_t *__restrict__ r_scales) {
-  const int lane = threadIdx.x & 63;
-  const int64_t span0 = ((int64_t)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6)) * 256;
-  float v[kUnroll][8];
-#pragma unroll
-  for (int u = 0; u < kUnroll; ++u) {
-    // Lanes past the end load the last chunk (never out of bounds) and skip
-    // their stores; nchunks is a multiple of 4, so quads stay whole.
-    const int64_t ch = span0 + span_chunk(lane, u);
-    load8<BF16_IN>(x, ch < nchunks ? ch : nchunks - 1, v[u]);
-  }
-  uint32_t qsw[kUnroll], rsw[kUnroll], qbytes[kUnroll], rbytes[kUnroll];
-#pragma unroll
-  for (int u = 0; u < kUnroll; ++u) {
-    const int64_t ch = span0 + span_chunk(lane, u);
-    uint32_t qc, qb, rc = 0, rb = 0;
-    quantize8<RES>(v[u], qc, qb, rc, rb);
-    qbytes[u] = qb;
-    qsw[u] = gather_row4(qb);
-    if constexpr (RES) {
-      rbytes[u] = rb;
-      rsw[u] = gather_row4(rb);
-    }
-    if (ch < nchunks) {
-      q_codes[ch] = qc;
-      if constexpr (RES) r_codes[ch] = rc;
-    }
-  }
-  const int64_t nblocks = nchunks >> 2;
-  store_span_scales(q_scales, span0 >> 2, nblocks, lane, qsw, qbytes);
-  if constexpr (RES) store_span_scales(r_scales, span0 >> 2, nblocks, lane, rsw, rbytes);
-}
+    const void *__restrict__ x, const void *__restrict__ x2, int64_t nblocks,
+    uint8_t *__restrict__ q_codes, uint8_t *__restrict__ q_scales,
+    uint8_t *__restrict__ r_codes, uint8_t *__restrict__ r_scales,
+    uint16_t *__restrict__ h_out) {
+  constexpr int kE = BF16_IN ? 8 : 4;             // elements per lane and step
+  constexpr int kLanesPerBlock = kBlock / kE;
+  constexpr int kSteps = kSpanBlocks * kLanesPerBlock / 64;
+  constexpr int kCodeBytes = kE / 2;              // per lane and step
+  __shared__ Stage stage[kThreads / 64][RES ? 2 : 1];
 
-template <bool BF16_IN, bool RES>
-__global__ __launch_bounds__(kThreads) void swiglu_quantize_kernel(
-    const void *__restrict__ g, const void *__restrict__ u, int64_t nchunks,
-    uint32_t *__restrict__ q_codes, uint8_t *__restrict__ q_scales,
-    uint32_t *__restrict__ r_codes, uint8_t *__restrict__ r_scales,
-    u32x4 *__restrict__ h_out) {
-  const int lane = threadIdx.x & 63;
-  const int64_t span0 = ((int64_t)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6)) * 256;
-  float gv[kUnroll][8], uv[kUnroll][8];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t blk0 = ((int64_t)blockIdx.x * (kThreads / 64) + wave) * kSpanBlocks;
+  const int64_t nunits = nblocks * kLanesPerBlock;   // 16-byte input units
+  const u32x4 *xin = reinterpret_cast<const u32x4 *>(x);
+  const u32x4 *xin2 = reinterpret_cast<const u32x4 *>(x2);
+
+  // Unit of (step u, lane): blk0 * kLanesPerBlock + 64 u + lane.  Lanes past
+  // the end load the last unit (never out of bounds); their blocks are not
+  // stored, and a block is either wholly inside or wholly past the end.
+  u32x4 in[kSteps], in2[SWIGLU ? kSteps : 1];
 #pragma unroll
-  for (int i = 0; i < kUnroll; ++i) {
-    const int64_t ch = span0 + span_chunk(lane, i);
-    const int64_t c = ch < nchunks ? ch : nchunks - 1;
-    load8<BF16_IN>(g, c, gv[i]);
-    load8<BF16_IN>(u, c, uv[i]);
+  for (int u = 0; u < kSteps; ++u) {
+    int64_t unit = blk0 * kLanesPerBlock + 64 * u + lane;
+    unit = unit < nunits ? unit : nunits - 1;
+    in[u] = __builtin_nontemporal_load(xin + unit);
+    if constexpr (SWIGLU) in2[u] = __builtin_nontemporal_load(xin2 + unit);
   }
-  uint32_t qsw[kUnroll], rsw[kUnroll], qbytes[kUnroll], rbytes[kUnroll];
+
+  Stage &sq = stage[wave][0];
+  Stage &sr = stage[wave][RES ? 1 : 0];
 #pragma unroll
-  for (int i = 0; i < kUnroll; ++i) {
-    const int64_t ch = span0 + span_chunk(lane, i);
-    float h[8];
-    uint32_t hb[8];
+  for (int u = 0; u < kSteps; ++u) {
+    const int64_t unit = blk0 * kLanesPerBlock + 64 * u + lane;
+    float v[kE];
+    if constexpr (SWIGLU) {
+      float g[kE], w[kE];
+      uint32_t hb[kE];
+      unpack<BF16_IN>(in[u], g);
+      unpack<BF16_IN>(in2[u], w);
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      hb[j] = swiglu_bits(gv[i][j], uv[i][j]);
-      h[j] = __uint_as_float(hb[j]);
-    }
-    uint32_t qc, qb, rc = 0, rb = 0;
-    quantize8<RES>(h, qc, qb, rc, rb);
-    qbytes[i] = qb;
-    qsw[i] = gather_row4(qb);
-    if constexpr (RES) {
-      rbytes[i] = rb;
-      rsw[i] = gather_row4(rb);
-    }
-    if (ch < nchunks) {
-      q_codes[ch] = qc;
-      if constexpr (RES) r_codes[ch] = rc;
-      if (h_out) {
-        u32x4 w;
-        w.x = (hb[0] >> 16) | hb[1];
-        w.y = (hb[2] >> 16) | hb[3];
-        w.z = (hb[4] >> 16) | hb[5];
-        w.w = (hb[6] >> 16) | hb[7];
-        h_out[ch] = w;
+      for (int j = 0; j < kE; ++j) {
+        hb[j] = swiglu_bits(g[j], w[j]);
+        v[j] = __uint_as_float(hb[j]);
       }
+      if (h_out && unit < nunits) {
+        uint32_t p[kE / 2];
+#pragma unroll
+        for (int j = 0; j < kE / 2; ++j) p[j] = (hb[2 * j] >> 16) | (hb[2 * j + 1] & 0xFFFF0000u);
+        if constexpr (BF16_IN)
+          *reinterpret_cast<u32x4 *>(h_out + kE * unit) = u32x4{p[0], p[1], p[2], p[3]};
+        else
+          *reinterpret_cast<uint2 *>(h_out + kE * unit) = make_uint2(p[0], p[1]);
+      }
+    } else {
+      unpack<BF16_IN>(in[u], v);
+    }
+    const int pos = 64 * u + lane;                 // lane-unit within the span
+    const int sblk = pos / kLanesPerBlock;         // block within the span
+    const bool leader = (lane & (kLanesPerBlock - 1)) == 0;
+
+    const uint32_t qb = scale_byte(group_max<kLanesPerBlock>(absmax(v)));
+    const float qsc = scale_operand(qb);
+    const uint32_t qc = encode(v, qsc);
+    if constexpr (kCodeBytes == 4) *reinterpret_cast<uint32_t *>(sq.codes + 4 * pos) = qc;
+    else *reinterpret_cast<uint16_t *>(sq.codes + 2 * pos) = (uint16_t)qc;
+    if (leader) sq.scales[sblk] = (uint8_t)qb;
+    if constexpr (RES) {
+      float d[kE], r[kE];
+      decode(qc, qsc, d);
+#pragma unroll
+      for (int j = 0; j < kE; ++j) r[j] = v[j] - d[j];
+      const uint32_t rb = scale_byte(group_max<kLanesPerBlock>(absmax(r)));
+      const uint32_t rc = encode(r, scale_operand(rb));
+      if constexpr (kCodeBytes == 4) *reinterpret_cast<uint32_t *>(sr.codes + 4 * pos) = rc;
+      else *reinterpret_cast<uint16_t *>(sr.codes + 2 * pos) = (uint16_t)rc;
+      if (leader) sr.scales[sblk] = (uint8_t)rb;
     }
   }
-  const int64_t nblocks = nchunks >> 2;
-  store_span_scales(q_scales, span0 >> 2, nblocks, lane, qsw, qbytes);
-  if constexpr (RES) store_span_scales(r_scales, span0 >> 2, nblocks, lane, rsw, rbytes);
+  // The staging area is private to the wave and LDS serves a wave's
+  // accesses in order, so no workgroup barrier is needed.
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+
+  const int64_t b = blk0 + lane;                   // block stored by this lane
+  const u32x4 cq = *reinterpret_cast<const u32x4 *>(sq.codes + 16 * lane);
+  if (b < nblocks) store16<NT_STORE>(q_codes + 16 * b, cq);
+  if constexpr (RES) {
+    const u32x4 cr = *reinterpret_cast<const u32x4 *>(sr.codes + 16 * lane);
+    if (b < nblocks) store16<NT_STORE>(r_codes + 16 * b, cr);
+  }
+  const bool vec = blk0 + kSpanBlocks <= nblocks &&
+                   ((reinterpret_cast<uintptr_t>(q_scales) |
+                     reinterpret_cast<uintptr_t>(RES ? r_scales : q_scales)) & 15) == 0;
+  if (vec) {
+    // Lanes 0-3: primary scale bytes, lanes 4-7: residual, 16 each.
+    if (lane < 4)
+      store16<NT_STORE>(q_scales + blk0 + 16 * lane,
+                        *reinterpret_cast<const u32x4 *>(sq.scales + 16 * lane));
+    else if (RES && lane < 8)
+      store16<NT_STORE>(r_scales + blk0 + 16 * (lane - 4),
+                        *reinterpret_cast<const u32x4 *>(sr.scales + 16 * (lane - 4)));
+  } else if (b < nblocks) {
+    q_scales[b] = sq.scales[lane];
+    if constexpr (RES) r_scales[b] = sr.scales[lane];
+  }
 }
 
 __global__ __launch_bounds__(kThreads) void dequant_kernel(
@@ -265,8 +258,28 @@ __global__ __launch_bounds__(kThreads) void fallback_map_kernel(
   if (tid == 0) phi[blockIdx.x] = (uint8_t)(flag != 0);
 }
 
-inline unsigned grid_for(int64_t nchunks, int64_t per_block) {
-  return (unsigned)((nchunks + per_block - 1) / per_block);
+inline unsigned grid_for(int64_t n, int64_t per_block) {
+  return (unsigned)((n + per_block - 1) / per_block);
+}
+
+// Streaming stores once the job's traffic exceeds the last-level cache.
+inline bool nt_stores(int64_t nelem, int64_t in_bytes_per_elem, bool res) {
+  const int64_t bytes = nelem * in_bytes_per_elem + (res ? 2 : 1) * (nelem / 2 + nelem / 32);
+  return bytes > kLastLevelCacheBytes;
+}
+
+template <bool BF16_IN, bool RES, bool SWIGLU>
+hipError_t launch_q(const void *x, const void *x2, int64_t nelem, bool nt, uint8_t *qc,
+                    uint8_t *qs, uint8_t *rc, uint8_t *rs, uint16_t *h, hipStream_t stream) {
+  const int64_t nblocks = nelem / kBlock;
+  const dim3 grid(grid_for(nblocks, (kThreads / 64) * kSpanBlocks)), block(kThreads);
+  if (nt)
+    quantize_kernel<BF16_IN, RES, true, SWIGLU><<<grid, block, 0, stream>>>(x, x2, nblocks, qc, qs,
+                                                                           rc, rs, h);
+  else
+    quantize_kernel<BF16_IN, RES, false, SWIGLU><<<grid, block, 0, stream>>>(x, x2, nblocks, qc, qs,
+                                                                            rc, rs, h);
+  return hipGetLastError();
 }
 
 }  // namespace
@@ -275,22 +288,20 @@ hipError_t launch_quantize(const void *x, bool bf16_in, int64_t nelem,
                            uint8_t *q_codes, uint8_t *q_scales,
                            uint8_t *r_codes, uint8_t *r_scales,
                            hipStream_t stream) {
-  const int64_t nchunks = nelem / kChunk;
-  const dim3 grid(grid_for(nchunks, kThreads * kUnroll)), block(kThreads);
-  uint32_t *qc = reinterpret_cast<uint32_t *>(q_codes);
-  uint32_t *rc = reinterpret_cast<uint32_t *>(r_codes);
+  const bool res = r_codes != nullptr;
+  const bool nt = nt_stores(nelem, bf16_in ? 2 : 4, res);
   if (bf16_in) {
-    if (r_codes)
-      quantize_kernel<true, true><<<grid, block, 0, stream>>>(x, nchunks, qc, q_scales, rc, r_scales);
-    else
-      quantize_kernel<true, false><<<grid, block, 0, stream>>>(x, nchunks, qc, q_scales, rc, r_scales);
-  } else {
-    if (r_codes)
-      quantize_kernel<false, true><<<grid, block, 0, stream>>>(x, nchunks, qc, q_scales, rc, r_scales);
-    else
-      quantize_kernel<false, false><<<grid, block, 0, stream>>>(x, nchunks, qc, q_scales, rc, r_scales);
+    if (res)
+      return launch_q<true, true, false>(x, nullptr, nelem, nt, q_codes, q_scales, r_codes,
+                                         r_scales, nullptr, stream);
+    return launch_q<true, false, false>(x, nullptr, nelem, nt, q_codes, q_scales, nullptr,
+                                        nullptr, nullptr, stream);
   }
-  return hipGetLastError();
+  if (res)
+    return launch_q<false, true, false>(x, nullptr, nelem, nt, q_codes, q_scales, r_codes,
+                                        r_scales, nullptr, stream);
+  return launch_q<false, false, false>(x, nullptr, nelem, nt, q_codes, q_scales, nullptr,
+                                       nullptr, nullptr, stream);
 }
 
 hipError_t launch_swiglu_quantize(const void *g, const void *u, bool bf16_in,
@@ -298,23 +309,20 @@ hipError_t launch_swiglu_quantize(const void *g, const void *u, bool bf16_in,
                                   uint8_t *q_scales, uint8_t *r_codes,
                                   uint8_t *r_scales, uint16_t *h_out,
                                   hipStream_t stream) {
-  const int64_t nchunks = nelem / kChunk;
-  const dim3 grid(grid_for(nchunks, kThreads * kUnroll)), block(kThreads);
-  uint32_t *qc = reinterpret_cast<uint32_t *>(q_codes);
-  uint32_t *rc = reinterpret_cast<uint32_t *>(r_codes);
-  u32x4 *h = reinterpret_cast<u32x4 *>(h_out);
+  const bool res = r_codes != nullptr;
+  const bool nt = nt_stores(nelem, bf16_in ? 4 : 8, res);
   if (bf16_in) {
-    if (r_codes)
-      swiglu_quantize_kernel<true, true><<<grid, block, 0, stream>>>(g, u, nchunks, qc, q_scales, rc, r_scales, h);
-    else
-      swiglu_quantize_kernel<true, false><<<grid, block, 0, stream>>>(g, u, nchunks, qc, q_scales, rc, r_scales, h);
-  } else {
-    if (r_codes)
-      swiglu_quantize_kernel<false, true><<<grid, block, 0, stream>>>(g, u, nchunks, qc, q_scales, rc, r_scales, h);
-    else
-      swiglu_quantize_kernel<false, false><<<grid, block, 0, stream>>>(g, u, nchunks, qc, q_scales, rc, r_scales, h);
+    if (res)
+      return launch_q<true, true, true>(g, u, nelem, nt, q_codes, q_scales, r_codes, r_scales,
+                                        h_out, stream);
+    return launch_q<true, false, true>(g, u, nelem, nt, q_codes, q_scales, nullptr, nullptr,
+                                       h_out, stream);
   }
-  return hipGetLastError();
+  if (res)
+    return launch_q<false, true, true>(g, u, nelem, nt, q_codes, q_scales, r_codes, r_scales,
+                                       h_out, stream);
+  return launch_q<false, false, true>(g, u, nelem, nt, q_codes, q_scales, nullptr, nullptr,
+                                      h_out, stream);
 }
 
 hipError_t launch_dequant(const uint8_t *codes, const uint8_t *scales,

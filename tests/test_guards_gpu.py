@@ -7,6 +7,7 @@ import pytest
 import torch
 
 import paper_2608_26581_amd as rfq
+from paper_2608_26581_amd import rfq as binding
 from paper_2608_26581_amd import workloads as wl
 
 pytestmark = pytest.mark.gpu
@@ -87,6 +88,16 @@ def test_swiglu_outputs_stay_in_bounds(M, Nh, K):
     rfq.rfq_swiglu_quantize_act(g.to(torch.bfloat16), u.to(torch.bfloat16),
                                 out=[b.t for b in hb])
     _check_all(hb, "swiglu_quantize")
+    for dt in (torch.float32, torch.bfloat16):
+        gd, ud = g.to(dt), u.to(dt)
+        hb = _codes(M, Nh) + _codes(M, Nh)
+        h = Guarded((M, Nh), torch.bfloat16)
+        st = binding.load().rfq_swiglu_quantize_act(
+            binding._ptr(gd), binding._ptr(ud), binding._dtype_code(gd), M, Nh,
+            *[binding._ptr(b.t) for b in hb], binding._ptr(h.t), binding._stream(None))
+        assert st == 0
+        _check_all(hb, "swiglu_quantize %s" % dt)
+        h.check("swiglu_quantize h %s" % dt)
     x = torch.from_numpy(rng.standard_normal((M, K)).astype(np.float32)).cuda()
     q = rfq.rfq_quantize_act(x)
     wgu = rfq.rfq_quantize_weight(torch.from_numpy(

@@ -141,6 +141,28 @@ def test_quantize_special_values(orc):
             _assert_codes_equal(g, orc.quantize(arr.astype(np.float64)), "special %s" % dt)
 
 
+@pytest.mark.parametrize("M,K", [(64, 4096), (5, 96), (3, 2080)])
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_quantize_unaligned_scale_pointers(orc, M, K, dtype):
+    """Scale tensors may start at any byte (only code tensors must be 16-byte
+    aligned): outputs at an odd offset equal the oracle's."""
+    data = wl.generate(wl.WORKLOADS["quant"].scaled(M=M, K=K, weights=()), seed=21)
+    x = torch.from_numpy(data["x"]).cuda().to(dtype)
+    xr = data["x"] if dtype == torch.float32 else \
+        wl.bf16_bits_to_f32(wl.f32_to_bf16_bits(data["x"]))
+    _say("unaligned scales M=%d K=%d %s" % (M, K, dtype))
+    raw = [torch.empty(M * K // 32 + 1, dtype=torch.uint8, device="cuda") for _ in range(2)]
+    qs, rs = [r[1:].view(M, K // 32) for r in raw]
+    qc = torch.empty((M, K // 2), dtype=torch.uint8, device="cuda")
+    rc = torch.empty((M, K // 2), dtype=torch.uint8, device="cuda")
+    rfq.rfq_quantize_act(x, out=[qc, qs, rc, rs])
+    _assert_codes_equal([host(t) for t in (qc, qs, rc, rs)], orc.quantize(xr), "unaligned act")
+    wc = torch.empty((M, K // 2), dtype=torch.uint8, device="cuda")
+    rfq.rfq_quantize_weight(x, out=[wc, qs])
+    o = orc.quantize(xr, residual=False)
+    _assert_codes_equal([host(wc), host(qs)], o[:2], "unaligned weight")
+
+
 def test_power_of_two_equivariance():
     """Metamorphic: scaling X by 2^j keeps every code and shifts every scale
     byte by j; the product scales by exactly 2^j (no oracle involved)."""
@@ -258,14 +280,21 @@ def test_gemm_identity_weight_matches_dequant():
 
 # ---------------------------------------------------------------- SwiGLU
 @pytest.mark.parametrize("M,Nh", [(3, 96), (64, 12288), (257, 640)])
-def test_swiglu_quantize(orc, M, Nh):
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_swiglu_quantize(orc, M, Nh, dtype):
     rng = np.random.default_rng(M * Nh)
-    gb = wl.f32_to_bf16_bits((rng.standard_normal((M, Nh)) * 2).astype(np.float32))
-    ub = wl.f32_to_bf16_bits(rng.standard_normal((M, Nh)).astype(np.float32))
-    g, u = dev_bf16(gb), dev_bf16(ub)
+    gf = (rng.standard_normal((M, Nh)) * 2).astype(np.float32)
+    uf = rng.standard_normal((M, Nh)).astype(np.float32)
+    if dtype == torch.bfloat16:
+        gb, ub = wl.f32_to_bf16_bits(gf), wl.f32_to_bf16_bits(uf)
+        g, u = dev_bf16(gb), dev_bf16(ub)
+        gf, uf = wl.bf16_bits_to_f32(gb), wl.bf16_bits_to_f32(ub)
+    else:
+        g, u = dev(gf), dev(uf)
+    _say("swiglu quantize M=%d Nh=%d %s" % (M, Nh, dtype))
     qc, qs, rc, rs, h = rfq.rfq_swiglu_quantize_act(g, u, return_h=True)
     hg = host_bf16_as_f32(h).astype(np.float64)
-    href = orc.swiglu(wl.bf16_bits_to_f32(gb), wl.bf16_bits_to_f32(ub))
+    href = orc.swiglu(gf, uf)
     ulp = np.exp2(np.floor(np.log2(np.maximum(np.abs(href), 2.0 ** -126))) - 7)
     assert np.all(np.abs(hg - href) <= ulp)
     _assert_codes_equal([host(t) for t in (qc, qs, rc, rs)], orc.quantize(hg), "swiglu")
