@@ -41,8 +41,11 @@ METRIC = "RFQ-MXFP4 GEMM TFLOP/s + quantizer GB/s (Qwen3-VL-like 4096×4096×122
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=50)
-    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--steps", type=int, default=200)
+    # Untimed steps before the timed region: about 0.1 s of GPU work, after
+    # which the GPU's clock has settled (measured on MI355X: the first tens
+    # of milliseconds of sustained matrix-core load run 10-20% slower).
+    p.add_argument("--warmup", type=int, default=400)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-extras", action="store_true",
                    help="skip the secondary workloads and the accuracy diagnostics")
