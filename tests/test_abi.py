@@ -34,6 +34,19 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(lib, name), name
 
 
+def test_library_resolves_every_symbol_at_load():
+    """Loading with immediate binding fails on any undefined symbol: a kernel
+    whose host-side launch handle the compiler dropped would otherwise show
+    up only when that kernel is first launched."""
+    import subprocess
+    import sys
+    code = ("import ctypes, os, sys; ctypes.CDLL(sys.argv[1], mode=os.RTLD_NOW); "
+            "print('resolved')")
+    res = subprocess.run([sys.executable, "-c", code, binding.LIB_PATH],
+                         capture_output=True, text=True, timeout=120)
+    assert res.returncode == 0 and "resolved" in res.stdout, res.stderr
+
+
 def test_binding_names_match_the_c_names():
     for name in declared_functions():
         assert callable(getattr(rfq, name)), name
