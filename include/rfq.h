@@ -208,6 +208,34 @@ rfq_status rfq_gemm_swiglu_quantize(const uint8_t *q_codes, const uint8_t *q_sca
                                     uint8_t *hr_codes, uint8_t *hr_scales,
                                     void *h_out, void *hip_stream);
 
+/*
+ * Streaming form of the RFQ product (Algorithm 1 with the quantization of the
+ * activation tile inside the product loop; Eq. 8-11): Z = (deq q + deq r)
+ * deq(w)^T where q, r are the primary and residual MXFP4 codes of X exactly
+ * as rfq_quantize_act would write them, but formed block by block in
+ * registers right before the products that use them - neither the residual
+ * nor any activation code is written to memory.  Meant for few activation
+ * rows (decode): each 16-row slice of W re-quantizes the activations it
+ * multiplies, so the quantization is repeated N/16 times.
+ *   x        [M][K] row-major, x_dtype (bf16 or fp32); 16-byte aligned.
+ *   residual nonzero: primary and residual terms (phi = 1); zero: primary
+ *            only (plain MXFP4, phi = 0).
+ *   w_codes  [N][K/2], w_scales [N][K/32]: rfq_quantize_weight output;
+ *            both 16-byte aligned.
+ *   M, N, K: K a multiple of 512; M at most 1048560 (65535 row slices of
+ *            16); X and the weight codes below 2 GiB each.
+ *   z        [M][N] row-major, z_dtype; 16-byte aligned.
+ * For M <= 64 the result is bit-identical to rfq_quantize_act followed by
+ * rfq_gemm (which multiplies such few rows with the same kernel structure);
+ * otherwise it agrees within the product's rounding (fp32 accumulation in an
+ * unspecified order).  Errors: RFQ_ERR_SHAPE for the shape conditions above,
+ * otherwise as rfq_gemm.  Asynchronous on hip_stream.
+ */
+rfq_status rfq_gemm_stream(const void *x, rfq_dtype x_dtype, int residual,
+                           const uint8_t *w_codes, const uint8_t *w_scales,
+                           int64_t M, int64_t N, int64_t K,
+                           void *z, rfq_dtype z_dtype, void *hip_stream);
+
 /* Static, never-NULL description of a status code. */
 const char *rfq_status_str(rfq_status s);
 

@@ -212,6 +212,31 @@ rfq_status rfq_gemm_swiglu_quantize(const uint8_t *q_codes, const uint8_t *q_sca
                                           static_cast<hipStream_t>(hip_stream)));
 }
 
+rfq_status rfq_gemm_stream(const void *x, rfq_dtype x_dtype, int residual,
+                           const uint8_t *w_codes, const uint8_t *w_scales,
+                           int64_t M, int64_t N, int64_t K,
+                           void *z, rfq_dtype z_dtype, void *hip_stream) {
+  if (!valid_dtype(x_dtype) || !valid_dtype(z_dtype)) return RFQ_ERR_DTYPE;
+  rfq_status s = check_k(M, K);
+  if (s != RFQ_OK) return s;
+  if (N < 0 || (K % 512) != 0) return RFQ_ERR_SHAPE;
+  // One workgroup per 16 x 16 output block: N/16 along the grid's x axis,
+  // M/16 along its y axis (at most 65535); buffer ranges (X bytes, weight
+  // code bytes) are 31-bit.
+  if ((M + 15) / 16 > 65535 || (N + 15) / 16 > INT32_MAX) return RFQ_ERR_SHAPE;
+  const int64_t limit = int64_t(1) << 31;
+  const int64_t xbytes = x_dtype == RFQ_BF16 ? 2 : 4;
+  if (M * K >= limit / xbytes || N * (K / 2) >= limit) return RFQ_ERR_SHAPE;
+  if (M == 0 || N == 0) return RFQ_OK;
+  if (!x || !w_codes || !w_scales || !z) return RFQ_ERR_NULL;
+  if (!aligned(x, 16) || !aligned(w_codes, 16) || !aligned(w_scales, 16) || !aligned(z, 16))
+    return RFQ_ERR_ALIGN;
+  if ((s = check_device()) != RFQ_OK) return s;
+  return launched(rfq::launch_gemm_stream(x, x_dtype == RFQ_BF16, residual != 0, w_codes,
+                                          w_scales, M, N, K, z, z_dtype == RFQ_BF16,
+                                          static_cast<hipStream_t>(hip_stream)));
+}
+
 const char *rfq_status_str(rfq_status s) {
   switch (s) {
     case RFQ_OK: return "ok";

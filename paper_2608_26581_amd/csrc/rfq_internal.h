@@ -68,6 +68,24 @@ hipError_t launch_gemm_large(const uint8_t *q_codes, const uint8_t *q_scales,
                              int64_t M, int64_t N, int64_t K, void *z, bool z_bf16,
                              hipStream_t stream);
 
+// Product for few activation rows (M <= kSkinnyMaxRows, K a multiple of 512,
+// 16-byte aligned scale tensors, code tensors below 2 GiB): one workgroup per
+// 16 weight rows and 16 activation rows.
+constexpr int64_t kSkinnyMaxRows = 64;
+bool gemm_skinny_applies(const uint8_t *q_scales, const uint8_t *r_scales,
+                         const uint8_t *w_scales, int64_t M, int64_t N, int64_t K);
+hipError_t launch_gemm_skinny(const uint8_t *q_codes, const uint8_t *q_scales,
+                              const uint8_t *r_codes, const uint8_t *r_scales,
+                              const uint8_t *w_codes, const uint8_t *w_scales, int64_t M,
+                              int64_t N, int64_t K, void *z, bool z_bf16, hipStream_t stream);
+
+// Streaming form of the product: X[M][K] (bf16 or fp32) is quantized inside
+// the product's K loop (primary and, with residual, the quantized residual);
+// K a multiple of 512, W's scale tensor 16-byte aligned.
+hipError_t launch_gemm_stream(const void *x, bool x_bf16, bool residual, const uint8_t *w_codes,
+                              const uint8_t *w_scales, int64_t M, int64_t N, int64_t K, void *z,
+                              bool z_bf16, hipStream_t stream);
+
 // RFQ product with a fallback-indicator map phi[ceil(M/64)][ceil(K/256)]
 // (residual operand required; K up to 2^20): the residual term of a tile is
 // included where its byte is nonzero.

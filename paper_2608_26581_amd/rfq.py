@@ -29,6 +29,7 @@ _STATUS_NAMES = {
 EXPORTS = (
     "rfq_quantize_act", "rfq_quantize_weight", "rfq_gemm", "rfq_dequant",
     "rfq_swiglu_quantize_act", "rfq_gemm_phi", "rfq_fallback_map", "rfq_gemm_swiglu_quantize",
+    "rfq_gemm_stream",
     "rfq_status_str", "rfq_abi_version",
 )
 
@@ -65,9 +66,10 @@ def load():
     lib.rfq_gemm_swiglu_quantize.argtypes = [P, P, P, P, P, P, I64, I64, I64, P, P, P, P, P, P]
     lib.rfq_gemm_phi.argtypes = [P, P, P, P, P, P, P, I64, I64, I64, P, I32, P]
     lib.rfq_fallback_map.argtypes = [P, P, I64, I64, I32, I32, P, P]
+    lib.rfq_gemm_stream.argtypes = [P, I32, I32, P, P, I64, I64, I64, P, I32, P]
     for f in ("rfq_quantize_act", "rfq_quantize_weight", "rfq_gemm", "rfq_dequant",
               "rfq_swiglu_quantize_act", "rfq_gemm_swiglu_quantize", "rfq_gemm_phi",
-              "rfq_fallback_map"):
+              "rfq_fallback_map", "rfq_gemm_stream"):
         getattr(lib, f).restype = I32
     lib.rfq_status_str.argtypes = [I32]
     lib.rfq_status_str.restype = ctypes.c_char_p
@@ -158,6 +160,23 @@ def rfq_gemm(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales,
                          _ptr(w_codes), _ptr(w_scales), M, N, K, _ptr(z), _dtype_code(z),
                          _stream(stream))
     _check("rfq_gemm", st)
+    return z
+
+
+def rfq_gemm_stream(x, w_codes, w_scales, residual=True, out_dtype=torch.float32, out=None,
+                    stream=None):
+    """Streaming form: Z[M][N] from X[M][K] (bf16 or fp32) quantized inside the
+    product's K loop (primary and, with residual, the quantized residual)."""
+    _need(x, "x")
+    M, K = x.shape
+    N = w_codes.shape[0]
+    if w_codes.shape[1] * 2 != K:
+        raise ValueError("K mismatch between activations and weight codes")
+    z = out if out is not None else torch.empty((M, N), dtype=out_dtype, device=x.device)
+    st = load().rfq_gemm_stream(_ptr(x), _dtype_code(x), int(bool(residual)), _ptr(w_codes),
+                                _ptr(w_scales), M, N, K, _ptr(z), _dtype_code(z),
+                                _stream(stream))
+    _check("rfq_gemm_stream", st)
     return z
 
 

@@ -139,6 +139,40 @@ def test_gemm_validation():
     assert call(a4=None, a5=None, a9=None, a7=0) == OK
 
 
+def test_gemm_stream_validation():
+    g = _lib().rfq_gemm_stream
+    # x, x_dtype, residual, w_codes, w_scales, M, N, K, z, z_dtype, stream
+    args = [A, 1, 1, A, A, 8, 8, 512, A, 0, None]
+
+    def call(**kw):
+        a = list(args)
+        for k, v in kw.items():
+            a[int(k[1:])] = v
+        return g(*a)
+
+    assert call(a0=None) == ENULL
+    assert call(a3=None) == ENULL
+    assert call(a4=None) == ENULL
+    assert call(a8=None) == ENULL
+    assert call(a1=2) == EDTYPE
+    assert call(a9=7) == EDTYPE
+    assert call(a7=256) == ESHAPE                      # K not a multiple of 512
+    assert call(a7=96) == ESHAPE
+    assert call(a7=0) == ESHAPE
+    assert call(a5=-1) == ESHAPE
+    assert call(a6=-1) == ESHAPE
+    assert call(a5=1 << 20, a7=1 << 12) == ESHAPE      # X of 8 GiB: above the 2 GiB limit
+    assert call(a5=65535 * 16 + 1, a6=1) == ESHAPE   # more than 65535 row slices
+    assert call(a0=MIS) == EALIGN
+    assert call(a3=MIS) == EALIGN
+    assert call(a4=MIS) == EALIGN
+    assert call(a8=MIS) == EALIGN
+    assert call(a5=0) == OK
+    assert call(a6=0) == OK
+    assert call(a0=None, a8=None, a5=0) == OK
+    assert call(a3=None, a4=None, a8=None, a6=0) == OK
+
+
 def test_dequant_and_swiglu_validation():
     d = _lib().rfq_dequant
     assert d(None, A, 4, 64, A, None) == ENULL
@@ -213,3 +247,4 @@ def test_valid_arguments_without_a_gpu_report_device_error():
         pytest.skip("a GPU is present; fake pointers must not reach a launch")
     assert _lib().rfq_quantize_act(A, 1, 4, 64, A, A, A, A, None) == EDEVICE
     assert _lib().rfq_gemm(A, A, A, A, A, A, 8, 8, 64, A, 0, None) == EDEVICE
+    assert _lib().rfq_gemm_stream(A, 1, 1, A, A, 8, 8, 512, A, 0, None) == EDEVICE

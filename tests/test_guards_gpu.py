@@ -42,7 +42,8 @@ def _check_all(bufs, what):
         b.check("%s[%d]" % (what, i))
 
 
-@pytest.mark.parametrize("M,N,K", [(131, 97, 512), (131, 97, 96), (1, 1, 1024), (257, 300, 1536)])
+@pytest.mark.parametrize("M,N,K", [(131, 97, 512), (131, 97, 96), (1, 1, 1024), (257, 300, 1536),
+                                   (37, 77, 1024)])
 def test_outputs_stay_in_bounds(M, N, K):
     w = wl.WORKLOADS["qwen"].scaled(M=M, K=K, weights=(("w", K, N),))
     data = wl.generate(w, seed=31)
@@ -74,6 +75,11 @@ def test_outputs_stay_in_bounds(M, N, K):
     zb = Guarded((M, N), torch.bfloat16)
     rfq.rfq_gemm_phi(*q, *wq, pb.t, out=zb.t)
     zb.check("gemm_phi")
+    if K % 512 == 0:
+        for dt in (torch.float32, torch.bfloat16):
+            zb = Guarded((M, N), dt)
+            rfq.rfq_gemm_stream(xb, *wq, out=zb.t)
+            zb.check("gemm_stream %s" % dt)
     db = Guarded((M, K), torch.float32)
     rfq.rfq_dequant(q[0], q[1], out=db.t)
     db.check("dequant")

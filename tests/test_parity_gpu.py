@@ -223,6 +223,12 @@ GEMM_SMALL = [
     ("qwen", 70, 300, 640),         # K a multiple of 128 but not of 512
     ("qwen", 1, 1, 32),
     ("qwen", 3, 130, 96),
+    # few activation rows, K a multiple of 512: the skinny kernel
+    ("qwen", 1, 300, 512),
+    ("qwen", 16, 256, 1024),
+    ("qwen", 37, 130, 2048),          # three row slices, ragged
+    ("wan", 64, 200, 5120),           # K range split unevenly over the waves
+    ("qwen", 5, 1, 512),
 ]
 
 
@@ -265,6 +271,71 @@ def test_gemm_full_size_sampled(orc, name):
     zr, bound = orc.gemm_sampled(*hq, *hw, rows, cols)
     assert_gemm_close(z32[rows, cols], zr, bound, False, "full fp32")
     assert_gemm_close(zbf[rows, cols], zr, bound, True, "full bf16")
+
+
+# ---------------------------------------------------- streaming form
+STREAM = [
+    ("qwen", 1, 300, 512),
+    ("qwen", 16, 256, 1024),
+    ("qwen", 37, 130, 2048),
+    ("wan", 64, 200, 5120),
+    ("qwen", 100, 97, 512),           # more rows than the codes path's skinny kernel
+]
+
+
+@pytest.mark.parametrize("name,M,N,K", STREAM)
+@pytest.mark.parametrize("xdt", [torch.bfloat16, torch.float32])
+@pytest.mark.parametrize("residual", [True, False])
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
+def test_gemm_stream_matches_oracle(orc, name, M, N, K, xdt, residual, out_dtype):
+    """The activations quantized inside the product give the oracle's product
+    of the oracle's codes of X, within the product's tolerance."""
+    data = _gemm_case(name, M, N, K, seed=3 * M + N + K)
+    xr = data["x"] if xdt == torch.float32 else wl.bf16_bits_to_f32(data["x_bf16"])
+    x = dev(data["x"]) if xdt == torch.float32 else dev_bf16(data["x_bf16"])
+    _say("gemm_stream %s M=%d N=%d K=%d x=%s residual=%s out=%s" %
+         (name, M, N, K, xdt, residual, out_dtype))
+    w = rfq.rfq_quantize_weight(dev(data["w"]))
+    z = rfq.rfq_gemm_stream(x, *w, residual=residual, out_dtype=out_dtype)
+    zh = host(z) if out_dtype == torch.float32 else host_bf16_as_f32(z)
+    oq = orc.quantize(xr, residual=residual)
+    zr, bound = orc.gemm(*oq, host(w[0]), host(w[1]))
+    assert_gemm_close(zh, zr, bound, out_dtype == torch.bfloat16, "gemm_stream %s" % name)
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 300, 512), (16, 256, 1024), (64, 200, 5120), (23, 515, 2048)])
+@pytest.mark.parametrize("residual", [True, False])
+def test_gemm_stream_bit_identical_to_quantize_then_gemm(M, N, K, residual):
+    """Up to 64 rows both forms run the same product structure on the same
+    codes: the streaming form must reproduce quantize + product bit for bit."""
+    data = _gemm_case("qwen", M, N, K, seed=M * N + K)
+    x = dev_bf16(data["x_bf16"])
+    w = rfq.rfq_quantize_weight(dev(data["w"]))
+    _say("gemm_stream vs codes M=%d N=%d K=%d residual=%s" % (M, N, K, residual))
+    for dt in (torch.float32, torch.bfloat16):
+        zs = rfq.rfq_gemm_stream(x, *w, residual=residual, out_dtype=dt)
+        q = rfq.rfq_quantize_act(x, residual=residual)
+        zc = rfq.rfq_gemm(*q, *w, out_dtype=dt)
+        assert torch.equal(zs.view(torch.int16) if dt == torch.bfloat16 else zs.view(torch.int32),
+                           zc.view(torch.int16) if dt == torch.bfloat16 else zc.view(torch.int32))
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 12288, 4096), (16, 12288, 4096), (8, 4096, 12288)])
+def test_decode_shapes_full(orc, M, N, K):
+    """Decode-sized products at the workloads' weight shapes, every output
+    checked, in both forms (codes in and streaming)."""
+    data = _gemm_case("qwen", M, N, K, seed=N + M)
+    x = dev_bf16(data["x_bf16"])
+    w = rfq.rfq_quantize_weight(dev(data["w"]))
+    _say("decode M=%d N=%d K=%d" % (M, N, K))
+    q = rfq.rfq_quantize_act(x)
+    zc = host(rfq.rfq_gemm(*q, *w))
+    zs = host(rfq.rfq_gemm_stream(x, *w))
+    hq = [host(t) for t in q]
+    _assert_codes_equal(hq, orc.quantize(wl.bf16_bits_to_f32(data["x_bf16"])), "decode x")
+    zr, bound = orc.gemm(*hq, host(w[0]), host(w[1]))
+    assert_gemm_close(zc, zr, bound, False, "decode codes")
+    assert_gemm_close(zs, zr, bound, False, "decode stream")
 
 
 def test_gemm_identity_weight_matches_dequant():
