@@ -289,9 +289,11 @@ def _per_launch_ms(torch, stream, fn, reps):
 def secondary(torch, rfq, wl, x, w, stream):
     """Rates reported beside the headline step: the product without the
     residual (plain MXFP4), the bf16 matrix product of the same shape
-    (hipBLASLt through torch), the product on the Wan2.2-DiT-like shape, and
-    the chained SwiGLU MLP block (quantize -> gate and up products ->
-    SwiGLU + quantize -> down product, weights quantized beforehand)."""
+    (hipBLASLt through torch), decode-sized products (1 and 16 activation
+    rows, codes in and streaming form), the product on the Wan2.2-DiT-like
+    shape, and the chained SwiGLU MLP block (quantize -> gate and up
+    products -> SwiGLU + quantize -> down product, weights quantized
+    beforehand)."""
     out = {}
     M, K = x.shape
     N = w.shape[0]
@@ -329,7 +331,32 @@ def secondary(torch, rfq, wl, x, w, stream):
     out["rfq_gemm_phi_scale_threshold"] = {
         "ms": round(ms, 5), "threshold_byte": thr, "tiles_on": round(on, 4),
         "exec_tflops": round((2.0 + 2.0 * on) * M * N * K / ms / 1e9, 1)}
-    del q, wq, z, wt, phi
+    del q, z, wt, phi
+
+    # Decode-sized products on the same weight: few activation rows, codes in
+    # (rfq_quantize_act + rfq_gemm, whose few-row kernel streams W) and the
+    # streaming form (rfq_gemm_stream, activations quantized inside the
+    # product).  Ten weight copies (267 MB, beyond the last-level cache) are
+    # rotated, as a model's many layers would be.
+    wcs = [(torch.roll(wq[0], 97 * s, 0), torch.roll(wq[1], 97 * s, 0)) for s in range(10)]
+    w_bytes = N * K // 2 + N * K // 32
+    for md in (1, 16):
+        xd = x[:md].contiguous()
+        qd = rfq.rfq_quantize_act(xd)
+        zd = torch.empty((md, N), dtype=torch.bfloat16, device=x.device)
+
+        def codes_path(i):
+            rfq.rfq_quantize_act(xd, out=qd, stream=stream)
+            rfq.rfq_gemm(*qd, *wcs[i % 10], out=zd, stream=stream)
+
+        ms_c = _per_launch_ms(torch, stream, codes_path, 50)
+        ms_s = _per_launch_ms(torch, stream, lambda i: rfq.rfq_gemm_stream(
+            xd, *wcs[i % 10], out=zd, stream=stream), 50)
+        out["decode_%dx%dx%d" % (md, K, N)] = {
+            "quantize_then_gemm_ms": round(ms_c, 5), "stream_ms": round(ms_s, 5),
+            "w_gbs_quantize_then_gemm": round(w_bytes / ms_c / 1e6, 1),
+            "w_gbs_stream": round(w_bytes / ms_s / 1e6, 1)}
+    del wq, wcs
 
     # Wan2.2-DiT-like product: X 32768x5120, W 5120x13824.
     d = wl.generate(wl.WORKLOADS["wan"], seed=0)
