@@ -154,11 +154,11 @@ def main():
           torch.empty((qk.M, qk.K // 32), dtype=torch.uint8, device=dev),
           torch.empty((qk.M, qk.K // 2), dtype=torch.uint8, device=dev),
           torch.empty((qk.M, qk.K // 32), dtype=torch.uint8, device=dev)]
-    for i in range(5):
+    for i in range(20):
         rfq.rfq_quantize_act(qx[i % Q_SETS], out=qo, stream=stream)
     # Back-to-back launches between one pair of events: an event recorded
     # between two short kernels adds a few microseconds of its own.
-    qreps = 50
+    qreps = 200
     qa = torch.cuda.Event(enable_timing=True)
     qb = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()

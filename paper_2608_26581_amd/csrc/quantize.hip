@@ -33,7 +33,10 @@
 namespace rfq {
 namespace {
 
-constexpr int kThreads = 256;
+constexpr int kThreads = 256;        // dequantization and the phi map
+// Quantizers: one wave per workgroup (measured on MI355X, 8192 x 4096 bf16:
+// 18.3 us against 18.6 us with four waves per workgroup).
+constexpr int kQuantThreads = 64;
 constexpr int kSpanBlocks = 64;                       // blocks per wave span
 constexpr int kSpanCodeBytes = kSpanBlocks * kBlock / 2;
 constexpr int64_t kLastLevelCacheBytes = int64_t(256) << 20;
@@ -105,7 +108,7 @@ struct Stage {
 // Quantizer kernel (SWIGLU: the input is h = bf16(silu(g) u) of g = x and
 // u = x2, optionally written to h_out).  nblocks = elements / 32.
 template <bool BF16_IN, bool RES, bool NT_STORE, bool SWIGLU>
-__global__ __launch_bounds__(kThreads) void quantize_kernel(
+__global__ __launch_bounds__(kQuantThreads) void quantize_kernel(
     const void *__restrict__ x, const void *__restrict__ x2, int64_t nblocks,
     uint8_t *__restrict__ q_codes, uint8_t *__restrict__ q_scales,
     uint8_t *__restrict__ r_codes, uint8_t *__restrict__ r_scales,
@@ -114,10 +117,10 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
   constexpr int kLanesPerBlock = kBlock / kE;
   constexpr int kSteps = kSpanBlocks * kLanesPerBlock / 64;
   constexpr int kCodeBytes = kE / 2;              // per lane and step
-  __shared__ Stage stage[kThreads / 64][RES ? 2 : 1];
+  __shared__ Stage stage[kQuantThreads / 64][RES ? 2 : 1];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int64_t blk0 = ((int64_t)blockIdx.x * (kThreads / 64) + wave) * kSpanBlocks;
+  const int64_t blk0 = ((int64_t)blockIdx.x * (kQuantThreads / 64) + wave) * kSpanBlocks;
   const int64_t nunits = nblocks * kLanesPerBlock;   // 16-byte input units
   const u32x4 *xin = reinterpret_cast<const u32x4 *>(x);
   const u32x4 *xin2 = reinterpret_cast<const u32x4 *>(x2);
@@ -272,7 +275,7 @@ template <bool BF16_IN, bool RES, bool SWIGLU>
 hipError_t launch_q(const void *x, const void *x2, int64_t nelem, bool nt, uint8_t *qc,
                     uint8_t *qs, uint8_t *rc, uint8_t *rs, uint16_t *h, hipStream_t stream) {
   const int64_t nblocks = nelem / kBlock;
-  const dim3 grid(grid_for(nblocks, (kThreads / 64) * kSpanBlocks)), block(kThreads);
+  const dim3 grid(grid_for(nblocks, (kQuantThreads / 64) * kSpanBlocks)), block(kQuantThreads);
   if (nt)
     quantize_kernel<BF16_IN, RES, true, SWIGLU><<<grid, block, 0, stream>>>(x, x2, nblocks, qc, qs,
                                                                            rc, rs, h);
