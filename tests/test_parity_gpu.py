@@ -550,6 +550,36 @@ def test_gemm_swiglu_fused_full_size_and_down_product(orc):
 
 
 # ---------------------------------------------------------------- edges
+def test_codes_beyond_4gib(orc):
+    """Maximum sizes: an activation tensor whose code tensors pass 2^32
+    bytes (the product then runs on the kernel with 64-bit offsets).  Codes
+    are checked bit-exactly and the product within tolerance on rows around
+    the 4 GiB byte boundary, the last row and random rows."""
+    M, K, N = (1 << 21) + 48, 4096, 64
+    assert M * K // 2 > 1 << 32
+    _say("beyond 4 GiB: M=%d K=%d N=%d" % (M, K, N))
+    gen = torch.Generator(device="cuda").manual_seed(7)
+    x = torch.randn((M, K), generator=gen, device="cuda", dtype=torch.float32).to(torch.bfloat16)
+    q = rfq.rfq_quantize_act(x)
+    data = _gemm_case("qwen", 8, N, K, seed=99)
+    w = rfq.rfq_quantize_weight(dev(data["w"]))
+    z = rfq.rfq_gemm(*q, *w)
+    boundary = (1 << 32) // (K // 2)               # first row whose codes start at 2^32
+    rows = np.unique(np.concatenate([
+        [0, boundary - 2, boundary - 1, boundary, boundary + 1, M - 2, M - 1],
+        np.random.default_rng(3).integers(0, M, 24)]))
+    idx = torch.from_numpy(rows).cuda()
+    xr = host_bf16_as_f32(x.index_select(0, idx).contiguous())
+    g = [host(t.index_select(0, idx)) for t in q]
+    zr_rows = host(z.index_select(0, idx))
+    del x, q, z
+    torch.cuda.empty_cache()
+    ref = orc.quantize(xr)
+    _assert_codes_equal(g, ref, "beyond 4 GiB")
+    zr, bound = orc.gemm(*ref, host(w[0]), host(w[1]))
+    assert_gemm_close(zr_rows, zr, bound, False, "beyond 4 GiB product")
+
+
 def test_empty_inputs_are_noops():
     x = torch.empty((0, 64), dtype=torch.bfloat16, device="cuda")
     q = rfq.rfq_quantize_act(x)
