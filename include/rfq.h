@@ -35,6 +35,12 @@
  *     inside kernels surface at the caller's next synchronization, as in HIP.
  *   - Empty work: rows == 0 (or N == 0 for the product) is a valid no-op;
  *     the pointers of such a call are not read and may be NULL.
+ *   - Size limits (RFQ_ERR_SHAPE beyond them; one launch covers at most
+ *     2^32 - 1 work items): K <= 2^31 in every call; quantizers at most
+ *     2^32 - 64 MX blocks (rows * K / 32); products M, N < 2^31 and
+ *     ceil(M/128) * ceil(N/128) * 256 < 2^32 (about M * N < 2^38, far beyond
+ *     what fits in memory); dequantization and the phi map rows * K <= 2^56.
+ *     Calls with further limits state them.
  *   - Thread safety: calls may be issued from several host threads; calls on
  *     one stream execute in issue order.
  */
@@ -50,7 +56,7 @@ extern "C" {
 typedef enum {
     RFQ_OK = 0,
     RFQ_ERR_NULL = 1,    /* a required pointer is NULL, or an optional pair is half given */
-    RFQ_ERR_SHAPE = 2,   /* negative size, K < 32 or K not a multiple of 32 */
+    RFQ_ERR_SHAPE = 2,   /* negative size, K < 32 or not a multiple of 32, or a size limit */
     RFQ_ERR_DTYPE = 3,   /* unknown rfq_dtype value */
     RFQ_ERR_ALIGN = 4,   /* a pointer violates the alignment stated for it */
     RFQ_ERR_DEVICE = 5,  /* no current HIP device, or it is not gfx950 */
@@ -223,7 +229,8 @@ rfq_status rfq_gemm_swiglu_quantize(const uint8_t *q_codes, const uint8_t *q_sca
  *   w_codes  [N][K/2], w_scales [N][K/32]: rfq_quantize_weight output;
  *            both 16-byte aligned.
  *   M, N, K: K a multiple of 512; M at most 1048560 (65535 row slices of
- *            16); X and the weight codes below 2 GiB each.
+ *            16); N at most 268435440 (2^24 - 1 column slices of 16); X and
+ *            the weight codes below 2 GiB each.
  *   z        [M][N] row-major, z_dtype; 16-byte aligned.
  * For M <= 64 the result is bit-identical to rfq_quantize_act followed by
  * rfq_gemm (which multiplies such few rows with the same kernel structure);

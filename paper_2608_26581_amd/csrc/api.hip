@@ -26,9 +26,36 @@ bool aligned(const void *p, uintptr_t a) {
 
 bool valid_dtype(rfq_dtype d) { return d == RFQ_F32 || d == RFQ_BF16; }
 
+// Size limits.  K is capped so that every byte count and stage counter below
+// stays in range; a launch's work-item count (grid times workgroup) must fit
+// 32 bits; dequantization and the phi map loop over their grid, so only
+// int64 overflow bounds them.
+constexpr int64_t kMaxK = int64_t(1) << 31;
+constexpr int64_t kMaxWorkItems = UINT32_MAX;
+constexpr int64_t kMaxElements = int64_t(1) << 56;
+
+// a * b > limit for a, b >= 0, computed without overflow.
+bool exceeds(int64_t a, int64_t b, int64_t limit) { return a != 0 && b > limit / a; }
+
 rfq_status check_k(int64_t rows, int64_t K) {
-  if (rows < 0 || K < 32 || (K % 32) != 0) return RFQ_ERR_SHAPE;
+  if (rows < 0 || K < 32 || (K % 32) != 0 || K > kMaxK) return RFQ_ERR_SHAPE;
   return RFQ_OK;
+}
+
+// Quantizers: one 64-lane wave per 64 MX blocks, so the launch covers the
+// block count rounded up to 64.
+bool quantizer_fits(int64_t rows, int64_t K) {
+  return !exceeds(rows, K / 32, kMaxWorkItems - 63);
+}
+
+// Products: one workgroup per output tile, 128 x 128 tiles of 256 work items
+// (general kernel) or 256 x 256 tiles of 512 (large-tile kernel).  With M
+// and N below 2^31 neither product overflows.
+bool product_fits(int64_t M, int64_t N) {
+  if (M > INT32_MAX || N > INT32_MAX) return false;
+  const int64_t general = ((M + 127) / 128) * ((N + 127) / 128) * 256;
+  const int64_t large = ((M + 255) / 256) * ((N + 255) / 256) * 512;
+  return general <= kMaxWorkItems && large <= kMaxWorkItems;
 }
 
 // Confirms that the current device is a gfx950 GPU (cached per device).
@@ -59,6 +86,7 @@ rfq_status rfq_quantize_act(const void *x, rfq_dtype x_dtype, int64_t M, int64_t
   if (!valid_dtype(x_dtype)) return RFQ_ERR_DTYPE;
   rfq_status s = check_k(M, K);
   if (s != RFQ_OK) return s;
+  if (!quantizer_fits(M, K)) return RFQ_ERR_SHAPE;
   if (M == 0) return RFQ_OK;
   if (!x || !q_codes || !q_scales) return RFQ_ERR_NULL;
   if ((r_codes == nullptr) != (r_scales == nullptr)) return RFQ_ERR_NULL;
@@ -76,6 +104,7 @@ rfq_status rfq_quantize_weight(const void *w, rfq_dtype w_dtype, int64_t N, int6
   if (!valid_dtype(w_dtype)) return RFQ_ERR_DTYPE;
   rfq_status s = check_k(N, K);
   if (s != RFQ_OK) return s;
+  if (!quantizer_fits(N, K)) return RFQ_ERR_SHAPE;
   if (N == 0) return RFQ_OK;
   if (!w || !w_codes || !w_scales) return RFQ_ERR_NULL;
   if (!aligned(w, 16) || !aligned(w_codes, 16)) return RFQ_ERR_ALIGN;
@@ -93,10 +122,7 @@ rfq_status rfq_gemm(const uint8_t *q_codes, const uint8_t *q_scales,
   if (!valid_dtype(z_dtype)) return RFQ_ERR_DTYPE;
   rfq_status s = check_k(M, K);
   if (s != RFQ_OK) return s;
-  if (N < 0) return RFQ_ERR_SHAPE;
-  if (M > INT32_MAX || N > INT32_MAX) return RFQ_ERR_SHAPE;
-  // Output tiles are at least 64 x 64 and their count must fit one grid axis.
-  if (((M + 63) / 64) * ((N + 63) / 64) > INT32_MAX) return RFQ_ERR_SHAPE;
+  if (N < 0 || !product_fits(M, N)) return RFQ_ERR_SHAPE;
   if (M == 0 || N == 0) return RFQ_OK;
   if (!q_codes || !q_scales || !w_codes || !w_scales || !z) return RFQ_ERR_NULL;
   if ((r_codes == nullptr) != (r_scales == nullptr)) return RFQ_ERR_NULL;
@@ -113,6 +139,7 @@ rfq_status rfq_dequant(const uint8_t *codes, const uint8_t *scales, int64_t rows
                        int64_t K, float *out, void *hip_stream) {
   rfq_status s = check_k(rows, K);
   if (s != RFQ_OK) return s;
+  if (exceeds(rows, K, kMaxElements)) return RFQ_ERR_SHAPE;
   if (rows == 0) return RFQ_OK;
   if (!codes || !scales || !out) return RFQ_ERR_NULL;
   if (!aligned(codes, 16) || !aligned(out, 16)) return RFQ_ERR_ALIGN;
@@ -129,6 +156,7 @@ rfq_status rfq_swiglu_quantize_act(const void *g, const void *u, rfq_dtype dt,
   if (!valid_dtype(dt)) return RFQ_ERR_DTYPE;
   rfq_status s = check_k(M, Nh);
   if (s != RFQ_OK) return s;
+  if (!quantizer_fits(M, Nh)) return RFQ_ERR_SHAPE;
   if (M == 0) return RFQ_OK;
   if (!g || !u || !q_codes || !q_scales) return RFQ_ERR_NULL;
   if ((r_codes == nullptr) != (r_scales == nullptr)) return RFQ_ERR_NULL;
@@ -153,9 +181,7 @@ rfq_status rfq_gemm_phi(const uint8_t *q_codes, const uint8_t *q_scales,
   if (!valid_dtype(z_dtype)) return RFQ_ERR_DTYPE;
   rfq_status s = check_k(M, K);
   if (s != RFQ_OK) return s;
-  if (N < 0 || K > (int64_t(1) << 20)) return RFQ_ERR_SHAPE;
-  if (M > INT32_MAX || N > INT32_MAX) return RFQ_ERR_SHAPE;
-  if (((M + 63) / 64) * ((N + 63) / 64) > INT32_MAX) return RFQ_ERR_SHAPE;
+  if (N < 0 || K > (int64_t(1) << 20) || !product_fits(M, N)) return RFQ_ERR_SHAPE;
   if (M == 0 || N == 0) return RFQ_OK;
   if (!q_codes || !q_scales || !r_scales || !w_codes || !w_scales || !z) return RFQ_ERR_NULL;
   if (!aligned(q_codes, 16) || !aligned(w_codes, 16) || !aligned(r_codes, 16) ||
@@ -173,6 +199,7 @@ rfq_status rfq_fallback_map(const uint8_t *r_codes, const uint8_t *q_scales, int
   rfq_status s = check_k(M, K);
   if (s != RFQ_OK) return s;
   if (rule != RFQ_PHI_RESIDUAL_NONZERO && rule != RFQ_PHI_SCALE_AT_LEAST) return RFQ_ERR_SHAPE;
+  if (exceeds(M, K, kMaxElements)) return RFQ_ERR_SHAPE;
   if (M == 0) return RFQ_OK;
   if (!phi || (rule == RFQ_PHI_RESIDUAL_NONZERO ? !r_codes : !q_scales)) return RFQ_ERR_NULL;
   if (rule == RFQ_PHI_RESIDUAL_NONZERO && !aligned(r_codes, 16)) return RFQ_ERR_ALIGN;
@@ -191,7 +218,7 @@ rfq_status rfq_gemm_swiglu_quantize(const uint8_t *q_codes, const uint8_t *q_sca
   rfq_status s = check_k(M, K);
   if (s != RFQ_OK) return s;
   if (Nh < 0 || (Nh % 32) != 0 || (K % 512) != 0) return RFQ_ERR_SHAPE;
-  if (M > INT32_MAX || 2 * Nh > INT32_MAX) return RFQ_ERR_SHAPE;
+  if (Nh > INT32_MAX || !product_fits(M, 2 * Nh)) return RFQ_ERR_SHAPE;
   // Byte offsets inside each code tensor are 32-bit.
   const int64_t limit = int64_t(1) << 32;
   if (M * (K / 2) >= limit || 2 * Nh * (K / 2) >= limit) return RFQ_ERR_SHAPE;
@@ -220,10 +247,10 @@ rfq_status rfq_gemm_stream(const void *x, rfq_dtype x_dtype, int residual,
   rfq_status s = check_k(M, K);
   if (s != RFQ_OK) return s;
   if (N < 0 || (K % 512) != 0) return RFQ_ERR_SHAPE;
-  // One workgroup per 16 x 16 output block: N/16 along the grid's x axis,
-  // M/16 along its y axis (at most 65535); buffer ranges (X bytes, weight
-  // code bytes) are 31-bit.
-  if ((M + 15) / 16 > 65535 || (N + 15) / 16 > INT32_MAX) return RFQ_ERR_SHAPE;
+  // One 256-work-item workgroup per 16 x 16 output block: N/16 along the
+  // grid's x axis, M/16 along its y axis (at most 65535); buffer ranges (X
+  // bytes, weight code bytes) are 31-bit.
+  if (M > 65535 * 16 || N > kMaxWorkItems / 256 * 16) return RFQ_ERR_SHAPE;
   const int64_t limit = int64_t(1) << 31;
   const int64_t xbytes = x_dtype == RFQ_BF16 ? 2 : 4;
   if (M * K >= limit / xbytes || N * (K / 2) >= limit) return RFQ_ERR_SHAPE;
@@ -241,7 +268,7 @@ const char *rfq_status_str(rfq_status s) {
   switch (s) {
     case RFQ_OK: return "ok";
     case RFQ_ERR_NULL: return "null pointer (or half of an optional pair)";
-    case RFQ_ERR_SHAPE: return "bad shape (negative size, or K not a positive multiple of 32)";
+    case RFQ_ERR_SHAPE: return "bad shape (negative size, K not a positive multiple of 32, or a size limit)";
     case RFQ_ERR_DTYPE: return "unknown dtype";
     case RFQ_ERR_ALIGN: return "misaligned pointer";
     case RFQ_ERR_DEVICE: return "no gfx950 device current";

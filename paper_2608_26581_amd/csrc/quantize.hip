@@ -40,6 +40,9 @@ constexpr int kQuantThreads = 64;
 constexpr int kSpanBlocks = 64;                       // blocks per wave span
 constexpr int kSpanCodeBytes = kSpanBlocks * kBlock / 2;
 constexpr int64_t kLastLevelCacheBytes = int64_t(256) << 20;
+// Workgroups of the kernels that loop over their grid (dequantization and
+// the phi map): enough to fill the GPU many times over.
+constexpr int64_t kMaxLoopGrid = int64_t(1) << 16;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
@@ -219,46 +222,50 @@ __global__ __launch_bounds__(kQuantThreads) void quantize_kernel(
 __global__ __launch_bounds__(kThreads) void dequant_kernel(
     const uint32_t *__restrict__ codes, const uint8_t *__restrict__ scales,
     int64_t nchunks, float4 *__restrict__ out) {
-  const int64_t ch = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  if (ch >= nchunks) return;
-  float d[8];
-  decode8(codes[ch], scale_operand(scales[ch >> 2]), d);
-  out[2 * ch] = make_float4(d[0], d[1], d[2], d[3]);
-  out[2 * ch + 1] = make_float4(d[4], d[5], d[6], d[7]);
+  const int64_t stride = (int64_t)gridDim.x * kThreads;
+  for (int64_t ch = (int64_t)blockIdx.x * kThreads + threadIdx.x; ch < nchunks; ch += stride) {
+    float d[8];
+    decode8(codes[ch], scale_operand(scales[ch >> 2]), d);
+    out[2 * ch] = make_float4(d[0], d[1], d[2], d[3]);
+    out[2 * ch + 1] = make_float4(d[4], d[5], d[6], d[7]);
+  }
 }
 
-// Fallback-indicator map over tiles of 64 rows by 256 reduction columns
-// (one workgroup per tile): rule 0 marks tiles where a residual code has a
-// nonzero magnitude, rule 1 tiles holding a primary scale byte >= threshold.
+// Fallback-indicator map over tiles of 64 rows by 256 reduction columns (a
+// workgroup per tile, looping over the grid): rule 0 marks tiles where a
+// residual code has a nonzero magnitude, rule 1 tiles holding a primary
+// scale byte >= threshold.
 __global__ __launch_bounds__(kThreads) void fallback_map_kernel(
     const uint8_t *__restrict__ r_codes, const uint8_t *__restrict__ q_scales, int64_t M,
-    int64_t K, int rule, int threshold, int pcols, uint8_t *__restrict__ phi) {
-  const int64_t p = blockIdx.x / pcols, c = blockIdx.x % pcols;
+    int64_t K, int rule, int threshold, int pcols, int64_t tiles, uint8_t *__restrict__ phi) {
   const int tid = threadIdx.x;
-  const int64_t m = 64 * p + tid / 4;
-  int flag = 0;
-  if (m < M) {
-    if (rule == 0) {
-      const int64_t kb = K / 2;
+  for (int64_t t = blockIdx.x; t < tiles; t += gridDim.x) {
+    const int64_t p = t / pcols, c = t % pcols;
+    const int64_t m = 64 * p + tid / 4;
+    int flag = 0;
+    if (m < M) {
+      if (rule == 0) {
+        const int64_t kb = K / 2;
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int64_t b = 128 * c + 32 * (tid & 3) + 16 * h;
-        if (b < kb) {
-          const u32x4 v = *reinterpret_cast<const u32x4 *>(r_codes + m * kb + b);
-          flag |= ((v.x | v.y | v.z | v.w) & 0x77777777u) != 0;
+        for (int h = 0; h < 2; ++h) {
+          const int64_t b = 128 * c + 32 * (tid & 3) + 16 * h;
+          if (b < kb) {
+            const u32x4 v = *reinterpret_cast<const u32x4 *>(r_codes + m * kb + b);
+            flag |= ((v.x | v.y | v.z | v.w) & 0x77777777u) != 0;
+          }
+        }
+      } else {
+        const int64_t nb = K / 32;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int64_t b = 8 * c + 2 * (tid & 3) + h;
+          if (b < nb) flag |= (int)q_scales[m * nb + b] >= threshold;
         }
       }
-    } else {
-      const int64_t nb = K / 32;
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int64_t b = 8 * c + 2 * (tid & 3) + h;
-        if (b < nb) flag |= (int)q_scales[m * nb + b] >= threshold;
-      }
     }
+    flag = __syncthreads_or(flag);
+    if (tid == 0) phi[t] = (uint8_t)(flag != 0);
   }
-  flag = __syncthreads_or(flag);
-  if (tid == 0) phi[blockIdx.x] = (uint8_t)(flag != 0);
 }
 
 inline unsigned grid_for(int64_t n, int64_t per_block) {
@@ -331,7 +338,8 @@ hipError_t launch_swiglu_quantize(const void *g, const void *u, bool bf16_in,
 hipError_t launch_dequant(const uint8_t *codes, const uint8_t *scales,
                           int64_t nelem, float *out, hipStream_t stream) {
   const int64_t nchunks = nelem / kChunk;
-  dequant_kernel<<<grid_for(nchunks, kThreads), kThreads, 0, stream>>>(
+  const int64_t wgs = (nchunks + kThreads - 1) / kThreads;
+  dequant_kernel<<<(unsigned)(wgs < kMaxLoopGrid ? wgs : kMaxLoopGrid), kThreads, 0, stream>>>(
       reinterpret_cast<const uint32_t *>(codes), scales, nchunks,
       reinterpret_cast<float4 *>(out));
   return hipGetLastError();
@@ -342,8 +350,8 @@ hipError_t launch_fallback_map(const uint8_t *r_codes, const uint8_t *q_scales, 
                                hipStream_t stream) {
   const int pcols = (int)((K + 255) / 256);
   const int64_t tiles = ((M + 63) / 64) * pcols;
-  fallback_map_kernel<<<(unsigned)tiles, kThreads, 0, stream>>>(r_codes, q_scales, M, K, rule,
-                                                                 threshold, pcols, phi);
+  fallback_map_kernel<<<(unsigned)(tiles < kMaxLoopGrid ? tiles : kMaxLoopGrid), kThreads, 0,
+                        stream>>>(r_codes, q_scales, M, K, rule, threshold, pcols, tiles, phi);
   return hipGetLastError();
 }
 

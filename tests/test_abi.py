@@ -241,6 +241,36 @@ def test_gemm_phi_and_fallback_map_validation():
     assert m(A, A, 0, 64, 0, 0, A, None) == OK
 
 
+def test_size_limits():
+    """Sizes past the stated limits are shape errors, reported before any
+    device call (one launch covers at most 2^32 - 1 work items; products of
+    sizes never overflow)."""
+    lib = _lib()
+    q = lib.rfq_quantize_act
+    assert q(A, 1, 4, (1 << 31) + 32, A, A, A, A, None) == ESHAPE      # K above 2^31
+    assert q(A, 1, 1 << 32, 64, A, A, A, A, None) == ESHAPE            # 2^33 MX blocks
+    assert q(A, 1, 1 << 62, 1 << 20, A, A, A, A, None) == ESHAPE       # M * K overflows int64
+    assert q(A, 1, (1 << 32) - 63, 32, A, A, A, A, None) == ESHAPE     # one block too many
+    assert lib.rfq_quantize_weight(A, 0, 1 << 40, 1 << 10, A, A, None) == ESHAPE
+    assert lib.rfq_swiglu_quantize_act(A, A, 1, 1 << 33, 64, A, A, A, A, None, None) == ESHAPE
+    g = lib.rfq_gemm
+    assert g(A, A, A, A, A, A, 1 << 21, 1 << 21, 64, A, 0, None) == ESHAPE   # tile grid > 2^32
+    assert g(A, A, A, A, A, A, 1 << 31, 1, 64, A, 0, None) == ESHAPE         # M not below 2^31
+    assert g(A, A, A, A, A, A, 8, 8, 1 << 40, A, 0, None) == ESHAPE          # K above 2^31
+    f = lib.rfq_gemm_phi
+    assert f(A, A, A, A, A, A, A, 1 << 21, 1 << 21, 64, A, 0, None) == ESHAPE
+    d = lib.rfq_dequant
+    assert d(A, A, 1 << 40, 1 << 20, A, None) == ESHAPE                 # 2^60 elements
+    assert d(A, A, 1 << 62, 64, A, None) == ESHAPE                      # rows * K overflows int64
+    m = lib.rfq_fallback_map
+    assert m(A, A, 1 << 40, 1 << 20, 0, 0, A, None) == ESHAPE
+    s = lib.rfq_gemm_stream
+    assert s(A, 1, 1, A, A, 8, 1 << 28, 512, A, 0, None) == ESHAPE     # 2^24 column slices
+    assert s(A, 1, 1, A, A, 8, 8, 1 << 40, A, 0, None) == ESHAPE       # K above 2^31
+    sw = lib.rfq_gemm_swiglu_quantize
+    assert sw(A, A, A, A, A, A, 64, 1 << 31, 512, A, A, A, A, None, None) == ESHAPE
+
+
 def test_valid_arguments_without_a_gpu_report_device_error():
     import torch
     if torch.cuda.is_available():

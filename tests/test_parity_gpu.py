@@ -213,6 +213,24 @@ def test_dequant_all_codes_and_scales(orc):
     assert np.array_equal(d, want)
 
 
+def test_dequant_beyond_one_grid_pass(orc):
+    """More 8-element chunks than one pass of the dequantization grid covers
+    (65536 workgroups of 256 lanes): every element is written, exactly."""
+    rows, K = 4160, 40960                          # 21.3 M chunks
+    gen = torch.Generator(device="cuda").manual_seed(7)
+    codes = torch.randint(0, 256, (rows, K // 2), dtype=torch.uint8, device="cuda", generator=gen)
+    scales = torch.randint(100, 150, (rows, K // 32), dtype=torch.uint8, device="cuda",
+                           generator=gen)
+    out = torch.full((rows, K), float("nan"), device="cuda")
+    _say("dequant %dx%d (several grid passes)" % (rows, K))
+    rfq.rfq_dequant(codes, scales, out=out)
+    assert not torch.isnan(out).any()
+    wrap_row = 65536 * 256 // (K // 8)             # first row of the second pass
+    sel = [0, 1, wrap_row - 1, wrap_row, wrap_row + 1, rows - 1]
+    got = host(out[sel]).astype(np.float64)
+    assert np.array_equal(got, orc.dequant(host(codes[sel]), host(scales[sel])))
+
+
 # ---------------------------------------------------------------- product
 GEMM_SMALL = [
     ("tiny", 64, 256, 256),
@@ -494,6 +512,41 @@ def test_fallback_map_rules(orc, M, K):
     zphi = rfq.rfq_gemm_phi(*q, *wq, phi0)
     assert torch.equal(zphi.abs(), z1.abs()) and torch.equal(zphi == 0, z1 == 0)
     assert np.array_equal(host(zphi)[host(zphi) != 0], host(z1)[host(z1) != 0])
+
+
+def test_fallback_map_beyond_one_grid_pass():
+    """More tiles than one pass of the map's grid (65536 workgroups): every
+    tile is decided.  Codes and scales are zero except for chosen bytes, so
+    the expected maps follow from the construction: rule 0 marks a tile where
+    a residual code has a nonzero magnitude (negative zero, code 0x8, does not
+    count); rule 1 where a primary scale byte reaches the threshold."""
+    M, K = 64 * 257 + 5, 256 * 256                 # 258 x 256 = 66048 tiles
+    pr, pc = (M + 63) // 64, K // 256
+    rng = np.random.default_rng(11)
+    tiles = np.unique(np.concatenate([rng.integers(0, pr * pc, 3000),
+                                      [0, 65535, 65536, 65537, pr * pc - 1]]))
+    p, c = tiles // pc, tiles % pc
+    m = np.minimum(64 * p + rng.integers(0, 64, tiles.size), M - 1)
+    # Residual codes: one byte per chosen tile; 0x80, 0x88 and 0x08 hold only
+    # zero magnitudes.
+    byte = 128 * c + rng.integers(0, 128, tiles.size)
+    val = rng.choice(np.uint8([0x01, 0x70, 0x80, 0x88, 0x08, 0x3B]), tiles.size)
+    rc = torch.zeros((M, K // 2), dtype=torch.uint8, device="cuda")
+    rc[torch.from_numpy(m).cuda(), torch.from_numpy(byte).cuda()] = torch.from_numpy(val).cuda()
+    want0 = np.zeros((pr, pc), np.uint8)
+    want0[p[(val & 0x77) != 0], c[(val & 0x77) != 0]] = 1
+    # Primary scale bytes: one per chosen tile, below, at or above the threshold.
+    thr = 131
+    kb = 8 * c + rng.integers(0, 8, tiles.size)
+    sv = rng.choice(np.uint8([thr - 1, thr, 255, 1]), tiles.size)
+    qs = torch.zeros((M, K // 32), dtype=torch.uint8, device="cuda")
+    qs[torch.from_numpy(m).cuda(), torch.from_numpy(kb).cuda()] = torch.from_numpy(sv).cuda()
+    want1 = np.zeros((pr, pc), np.uint8)
+    want1[p[sv >= thr], c[sv >= thr]] = 1
+    _say("fallback map M=%d K=%d (%d tiles)" % (M, K, pr * pc))
+    assert np.array_equal(host(rfq.rfq_fallback_map(rc, qs, rfq.RFQ_PHI_RESIDUAL_NONZERO)), want0)
+    assert np.array_equal(host(rfq.rfq_fallback_map(None, qs, rfq.RFQ_PHI_SCALE_AT_LEAST, thr)),
+                          want1)
 
 
 # --------------------------------------------------- fused SwiGLU epilogue
