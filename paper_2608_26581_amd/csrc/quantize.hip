@@ -103,7 +103,7 @@ __device__ __forceinline__ void unpack(const u32x4 &w, float (&v)[BF16_IN ? 8 : 
 
 // Wave-private staging of one code stream: the span's codes in tensor order,
 // then its scale bytes.
-struct Stage {
+struct alignas(16) Stage {
   uint8_t codes[kSpanCodeBytes];
   uint8_t scales[kSpanBlocks];
 };
