@@ -228,12 +228,12 @@ rfq_status rfq_gemm_swiglu_quantize(const uint8_t *q_codes, const uint8_t *q_sca
  *            only (plain MXFP4, phi = 0).
  *   w_codes  [N][K/2], w_scales [N][K/32]: rfq_quantize_weight output;
  *            both 16-byte aligned.
- *   M, N, K: K a multiple of 512; M at most 1048560 (65535 row slices of
- *            16); N at most 268435440 (2^24 - 1 column slices of 16); X and
- *            the weight codes below 2 GiB each.
+ *   M, N, K: K a multiple of 512; M at most 1048560; N at most 268435440
+ *            (2^24 - 1 column slices of 16); X and the weight codes below
+ *            2 GiB each.
  *   z        [M][N] row-major, z_dtype; 16-byte aligned.
- * For M <= 64 the result is bit-identical to rfq_quantize_act followed by
- * rfq_gemm (which multiplies such few rows with the same kernel structure);
+ * For M <= 128 the result is bit-identical to rfq_quantize_act followed by
+ * rfq_gemm (which multiplies such few rows in the same accumulation order);
  * otherwise it agrees within the product's rounding (fp32 accumulation in an
  * unspecified order).  Errors: RFQ_ERR_SHAPE for the shape conditions above,
  * otherwise as rfq_gemm.  Asynchronous on hip_stream.

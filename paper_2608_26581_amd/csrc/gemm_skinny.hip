@@ -10,10 +10,10 @@
 //
 // With few rows the product is bound by streaming W's codes from memory, and
 // the large-tile kernels (256 activation rows per tile) would leave most of the
-// chip idle.  Here a workgroup owns 16 rows of W (one fragment) and 16
-// activation rows, and its four waves split K into four contiguous ranges;
-// the four partial 16 x 16 results are summed in a fixed order through LDS.
-// The grid is (N/16) x (M/16) workgroups, so W is read once per 16
+// chip idle.  Here a workgroup owns 32 rows of W (two fragments; one in the
+// streaming form) and up to four 16-row activation slices, and its four waves
+// split K into four contiguous ranges; the partial 16 x 16 results of the
+// waves are summed in a fixed order through LDS.  W is read once per 64
 // activation rows.
 //
 // Instruction: v_mfma_scale_f32_16x16x128_f8f6f4 with E2M1 operands (format
@@ -26,9 +26,10 @@
 // issues the next group's loads before multiplying the current one.  Per
 // group a lane loads 4 x 16 code bytes of its W row and the 16 scale bytes of
 // the row's group (scale byte of k-step j, lane group g: byte g of word j);
-// codes in, the same for q and r.  Rows past M or N are clamped to the last
-// row for loading: an activation row only reaches its own output column of
-// the MFMA result, and those columns are not stored.
+// codes in, the same for q and r of each slice, one slice ahead.  W rows past
+// N are clamped to the last row for loading, activation rows past M to the
+// last row or to zeros: an activation row only reaches its own output column
+// of the MFMA result, and those columns are not stored.
 //
 // Streaming form: per group, the wave first quantizes the activation blocks
 // of its 16-row slice that exist (rows < M), one block per lane and 64 blocks
@@ -117,21 +118,10 @@ __device__ __forceinline__ void quantize_block(const float (&v)[E], u32x4 &qc, u
   rc = u32x4{c[0], c[1], c[2], c[3]};
 }
 
-// Fixed-order sum of the four waves' partial 16 x 16 results and the store
-// of Z (rows m0 + l mod 16, columns n0 + 4 (l/16) .. +3).
+// Store of one 16 x 16 result: Z rows m0 + l mod 16, columns n0 + 4 (l/16) .. +3.
 template <bool ZBF16>
-__device__ __forceinline__ void reduce_store(v4f (&partial)[kSkThreads / 64][64], const v4f &acc,
-                                             int wave, int lane, int64_t m0, int64_t n0,
-                                             int64_t M, int64_t N, void *z) {
-  partial[wave][lane] = acc;
-  __syncthreads();
-  if (wave != 0) return;
-  v4f s = partial[0][lane];
-#pragma unroll
-  for (int w = 1; w < kSkThreads / 64; ++w) {
-    const v4f p = partial[w][lane];
-    s = v4f{s[0] + p[0], s[1] + p[1], s[2] + p[2], s[3] + p[3]};
-  }
+__device__ __forceinline__ void store_tile(const v4f &s, int lane, int64_t m0, int64_t n0,
+                                           int64_t M, int64_t N, void *z) {
   const int64_t m = m0 + (lane & 15);
   const int64_t n = n0 + 4 * (lane >> 4);
   if (m >= M) return;
@@ -159,20 +149,48 @@ __device__ __forceinline__ void reduce_store(v4f (&partial)[kSkThreads / 64][64]
   }
 }
 
-template <bool RES, bool ZBF16>
-__global__ __launch_bounds__(kSkThreads) void rfq_gemm_skinny_kernel(
+// Fixed-order sum of the four waves' partial 16 x 16 results and its store.
+template <bool ZBF16>
+__device__ __forceinline__ void reduce_store(v4f (&partial)[kSkThreads / 64][64], const v4f &acc,
+                                             int wave, int lane, int64_t m0, int64_t n0,
+                                             int64_t M, int64_t N, void *z) {
+  partial[wave][lane] = acc;
+  __syncthreads();
+  if (wave != 0) return;
+  v4f s = partial[0][lane];
+#pragma unroll
+  for (int w = 1; w < kSkThreads / 64; ++w) {
+    const v4f p = partial[w][lane];
+    s = v4f{s[0] + p[0], s[1] + p[1], s[2] + p[2], s[3] + p[3]};
+  }
+  store_tile<ZBF16>(s, lane, m0, n0, M, N, z);
+}
+
+// Codes in: a workgroup owns kSkFrags fragments of W (32 rows) and up to S
+// activation slices of 16 rows.  Each wave holds a group of W in registers
+// while it multiplies every slice against it, so W is read once per launch
+// (for M <= 16 S) and the activation codes once per 32 W rows.  The next
+// slice's codes (or the next group's first slice) are loaded while the
+// current one is multiplied.  Per output the accumulation order is that of
+// a single slice: groups, k-steps, primary then residual, then the
+// fixed-order sum over the four waves.
+constexpr int kSkFrags = 2;
+struct WPair { WGroup f[kSkFrags]; };
+
+template <bool RES, bool ZBF16, int S>
+__global__ __launch_bounds__(kSkThreads, 2) void rfq_gemm_skinny_kernel(
     const uint8_t *__restrict__ qc, const uint8_t *__restrict__ qs,
     const uint8_t *__restrict__ rc, const uint8_t *__restrict__ rs,
     const uint8_t *__restrict__ wc, const uint8_t *__restrict__ ws, int64_t M, int64_t N,
     int64_t K, void *__restrict__ z) {
-  __shared__ v4f partial[kSkThreads / 64][64];
+  __shared__ v4f partial[kSkThreads / 64][kSkFrags * S][64];
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int row = lane & 15, g = lane >> 4;
-  const int64_t n0 = (int64_t)blockIdx.x * kSkRows, m0 = (int64_t)blockIdx.y * kSkRows;
-  const int64_t wn = min(n0 + row, N - 1);
-  const int64_t xm = min(m0 + row, M - 1);
+  const int64_t n0 = (int64_t)blockIdx.x * (kSkFrags * kSkRows);
+  const int64_t m0 = (int64_t)blockIdx.y * (S * kSkRows);
+  const int slices = (int)min<int64_t>(S, (M - m0 + kSkRows - 1) / kSkRows);
   const int64_t kbytes = K / 2, kblocks = K / 32;
 
   // This wave's groups of 4 k-steps: [gb, ge) of K / 512.
@@ -180,23 +198,32 @@ __global__ __launch_bounds__(kSkThreads) void rfq_gemm_skinny_kernel(
   const int gb = (ngroups * wave) / 4, ge = (ngroups * (wave + 1)) / 4;
 
   const __amdgpu_buffer_rsrc_t rwc = rsrc(wc, N * kbytes), rws = rsrc(ws, N * kblocks);
-  const uint32_t w_off = (uint32_t)wn * (uint32_t)kbytes + 16 * g;
-  const uint32_t ws_off = (uint32_t)wn * (uint32_t)kblocks;
-  auto load_w = [&](WGroup &w, int gi) {
+  uint32_t w_off[kSkFrags], ws_off[kSkFrags];
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      w.c[j] = __builtin_amdgcn_raw_buffer_load_b128(rwc, w_off, gi * (kSkGroupK / 2) + 64 * j, 0);
-    w.s = __builtin_amdgcn_raw_buffer_load_b128(rws, ws_off, gi * (kSkGroupK / 32), 0);
+  for (int f = 0; f < kSkFrags; ++f) {
+    const int64_t wn = min(n0 + kSkRows * f + row, N - 1);
+    w_off[f] = (uint32_t)wn * (uint32_t)kbytes + 16 * g;
+    ws_off[f] = (uint32_t)wn * (uint32_t)kblocks;
+  }
+  auto load_w = [&](WPair &w, int gi) {
+#pragma unroll
+    for (int f = 0; f < kSkFrags; ++f) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        w.f[f].c[j] = __builtin_amdgcn_raw_buffer_load_b128(rwc, w_off[f],
+                                                            gi * (kSkGroupK / 2) + 64 * j, 0);
+      w.f[f].s = __builtin_amdgcn_raw_buffer_load_b128(rws, ws_off[f], gi * (kSkGroupK / 32), 0);
+    }
   };
 
   const __amdgpu_buffer_rsrc_t rxa = rsrc(qc, M * kbytes), rxb = rsrc(RES ? rc : qc, M * kbytes);
   const __amdgpu_buffer_rsrc_t rxs = rsrc(qs, M * kblocks), rxt = rsrc(RES ? rs : qs, M * kblocks);
-  const uint32_t xc_off = (uint32_t)xm * (uint32_t)kbytes + 16 * g;
-  const uint32_t xs_off = (uint32_t)xm * (uint32_t)kblocks;
-  v4f acc = v4f{0.0f, 0.0f, 0.0f, 0.0f};
-
-  // W and activation codes of a whole group in flight.
-  auto load_x = [&](XGroup &xg, int gi) {
+  // Activation codes of slice sl of group gi (rows past M clamped to the last).
+  auto load_x = [&](XGroup &xg, int gi, int sl) {
+    const uint32_t xm = (uint32_t)min(m0 + kSkRows * sl + row, M - 1);
+    const bool live = sl < slices;
+    const uint32_t xc_off = live ? xm * (uint32_t)kbytes + 16 * g : 0x80000000u;
+    const uint32_t xs_off = live ? xm * (uint32_t)kblocks : 0x80000000u;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       xg.q[j] = __builtin_amdgcn_raw_buffer_load_b128(rxa, xc_off, gi * (kSkGroupK / 2) + 64 * j, 0);
@@ -207,33 +234,74 @@ __global__ __launch_bounds__(kSkThreads) void rfq_gemm_skinny_kernel(
     if constexpr (RES)
       xg.rs = __builtin_amdgcn_raw_buffer_load_b128(rxt, xs_off, gi * (kSkGroupK / 32), 0);
   };
-  auto compute = [&](const WGroup &w, const XGroup &xg) {
+
+  v4f acc[S][kSkFrags];
+#pragma unroll
+  for (int sl = 0; sl < S; ++sl)
+#pragma unroll
+    for (int f = 0; f < kSkFrags; ++f) acc[sl][f] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+
+  auto compute = [&](const WPair &w, const XGroup &xg, v4f (&a)[kSkFrags]) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const uint32_t wsc = scale_of(w.s, j, g);
-      acc = mma16(w.c[j], wsc, xg.q[j], scale_of(xg.qs, j, g), acc);
-      if constexpr (RES) acc = mma16(w.c[j], wsc, xg.r[j], scale_of(xg.rs, j, g), acc);
+#pragma unroll
+      for (int f = 0; f < kSkFrags; ++f) {
+        const uint32_t wsc = scale_of(w.f[f].s, j, g);
+        a[f] = mma16(w.f[f].c[j], wsc, xg.q[j], scale_of(xg.qs, j, g), a[f]);
+        if constexpr (RES) a[f] = mma16(w.f[f].c[j], wsc, xg.r[j], scale_of(xg.rs, j, g), a[f]);
+      }
+    }
+  };
+  // One group: every slice against the group's W.  Slice sl of the group is
+  // in buffer xa for even sl and xb for odd sl; at each slice the following
+  // unit (the next slice, or the next group's first slice) is requested into
+  // the other buffer before the current one is waited for.  Slices past M
+  // load zeros without touching memory and skip their MFMAs.  With S even
+  // the next group again starts in xa; with S = 1 the buffers swap roles.
+  auto group = [&](const WPair &w, int gi, XGroup &xa, XGroup &xb) {
+#pragma unroll
+    for (int sl = 0; sl < S; ++sl) {
+      XGroup &cur = (sl & 1) ? xb : xa;
+      XGroup &nxt = (sl & 1) ? xa : xb;
+      if (sl + 1 < S) load_x(nxt, gi, sl + 1);
+      else if (gi + 1 < ge) load_x(nxt, gi + 1, 0);
+      if (sl < slices) compute(w, cur, acc[sl]);
     }
   };
   if (gb < ge) {
-    WGroup w0, w1;
-    XGroup x0, x1;
+    WPair w0, w1;
+    XGroup xa, xb;
     load_w(w0, gb);
-    load_x(x0, gb);
+    load_x(xa, gb, 0);
     int gi = gb;
     for (; gi + 1 < ge; gi += 2) {
       load_w(w1, gi + 1);
-      load_x(x1, gi + 1);
-      compute(w0, x0);
-      if (gi + 2 < ge) {
-        load_w(w0, gi + 2);
-        load_x(x0, gi + 2);
-      }
-      compute(w1, x1);
+      group(w0, gi, xa, xb);
+      if (gi + 2 < ge) load_w(w0, gi + 2);
+      if constexpr (S % 2 == 0) group(w1, gi + 1, xa, xb);
+      else group(w1, gi + 1, xb, xa);
     }
-    if (gi < ge) compute(w0, x0);
+    if (gi < ge) group(w0, gi, xa, xb);
   }
-  reduce_store<ZBF16>(partial, acc, wave, lane, m0, n0, M, N, z);
+
+  // Fixed-order sum over the four waves; output (fragment f, slice sl) is
+  // summed and stored by wave (f S + sl) mod 4.
+#pragma unroll
+  for (int f = 0; f < kSkFrags; ++f)
+#pragma unroll
+    for (int sl = 0; sl < S; ++sl) partial[wave][f * S + sl][lane] = acc[sl][f];
+  __syncthreads();
+  for (int p = wave; p < kSkFrags * S; p += kSkThreads / 64) {
+    const int f = p / S, sl = p % S;
+    if (sl >= slices) continue;
+    v4f s = partial[0][p][lane];
+#pragma unroll
+    for (int w = 1; w < kSkThreads / 64; ++w) {
+      const v4f q = partial[w][p][lane];
+      s = v4f{s[0] + q[0], s[1] + q[1], s[2] + q[2], s[3] + q[3]};
+    }
+    store_tile<ZBF16>(s, lane, m0 + kSkRows * sl, n0 + kSkRows * f, M, N, z);
+  }
 }
 
 // Wave-private LDS area of the streaming form: the codes of one group (16
@@ -248,11 +316,17 @@ struct alignas(16) StreamArea {
   uint8_t rs[kSkRows * kGroupBlocks];
 };
 
-template <bool RES, bool ZBF16, bool XF32>
-__global__ __launch_bounds__(kSkThreads) void rfq_gemm_stream_kernel(
+// The streaming form holds one W fragment per workgroup (16 rows): with the
+// quantizer's registers a second fragment would spill.
+constexpr int kStFrags = 1;
+struct StW { WGroup f[kStFrags]; };
+
+// (fp32 input: one wave per SIMD; its registers do not fit two without spilling.)
+template <bool RES, bool ZBF16, bool XF32, int S>
+__global__ __launch_bounds__(kSkThreads, XF32 ? 1 : 2) void rfq_gemm_stream_kernel(
     const void *__restrict__ x, const uint8_t *__restrict__ wc, const uint8_t *__restrict__ ws,
     int64_t M, int64_t N, int64_t K, void *__restrict__ z) {
-  __shared__ v4f partial[kSkThreads / 64][64];
+  __shared__ v4f partial[kSkThreads / 64][kStFrags * S][64];
   __shared__ StreamArea area[kSkThreads / 64];
   constexpr int kElem = XF32 ? 4 : 2;
   constexpr int kPieces = 32 * kElem / 16;        // 16-byte loads per block
@@ -260,43 +334,54 @@ __global__ __launch_bounds__(kSkThreads) void rfq_gemm_stream_kernel(
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int row = lane & 15, g = lane >> 4;
-  const int64_t n0 = (int64_t)blockIdx.x * kSkRows, m0 = (int64_t)blockIdx.y * kSkRows;
-  const int64_t wn = min(n0 + row, N - 1);
+  const int64_t n0 = (int64_t)blockIdx.x * (kStFrags * kSkRows);
+  const int64_t m0 = (int64_t)blockIdx.y * (S * kSkRows);
+  const int slices = (int)min<int64_t>(S, (M - m0 + kSkRows - 1) / kSkRows);
   const int64_t kbytes = K / 2, kblocks = K / 32;
   const int ngroups = (int)(K / kSkGroupK);
   const int gb = (ngroups * wave) / 4, ge = (ngroups * (wave + 1)) / 4;
 
   const __amdgpu_buffer_rsrc_t rwc = rsrc(wc, N * kbytes), rws = rsrc(ws, N * kblocks);
-  const uint32_t w_off = (uint32_t)wn * (uint32_t)kbytes + 16 * g;
-  const uint32_t ws_off = (uint32_t)wn * (uint32_t)kblocks;
-  auto load_w = [&](WGroup &w, int gi) {
+  uint32_t w_off[kStFrags], ws_off[kStFrags];
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      w.c[j] = __builtin_amdgcn_raw_buffer_load_b128(rwc, w_off, gi * (kSkGroupK / 2) + 64 * j, 0);
-    w.s = __builtin_amdgcn_raw_buffer_load_b128(rws, ws_off, gi * (kSkGroupK / 32), 0);
+  for (int f = 0; f < kStFrags; ++f) {
+    const int64_t wn = min(n0 + kSkRows * f + row, N - 1);
+    w_off[f] = (uint32_t)wn * (uint32_t)kbytes + 16 * g;
+    ws_off[f] = (uint32_t)wn * (uint32_t)kblocks;
+  }
+  auto load_w = [&](StW &w, int gi) {
+#pragma unroll
+    for (int f = 0; f < kStFrags; ++f) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        w.f[f].c[j] = __builtin_amdgcn_raw_buffer_load_b128(rwc, w_off[f],
+                                                            gi * (kSkGroupK / 2) + 64 * j, 0);
+      w.f[f].s = __builtin_amdgcn_raw_buffer_load_b128(rws, ws_off[f], gi * (kSkGroupK / 32), 0);
+    }
   };
 
-  // Quantization rounds: in round rd lane l takes block t = 64 rd + l of the
-  // group, row t / 16 and block t mod 16 of the slice; rows that exist are
-  // [0, live).  Lanes past them load nothing (offsets beyond the buffer
-  // return zeros without touching memory) and write nothing.
-  const int live = (int)min<int64_t>(kSkRows, M - m0);
-  const int rounds = (live * kGroupBlocks + 63) / 64;
-  const __amdgpu_buffer_rsrc_t rx = rsrc(x, M * K * kElem);
-  auto x_off = [&](int rd) {
-    const int t = 64 * rd + lane;
-    return (t >> 4) < live ? (uint32_t)(((m0 + (t >> 4)) * K + 32 * (t & 15)) * kElem)
-                           : 0x80000000u;
+  // Quantization rounds of slice sl: in round rd lane l takes block
+  // t = 64 rd + l of the group, row t / 16 and block t mod 16 of the slice;
+  // the slice's rows that exist are [0, live(sl)).  Lanes past them load
+  // nothing (offsets beyond the buffer return zeros without touching
+  // memory) and write nothing.
+  auto live_rows = [&](int sl) {
+    return (int)max<int64_t>(0, min<int64_t>(kSkRows, M - m0 - kSkRows * sl));
   };
+  const __amdgpu_buffer_rsrc_t rx = rsrc(x, M * K * kElem);
   struct XRound { u32x4 v[kPieces]; };
-  auto load_round = [&](XRound &xr, int gi, int rd) {
-    const uint32_t off = x_off(rd);
+  auto load_round = [&](XRound &xr, int gi, int sl, int rd) {
+    const int t = 64 * rd + lane;
+    const uint32_t off =
+        (t >> 4) < live_rows(sl)
+            ? (uint32_t)(((m0 + kSkRows * sl + (t >> 4)) * K + 32 * (t & 15)) * kElem)
+            : 0x80000000u;
 #pragma unroll
     for (int p = 0; p < kPieces; ++p)
       xr.v[p] = __builtin_amdgcn_raw_buffer_load_b128(rx, off, gi * kSkGroupK * kElem + 16 * p, 0);
   };
   StreamArea &A = area[wave];
-  auto quantize_round = [&](const XRound &xr, int rd) {
+  auto quantize_round = [&](const XRound &xr, int live, int rd) {
     const int t = 64 * rd + lane;
     const int xr_row = t >> 4, xb = t & 15;
     if (xr_row >= live) return;
@@ -330,27 +415,32 @@ __global__ __launch_bounds__(kSkThreads) void rfq_gemm_stream_kernel(
     }
   };
 
-  v4f acc = v4f{0.0f, 0.0f, 0.0f, 0.0f};
-  // One group: quantize its rounds into the LDS area (xn holds round 0 on
-  // entry and round 0 of the next group on exit), then multiply it.
+  // One unit (group gi, slice sl): quantize the slice's blocks of the group
+  // into the LDS area (xn holds the unit's round 0 on entry and the next
+  // unit's round 0 on exit), then multiply them with both W fragments.
+  // Units run slice by slice, so only one slice's accumulators are live (the
+  // slices' passes over the wave's W range re-read it from L2).
   XRound xn, xa, xb;
-  auto group = [&](const WGroup &w, int gi) {
+  auto unit = [&](const StW &w, int gi, int sl, v4f (&a)[kStFrags]) {
+    const int live = live_rows(sl);
+    const int rounds = (live * kGroupBlocks + 63) / 64;
     xa = xn;
-    if (rounds > 1) load_round(xb, gi, 1);
-    if (gi + 1 < ge) load_round(xn, gi + 1, 0);
-    quantize_round(xa, 0);
+    if (rounds > 1) load_round(xb, gi, sl, 1);
+    if (gi + 1 < ge) load_round(xn, gi + 1, sl, 0);
+    else if (sl + 1 < slices) load_round(xn, gb, sl + 1, 0);
+    quantize_round(xa, live, 0);
     if (rounds > 1) {
-      if (rounds > 2) load_round(xa, gi, 2);
-      quantize_round(xb, 1);
+      if (rounds > 2) load_round(xa, gi, sl, 2);
+      quantize_round(xb, live, 1);
       if (rounds > 2) {
-        if (rounds > 3) load_round(xb, gi, 3);
-        quantize_round(xa, 2);
-        if (rounds > 3) quantize_round(xb, 3);
+        if (rounds > 3) load_round(xb, gi, sl, 3);
+        quantize_round(xa, live, 2);
+        if (rounds > 3) quantize_round(xb, live, 3);
       }
     }
     // The area is private to the wave and LDS serves a wave's accesses in
     // order: the writes above are seen by the reads below, and the reads
-    // below precede the next group's writes.
+    // below precede the next unit's writes.
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     const u32x4 sq = *reinterpret_cast<const u32x4 *>(A.qs + row * kGroupBlocks);
@@ -358,51 +448,92 @@ __global__ __launch_bounds__(kSkThreads) void rfq_gemm_stream_kernel(
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int chunk = 16 * (row * kGroupBlocks + ((4 * j + g) ^ row));
-      const uint32_t wsc = scale_of(w.s, j, g);
-      acc = mma16(w.c[j], wsc, *reinterpret_cast<const u32x4 *>(A.q + chunk), scale_of(sq, j, g),
-                  acc);
-      if constexpr (RES)
-        acc = mma16(w.c[j], wsc, *reinterpret_cast<const u32x4 *>(A.r + chunk),
-                    scale_of(sr, j, g), acc);
+      const u32x4 cq = *reinterpret_cast<const u32x4 *>(A.q + chunk);
+      const u32x4 cr = RES ? *reinterpret_cast<const u32x4 *>(A.r + chunk) : cq;
+#pragma unroll
+      for (int f = 0; f < kStFrags; ++f) {
+        const uint32_t wsc = scale_of(w.f[f].s, j, g);
+        a[f] = mma16(w.f[f].c[j], wsc, cq, scale_of(sq, j, g), a[f]);
+        if constexpr (RES) a[f] = mma16(w.f[f].c[j], wsc, cr, scale_of(sr, j, g), a[f]);
+      }
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
   };
-  if (gb < ge) {
-    WGroup w0, w1;
-    load_w(w0, gb);
-    load_round(xn, gb, 0);
-    int gi = gb;
-    for (; gi + 1 < ge; gi += 2) {
-      load_w(w1, gi + 1);
-      group(w0, gi);
-      if (gi + 2 < ge) load_w(w0, gi + 2);
-      group(w1, gi + 1);
+  if (gb < ge) load_round(xn, gb, 0, 0);
+  for (int sl = 0; sl < slices; ++sl) {
+    v4f a[kStFrags];
+#pragma unroll
+    for (int f = 0; f < kStFrags; ++f) a[f] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+    if (gb < ge) {
+      StW w0, w1;
+      load_w(w0, gb);
+      int gi = gb;
+      for (; gi + 1 < ge; gi += 2) {
+        load_w(w1, gi + 1);
+        unit(w0, gi, sl, a);
+        if (gi + 2 < ge) load_w(w0, gi + 2);
+        unit(w1, gi + 1, sl, a);
+      }
+      if (gi < ge) unit(w0, gi, sl, a);
     }
-    if (gi < ge) group(w0, gi);
+#pragma unroll
+    for (int f = 0; f < kStFrags; ++f) partial[wave][f * S + sl][lane] = a[f];
   }
-  reduce_store<ZBF16>(partial, acc, wave, lane, m0, n0, M, N, z);
+
+  // Fixed-order sum over the four waves, as in the codes-in form.
+  __syncthreads();
+  for (int p = wave; p < kStFrags * S; p += kSkThreads / 64) {
+    const int f = p / S, sl = p % S;
+    if (sl >= slices) continue;
+    v4f s = partial[0][p][lane];
+#pragma unroll
+    for (int w = 1; w < kSkThreads / 64; ++w) {
+      const v4f q = partial[w][p][lane];
+      s = v4f{s[0] + q[0], s[1] + q[1], s[2] + q[2], s[3] + q[3]};
+    }
+    store_tile<ZBF16>(s, lane, m0 + kSkRows * sl, n0 + kSkRows * f, M, N, z);
+  }
 }
 
-inline dim3 skinny_grid(int64_t M, int64_t N) {
-  return dim3((unsigned)((N + kSkRows - 1) / kSkRows), (unsigned)((M + kSkRows - 1) / kSkRows));
+template <bool RES, bool ZBF16, int S>
+hipError_t launch_sk_s(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc, const uint8_t *rs,
+                       const uint8_t *wc, const uint8_t *ws, int64_t M, int64_t N, int64_t K,
+                       void *z, hipStream_t stream) {
+  const dim3 grid((unsigned)((N + kSkFrags * kSkRows - 1) / (kSkFrags * kSkRows)),
+                  (unsigned)((M + S * kSkRows - 1) / (S * kSkRows)));
+  rfq_gemm_skinny_kernel<RES, ZBF16, S><<<grid, dim3(kSkThreads), 0, stream>>>(
+      qc, qs, rc, rs, wc, ws, M, N, K, z);
+  return hipGetLastError();
 }
 
+// Slices per workgroup: the fewest of 1, 2 or 4 that cover M's rows, at most
+// 4 (more slices per workgroup make the kernel spill, measured slower).
 template <bool RES, bool ZBF16>
 hipError_t launch_sk(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc, const uint8_t *rs,
                      const uint8_t *wc, const uint8_t *ws, int64_t M, int64_t N, int64_t K,
                      void *z, hipStream_t stream) {
-  rfq_gemm_skinny_kernel<RES, ZBF16><<<skinny_grid(M, N), dim3(kSkThreads), 0, stream>>>(
-      qc, qs, rc, rs, wc, ws, M, N, K, z);
+  if (M <= kSkRows) return launch_sk_s<RES, ZBF16, 1>(qc, qs, rc, rs, wc, ws, M, N, K, z, stream);
+  if (M <= 2 * kSkRows) return launch_sk_s<RES, ZBF16, 2>(qc, qs, rc, rs, wc, ws, M, N, K, z, stream);
+  return launch_sk_s<RES, ZBF16, 4>(qc, qs, rc, rs, wc, ws, M, N, K, z, stream);
+}
+
+template <bool RES, bool ZBF16, bool XF32, int S>
+hipError_t launch_st_s(const void *x, const uint8_t *wc, const uint8_t *ws, int64_t M, int64_t N,
+                       int64_t K, void *z, hipStream_t stream) {
+  const dim3 grid((unsigned)((N + kStFrags * kSkRows - 1) / (kStFrags * kSkRows)),
+                  (unsigned)((M + S * kSkRows - 1) / (S * kSkRows)));
+  rfq_gemm_stream_kernel<RES, ZBF16, XF32, S><<<grid, dim3(kSkThreads), 0, stream>>>(
+      x, wc, ws, M, N, K, z);
   return hipGetLastError();
 }
 
 template <bool RES, bool ZBF16, bool XF32>
 hipError_t launch_st(const void *x, const uint8_t *wc, const uint8_t *ws, int64_t M, int64_t N,
                      int64_t K, void *z, hipStream_t stream) {
-  rfq_gemm_stream_kernel<RES, ZBF16, XF32><<<skinny_grid(M, N), dim3(kSkThreads), 0, stream>>>(
-      x, wc, ws, M, N, K, z);
-  return hipGetLastError();
+  if (M <= kSkRows) return launch_st_s<RES, ZBF16, XF32, 1>(x, wc, ws, M, N, K, z, stream);
+  if (M <= 2 * kSkRows) return launch_st_s<RES, ZBF16, XF32, 2>(x, wc, ws, M, N, K, z, stream);
+  return launch_st_s<RES, ZBF16, XF32, 4>(x, wc, ws, M, N, K, z, stream);
 }
 
 }  // namespace

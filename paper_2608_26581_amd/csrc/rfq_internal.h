@@ -70,8 +70,8 @@ hipError_t launch_gemm_large(const uint8_t *q_codes, const uint8_t *q_scales,
 
 // Product for few activation rows (M <= kSkinnyMaxRows, K a multiple of 512,
 // 16-byte aligned scale tensors, code tensors below 2 GiB): one workgroup per
-// 16 weight rows and 16 activation rows.
-constexpr int64_t kSkinnyMaxRows = 64;
+// 32 weight rows and up to 64 activation rows.
+constexpr int64_t kSkinnyMaxRows = 128;
 bool gemm_skinny_applies(const uint8_t *q_scales, const uint8_t *r_scales,
                          const uint8_t *w_scales, int64_t M, int64_t N, int64_t K);
 hipError_t launch_gemm_skinny(const uint8_t *q_codes, const uint8_t *q_scales,

@@ -245,6 +245,9 @@ GEMM_SMALL = [
     ("qwen", 1, 300, 512),
     ("qwen", 16, 256, 1024),
     ("qwen", 37, 130, 2048),          # three row slices, ragged
+    ("qwen", 65, 33, 1536),           # five row slices in one workgroup row
+    ("qwen", 100, 300, 1024),         # two workgroup rows of up to 64 rows
+    ("qwen", 128, 260, 512),          # the few-row kernel's largest M
     ("wan", 64, 200, 5120),           # K range split unevenly over the waves
     ("qwen", 5, 1, 512),
 ]
@@ -297,7 +300,8 @@ STREAM = [
     ("qwen", 16, 256, 1024),
     ("qwen", 37, 130, 2048),
     ("wan", 64, 200, 5120),
-    ("qwen", 100, 97, 512),           # more rows than the codes path's skinny kernel
+    ("qwen", 100, 97, 512),           # two workgroup rows, the second ragged
+    ("qwen", 150, 97, 1024),          # more rows than the codes path's few-row kernel
 ]
 
 
@@ -321,11 +325,14 @@ def test_gemm_stream_matches_oracle(orc, name, M, N, K, xdt, residual, out_dtype
     assert_gemm_close(zh, zr, bound, out_dtype == torch.bfloat16, "gemm_stream %s" % name)
 
 
-@pytest.mark.parametrize("M,N,K", [(1, 300, 512), (16, 256, 1024), (64, 200, 5120), (23, 515, 2048)])
+@pytest.mark.parametrize("M,N,K", [(1, 300, 512), (16, 256, 1024), (64, 200, 5120), (23, 515, 2048),
+                                   (65, 97, 1536), (128, 300, 512), (100, 33, 2048)])
 @pytest.mark.parametrize("residual", [True, False])
 def test_gemm_stream_bit_identical_to_quantize_then_gemm(M, N, K, residual):
-    """Up to 64 rows both forms run the same product structure on the same
-    codes: the streaming form must reproduce quantize + product bit for bit."""
+    """Up to 128 rows both forms accumulate every output in the same order
+    (groups, k-steps, primary then residual, the same four-wave sum) on the
+    same codes: the streaming form must reproduce quantize + product bit for
+    bit."""
     data = _gemm_case("qwen", M, N, K, seed=M * N + K)
     x = dev_bf16(data["x_bf16"])
     w = rfq.rfq_quantize_weight(dev(data["w"]))
@@ -338,7 +345,8 @@ def test_gemm_stream_bit_identical_to_quantize_then_gemm(M, N, K, residual):
                            zc.view(torch.int16) if dt == torch.bfloat16 else zc.view(torch.int32))
 
 
-@pytest.mark.parametrize("M,N,K", [(1, 12288, 4096), (16, 12288, 4096), (8, 4096, 12288)])
+@pytest.mark.parametrize("M,N,K", [(1, 12288, 4096), (16, 12288, 4096), (8, 4096, 12288),
+                                   (100, 4096, 4096)])
 def test_decode_shapes_full(orc, M, N, K):
     """Decode-sized products at the workloads' weight shapes, every output
     checked, in both forms (codes in and streaming)."""
