@@ -110,9 +110,48 @@ def _dtype_code(t):
     raise TypeError("unsupported dtype %s (bf16 or fp32)" % t.dtype)
 
 
-def _need(t, name):
-    if not t.is_cuda or not t.is_contiguous():
-        raise ValueError("%s must be a contiguous device tensor" % name)
+# Argument checks.  The C ABI takes raw pointers and cannot see how large a
+# buffer is or where it lives, so every tensor is checked here before its
+# pointer is passed on: a device tensor of the current device, contiguous,
+# of the stated dtype and exact shape.
+
+def _need(t, name, dtypes=None, shape=None):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError("%s must be a device tensor" % name)
+    if t.device.index != torch.cuda.current_device():
+        raise ValueError("%s is on %s, not on the current device cuda:%d" %
+                         (name, t.device, torch.cuda.current_device()))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if dtypes is not None and t.dtype not in dtypes:
+        raise TypeError("%s must be %s, not %s" % (name, " or ".join(map(str, dtypes)), t.dtype))
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError("%s must have shape %s, not %s" % (name, tuple(shape), tuple(t.shape)))
+
+
+_U8 = (torch.uint8,)
+_FLOAT = (torch.float32, torch.bfloat16)
+
+
+def _need_codes(codes, scales, rows, K, name):
+    """An MXFP4 operand: codes [rows][K/2] and scales [rows][K/32], uint8."""
+    _need(codes, name + " codes", _U8, (rows, K // 2))
+    _need(scales, name + " scales", _U8, (rows, K // 32))
+
+
+def _need_pair(codes, scales, rows, K, name):
+    """An optional operand: both tensors or neither."""
+    if (codes is None) != (scales is None):
+        raise ValueError("%s codes and scales must both be given or both be None" % name)
+    if codes is not None:
+        _need_codes(codes, scales, rows, K, name)
+
+
+def _shape_of_codes(codes, name):
+    """(rows, K) of a codes tensor [rows][K/2]."""
+    if not isinstance(codes, torch.Tensor) or codes.dim() != 2:
+        raise ValueError("%s must be a 2-D tensor [rows][K/2]" % name)
+    return codes.shape[0], codes.shape[1] * 2
 
 
 def _codes_out(rows, K, device):
@@ -120,16 +159,35 @@ def _codes_out(rows, K, device):
             torch.empty((rows, K // 32), dtype=torch.uint8, device=device))
 
 
+def _outputs(out, rows, K, device, residual, name):
+    """Codes outputs (qc, qs, rc, rs): allocated, or the caller's checked."""
+    if out is None:
+        qc, qs = _codes_out(rows, K, device)
+        rc, rs = _codes_out(rows, K, device) if residual else (None, None)
+        return qc, qs, rc, rs
+    qc, qs, rc, rs = out
+    _need_codes(qc, qs, rows, K, name + " primary")
+    _need_pair(rc, rs, rows, K, name + " residual")
+    return qc, qs, rc, rs
+
+
+def _z_out(out, out_dtype, M, N, device):
+    if out is None:
+        if out_dtype not in _FLOAT:
+            raise TypeError("out_dtype must be torch.float32 or torch.bfloat16")
+        return torch.empty((M, N), dtype=out_dtype, device=device)
+    _need(out, "out", _FLOAT, (M, N))
+    return out
+
+
 def rfq_quantize_act(x, residual=True, out=None, stream=None):
     """X[M][K] -> (q_codes, q_scales, r_codes, r_scales); r_* are None when
     residual is False.  out may supply the four (or two) output tensors."""
-    _need(x, "x")
+    _need(x, "x", _FLOAT)
+    if x.dim() != 2:
+        raise ValueError("x must be 2-D [M][K]")
     M, K = x.shape
-    if out is None:
-        qc, qs = _codes_out(M, K, x.device)
-        rc, rs = _codes_out(M, K, x.device) if residual else (None, None)
-    else:
-        qc, qs, rc, rs = out
+    qc, qs, rc, rs = _outputs(out, M, K, x.device, residual, "out")
     st = load().rfq_quantize_act(_ptr(x), _dtype_code(x), M, K, _ptr(qc), _ptr(qs),
                                  _ptr(rc), _ptr(rs), _stream(stream))
     _check("rfq_quantize_act", st)
@@ -138,9 +196,15 @@ def rfq_quantize_act(x, residual=True, out=None, stream=None):
 
 def rfq_quantize_weight(w, out=None, stream=None):
     """W[N][K] -> (w_codes, w_scales)."""
-    _need(w, "w")
+    _need(w, "w", _FLOAT)
+    if w.dim() != 2:
+        raise ValueError("w must be 2-D [N][K]")
     N, K = w.shape
-    wc, ws = _codes_out(N, K, w.device) if out is None else out
+    if out is None:
+        wc, ws = _codes_out(N, K, w.device)
+    else:
+        wc, ws = out
+        _need_codes(wc, ws, N, K, "out")
     st = load().rfq_quantize_weight(_ptr(w), _dtype_code(w), N, K, _ptr(wc), _ptr(ws),
                                     _stream(stream))
     _check("rfq_quantize_weight", st)
@@ -150,12 +214,14 @@ def rfq_quantize_weight(w, out=None, stream=None):
 def rfq_gemm(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales,
              out_dtype=torch.float32, out=None, stream=None):
     """Z[M][N] = (deq q + deq r) deq(w)^T; r_* None gives plain MXFP4."""
-    M = q_codes.shape[0]
-    K = q_codes.shape[1] * 2
-    N = w_codes.shape[0]
-    if w_codes.shape[1] * 2 != K:
+    M, K = _shape_of_codes(q_codes, "q codes")
+    N, Kw = _shape_of_codes(w_codes, "w codes")
+    if Kw != K:
         raise ValueError("K mismatch between activation and weight codes")
-    z = out if out is not None else torch.empty((M, N), dtype=out_dtype, device=q_codes.device)
+    _need_codes(q_codes, q_scales, M, K, "q")
+    _need_pair(r_codes, r_scales, M, K, "r")
+    _need_codes(w_codes, w_scales, N, K, "w")
+    z = _z_out(out, out_dtype, M, N, q_codes.device)
     st = load().rfq_gemm(_ptr(q_codes), _ptr(q_scales), _ptr(r_codes), _ptr(r_scales),
                          _ptr(w_codes), _ptr(w_scales), M, N, K, _ptr(z), _dtype_code(z),
                          _stream(stream))
@@ -167,12 +233,15 @@ def rfq_gemm_stream(x, w_codes, w_scales, residual=True, out_dtype=torch.float32
                     stream=None):
     """Streaming form: Z[M][N] from X[M][K] (bf16 or fp32) quantized inside the
     product's K loop (primary and, with residual, the quantized residual)."""
-    _need(x, "x")
+    _need(x, "x", _FLOAT)
+    if x.dim() != 2:
+        raise ValueError("x must be 2-D [M][K]")
     M, K = x.shape
-    N = w_codes.shape[0]
-    if w_codes.shape[1] * 2 != K:
+    N, Kw = _shape_of_codes(w_codes, "w codes")
+    if Kw != K:
         raise ValueError("K mismatch between activations and weight codes")
-    z = out if out is not None else torch.empty((M, N), dtype=out_dtype, device=x.device)
+    _need_codes(w_codes, w_scales, N, K, "w")
+    z = _z_out(out, out_dtype, M, N, x.device)
     st = load().rfq_gemm_stream(_ptr(x), _dtype_code(x), int(bool(residual)), _ptr(w_codes),
                                 _ptr(w_scales), M, N, K, _ptr(z), _dtype_code(z),
                                 _stream(stream))
@@ -184,14 +253,16 @@ def rfq_gemm_phi(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, phi,
                  out_dtype=torch.float32, out=None, stream=None):
     """RFQ product with a fallback-indicator map phi[ceil(M/64)][ceil(K/256)]
     (uint8; None: phi = 1)."""
-    M = q_codes.shape[0]
-    K = q_codes.shape[1] * 2
-    N = w_codes.shape[0]
-    if w_codes.shape[1] * 2 != K:
+    M, K = _shape_of_codes(q_codes, "q codes")
+    N, Kw = _shape_of_codes(w_codes, "w codes")
+    if Kw != K:
         raise ValueError("K mismatch between activation and weight codes")
-    if phi is not None and tuple(phi.shape) != ((M + 63) // 64, (K + 255) // 256):
-        raise ValueError("phi must be [ceil(M/64)][ceil(K/256)]")
-    z = out if out is not None else torch.empty((M, N), dtype=out_dtype, device=q_codes.device)
+    _need_codes(q_codes, q_scales, M, K, "q")
+    _need_pair(r_codes, r_scales, M, K, "r")
+    _need_codes(w_codes, w_scales, N, K, "w")
+    if phi is not None:
+        _need(phi, "phi", _U8, ((M + 63) // 64, (K + 255) // 256))
+    z = _z_out(out, out_dtype, M, N, q_codes.device)
     st = load().rfq_gemm_phi(_ptr(q_codes), _ptr(q_scales), _ptr(r_codes), _ptr(r_scales),
                              _ptr(w_codes), _ptr(w_scales), _ptr(phi), M, N, K, _ptr(z),
                              _dtype_code(z), _stream(stream))
@@ -203,10 +274,19 @@ def rfq_fallback_map(r_codes, q_scales, rule, threshold=0, out=None, stream=None
     """phi[ceil(M/64)][ceil(K/256)] by RFQ_PHI_RESIDUAL_NONZERO (reads r_codes)
     or RFQ_PHI_SCALE_AT_LEAST (reads q_scales; phi = 1 where a scale byte >=
     threshold)."""
-    M = q_scales.shape[0]
-    K = q_scales.shape[1] * 32
-    phi = out if out is not None else torch.empty(((M + 63) // 64, (K + 255) // 256),
-                                                  dtype=torch.uint8, device=q_scales.device)
+    if not isinstance(q_scales, torch.Tensor) or q_scales.dim() != 2:
+        raise ValueError("q_scales must be a 2-D tensor [M][K/32] (it gives M and K)")
+    M, K = q_scales.shape[0], q_scales.shape[1] * 32
+    if rule == RFQ_PHI_RESIDUAL_NONZERO:
+        _need(r_codes, "r codes", _U8, (M, K // 2))
+    else:
+        _need(q_scales, "q scales", _U8, (M, K // 32))
+    shape = ((M + 63) // 64, (K + 255) // 256)
+    if out is None:
+        phi = torch.empty(shape, dtype=torch.uint8, device=q_scales.device)
+    else:
+        phi = out
+        _need(phi, "out", _U8, shape)
     st = load().rfq_fallback_map(_ptr(r_codes), _ptr(q_scales), M, K, int(rule), int(threshold),
                                  _ptr(phi), _stream(stream))
     _check("rfq_fallback_map", st)
@@ -215,8 +295,13 @@ def rfq_fallback_map(r_codes, q_scales, rule, threshold=0, out=None, stream=None
 
 def rfq_dequant(codes, scales, out=None, stream=None):
     """codes[rows][K/2], scales[rows][K/32] -> fp32 [rows][K]."""
-    rows, K = codes.shape[0], codes.shape[1] * 2
-    o = out if out is not None else torch.empty((rows, K), dtype=torch.float32, device=codes.device)
+    rows, K = _shape_of_codes(codes, "codes")
+    _need_codes(codes, scales, rows, K, "dequantization input")
+    if out is None:
+        o = torch.empty((rows, K), dtype=torch.float32, device=codes.device)
+    else:
+        o = out
+        _need(o, "out", (torch.float32,), (rows, K))
     st = load().rfq_dequant(_ptr(codes), _ptr(scales), rows, K, _ptr(o), _stream(stream))
     _check("rfq_dequant", st)
     return o
@@ -224,16 +309,12 @@ def rfq_dequant(codes, scales, out=None, stream=None):
 
 def rfq_swiglu_quantize_act(g, u, residual=True, return_h=False, out=None, stream=None):
     """h = bf16(silu(g) * u) -> RFQ codes; returns (qc, qs, rc, rs, h or None)."""
-    _need(g, "g")
-    _need(u, "u")
-    if g.shape != u.shape or g.dtype != u.dtype:
-        raise ValueError("g and u must have the same shape and dtype")
+    _need(g, "g", _FLOAT)
+    _need(u, "u", _FLOAT)
+    if g.shape != u.shape or g.dtype != u.dtype or g.dim() != 2:
+        raise ValueError("g and u must be 2-D with the same shape and dtype")
     M, Nh = g.shape
-    if out is None:
-        qc, qs = _codes_out(M, Nh, g.device)
-        rc, rs = _codes_out(M, Nh, g.device) if residual else (None, None)
-    else:
-        qc, qs, rc, rs = out
+    qc, qs, rc, rs = _outputs(out, M, Nh, g.device, residual, "out")
     h = torch.empty((M, Nh), dtype=torch.bfloat16, device=g.device) if return_h else None
     st = load().rfq_swiglu_quantize_act(_ptr(g), _ptr(u), _dtype_code(g), M, Nh, _ptr(qc),
                                         _ptr(qs), _ptr(rc), _ptr(rs), _ptr(h), _stream(stream))
@@ -247,16 +328,17 @@ def rfq_gemm_swiglu_quantize(q_codes, q_scales, r_codes, r_scales, wgu_codes, wg
     wgu_* are the quantized interleaved gate/up weights [2 Nh][K]
     (interleave_gate_up).  Returns (hq_codes, hq_scales, hr_codes, hr_scales,
     h or None); hr_* are None when residual is False."""
-    M = q_codes.shape[0]
-    K = q_codes.shape[1] * 2
-    Nh = wgu_codes.shape[0] // 2
-    if wgu_codes.shape[1] * 2 != K:
+    M, K = _shape_of_codes(q_codes, "q codes")
+    N2, Kw = _shape_of_codes(wgu_codes, "gate/up codes")
+    if Kw != K:
         raise ValueError("K mismatch between activation and weight codes")
-    if out is None:
-        hqc, hqs = _codes_out(M, Nh, q_codes.device)
-        hrc, hrs = _codes_out(M, Nh, q_codes.device) if residual else (None, None)
-    else:
-        hqc, hqs, hrc, hrs = out
+    if N2 % 2:
+        raise ValueError("gate/up codes must have an even number of rows [2 Nh][K/2]")
+    Nh = N2 // 2
+    _need_codes(q_codes, q_scales, M, K, "q")
+    _need_pair(r_codes, r_scales, M, K, "r")
+    _need_codes(wgu_codes, wgu_scales, N2, K, "gate/up")
+    hqc, hqs, hrc, hrs = _outputs(out, M, Nh, q_codes.device, residual, "out")
     h = (torch.empty((M, Nh), dtype=torch.bfloat16, device=q_codes.device)
          if return_h else None)
     st = load().rfq_gemm_swiglu_quantize(

@@ -271,6 +271,29 @@ def test_size_limits():
     assert sw(A, A, A, A, A, A, 64, 1 << 31, 512, A, A, A, A, None, None) == ESHAPE
 
 
+def test_binding_rejects_host_tensors():
+    """The binding passes only device pointers on: host tensors are refused
+    before any library call (a host pointer would fault in a kernel)."""
+    import torch
+    x = torch.zeros(4, 64)
+    c = torch.zeros(4, 32, dtype=torch.uint8)
+    s = torch.zeros(4, 2, dtype=torch.uint8)
+    calls = [
+        lambda: binding.rfq_quantize_act(x),
+        lambda: binding.rfq_quantize_weight(x),
+        lambda: binding.rfq_gemm(c, s, None, None, c, s),
+        lambda: binding.rfq_gemm_phi(c, s, c, s, c, s, None),
+        lambda: binding.rfq_gemm_stream(x, c, s),
+        lambda: binding.rfq_dequant(c, s),
+        lambda: binding.rfq_fallback_map(c, s, binding.RFQ_PHI_RESIDUAL_NONZERO),
+        lambda: binding.rfq_swiglu_quantize_act(x, x),
+        lambda: binding.rfq_gemm_swiglu_quantize(c, s, None, None, c, s),
+    ]
+    for call in calls:
+        with pytest.raises(ValueError, match="device tensor"):
+            call()
+
+
 def test_valid_arguments_without_a_gpu_report_device_error():
     import torch
     if torch.cuda.is_available():

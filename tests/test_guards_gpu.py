@@ -111,3 +111,47 @@ def test_swiglu_outputs_stay_in_bounds(M, Nh, K):
     fb = _codes(M, Nh) + _codes(M, Nh)
     rfq.rfq_gemm_swiglu_quantize(*q, *wgu, out=[b.t for b in fb])
     _check_all(fb, "gemm_swiglu_quantize")
+
+
+def test_binding_rejects_bad_tensors():
+    """The binding refuses tensors whose pointer the kernels could not use
+    safely (wrong shape, dtype, layout, or a half-given operand pair) before
+    calling the library."""
+    M, N, K = 8, 64, 512
+    x = torch.randn(M, K, device="cuda")
+    w = torch.randn(N, K, device="cuda")
+    q = binding.rfq_quantize_act(x)
+    wq = binding.rfq_quantize_weight(w)
+    bad = [
+        # scales with too few rows: the kernel would read past them
+        (ValueError, lambda: binding.rfq_gemm(q[0], q[1][:M - 1], q[2], q[3], *wq)),
+        (ValueError, lambda: binding.rfq_gemm(q[0], q[1], q[2], q[3], wq[0], wq[1][:, :8])),
+        (ValueError, lambda: binding.rfq_gemm(q[0], q[1], q[2], None, *wq)),
+        (TypeError, lambda: binding.rfq_gemm(q[0].view(torch.int8), q[1], q[2], q[3], *wq)),
+        (ValueError, lambda: binding.rfq_gemm(q[0], q[1], q[2], q[3], *wq,
+                                              out=torch.empty(M, N - 1, device="cuda"))),
+        (TypeError, lambda: binding.rfq_gemm(q[0], q[1], q[2], q[3], *wq,
+                                             out=torch.empty(M, N, device="cuda",
+                                                             dtype=torch.float16))),
+        (ValueError, lambda: binding.rfq_gemm_phi(*q, *wq, torch.ones(1, 1, dtype=torch.uint8,
+                                                                       device="cuda"))),
+        (ValueError, lambda: binding.rfq_gemm_stream(x.t(), *wq)),          # not contiguous
+        (ValueError, lambda: binding.rfq_gemm_stream(x, wq[0][:, :128], wq[1][:, :8])),
+        (TypeError, lambda: binding.rfq_quantize_act(x.to(torch.float16))),
+        (ValueError, lambda: binding.rfq_quantize_act(
+            x, out=(q[0][:4], q[1], q[2], q[3]))),
+        (ValueError, lambda: binding.rfq_dequant(q[0], q[1][:, :4])),
+        (ValueError, lambda: binding.rfq_dequant(q[0], q[1], out=torch.empty(M, K - 32,
+                                                                             device="cuda"))),
+        (ValueError, lambda: binding.rfq_fallback_map(q[2][:4], q[1],
+                                                      binding.RFQ_PHI_RESIDUAL_NONZERO)),
+        (ValueError, lambda: binding.rfq_gemm_swiglu_quantize(q[0], q[1], q[2], q[3],
+                                                              wq[0][:63], wq[1][:63])),
+    ]
+    for i, (exc, call) in enumerate(bad):
+        with pytest.raises(exc):
+            call()
+    # The valid calls still work after the refused ones.
+    z = binding.rfq_gemm(*q, *wq)
+    torch.cuda.synchronize()
+    assert z.shape == (M, N) and torch.isfinite(z).all()
