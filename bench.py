@@ -286,6 +286,32 @@ def _per_launch_ms(torch, stream, fn, reps):
     return a.elapsed_time(b) / reps
 
 
+def _graph_ms(torch, layer, layers, reps=20):
+    """Per-layer time of `layers` calls of layer(i) captured in one HIP graph
+    (warmed up on a side stream first, as capture requires) and replayed
+    `reps` times between one pair of events."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for i in range(layers):
+            layer(i)
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for i in range(layers):
+            layer(i)
+    graph.replay()
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        graph.replay()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / (reps * layers)
+
+
 def secondary(torch, rfq, wl, x, w, stream):
     """Rates reported beside the headline step: the product without the
     residual (plain MXFP4), the bf16 matrix product of the same shape
@@ -352,10 +378,17 @@ def secondary(torch, rfq, wl, x, w, stream):
         ms_c = _per_launch_ms(torch, stream, codes_path, 50)
         ms_s = _per_launch_ms(torch, stream, lambda i: rfq.rfq_gemm_stream(
             xd, *wcs[i % 10], out=zd, stream=stream), 50)
+        # The same ten layers captured once into a HIP graph and replayed:
+        # the launch overhead of back-to-back calls leaves the timing.
+        gc_ms = _graph_ms(torch, lambda i: (rfq.rfq_quantize_act(xd, out=qd),
+                                            rfq.rfq_gemm(*qd, *wcs[i], out=zd)), 10)
+        gs_ms = _graph_ms(torch, lambda i: rfq.rfq_gemm_stream(xd, *wcs[i], out=zd), 10)
         out["decode_%dx%dx%d" % (md, K, N)] = {
             "quantize_then_gemm_ms": round(ms_c, 5), "stream_ms": round(ms_s, 5),
             "w_gbs_quantize_then_gemm": round(w_bytes / ms_c / 1e6, 1),
-            "w_gbs_stream": round(w_bytes / ms_s / 1e6, 1)}
+            "w_gbs_stream": round(w_bytes / ms_s / 1e6, 1),
+            "hip_graph_quantize_then_gemm_ms": round(gc_ms, 5),
+            "hip_graph_stream_ms": round(gs_ms, 5)}
     del wq, wcs
 
     # Wan2.2-DiT-like product: X 32768x5120, W 5120x13824.

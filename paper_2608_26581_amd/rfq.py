@@ -88,13 +88,20 @@ def rfq_abi_version():
 
 
 def _ptr(t):
-    return None if t is None else ctypes.c_void_p(t.data_ptr())
+    return None if t is None else t.data_ptr()
 
 
-def _stream(stream):
-    if stream is None:
-        stream = torch.cuda.current_stream()
-    return ctypes.c_void_p(stream.cuda_stream)
+# The current stream's raw handle: torch's direct accessor when it has one
+# (a fraction of a microsecond), else the public Stream object (a few).
+_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+
+
+def _stream(stream, dev=None):
+    if stream is not None:
+        return stream.cuda_stream
+    if _raw_stream is not None:
+        return _raw_stream(torch.cuda.current_device() if dev is None else dev)
+    return torch.cuda.current_stream().cuda_stream
 
 
 def _check(func, status):
@@ -115,36 +122,58 @@ def _dtype_code(t):
 # pointer is passed on: a device tensor of the current device, contiguous,
 # of the stated dtype and exact shape.
 
-def _need(t, name, dtypes=None, shape=None):
+def _need(t, name, dtypes=None, shape=None, dev=None):
+    """Raises unless t is a contiguous tensor of device dev (default: the
+    current device) with a dtype in dtypes and the given shape.  One combined
+    test on the common path: the binding runs once per call of small
+    decode-sized products, where host time counts."""
+    try:
+        if (t.is_cuda and t.is_contiguous() and (dtypes is None or t.dtype in dtypes)
+                and (shape is None or t.shape == shape)
+                and t.get_device() == (torch.cuda.current_device() if dev is None else dev)):
+            return
+    except AttributeError:
+        pass
     if not isinstance(t, torch.Tensor) or not t.is_cuda:
         raise ValueError("%s must be a device tensor" % name)
-    if t.device.index != torch.cuda.current_device():
-        raise ValueError("%s is on %s, not on the current device cuda:%d" %
-                         (name, t.device, torch.cuda.current_device()))
+    cur = torch.cuda.current_device() if dev is None else dev
+    if t.get_device() != cur:
+        raise ValueError("%s is on %s, not on the current device cuda:%d" % (name, t.device, cur))
     if not t.is_contiguous():
         raise ValueError("%s must be contiguous" % name)
     if dtypes is not None and t.dtype not in dtypes:
         raise TypeError("%s must be %s, not %s" % (name, " or ".join(map(str, dtypes)), t.dtype))
-    if shape is not None and tuple(t.shape) != tuple(shape):
-        raise ValueError("%s must have shape %s, not %s" % (name, tuple(shape), tuple(t.shape)))
+    raise ValueError("%s must have shape %s, not %s" % (name, tuple(shape), tuple(t.shape)))
 
 
 _U8 = (torch.uint8,)
 _FLOAT = (torch.float32, torch.bfloat16)
 
 
-def _need_codes(codes, scales, rows, K, name):
+def _ok(t, dtypes, shape, dev):
+    """The common case of _need in one expression (no message to build)."""
+    try:
+        return (t.is_cuda and t.is_contiguous() and t.dtype in dtypes and t.shape == shape
+                and t.get_device() == dev)
+    except AttributeError:
+        return False
+
+
+def _need_codes(codes, scales, rows, K, name, dev=None):
     """An MXFP4 operand: codes [rows][K/2] and scales [rows][K/32], uint8."""
-    _need(codes, name + " codes", _U8, (rows, K // 2))
-    _need(scales, name + " scales", _U8, (rows, K // 32))
+    if (dev is not None and _ok(codes, _U8, (rows, K // 2), dev)
+            and _ok(scales, _U8, (rows, K // 32), dev)):
+        return
+    _need(codes, name + " codes", _U8, (rows, K // 2), dev)
+    _need(scales, name + " scales", _U8, (rows, K // 32), dev)
 
 
-def _need_pair(codes, scales, rows, K, name):
+def _need_pair(codes, scales, rows, K, name, dev=None):
     """An optional operand: both tensors or neither."""
     if (codes is None) != (scales is None):
         raise ValueError("%s codes and scales must both be given or both be None" % name)
     if codes is not None:
-        _need_codes(codes, scales, rows, K, name)
+        _need_codes(codes, scales, rows, K, name, dev)
 
 
 def _shape_of_codes(codes, name):
@@ -159,24 +188,25 @@ def _codes_out(rows, K, device):
             torch.empty((rows, K // 32), dtype=torch.uint8, device=device))
 
 
-def _outputs(out, rows, K, device, residual, name):
+def _outputs(out, rows, K, device, residual, name, dev=None):
     """Codes outputs (qc, qs, rc, rs): allocated, or the caller's checked."""
     if out is None:
         qc, qs = _codes_out(rows, K, device)
         rc, rs = _codes_out(rows, K, device) if residual else (None, None)
         return qc, qs, rc, rs
     qc, qs, rc, rs = out
-    _need_codes(qc, qs, rows, K, name + " primary")
-    _need_pair(rc, rs, rows, K, name + " residual")
+    _need_codes(qc, qs, rows, K, name + " primary", dev)
+    _need_pair(rc, rs, rows, K, name + " residual", dev)
     return qc, qs, rc, rs
 
 
-def _z_out(out, out_dtype, M, N, device):
+def _z_out(out, out_dtype, M, N, device, dev=None):
     if out is None:
         if out_dtype not in _FLOAT:
             raise TypeError("out_dtype must be torch.float32 or torch.bfloat16")
         return torch.empty((M, N), dtype=out_dtype, device=device)
-    _need(out, "out", _FLOAT, (M, N))
+    if dev is None or not _ok(out, _FLOAT, (M, N), dev):
+        _need(out, "out", _FLOAT, (M, N), dev)
     return out
 
 
@@ -184,12 +214,13 @@ def rfq_quantize_act(x, residual=True, out=None, stream=None):
     """X[M][K] -> (q_codes, q_scales, r_codes, r_scales); r_* are None when
     residual is False.  out may supply the four (or two) output tensors."""
     _need(x, "x", _FLOAT)
+    dev = x.get_device()
     if x.dim() != 2:
         raise ValueError("x must be 2-D [M][K]")
     M, K = x.shape
-    qc, qs, rc, rs = _outputs(out, M, K, x.device, residual, "out")
+    qc, qs, rc, rs = _outputs(out, M, K, x.device, residual, "out", dev)
     st = load().rfq_quantize_act(_ptr(x), _dtype_code(x), M, K, _ptr(qc), _ptr(qs),
-                                 _ptr(rc), _ptr(rs), _stream(stream))
+                                 _ptr(rc), _ptr(rs), _stream(stream, dev))
     _check("rfq_quantize_act", st)
     return qc, qs, rc, rs
 
@@ -218,13 +249,15 @@ def rfq_gemm(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales,
     N, Kw = _shape_of_codes(w_codes, "w codes")
     if Kw != K:
         raise ValueError("K mismatch between activation and weight codes")
-    _need_codes(q_codes, q_scales, M, K, "q")
-    _need_pair(r_codes, r_scales, M, K, "r")
-    _need_codes(w_codes, w_scales, N, K, "w")
-    z = _z_out(out, out_dtype, M, N, q_codes.device)
+    _need(q_codes, "q codes", _U8, (M, K // 2))
+    dev = q_codes.get_device()
+    _need_codes(q_codes, q_scales, M, K, "q", dev)
+    _need_pair(r_codes, r_scales, M, K, "r", dev)
+    _need_codes(w_codes, w_scales, N, K, "w", dev)
+    z = _z_out(out, out_dtype, M, N, q_codes.device, dev)
     st = load().rfq_gemm(_ptr(q_codes), _ptr(q_scales), _ptr(r_codes), _ptr(r_scales),
                          _ptr(w_codes), _ptr(w_scales), M, N, K, _ptr(z), _dtype_code(z),
-                         _stream(stream))
+                         _stream(stream, dev))
     _check("rfq_gemm", st)
     return z
 
@@ -234,17 +267,18 @@ def rfq_gemm_stream(x, w_codes, w_scales, residual=True, out_dtype=torch.float32
     """Streaming form: Z[M][N] from X[M][K] (bf16 or fp32) quantized inside the
     product's K loop (primary and, with residual, the quantized residual)."""
     _need(x, "x", _FLOAT)
+    dev = x.get_device()
     if x.dim() != 2:
         raise ValueError("x must be 2-D [M][K]")
     M, K = x.shape
     N, Kw = _shape_of_codes(w_codes, "w codes")
     if Kw != K:
         raise ValueError("K mismatch between activations and weight codes")
-    _need_codes(w_codes, w_scales, N, K, "w")
-    z = _z_out(out, out_dtype, M, N, x.device)
+    _need_codes(w_codes, w_scales, N, K, "w", dev)
+    z = _z_out(out, out_dtype, M, N, x.device, dev)
     st = load().rfq_gemm_stream(_ptr(x), _dtype_code(x), int(bool(residual)), _ptr(w_codes),
                                 _ptr(w_scales), M, N, K, _ptr(z), _dtype_code(z),
-                                _stream(stream))
+                                _stream(stream, dev))
     _check("rfq_gemm_stream", st)
     return z
 

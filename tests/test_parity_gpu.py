@@ -664,3 +664,58 @@ def test_stream_argument_is_honoured(orc):
     s.synchronize()
     zr, bound = orc.gemm(*[host(t) for t in q], host(w[0]), host(w[1]))
     assert_gemm_close(host(z), zr, bound, False, "stream")
+
+
+# ------------------------------------------------------------- HIP graphs
+@pytest.mark.parametrize("M,N,K", [(16, 1024, 2048), (300, 512, 1024)])
+def test_path_replays_from_a_hip_graph(M, N, K):
+    """The quantizer, the product and its streaming form capture into a HIP
+    graph (no allocation, memset or host synchronisation inside the calls);
+    every replay, with eager work between replays, reproduces the eager
+    results, and new input values flow through the captured graph."""
+    gen = torch.Generator(device="cuda").manual_seed(M + N + K)
+    x = torch.randn((M, K), generator=gen, device="cuda").to(torch.bfloat16)
+    w = rfq.rfq_quantize_weight(torch.randn((N, K), generator=gen, device="cuda") * 0.02)
+    q = [torch.empty((M, K // 2), dtype=torch.uint8, device="cuda"),
+         torch.empty((M, K // 32), dtype=torch.uint8, device="cuda"),
+         torch.empty((M, K // 2), dtype=torch.uint8, device="cuda"),
+         torch.empty((M, K // 32), dtype=torch.uint8, device="cuda")]
+    z = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    zs = torch.empty((M, N), dtype=torch.float32, device="cuda")
+
+    def path():
+        rfq.rfq_quantize_act(x, out=q)
+        rfq.rfq_gemm(*q, *w, out=z)
+        rfq.rfq_gemm_stream(x, *w, out=zs)
+
+    def eager_results():
+        path()
+        torch.cuda.synchronize()
+        return [t.clone() for t in q] + [z.clone(), zs.clone()]
+
+    want = eager_results()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        path()
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        path()
+    _say("graph replay M=%d N=%d K=%d" % (M, N, K))
+    for i in range(4):
+        for t in q + [z, zs]:
+            t.zero_()
+        torch.randn((1024, 1024), generator=gen, device="cuda").sum()   # eager work between
+        graph.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(q + [z, zs], want):
+            assert torch.equal(a, b), "replay %d differs from the eager result" % i
+    x.copy_(torch.randn((M, K), generator=gen, device="cuda").to(torch.bfloat16))
+    want = eager_results()
+    for t in q + [z, zs]:
+        t.zero_()
+    graph.replay()
+    torch.cuda.synchronize()
+    for a, b in zip(q + [z, zs], want):
+        assert torch.equal(a, b), "replay with new inputs differs from the eager result"
