@@ -1,4 +1,5 @@
-"""Python access to the CPU oracle (oracle/rfq_oracle.c) through ctypes.
+"""Python access to the CPU oracle (oracle/rfq_oracle.c for MXFP4,
+oracle/hif4_oracle.c for HiF4) through ctypes.
 
 TEST INFRASTRUCTURE ONLY: imported by the test suite, by the smoke check and
 by the CPU-baseline leg of the benchmark, never by the product path.  It shares
@@ -11,7 +12,7 @@ import subprocess
 import numpy as np
 
 ORACLE_DIR = os.path.dirname(os.path.abspath(__file__))
-SRC = os.path.join(ORACLE_DIR, "rfq_oracle.c")
+SRCS = [os.path.join(ORACLE_DIR, "rfq_oracle.c"), os.path.join(ORACLE_DIR, "hif4_oracle.c")]
 LIB = os.path.join(ORACLE_DIR, "liboracle.so")
 CFLAGS = ["-O2", "-std=c99", "-fopenmp", "-fPIC", "-shared", "-Wall", "-Wextra"]
 
@@ -20,7 +21,7 @@ _lib = None
 
 def build(extra_flags=(), out=LIB):
     """Compile the oracle with gcc (plain -O2, no fast-math)."""
-    cmd = ["gcc", *CFLAGS, *extra_flags, SRC, "-o", out + ".tmp", "-lm"]
+    cmd = ["gcc", *CFLAGS, *extra_flags, *SRCS, "-o", out + ".tmp", "-lm"]
     subprocess.run(cmd, check=True)
     os.replace(out + ".tmp", out)
     return out
@@ -49,6 +50,18 @@ def _load(path=LIB):
                                         ctypes.POINTER(ctypes.c_int64), I64, D, D]
     lib.oracle_swiglu.argtypes = [D, D, I64, D]
     lib.oracle_residual.argtypes = [D, I64, I64, D]
+    U32 = ctypes.POINTER(ctypes.c_uint32)
+    lib.oracle_hif4_macro_value.argtypes = [ctypes.c_int]
+    lib.oracle_hif4_macro_value.restype = ctypes.c_double
+    lib.oracle_hif4_macro_byte.argtypes = [ctypes.c_double]
+    lib.oracle_hif4_macro_byte.restype = ctypes.c_int
+    lib.oracle_hif4_value.argtypes = [ctypes.c_uint32, ctypes.c_int, ctypes.c_int]
+    lib.oracle_hif4_value.restype = ctypes.c_double
+    lib.oracle_hif4_quantize.argtypes = [D, I64, I64, U8, U32, U8, U32]
+    lib.oracle_hif4_dequant.argtypes = [U8, U32, I64, I64, D]
+    lib.oracle_hif4_gemm.argtypes = [U8, U32, U8, U32, U8, U32, I64, I64, I64, D, D]
+    for f in ("oracle_hif4_quantize", "oracle_hif4_dequant", "oracle_hif4_gemm"):
+        getattr(lib, f).restype = None
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = ctypes.c_int
     lib.oracle_set_num_threads.argtypes = [ctypes.c_int]
@@ -175,6 +188,59 @@ class Oracle:
         self.h.oracle_gemm_sampled(*[self._u8(a) for a in arrs], K,
                                    rows.ctypes.data_as(P), cols.ctypes.data_as(P),
                                    len(rows), self._d(z), self._d(b))
+        return z, b
+
+    # ---- HiF4 (oracle/hif4_oracle.c)
+    @staticmethod
+    def _u32(a):
+        if a is None:
+            return None
+        return a.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32))
+
+    def hif4_macro_value(self, byte):
+        return self.h.oracle_hif4_macro_value(int(byte))
+
+    def hif4_macro_byte(self, amax):
+        return self.h.oracle_hif4_macro_byte(float(amax))
+
+    def hif4_value(self, meta, i, code):
+        return self.h.oracle_hif4_value(int(meta), int(i), int(code))
+
+    def hif4_quantize(self, x, residual=True):
+        """x [rows][K] (K a multiple of 64) -> (q_codes, q_meta, r_codes,
+        r_meta): codes uint8 [rows][K/2], metadata uint32 [rows][K/64]; the
+        residual pair is None when residual is False."""
+        x = np.ascontiguousarray(x, dtype=np.float64)
+        rows, K = x.shape
+        assert K % 64 == 0
+        qc = np.zeros((rows, K // 2), np.uint8)
+        qm = np.zeros((rows, K // 64), np.uint32)
+        rc = np.zeros((rows, K // 2), np.uint8) if residual else None
+        rm = np.zeros((rows, K // 64), np.uint32) if residual else None
+        self.h.oracle_hif4_quantize(self._d(x), rows, K, self._u8(qc), self._u32(qm),
+                                    self._u8(rc), self._u32(rm))
+        return qc, qm, rc, rm
+
+    def hif4_dequant(self, codes, meta):
+        codes = np.ascontiguousarray(codes, np.uint8)
+        meta = np.ascontiguousarray(meta, np.uint32)
+        rows, K = codes.shape[0], codes.shape[1] * 2
+        out = np.empty((rows, K), np.float64)
+        self.h.oracle_hif4_dequant(self._u8(codes), self._u32(meta), rows, K, self._d(out))
+        return out
+
+    def hif4_gemm(self, qc, qm, rc, rm, wc, wm):
+        """Z[M][N] and bound[M][N] in fp64 of the HiF4 RFQ product (rc, rm
+        None: primary only)."""
+        qc, rc, wc = [np.ascontiguousarray(a, np.uint8) if a is not None else None
+                      for a in (qc, rc, wc)]
+        qm, rm, wm = [np.ascontiguousarray(a, np.uint32) if a is not None else None
+                      for a in (qm, rm, wm)]
+        M, K, N = qc.shape[0], qc.shape[1] * 2, wc.shape[0]
+        z = np.empty((M, N), np.float64)
+        b = np.empty((M, N), np.float64)
+        self.h.oracle_hif4_gemm(self._u8(qc), self._u32(qm), self._u8(rc), self._u32(rm),
+                                self._u8(wc), self._u32(wm), M, N, K, self._d(z), self._d(b))
         return z, b
 
     def swiglu(self, g, u):

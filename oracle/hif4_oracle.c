@@ -1,0 +1,227 @@
+/*
+ * hif4_oracle.c -- plain CPU oracle of RFQ with HiF4 codes.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may link, load or
+ * call this file; only the test suite, the smoke check and the CPU-baseline
+ * leg of the benchmark use it.  It shares no source, header, table or helper
+ * with the GPU library.
+ *
+ * Format (Sec. 3.2.3, Eq. 5-6): blocks of 64 consecutive elements along K.
+ * Per block, 32 bits of metadata: a macro scale S in unsigned E6M2 (6
+ * exponent bits with bias 48, 2 mantissa bits: S = 2^(E-48) (1 + M/4),
+ * Eq. 5), eight 1-bit micro-exponents E1_8 (one per 8 elements) and sixteen
+ * 1-bit micro-exponents E1_16 (one per 4 elements).  Per element a 4-bit
+ * S1P2 code: a sign bit and a 3-bit magnitude k meaning k/4 (1 integer and 2
+ * fractional bits).  Value of element i of a block (Eq. 6):
+ *     V_i = S * 2^(E1_8[i/8] + E1_16[i/4]) * (-1)^sign * k/4.
+ * Decoding follows Eq. 6 exactly.
+ *
+ * The paper does not give the encoder (how S and the micro-exponents are
+ * chosen, how elements are rounded): PARITY UNPINNED for those choices.
+ * This file takes the following reading, and the GPU library the same one:
+ *   1. S is the smallest E6M2 value with 7 S >= amax (7 = 1.75 * 2^2, the
+ *      largest element factor), so that no element saturates; an all-zero
+ *      block gets byte 0; an amax beyond 7 times the largest E6M2 value gets
+ *      byte 255 (its elements saturate at 1.75 * 4 * S).
+ *   2. The 4-element group j needs the smallest e_j in {0, 1, 2} with
+ *      1.75 * 2^e_j * S >= its max |x|.  The 8-element group g holding
+ *      groups 2g and 2g+1 takes E1_8[g] = 1 when one of them needs 2, else
+ *      0; then E1_16[j] = max(e_j - E1_8[g], 0).  (Among the bit choices
+ *      that avoid saturation this gives both groups their smallest possible
+ *      exponent, with E1_8 = 0 where two choices give the same exponents.)
+ *   3. Elements round |x| / (S 2^e) to the nearest k/4, k = 0..7, ties to
+ *      even k, saturating at 7; the sign is kept, also for a zero.  The
+ *      decision compares |x| with the exact midpoints (2k+1)/8 S 2^e.
+ *   4. RFQ (Sec. 4.3, Eq. 8-10): the residual x - V (exact in double and in
+ *      fp32) is quantized by the same encoder with its own metadata.
+ * Storage: codes as for MXFP4 (two per byte, element 2j in the low nibble,
+ * codes[row][K/2]); one metadata word per block, meta[row][K/64]: bits 0-7
+ * the E6M2 byte (E << 2 | M), bits 8-15 E1_8 (bit g for group g), bits
+ * 16-31 E1_16 (bit j for group j).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stddef.h>
+
+#ifndef ORACLE_PLANT
+#define ORACLE_PLANT 0
+#endif
+
+#define HIF4_BLOCK 64
+
+/* Macro scale of an E6M2 byte (Eq. 5). */
+double oracle_hif4_macro_value(int byte)
+{
+    int e = (byte >> 2) & 63, m = byte & 3;
+#if ORACLE_PLANT == 16
+    return ldexp(1.0 + m / 4.0, e - 47);       /* planted: bias 47 */
+#else
+    return ldexp(1.0 + m / 4.0, e - 48);
+#endif
+}
+
+/* Reading 1: the smallest E6M2 value S with 7 S >= amax.  Bytes are ordered
+ * by value (exponent field above mantissa field). */
+int oracle_hif4_macro_byte(double amax)
+{
+#if ORACLE_PLANT == 14
+    const double top = 6.0;                    /* planted: ignores the 1.75 * 4 maximum */
+#else
+    const double top = 7.0;
+#endif
+    for (int b = 0; b < 256; ++b)
+        if (top * oracle_hif4_macro_value(b) >= amax)
+            return b;
+    return 255;
+}
+
+/* Reading 3: code magnitude k of |x| = a on the grid k/4 * unit. */
+static int hif4_magnitude(double a, double unit)
+{
+    int k = 0;
+    for (int j = 0; j < 7; ++j) {
+        double mid = (2 * j + 1) / 8.0 * unit;
+        if (a > mid) {
+            k = j + 1;
+        } else {
+#if ORACLE_PLANT == 17
+            if (a == mid) k = j + 1;             /* planted: ties away from zero */
+#else
+            if (a == mid && (j & 1)) k = j + 1;  /* ties to the even magnitude */
+#endif
+            break;
+        }
+    }
+    return k;
+}
+
+/* Value of element i (0..63) of a block with metadata word `meta` (Eq. 6). */
+double oracle_hif4_value(uint32_t meta, int i, int code)
+{
+    int e8 = (meta >> (8 + i / 8)) & 1;
+    int e16 = (meta >> (16 + i / 4)) & 1;
+    double v = oracle_hif4_macro_value(meta & 255) * ldexp((code & 7) / 4.0, e8 + e16);
+    return (code & 8) ? -v : v;
+}
+
+static void put_nibble(uint8_t *row, int64_t k, int code)
+{
+    if (k & 1)
+        row[k >> 1] = (uint8_t)((row[k >> 1] & 0x0F) | (code << 4));
+    else
+        row[k >> 1] = (uint8_t)((row[k >> 1] & 0xF0) | code);
+}
+
+static int get_nibble(const uint8_t *row, int64_t k)
+{
+    return (k & 1) ? (row[k >> 1] >> 4) : (row[k >> 1] & 15);
+}
+
+/* Encodes one 64-element block x[0..63] (readings 1-3) into row codes at
+ * element offset k0; returns the metadata word; v receives the values. */
+static uint32_t hif4_block(const double *x, uint8_t *row, int64_t k0, double *v)
+{
+    double amax = 0.0;
+    for (int i = 0; i < HIF4_BLOCK; ++i)
+        if (fabs(x[i]) > amax) amax = fabs(x[i]);
+    int sb = oracle_hif4_macro_byte(amax);
+    double s = oracle_hif4_macro_value(sb);
+
+    int need[16];
+    for (int j = 0; j < 16; ++j) {
+        double g = 0.0;
+        for (int t = 0; t < 4; ++t)
+            if (fabs(x[4 * j + t]) > g) g = fabs(x[4 * j + t]);
+        int e = 0;
+        while (e < 2 && 1.75 * ldexp(s, e) < g) ++e;
+        need[j] = e;
+    }
+    uint32_t e8bits = 0, e16bits = 0;
+    for (int g = 0; g < 8; ++g) {
+        int a = need[2 * g], b = need[2 * g + 1];
+#if ORACLE_PLANT == 15
+        int e8 = (a >= 1 || b >= 1) ? 1 : 0;     /* planted: shared bit set too eagerly */
+#else
+        int e8 = (a == 2 || b == 2) ? 1 : 0;
+#endif
+        int ea = a - e8 < 0 ? 0 : a - e8;
+        int eb = b - e8 < 0 ? 0 : b - e8;
+        e8bits |= (uint32_t)e8 << g;
+        e16bits |= (uint32_t)ea << (2 * g);
+        e16bits |= (uint32_t)eb << (2 * g + 1);
+    }
+    uint32_t meta = (uint32_t)sb | (e8bits << 8) | (e16bits << 16);
+    for (int i = 0; i < HIF4_BLOCK; ++i) {
+        int e = (int)((e8bits >> (i / 8)) & 1) + (int)((e16bits >> (i / 4)) & 1);
+        int k = hif4_magnitude(fabs(x[i]), ldexp(s, e));
+        int code = (signbit(x[i]) ? 8 : 0) | k;
+        put_nibble(row, k0 + i, code);
+        v[i] = oracle_hif4_value(meta, i, code);
+    }
+    return meta;
+}
+
+/* HiF4 quantization of x[rows][K] (K a multiple of 64): primary codes and
+ * metadata, and (rc, rm non-NULL) those of the residual x - V (reading 4). */
+void oracle_hif4_quantize(const double *x, int64_t rows, int64_t K, uint8_t *qc,
+                          uint32_t *qm, uint8_t *rc, uint32_t *rm)
+{
+    const int64_t nb = K / HIF4_BLOCK;
+#pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < rows; ++r) {
+        double v[HIF4_BLOCK], res[HIF4_BLOCK], vr[HIF4_BLOCK];
+        for (int64_t b = 0; b < nb; ++b) {
+            const double *xb = x + r * K + b * HIF4_BLOCK;
+            qm[r * nb + b] = hif4_block(xb, qc + r * (K / 2), b * HIF4_BLOCK, v);
+            if (!rc) continue;
+            for (int i = 0; i < HIF4_BLOCK; ++i) res[i] = xb[i] - v[i];
+            rm[r * nb + b] = hif4_block(res, rc + r * (K / 2), b * HIF4_BLOCK, vr);
+        }
+    }
+}
+
+/* Values of codes[rows][K/2] with metadata meta[rows][K/64] (Eq. 6). */
+void oracle_hif4_dequant(const uint8_t *codes, const uint32_t *meta, int64_t rows,
+                         int64_t K, double *out)
+{
+    const int64_t nb = K / HIF4_BLOCK;
+#pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < rows; ++r)
+        for (int64_t k = 0; k < K; ++k)
+            out[r * K + k] = oracle_hif4_value(meta[r * nb + k / HIF4_BLOCK],
+                                               (int)(k % HIF4_BLOCK),
+                                               get_nibble(codes + r * (K / 2), k));
+}
+
+/* RFQ product with HiF4 codes (Eq. 11, phi = 1; phi = 0 without rc):
+ * z[m][n] = sum_k V_q[m][k] V_w[n][k] + sum_k V_r[m][k] V_w[n][k], each
+ * product exact in double (at most 6 significant bits per factor), the two
+ * sums kept apart in double; bound[m][n] = sum of the products' magnitudes. */
+void oracle_hif4_gemm(const uint8_t *qc, const uint32_t *qm, const uint8_t *rc,
+                      const uint32_t *rm, const uint8_t *wc, const uint32_t *wm,
+                      int64_t M, int64_t N, int64_t K, double *z, double *bound)
+{
+    const int64_t nb = K / HIF4_BLOCK;
+#pragma omp parallel for schedule(static)
+    for (int64_t m = 0; m < M; ++m)
+        for (int64_t n = 0; n < N; ++n) {
+            double sq = 0.0, sr = 0.0, bnd = 0.0;
+            for (int64_t k = 0; k < K; ++k) {
+                int i = (int)(k % HIF4_BLOCK);
+                double w = oracle_hif4_value(wm[n * nb + k / HIF4_BLOCK], i,
+                                             get_nibble(wc + n * (K / 2), k));
+                double q = oracle_hif4_value(qm[m * nb + k / HIF4_BLOCK], i,
+                                             get_nibble(qc + m * (K / 2), k));
+                sq += q * w;
+                bnd += fabs(q * w);
+                if (rc) {
+                    double rv = oracle_hif4_value(rm[m * nb + k / HIF4_BLOCK], i,
+                                                  get_nibble(rc + m * (K / 2), k));
+                    sr += rv * w;
+                    bnd += fabs(rv * w);
+                }
+            }
+            z[m * N + n] = sq + sr;
+            bound[m * N + n] = bnd;
+        }
+}

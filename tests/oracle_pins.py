@@ -14,7 +14,13 @@ Sources of truth used here:
   * invariants of the method (zero residual on grid values, power-of-two
     equivariance, idempotence, negation symmetry, monotone improvement, the
     half-error bound of the second stage);
-  * closed forms for the SwiGLU intermediate and bf16 rounding.
+  * closed forms for the SwiGLU intermediate and bf16 rounding;
+  * HiF4 (Sec. 3.2.3): the decode of Eq. 6 worked by hand and implemented
+    here independently; the encoder is this build's reading (parity
+    unpinned) and is pinned by its defining properties (smallest macro scale
+    with no saturation, smallest non-saturating micro-exponents under the
+    shared 8-element bit, nearest element with ties to even) checked by
+    brute force, and by a hand-worked block.
 """
 import math
 import os
@@ -420,6 +426,179 @@ def pin_fallback_map_rules(o):
     wc, ws, _, _ = o.quantize(w, residual=False)
     assert np.array_equal(o.gemm_phi(qc, qs, rc, rs, wc, ws, phi)[0],
                           o.gemm(qc, qs, rc, rs, wc, ws)[0])
+
+
+# -------------------------------------------------------------------- HiF4
+def hif4_macro_py(byte):
+    """E6M2 macro scale (Eq. 5): exponent field bias 48, two mantissa bits."""
+    return (1.0 + (byte & 3) / 4.0) * 2.0 ** ((byte >> 2) - 48)
+
+
+def hif4_decode_py(codes, meta):
+    """Independent Eq. 6 decode: V_i = S 2^(E1_8[i/8] + E1_16[i/4]) (+-) k/4."""
+    codes = np.asarray(codes, np.uint8)
+    meta = np.asarray(meta, np.uint64)
+    rows, K = codes.shape[0], codes.shape[1] * 2
+    nib = np.empty((rows, K), np.int64)
+    nib[:, 0::2] = codes & 0x0F
+    nib[:, 1::2] = codes >> 4
+    i = np.arange(K) % 64
+    blk = np.arange(K) // 64
+    m = meta[:, blk]                                            # [rows][K]
+    s = np.vectorize(hif4_macro_py)((m & 255).astype(np.int64))
+    e8 = ((m >> (8 + i // 8).astype(np.uint64)) & 1).astype(np.int64)
+    e16 = ((m >> (16 + i // 4).astype(np.uint64)) & 1).astype(np.int64)
+    mag = s * np.ldexp((nib & 7) / 4.0, e8 + e16)
+    return np.where(nib & 8, -mag, mag)
+
+
+def _hif4_golden(o, name):
+    g = read_golden(name)
+    meta = np.array([[int(g["meta"][0], 16)]], np.uint32)
+    codes = padded_bytes(g["codes"], 32).reshape(1, 32)
+    want = padded_floats(g["values"], 64)
+    return g, meta, codes, want
+
+
+def pin_hif4_golden_decode(o):
+    """H6: the decode of Eq. 6 on a block worked by hand (signs of zero too)."""
+    _, meta, codes, want = _hif4_golden(o, "h6_hif4_decode.txt")
+    for got in (o.hif4_dequant(codes, meta)[0], hif4_decode_py(codes, meta)[0]):
+        assert np.array_equal(got, want) and np.array_equal(np.signbit(got), np.signbit(want))
+    for i in (0, 4, 20, 63):
+        c = (codes[0, i // 2] >> (4 * (i & 1))) & 15
+        assert o.hif4_value(int(meta[0, 0]), i, int(c)) == want[i]
+
+
+def pin_hif4_golden_encode(o):
+    """H7: one block encoded by hand under this build's reading."""
+    g, meta, codes, want = _hif4_golden(o, "h7_hif4_encode.txt")
+    x = padded_floats(g["x"], 64).reshape(1, 64)
+    qc, qm, _, _ = o.hif4_quantize(x, residual=False)
+    assert int(qm[0, 0]) == int(meta[0, 0]), hex(int(qm[0, 0]))
+    assert np.array_equal(qc, codes), qc
+    got = o.hif4_dequant(qc, qm)[0]
+    assert np.array_equal(got, want) and np.array_equal(np.signbit(got), np.signbit(want))
+
+
+def pin_hif4_macro_scale_brute_force(o):
+    """Reading 1: the macro byte is the smallest of the 256 E6M2 values S with
+    7 S >= amax (exhaustive), values ordered with the byte."""
+    vals = [hif4_macro_py(b) for b in range(256)]
+    assert all(vals[b] < vals[b + 1] for b in range(255))
+    for b in range(256):
+        assert o.hif4_macro_value(b) == vals[b]
+    rng = np.random.default_rng(41)
+    amaxes = list(rng.lognormal(0, 8, 2000)) + [0.0, 1e-30, 7 * vals[0], 7 * vals[0] * 1.01,
+                                                7 * vals[255], 7 * vals[255] * 2, 1e30]
+    amaxes += [7 * v for v in vals[::5]] + [np.nextafter(7 * v, np.inf) for v in vals[::7]]
+    for a in amaxes:
+        want = next((b for b in range(256) if 7 * vals[b] >= a), 255)
+        assert o.hif4_macro_byte(a) == want, (a, want)
+
+
+def _hif4_blocks(seed, n):
+    """Blocks with varied spreads, outliers, zeros, exact ties and negative
+    zeros, for the brute-force pins."""
+    rng = np.random.default_rng(seed)
+    xs = []
+    for t in range(n):
+        x = rng.standard_normal(64) * np.exp(rng.uniform(-6, 6))
+        if t % 3 == 0:
+            x[rng.integers(0, 64, 3)] *= rng.uniform(5, 60)
+        if t % 4 == 1:
+            x[rng.integers(0, 64, 20)] = 0.0
+        if t % 5 == 2:
+            x[rng.integers(0, 64, 5)] = -0.0
+        xs.append(x)
+    # Blocks whose elements sit exactly on midpoints of their encoding grid.
+    for t in range(n // 4):
+        s = hif4_macro_py(int(rng.integers(150, 210)))
+        e = rng.integers(0, 3, 16)
+        k = rng.integers(0, 7, 64)
+        x = (2 * k + 1) / 8.0 * s * 2.0 ** np.repeat(e, 4) * rng.choice([-1.0, 1.0], 64)
+        x[0] = 7 * s * rng.choice([-1.0, 1.0])
+        xs.append(x)
+    return np.array(xs)
+
+
+def pin_hif4_encode_brute_force(o):
+    """Readings 1-3 by their defining properties, exhaustively: the macro
+    scale is the smallest with 7 S >= amax; per 8-element group, among the
+    eight settings of (E1_8, E1_16a, E1_16b) that saturate no element, the
+    one with the smallest total exponent, E1_8 = 0 on a tie; each element the
+    nearest of the eight grid values (ties to even k), sign kept."""
+    x = _hif4_blocks(43, 240)
+    qc, qm, _, _ = o.hif4_quantize(x, residual=False)
+    vals = [hif4_macro_py(b) for b in range(256)]
+    for r in range(x.shape[0]):
+        xb = x[r]
+        amax = np.abs(xb).max()
+        sb = next((b for b in range(256) if 7 * vals[b] >= amax), 255)
+        meta = int(qm[r, 0])
+        assert meta & 255 == sb, (r, meta & 255, sb)
+        s = vals[sb]
+        gmax = np.abs(xb).reshape(16, 4).max(1)
+        for g in range(8):
+            best = None
+            for e8 in (0, 1):
+                for ea in (0, 1):
+                    for eb in (0, 1):
+                        ta, tb = e8 + ea, e8 + eb
+                        if 1.75 * s * 2 ** ta < gmax[2 * g] or 1.75 * s * 2 ** tb < gmax[2 * g + 1]:
+                            continue
+                        key = (ta + tb, e8)
+                        if best is None or key < best[0]:
+                            best = (key, e8, ea, eb)
+            _, e8, ea, eb = best
+            assert (meta >> (8 + g)) & 1 == e8, (r, g)
+            assert (meta >> (16 + 2 * g)) & 1 == ea and (meta >> (17 + 2 * g)) & 1 == eb, (r, g)
+        for i in range(64):
+            c = (int(qc[r, i // 2]) >> (4 * (i & 1))) & 15
+            e = ((meta >> (8 + i // 8)) & 1) + ((meta >> (16 + i // 4)) & 1)
+            u = s * 2.0 ** e
+            d = [abs(abs(xb[i]) - k / 4.0 * u) for k in range(8)]
+            best = min(d)
+            ks = [k for k in range(8) if d[k] == best]
+            k_want = ks[0] if len(ks) == 1 else [k for k in ks if k % 2 == 0][0]
+            assert c & 7 == k_want, (r, i, xb[i], c, k_want)
+            assert bool(c & 8) == bool(np.signbit(xb[i])), (r, i)
+
+
+def pin_hif4_residual(o):
+    """RFQ with HiF4 (Eq. 9-10): the residual x - V is exact in fp32 for fp32
+    inputs, and its quantized form never moves an element away from x:
+    |x - V - Vr| <= |x - V| (zero is on the grid and rounding is to nearest)."""
+    x = _hif4_blocks(47, 120).astype(np.float32).astype(np.float64)
+    qc, qm, rc, rm = o.hif4_quantize(x)
+    v = hif4_decode_py(qc, qm.reshape(-1, 1))
+    vr = hif4_decode_py(rc, rm.reshape(-1, 1))
+    r64 = x - v
+    r32 = (x.astype(np.float32) - v.astype(np.float32)).astype(np.float64)
+    assert np.array_equal(r32, r64)
+    assert np.all(np.abs(x - v - vr) <= np.abs(x - v))
+    nz = np.abs(x - v).sum(1) > 0
+    assert np.all(np.abs(x - v - vr).sum(1)[nz] < np.abs(x - v).sum(1)[nz])
+    rq, rmq, _, _ = o.hif4_quantize(r64, residual=False)
+    assert np.array_equal(rq, rc) and np.array_equal(rmq, rm)
+
+
+def pin_hif4_gemm_brute_force(o):
+    """The HiF4 RFQ product against numpy on values decoded here (Eq. 6, 11)."""
+    rng = np.random.default_rng(53)
+    for M, N, K in ((3, 5, 64), (7, 4, 192), (2, 9, 128)):
+        x = rng.standard_normal((M, K)) * np.exp(rng.uniform(-3, 3, (M, 1)))
+        w = rng.normal(0, 0.02, (N, K))
+        qc, qm, rc, rm = o.hif4_quantize(x)
+        wc, wm, _, _ = o.hif4_quantize(w, residual=False)
+        z, bound = o.hif4_gemm(qc, qm, rc, rm, wc, wm)
+        dq, dr, dw = hif4_decode_py(qc, qm), hif4_decode_py(rc, rm), hif4_decode_py(wc, wm)
+        want = dq @ dw.T + dr @ dw.T
+        assert np.all(np.abs(z - want) <= 1e-12 * bound + 1e-300), (M, N, K)
+        assert np.allclose(bound, np.abs(dq) @ np.abs(dw).T + np.abs(dr) @ np.abs(dw).T,
+                           rtol=1e-12, atol=0)
+        z0, _ = o.hif4_gemm(qc, qm, None, None, wc, wm)
+        assert np.all(np.abs(z0 - dq @ dw.T) <= 1e-12 * bound + 1e-300)
 
 
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]
