@@ -243,6 +243,68 @@ rfq_status rfq_gemm_stream(const void *x, rfq_dtype x_dtype, int residual,
                            int64_t M, int64_t N, int64_t K,
                            void *z, rfq_dtype z_dtype, void *hip_stream);
 
+/*
+ * HiF4 form of the path (Sec. 3.2.3, Eq. 5-6).  A block is 64 consecutive
+ * elements of a row along K (K a positive multiple of 64, else
+ * RFQ_ERR_SHAPE).  Per block one uint32 metadata word:
+ *   bits 0-7   E6M2 macro scale byte E << 2 | M: S = 2^(E-48) (1 + M/4) (Eq. 5);
+ *   bits 8-15  E1_8: bit g is the micro-exponent of elements 8g .. 8g+7;
+ *   bits 16-31 E1_16: bit j is the micro-exponent of elements 4j .. 4j+3.
+ * Per element a 4-bit S1P2 code sign << 3 | k (magnitude k/4, k = 0..7),
+ * two per byte, element 2j in the low nibble of byte j.  Element i of a
+ * block is V_i = S 2^(E1_8[i/8] + E1_16[i/4]) (-1)^sign k/4 (Eq. 6).
+ * Layouts: codes [rows][K/2] bytes, meta [rows][K/64] uint32, row-major.
+ *
+ * The paper defines the decode, not the encoder.  This library encodes a
+ * block as follows: S is the smallest E6M2 value with 7 S >= the block's
+ * largest magnitude (byte 255 beyond 7 times the largest value, where
+ * elements saturate); a 4-element group needs the smallest e in {0, 1, 2}
+ * with 1.75 2^e S >= its largest magnitude; E1_8 of an 8-element group is 1
+ * when one of its two 4-element groups needs 2, and E1_16 = max(e - E1_8, 0);
+ * k = |x| / (S 2^(E1_8 + E1_16) / 4) rounded to nearest, ties to even, at most
+ * 7; the sign is kept, also for a zero.
+ */
+
+/*
+ * HiF4 RFQ quantizer: primary HiF4 code of x and, when r_codes and r_meta are
+ * given, the HiF4 code of the residual x - deq(primary) (Eq. 8-10 with HiF4
+ * codes); the residual is exact in fp32 and never written to memory.
+ * Without the residual pair this is the weight quantizer.
+ *   x        [rows][K] row-major, x_dtype; 16-byte aligned.
+ *   q_codes  [rows][K/2], q_meta [rows][K/64]; 4-byte aligned.
+ *   r_codes, r_meta: the same shapes, or both NULL.
+ * Non-finite inputs are outside the contract.  At most about 2^31 blocks
+ * (rows * K / 64) per call.
+ */
+rfq_status rfq_hif4_quantize(const void *x, rfq_dtype x_dtype, int64_t rows, int64_t K,
+                             uint8_t *q_codes, uint32_t *q_meta,
+                             uint8_t *r_codes, uint32_t *r_meta, void *hip_stream);
+
+/*
+ * HiF4 dequantization (Eq. 6): out[r][k] = V of the code, exact in fp32.
+ *   codes [rows][K/2], meta [rows][K/64] (4-byte aligned); out [rows][K]
+ *   fp32, 16-byte aligned.
+ */
+rfq_status rfq_hif4_dequant(const uint8_t *codes, const uint32_t *meta, int64_t rows, int64_t K,
+                            float *out, void *hip_stream);
+
+/*
+ * HiF4 RFQ product (Eq. 11 with HiF4 codes, phi = 1; phi = 0 when r_codes and
+ * r_meta are both NULL):
+ *   Z[m][n] = sum_k V_q[m][k] V_w[n][k] + sum_k V_r[m][k] V_w[n][k].
+ * Every product of two HiF4 values is exact; accumulation is fp32 in an
+ * unspecified order.  The output is fp32, or bf16 rounded to nearest even.
+ *   q_codes, r_codes, w_codes: [M][K/2], [M][K/2], [N][K/2], 16-byte aligned.
+ *   q_meta, r_meta, w_meta: [M][K/64], [M][K/64], [N][K/64], 4-byte aligned.
+ *   z        [M][N] row-major, z_dtype; 16-byte aligned.
+ *   M, N below 2^31 and ceil(M/128) ceil(N/256) < 2^23.
+ */
+rfq_status rfq_hif4_gemm(const uint8_t *q_codes, const uint32_t *q_meta,
+                         const uint8_t *r_codes, const uint32_t *r_meta,
+                         const uint8_t *w_codes, const uint32_t *w_meta,
+                         int64_t M, int64_t N, int64_t K,
+                         void *z, rfq_dtype z_dtype, void *hip_stream);
+
 /* Static, never-NULL description of a status code. */
 const char *rfq_status_str(rfq_status s);
 

@@ -58,6 +58,21 @@ bool product_fits(int64_t M, int64_t N) {
   return general <= kMaxWorkItems && large <= kMaxWorkItems;
 }
 
+// HiF4 calls: K a positive multiple of 64 (one metadata word per 64-element
+// block).  The quantizer runs 256 work items per 128 blocks; the product one
+// 512-work-item workgroup per 128 x 256 output tile.
+rfq_status check_k64(int64_t rows, int64_t K) {
+  if (rows < 0 || K < 64 || (K % 64) != 0 || K > kMaxK) return RFQ_ERR_SHAPE;
+  return RFQ_OK;
+}
+bool hif4_quantizer_fits(int64_t rows, int64_t K) {
+  return !exceeds(rows, K / 64, (kMaxWorkItems / 256) * 128);
+}
+bool hif4_product_fits(int64_t M, int64_t N) {
+  if (M > INT32_MAX || N > INT32_MAX) return false;
+  return ((M + 127) / 128) * ((N + 255) / 256) * 512 <= kMaxWorkItems;
+}
+
 // Confirms that the current device is a gfx950 GPU (cached per device).
 rfq_status check_device() {
   int dev = -1;
@@ -264,11 +279,65 @@ rfq_status rfq_gemm_stream(const void *x, rfq_dtype x_dtype, int residual,
                                           static_cast<hipStream_t>(hip_stream)));
 }
 
+rfq_status rfq_hif4_quantize(const void *x, rfq_dtype x_dtype, int64_t rows, int64_t K,
+                             uint8_t *q_codes, uint32_t *q_meta,
+                             uint8_t *r_codes, uint32_t *r_meta, void *hip_stream) {
+  if (!valid_dtype(x_dtype)) return RFQ_ERR_DTYPE;
+  rfq_status s = check_k64(rows, K);
+  if (s != RFQ_OK) return s;
+  if (!hif4_quantizer_fits(rows, K)) return RFQ_ERR_SHAPE;
+  if (rows == 0) return RFQ_OK;
+  if (!x || !q_codes || !q_meta) return RFQ_ERR_NULL;
+  if ((r_codes == nullptr) != (r_meta == nullptr)) return RFQ_ERR_NULL;
+  if (!aligned(x, 16) || !aligned(q_codes, 4) || !aligned(q_meta, 4) ||
+      (r_codes && (!aligned(r_codes, 4) || !aligned(r_meta, 4))))
+    return RFQ_ERR_ALIGN;
+  if ((s = check_device()) != RFQ_OK) return s;
+  return launched(rfq::launch_hif4_quantize(x, x_dtype == RFQ_BF16, rows * K, q_codes, q_meta,
+                                            r_codes, r_meta,
+                                            static_cast<hipStream_t>(hip_stream)));
+}
+
+rfq_status rfq_hif4_dequant(const uint8_t *codes, const uint32_t *meta, int64_t rows, int64_t K,
+                            float *out, void *hip_stream) {
+  rfq_status s = check_k64(rows, K);
+  if (s != RFQ_OK) return s;
+  if (exceeds(rows, K, kMaxElements)) return RFQ_ERR_SHAPE;
+  if (rows == 0) return RFQ_OK;
+  if (!codes || !meta || !out) return RFQ_ERR_NULL;
+  if (!aligned(codes, 4) || !aligned(meta, 4) || !aligned(out, 16)) return RFQ_ERR_ALIGN;
+  if ((s = check_device()) != RFQ_OK) return s;
+  return launched(rfq::launch_hif4_dequant(codes, meta, rows * K, out,
+                                           static_cast<hipStream_t>(hip_stream)));
+}
+
+rfq_status rfq_hif4_gemm(const uint8_t *q_codes, const uint32_t *q_meta,
+                         const uint8_t *r_codes, const uint32_t *r_meta,
+                         const uint8_t *w_codes, const uint32_t *w_meta,
+                         int64_t M, int64_t N, int64_t K,
+                         void *z, rfq_dtype z_dtype, void *hip_stream) {
+  if (!valid_dtype(z_dtype)) return RFQ_ERR_DTYPE;
+  rfq_status s = check_k64(M, K);
+  if (s != RFQ_OK) return s;
+  if (N < 0 || !hif4_product_fits(M, N)) return RFQ_ERR_SHAPE;
+  if (M == 0 || N == 0) return RFQ_OK;
+  if (!q_codes || !q_meta || !w_codes || !w_meta || !z) return RFQ_ERR_NULL;
+  if ((r_codes == nullptr) != (r_meta == nullptr)) return RFQ_ERR_NULL;
+  if (!aligned(q_codes, 16) || !aligned(w_codes, 16) || !aligned(q_meta, 4) ||
+      !aligned(w_meta, 4) || (r_codes && (!aligned(r_codes, 16) || !aligned(r_meta, 4))) ||
+      !aligned(z, 16))
+    return RFQ_ERR_ALIGN;
+  if ((s = check_device()) != RFQ_OK) return s;
+  return launched(rfq::launch_hif4_gemm(q_codes, q_meta, r_codes, r_meta, w_codes, w_meta, M, N,
+                                        K, z, z_dtype == RFQ_BF16,
+                                        static_cast<hipStream_t>(hip_stream)));
+}
+
 const char *rfq_status_str(rfq_status s) {
   switch (s) {
     case RFQ_OK: return "ok";
     case RFQ_ERR_NULL: return "null pointer (or half of an optional pair)";
-    case RFQ_ERR_SHAPE: return "bad shape (negative size, K not a positive multiple of 32, or a size limit)";
+    case RFQ_ERR_SHAPE: return "bad shape (negative size, K not a positive multiple of 32 (64 for HiF4), or a size limit)";
     case RFQ_ERR_DTYPE: return "unknown dtype";
     case RFQ_ERR_ALIGN: return "misaligned pointer";
     case RFQ_ERR_DEVICE: return "no gfx950 device current";

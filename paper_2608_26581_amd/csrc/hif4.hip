@@ -1,0 +1,504 @@
+// HiF4 form of the RFQ path on gfx950 (Sec. 3.2.3, Eq. 5-6, with the RFQ
+// steps of Sec. 4.3, Eq. 8-11): the quantizer (primary HiF4 code and, for
+// activations, the HiF4 code of the residual it leaves), dequantization and
+// the RFQ product.
+//
+// Format.  A block is 64 consecutive elements of a row along K.  Per block
+// one 32-bit metadata word: bits 0-7 the E6M2 macro scale byte (E << 2 | M,
+// S = 2^(E-48) (1 + M/4), Eq. 5), bits 8-15 the 1-bit micro-exponents of the
+// eight 8-element groups (E1_8, bit g for elements 8g..8g+7), bits 16-31
+// those of the sixteen 4-element groups (E1_16, bit j for elements 4j..4j+3).
+// Per element a 4-bit S1P2 code, sign << 3 | k with magnitude k/4, two per
+// byte, element 2j in the low nibble of byte j.  Value (Eq. 6):
+//     V_i = S 2^(E1_8[i/8] + E1_16[i/4]) (-1)^sign k/4.
+// With c = 4 + M this is V_i = +-k c 2^(E - 52 + e_i): at most 6 significant
+// bits with exponents in [-52, 19], so every value is exact in bf16 and every
+// product of two values is exact in fp32.
+//
+// Encoder.  The paper fixes the decode but not the encoder; this library
+// takes these choices (dequantization and the product are exact for any
+// metadata and codes):
+//   - S is the smallest E6M2 value with 7 S >= amax (7 = 1.75 * 2^2, the
+//     largest factor an element can carry), so no element saturates unless
+//     amax exceeds 7 times the largest E6M2 value (then byte 255);
+//   - the 4-element group j needs the smallest e_j in {0, 1, 2} with
+//     1.75 * 2^e_j * S >= its largest magnitude; the 8-element group g takes
+//     E1_8[g] = 1 when one of its two 4-element groups needs 2, and then
+//     E1_16[j] = max(e_j - E1_8[g], 0);
+//   - k is |x| / (S 2^e / 4) rounded to nearest, ties to even, at most 7; the
+//     sign is kept, also for a zero.
+// The rounding is k = rne(b / c) with b = |x| 2^(52 - E - e), an exact
+// scaling.  A quotient from the reciprocal of c, refined once with the exact
+// remainder fma(-y, c, b), is the correctly rounded b/c wherever the integer
+// rounding depends on it: an exact tie j + 1/2 is representable and comes
+// out exactly, and any other b/c lies at least ulp(b)/c > ulp(y)/2 away from
+// j + 1/2, more than the refined quotient's error.  The residual x - V is
+// exact in fp32 (V is the grid value nearest x, so the difference is a
+// multiple of the finer of ulp(x) and the grid's last bit and smaller than a
+// grid unit), so the second encode sees exactly the residual.
+//
+// Quantizer work decomposition: a lane owns 8 consecutive elements (one
+// 8-element group, 16 bytes of bf16 or 32 of fp32 input); the 8 lanes of a
+// block combine their maxima and metadata bits with DPP; a wave covers 32
+// blocks in 4 steps, each load instruction reading 1 KB (bf16) of contiguous
+// input and each code store writing 256 contiguous bytes.
+//
+// Product.  gfx950 has no matrix-core format for HiF4, so the product
+// decodes codes to bf16 and runs v_mfma_f32_32x32x16_bf16, whose products are
+// exact; accumulation is fp32.  A workgroup computes a 128 x 256 tile of Z
+// with 8 waves in two roles: four producer waves load the codes and metadata
+// of one K block (64 values) of the tile's 128 activation rows (and 128
+// residual rows) and 256 weight rows, decode them and write bf16 rows into
+// one of two LDS buffers, while four consumer waves (2 x 2, each a 64 x 128
+// sub-tile) multiply the other buffer; one workgroup barrier per K block
+// hands the buffers over.  Each SIMD holds one wave of each role, so
+// decoding (VALU) and multiplication (matrix core) overlap.  16-byte chunks of
+// an LDS row are XOR-swizzled by row so that fragment reads and row writes
+// are free of bank conflicts.  Rows past M or N are clamped to the last row
+// for loading; their results are not stored.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <atomic>
+
+#include "gemm_common.h"
+#include "rfq_internal.h"
+
+namespace rfq {
+namespace {
+
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+
+constexpr int kH = 64;                 // elements per HiF4 block
+constexpr int kQThreads = 256;
+constexpr int kQSteps = 4;             // 8-element units per lane
+constexpr int kLoopGrid = 1 << 16;     // dequantization grid cap (loops over the rest)
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
+}
+
+// Maximum and bitwise OR over aligned groups of 8 lanes (quad_perm 1,0,3,2,
+// quad_perm 2,3,0,1, then row_half_mirror, which pairs lane i with 7 - i).
+__device__ __forceinline__ float max8(float v) {
+  v = fmaxf(v, __uint_as_float(dpp_u<0xB1>(__float_as_uint(v))));
+  v = fmaxf(v, __uint_as_float(dpp_u<0x4E>(__float_as_uint(v))));
+  return fmaxf(v, __uint_as_float(dpp_u<0x141>(__float_as_uint(v))));
+}
+__device__ __forceinline__ uint32_t or8(uint32_t v) {
+  v |= dpp_u<0xB1>(v);
+  v |= dpp_u<0x4E>(v);
+  return v | dpp_u<0x141>(v);
+}
+
+// E6M2 value of byte b: (4 + (b & 3)) 2^((b >> 2) - 50), whose fp32 pattern
+// is (b + 316) << 21.
+__device__ __forceinline__ float macro_value(uint32_t b) {
+  return __uint_as_float((b + 316u) << 21);
+}
+
+// Smallest byte with 7 S >= amax.  The candidate rounds amax / 7 up to two
+// mantissa bits; it is off by at most one step, which the exact tests (7 S
+// has at most 6 significant bits) correct.
+__device__ __forceinline__ uint32_t macro_byte(float amax) {
+  const uint32_t u = __float_as_uint(amax * (1.0f / 7.0f));
+  int b = (int)(u >> 21) - 316 + ((u & 0x1FFFFFu) != 0 ? 1 : 0);
+  b = min(max(b, 0), 255);
+  if (b < 255 && 7.0f * macro_value((uint32_t)b) < amax) ++b;
+  if (b > 0 && 7.0f * macro_value((uint32_t)b - 1u) >= amax) --b;
+  return (uint32_t)b;
+}
+
+// 2^p for p in the normal range.
+__device__ __forceinline__ float pow2(int p) { return __uint_as_float((uint32_t)(p + 127) << 23); }
+
+// Encodes the 8 elements of this lane (8-element group g of its block): the
+// lane's 32 code bits, the block's metadata word (same in all 8 lanes) and,
+// with WANT_V, the values V of the codes.
+template <bool WANT_V>
+__device__ __forceinline__ uint32_t encode8(const float (&x)[8], int g, uint32_t &meta,
+                                            float (&v)[8]) {
+  float ga = fabsf(x[0]), gb = fabsf(x[4]);
+#pragma unroll
+  for (int i = 1; i < 4; ++i) {
+    ga = fmaxf(ga, fabsf(x[i]));
+    gb = fmaxf(gb, fabsf(x[4 + i]));
+  }
+  const uint32_t byte = macro_byte(max8(fmaxf(ga, gb)));
+  const float t0 = 1.75f * macro_value(byte);                // exact
+  const int na = (ga > t0) + (ga > 2.0f * t0), nb = (gb > t0) + (gb > 2.0f * t0);
+  const int e8 = (na == 2) | (nb == 2);
+  const int ea = max(na - e8, 0), eb = max(nb - e8, 0);
+  meta = byte | or8(((uint32_t)e8 << (8 + g)) | ((uint32_t)ea << (16 + 2 * g)) |
+                    ((uint32_t)eb << (17 + 2 * g)));
+  const int E = (int)(byte >> 2);
+  const float c = (float)(4 + (byte & 3));
+  const float rc = __builtin_amdgcn_rcpf(c);
+  uint32_t code = 0;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int e = e8 + (i < 4 ? ea : eb);
+    const float b = fabsf(x[i]) * pow2(52 - E - e);
+    const float y = b * rc;
+    const float yq = fmaf(fmaf(-y, c, b), rc, y);
+    const float kf = fminf(__builtin_rintf(yq), 7.0f);
+    code |= (((__float_as_uint(x[i]) >> 28) & 8u) | (uint32_t)kf) << (4 * i);
+    if constexpr (WANT_V) v[i] = copysignf(kf * (c * pow2(E - 52 + e)), x[i]);
+  }
+  return code;
+}
+
+template <bool BF16_IN>
+__device__ __forceinline__ void unpack8(const u32x4 (&w)[BF16_IN ? 1 : 2], float (&v)[8]) {
+  if constexpr (BF16_IN) {
+    const u32x4 a = w[0];
+    v[0] = __uint_as_float(a.x << 16); v[1] = __uint_as_float(a.x & 0xFFFF0000u);
+    v[2] = __uint_as_float(a.y << 16); v[3] = __uint_as_float(a.y & 0xFFFF0000u);
+    v[4] = __uint_as_float(a.z << 16); v[5] = __uint_as_float(a.z & 0xFFFF0000u);
+    v[6] = __uint_as_float(a.w << 16); v[7] = __uint_as_float(a.w & 0xFFFF0000u);
+  } else {
+    v[0] = __uint_as_float(w[0].x); v[1] = __uint_as_float(w[0].y);
+    v[2] = __uint_as_float(w[0].z); v[3] = __uint_as_float(w[0].w);
+    v[4] = __uint_as_float(w[1].x); v[5] = __uint_as_float(w[1].y);
+    v[6] = __uint_as_float(w[1].z); v[7] = __uint_as_float(w[1].w);
+  }
+}
+
+// nunits = elements / 8.  Lanes past the end load the last unit (never out
+// of bounds) and store nothing; a block is wholly inside or past the end.
+template <bool BF16_IN, bool RES>
+__global__ __launch_bounds__(kQThreads) void hif4_quantize_kernel(
+    const void *__restrict__ x, int64_t nunits, uint8_t *__restrict__ qc,
+    uint32_t *__restrict__ qm, uint8_t *__restrict__ rc, uint32_t *__restrict__ rm) {
+  constexpr int kLoads = BF16_IN ? 1 : 2;
+  const int lane = threadIdx.x & 63, g = lane & 7;
+  const int64_t u0 =
+      ((int64_t)blockIdx.x * (kQThreads / 64) + (threadIdx.x >> 6)) * (64 * kQSteps);
+  const u32x4 *xin = reinterpret_cast<const u32x4 *>(x);
+  u32x4 in[kQSteps][kLoads];
+#pragma unroll
+  for (int s = 0; s < kQSteps; ++s) {
+    int64_t u = u0 + 64 * s + lane;
+    u = u < nunits ? u : nunits - 1;
+#pragma unroll
+    for (int l = 0; l < kLoads; ++l) in[s][l] = __builtin_nontemporal_load(xin + kLoads * u + l);
+  }
+#pragma unroll
+  for (int s = 0; s < kQSteps; ++s) {
+    const int64_t u = u0 + 64 * s + lane;
+    float v[8], d[8];
+    unpack8<BF16_IN>(in[s], v);
+    uint32_t meta;
+    const uint32_t code = encode8<RES>(v, g, meta, d);
+    if (u < nunits) {
+      reinterpret_cast<uint32_t *>(qc)[u] = code;
+      if (g == 0) qm[u >> 3] = meta;
+    }
+    if constexpr (RES) {
+      float r[8], unused[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) r[i] = v[i] - d[i];
+      uint32_t rmeta;
+      const uint32_t rcode = encode8<false>(r, g, rmeta, unused);
+      if (u < nunits) {
+        reinterpret_cast<uint32_t *>(rc)[u] = rcode;
+        if (g == 0) rm[u >> 3] = rmeta;
+      }
+    }
+  }
+}
+
+// Unit (value of k = 1) of the two 4-element groups of 8-element group g:
+// c 2^(E - 52 + e).
+__device__ __forceinline__ void group_units(uint32_t meta, int g, float &ua, float &ub) {
+  const float base = (float)(4 + (meta & 3)) * pow2((int)((meta >> 2) & 63) - 52);
+  const uint32_t e8 = (meta >> (8 + g)) & 1u;
+  const uint32_t ea = e8 + ((meta >> (16 + 2 * g)) & 1u);
+  const uint32_t eb = e8 + ((meta >> (17 + 2 * g)) & 1u);
+  ua = __uint_as_float(__float_as_uint(base) + (ea << 23));
+  ub = __uint_as_float(__float_as_uint(base) + (eb << 23));
+}
+
+// One dequantization thread: 8 elements (one code word) to fp32.
+__global__ __launch_bounds__(256) void hif4_dequant_kernel(
+    const uint32_t *__restrict__ codes, const uint32_t *__restrict__ meta, int64_t nunits,
+    float4 *__restrict__ out) {
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  for (int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x; u < nunits; u += stride) {
+    const uint32_t w = codes[u];
+    float ua, ub;
+    group_units(meta[u >> 3], (int)(u & 7), ua, ub);
+    float d[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const uint32_t nib = (w >> (4 * i)) & 15u;
+      const float mag = (float)(nib & 7u) * (i < 4 ? ua : ub);
+      d[i] = (nib & 8u) ? -mag : mag;
+    }
+    out[2 * u] = make_float4(d[0], d[1], d[2], d[3]);
+    out[2 * u + 1] = make_float4(d[4], d[5], d[6], d[7]);
+  }
+}
+
+// ---------------------------------------------------------------- product
+
+constexpr int kBM = 128, kBN = 256;            // tile: activation rows x weight rows
+constexpr int kGThreads = 512;                 // 4 producer + 4 consumer waves
+constexpr int kRowBytes = kH * 2;              // one decoded bf16 row of a K block
+constexpr int kTM = 64, kTN = 128;             // consumer sub-tile
+constexpr int kFM = kTM / 32, kFN = kTN / 32;
+
+template <bool RES>
+struct HSmem {
+  static constexpr int kWRow0 = (RES ? 2 : 1) * kBM;    // q rows, r rows, then w rows
+  static constexpr int kRows = kWRow0 + kBN;
+  static constexpr int kBufBytes = kRows * kRowBytes;
+  static constexpr int kBytes = 2 * kBufBytes;
+};
+
+__device__ __forceinline__ int hswz(int row, int chunk) {
+  return row * kRowBytes + 16 * (chunk ^ ((row >> 1) & 7));
+}
+
+// bf16 pairs of the 8 elements of code word w (8-element group g of a block
+// with metadata meta): element 2p in the low half of pair p.
+__device__ __forceinline__ u32x4 decode8_bf16(uint32_t w, uint32_t meta, int g) {
+  float ua, ub;
+  group_units(meta, g, ua, ub);
+  const uint32_t lo = w & 0x07070707u, hi = (w >> 4) & 0x07070707u, w4 = w << 4;
+  uint32_t p[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const float u = q < 2 ? ua : ub;
+    const float f0 = (float)((lo >> (8 * q)) & 0xFFu) * u;   // element 2q (exact)
+    const float f1 = (float)((hi >> (8 * q)) & 0xFFu) * u;   // element 2q + 1
+    const uint32_t pair = __builtin_amdgcn_perm(__float_as_uint(f1), __float_as_uint(f0),
+                                                0x07060302u);
+    // Sign bits: bit 7 of byte q of w4 (element 2q) to bit 15, bit 7 of
+    // byte q of w (element 2q + 1) to bit 31.
+    const uint32_t sgn = __builtin_amdgcn_perm(w, w4, 0x000C000Cu | (q << 8) | ((4 + q) << 24));
+    p[q] = pair | (sgn & 0x80008000u);
+  }
+  return u32x4{p[0], p[1], p[2], p[3]};
+}
+
+template <bool RES, bool ZBF16>
+__global__ __launch_bounds__(kGThreads) void hif4_gemm_kernel(
+    const uint8_t *__restrict__ qc, const uint32_t *__restrict__ qm,
+    const uint8_t *__restrict__ rc, const uint32_t *__restrict__ rm,
+    const uint8_t *__restrict__ wc, const uint32_t *__restrict__ wm, int64_t M, int64_t N,
+    int64_t K, void *__restrict__ z) {
+  using S = HSmem<RES>;
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+
+  int tm, tn;
+  tile_coords<8>(blockIdx.x, (int)((M + kBM - 1) / kBM), (int)((N + kBN - 1) / kBN), tm, tn);
+  const int64_t m0 = (int64_t)tm * kBM, n0 = (int64_t)tn * kBN;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int nsteps = (int)(K / kH);
+  const int64_t kbytes = K / 2, kblocks = K / kH;
+
+  if (wave < 4) {
+    // ---- producer: (row, half) items; a half is 32 elements, 16 code bytes.
+    constexpr int kItems = S::kRows * 2 / 256;
+    const int pt = tid;                         // 0..255
+    const uint8_t *src[kItems];
+    const uint32_t *msrc[kItems];
+    int lrow[kItems];
+#pragma unroll
+    for (int i = 0; i < kItems; ++i) {
+      const int r = pt / 2 + 128 * i;
+      lrow[i] = r;
+      int64_t grow;
+      if (r >= S::kWRow0) {
+        grow = min(n0 + (r - S::kWRow0), N - 1);
+        src[i] = wc + grow * kbytes + 16 * (pt & 1);
+        msrc[i] = wm + grow * kblocks;
+      } else {
+        const bool is_r = RES && r >= kBM;
+        grow = min(m0 + (is_r ? r - kBM : r), M - 1);
+        src[i] = (is_r ? rc : qc) + grow * kbytes + 16 * (pt & 1);
+        msrc[i] = (is_r ? rm : qm) + grow * kblocks;
+      }
+    }
+    const int h = pt & 1;
+    u32x4 cw[kItems];
+    uint32_t mw[kItems];
+#pragma unroll
+    for (int i = 0; i < kItems; ++i) {
+      cw[i] = *reinterpret_cast<const u32x4 *>(src[i]);
+      mw[i] = msrc[i][0];
+    }
+    for (int s = 0; s < nsteps; ++s) {
+      uint8_t *buf = smem + (s & 1) * S::kBufBytes;
+#pragma unroll
+      for (int i = 0; i < kItems; ++i) {
+        const uint32_t d[4] = {cw[i].x, cw[i].y, cw[i].z, cw[i].w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          *reinterpret_cast<u32x4 *>(buf + hswz(lrow[i], 4 * h + q)) =
+              decode8_bf16(d[q], mw[i], 4 * h + q);
+      }
+      if (s + 1 < nsteps) {
+#pragma unroll
+        for (int i = 0; i < kItems; ++i) {
+          cw[i] = *reinterpret_cast<const u32x4 *>(src[i] + (int64_t)(s + 1) * 32);
+          mw[i] = msrc[i][s + 1];
+        }
+      }
+      __syncthreads();
+    }
+    return;
+  }
+
+  // ---- consumer: 2 x 2 waves, each 64 activation rows x 128 weight rows.
+  const int cw_ = wave - 4, wmi = cw_ >> 1, wni = cw_ & 1;
+  const int frow = lane & 31, half = lane >> 5;
+  v16f acc[kFM][kFN];
+#pragma unroll
+  for (int i = 0; i < kFM; ++i)
+#pragma unroll
+    for (int j = 0; j < kFN; ++j) acc[i][j] = v16f{};
+
+  auto frag = [&](const uint8_t *buf, int row, int kk) {
+    return *reinterpret_cast<const v8bf *>(buf + hswz(row, 2 * kk + half));
+  };
+  for (int s = 0; s < nsteps; ++s) {
+    __syncthreads();
+    const uint8_t *buf = smem + (s & 1) * S::kBufBytes;
+#pragma unroll
+    for (int kk = 0; kk < kH / 16; ++kk) {
+      v8bf wf[kFN], xf[kFM], rf[RES ? kFM : 1];
+#pragma unroll
+      for (int j = 0; j < kFN; ++j) wf[j] = frag(buf, S::kWRow0 + wni * kTN + 32 * j + frow, kk);
+#pragma unroll
+      for (int i = 0; i < kFM; ++i) {
+        xf[i] = frag(buf, wmi * kTM + 32 * i + frow, kk);
+        if constexpr (RES) rf[i] = frag(buf, kBM + wmi * kTM + 32 * i + frow, kk);
+      }
+#pragma unroll
+      for (int i = 0; i < kFM; ++i)
+#pragma unroll
+        for (int j = 0; j < kFN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[j], xf[i], acc[i][j], 0, 0, 0);
+      if constexpr (RES) {
+#pragma unroll
+        for (int i = 0; i < kFM; ++i)
+#pragma unroll
+          for (int j = 0; j < kFN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[j], rf[i], acc[i][j], 0, 0, 0);
+      }
+    }
+  }
+
+  // ---- epilogue: lane holds Z[m][n .. n+3] for n = 8a + 4 half (a = 0..3)
+  // of each fragment (weights are the first MFMA operand).
+  const bool vec_ok = (N & 3) == 0;
+#pragma unroll
+  for (int i = 0; i < kFM; ++i) {
+    const int64_t m = m0 + wmi * kTM + 32 * i + frow;
+    if (m >= M) continue;
+#pragma unroll
+    for (int j = 0; j < kFN; ++j) {
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+        const int64_t n = n0 + wni * kTN + 32 * j + 8 * a + 4 * half;
+        const v16f &c = acc[i][j];
+        if constexpr (ZBF16) {
+          uint16_t *zp = reinterpret_cast<uint16_t *>(z) + m * N + n;
+          if (vec_ok && n + 3 < N) {
+            uint2 w;
+            w.x = bf16_rne(c[4 * a]) | (bf16_rne(c[4 * a + 1]) << 16);
+            w.y = bf16_rne(c[4 * a + 2]) | (bf16_rne(c[4 * a + 3]) << 16);
+            *reinterpret_cast<uint2 *>(zp) = w;
+          } else {
+#pragma unroll
+            for (int b = 0; b < 4; ++b)
+              if (n + b < N) zp[b] = (uint16_t)bf16_rne(c[4 * a + b]);
+          }
+        } else {
+          float *zp = reinterpret_cast<float *>(z) + m * N + n;
+          if (vec_ok && n + 3 < N) {
+            *reinterpret_cast<float4 *>(zp) =
+                make_float4(c[4 * a], c[4 * a + 1], c[4 * a + 2], c[4 * a + 3]);
+          } else {
+#pragma unroll
+            for (int b = 0; b < 4; ++b)
+              if (n + b < N) zp[b] = c[4 * a + b];
+          }
+        }
+      }
+    }
+  }
+}
+
+template <bool RES, bool ZBF16>
+hipError_t launch_hg(const uint8_t *qc, const uint32_t *qm, const uint8_t *rc,
+                     const uint32_t *rm, const uint8_t *wc, const uint32_t *wm, int64_t M,
+                     int64_t N, int64_t K, void *z, hipStream_t stream) {
+  auto kern = hif4_gemm_kernel<RES, ZBF16>;
+  static std::atomic<bool> attr_done[kMaxDevices];
+  const hipError_t e =
+      set_lds_limit(attr_done, reinterpret_cast<const void *>(kern), HSmem<RES>::kBytes);
+  if (e != hipSuccess) return e;
+  const int64_t tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
+  kern<<<dim3((unsigned)tiles), dim3(kGThreads), HSmem<RES>::kBytes, stream>>>(
+      qc, qm, rc, rm, wc, wm, M, N, K, z);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_hif4_quantize(const void *x, bool bf16_in, int64_t nelem, uint8_t *q_codes,
+                                uint32_t *q_meta, uint8_t *r_codes, uint32_t *r_meta,
+                                hipStream_t stream) {
+  const int64_t nunits = nelem / 8;
+  const int64_t per_wg = (kQThreads / 64) * 64 * kQSteps;
+  const dim3 grid((unsigned)((nunits + per_wg - 1) / per_wg)), block(kQThreads);
+  if (bf16_in) {
+    if (r_codes)
+      hif4_quantize_kernel<true, true><<<grid, block, 0, stream>>>(x, nunits, q_codes, q_meta,
+                                                                  r_codes, r_meta);
+    else
+      hif4_quantize_kernel<true, false><<<grid, block, 0, stream>>>(x, nunits, q_codes, q_meta,
+                                                                   nullptr, nullptr);
+  } else {
+    if (r_codes)
+      hif4_quantize_kernel<false, true><<<grid, block, 0, stream>>>(x, nunits, q_codes, q_meta,
+                                                                   r_codes, r_meta);
+    else
+      hif4_quantize_kernel<false, false><<<grid, block, 0, stream>>>(x, nunits, q_codes, q_meta,
+                                                                    nullptr, nullptr);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_hif4_dequant(const uint8_t *codes, const uint32_t *meta, int64_t nelem,
+                               float *out, hipStream_t stream) {
+  const int64_t nunits = nelem / 8;
+  const int64_t wgs = (nunits + 255) / 256;
+  hif4_dequant_kernel<<<(unsigned)(wgs < kLoopGrid ? wgs : kLoopGrid), 256, 0, stream>>>(
+      reinterpret_cast<const uint32_t *>(codes), meta, nunits, reinterpret_cast<float4 *>(out));
+  return hipGetLastError();
+}
+
+hipError_t launch_hif4_gemm(const uint8_t *q_codes, const uint32_t *q_meta,
+                            const uint8_t *r_codes, const uint32_t *r_meta,
+                            const uint8_t *w_codes, const uint32_t *w_meta, int64_t M, int64_t N,
+                            int64_t K, void *z, bool z_bf16, hipStream_t stream) {
+  if (r_codes) {
+    if (z_bf16)
+      return launch_hg<true, true>(q_codes, q_meta, r_codes, r_meta, w_codes, w_meta, M, N, K, z,
+                                   stream);
+    return launch_hg<true, false>(q_codes, q_meta, r_codes, r_meta, w_codes, w_meta, M, N, K, z,
+                                  stream);
+  }
+  if (z_bf16)
+    return launch_hg<false, true>(q_codes, q_meta, nullptr, nullptr, w_codes, w_meta, M, N, K, z,
+                                  stream);
+  return launch_hg<false, false>(q_codes, q_meta, nullptr, nullptr, w_codes, w_meta, M, N, K, z,
+                                 stream);
+}
+
+}  // namespace rfq

@@ -116,4 +116,17 @@ hipError_t launch_gemm_swiglu(const uint8_t *q_codes, const uint8_t *q_scales,
                               uint8_t *hq_scales, uint8_t *hr_codes, uint8_t *hr_scales,
                               uint16_t *h_out, hipStream_t stream);
 
+// HiF4 quantizer (nelem a multiple of 64; r_codes == nullptr: primary only),
+// dequantization and RFQ product (K a multiple of 64); metadata words are
+// uint32 per 64-element block.
+hipError_t launch_hif4_quantize(const void *x, bool bf16_in, int64_t nelem, uint8_t *q_codes,
+                                uint32_t *q_meta, uint8_t *r_codes, uint32_t *r_meta,
+                                hipStream_t stream);
+hipError_t launch_hif4_dequant(const uint8_t *codes, const uint32_t *meta, int64_t nelem,
+                               float *out, hipStream_t stream);
+hipError_t launch_hif4_gemm(const uint8_t *q_codes, const uint32_t *q_meta,
+                            const uint8_t *r_codes, const uint32_t *r_meta,
+                            const uint8_t *w_codes, const uint32_t *w_meta, int64_t M, int64_t N,
+                            int64_t K, void *z, bool z_bf16, hipStream_t stream);
+
 }  // namespace rfq

@@ -29,7 +29,7 @@ _STATUS_NAMES = {
 EXPORTS = (
     "rfq_quantize_act", "rfq_quantize_weight", "rfq_gemm", "rfq_dequant",
     "rfq_swiglu_quantize_act", "rfq_gemm_phi", "rfq_fallback_map", "rfq_gemm_swiglu_quantize",
-    "rfq_gemm_stream",
+    "rfq_gemm_stream", "rfq_hif4_quantize", "rfq_hif4_dequant", "rfq_hif4_gemm",
     "rfq_status_str", "rfq_abi_version",
 )
 
@@ -67,9 +67,13 @@ def load():
     lib.rfq_gemm_phi.argtypes = [P, P, P, P, P, P, P, I64, I64, I64, P, I32, P]
     lib.rfq_fallback_map.argtypes = [P, P, I64, I64, I32, I32, P, P]
     lib.rfq_gemm_stream.argtypes = [P, I32, I32, P, P, I64, I64, I64, P, I32, P]
+    lib.rfq_hif4_quantize.argtypes = [P, I32, I64, I64, P, P, P, P, P]
+    lib.rfq_hif4_dequant.argtypes = [P, P, I64, I64, P, P]
+    lib.rfq_hif4_gemm.argtypes = [P, P, P, P, P, P, I64, I64, I64, P, I32, P]
     for f in ("rfq_quantize_act", "rfq_quantize_weight", "rfq_gemm", "rfq_dequant",
               "rfq_swiglu_quantize_act", "rfq_gemm_swiglu_quantize", "rfq_gemm_phi",
-              "rfq_fallback_map", "rfq_gemm_stream"):
+              "rfq_fallback_map", "rfq_gemm_stream", "rfq_hif4_quantize", "rfq_hif4_dequant",
+              "rfq_hif4_gemm"):
         getattr(lib, f).restype = I32
     lib.rfq_status_str.argtypes = [I32]
     lib.rfq_status_str.restype = ctypes.c_char_p
@@ -381,6 +385,87 @@ def rfq_gemm_swiglu_quantize(q_codes, q_scales, r_codes, r_scales, wgu_codes, wg
         _stream(stream))
     _check("rfq_gemm_swiglu_quantize", st)
     return hqc, hqs, hrc, hrs, h
+
+
+# ---- HiF4 (64-element blocks; codes [rows][K/2] uint8, meta [rows][K/64]
+# int32 holding the uint32 metadata words bit for bit).
+
+_I32 = (torch.int32,)
+
+
+def _need_hif4(codes, meta, rows, K, name, dev=None):
+    if (dev is not None and _ok(codes, _U8, (rows, K // 2), dev)
+            and _ok(meta, _I32, (rows, K // 64), dev)):
+        return
+    _need(codes, name + " codes", _U8, (rows, K // 2), dev)
+    _need(meta, name + " meta", _I32, (rows, K // 64), dev)
+
+
+def _hif4_out(rows, K, device):
+    return (torch.empty((rows, K // 2), dtype=torch.uint8, device=device),
+            torch.empty((rows, K // 64), dtype=torch.int32, device=device))
+
+
+def rfq_hif4_quantize(x, residual=True, out=None, stream=None):
+    """X[rows][K] (K a multiple of 64) -> (q_codes, q_meta, r_codes, r_meta)
+    in HiF4; r_* are None when residual is False (the weight quantizer)."""
+    _need(x, "x", _FLOAT)
+    dev = x.get_device()
+    if x.dim() != 2:
+        raise ValueError("x must be 2-D [rows][K]")
+    rows, K = x.shape
+    if out is None:
+        qc, qm = _hif4_out(rows, K, x.device)
+        rc, rm = _hif4_out(rows, K, x.device) if residual else (None, None)
+    else:
+        qc, qm, rc, rm = out
+        _need_hif4(qc, qm, rows, K, "out primary", dev)
+        if (rc is None) != (rm is None):
+            raise ValueError("residual codes and meta must both be given or both be None")
+        if rc is not None:
+            _need_hif4(rc, rm, rows, K, "out residual", dev)
+    st = load().rfq_hif4_quantize(_ptr(x), _dtype_code(x), rows, K, _ptr(qc), _ptr(qm),
+                                  _ptr(rc), _ptr(rm), _stream(stream, dev))
+    _check("rfq_hif4_quantize", st)
+    return qc, qm, rc, rm
+
+
+def rfq_hif4_dequant(codes, meta, out=None, stream=None):
+    """HiF4 codes[rows][K/2], meta[rows][K/64] -> fp32 [rows][K]."""
+    rows, K = _shape_of_codes(codes, "codes")
+    _need_hif4(codes, meta, rows, K, "dequantization input")
+    dev = codes.get_device()
+    if out is None:
+        o = torch.empty((rows, K), dtype=torch.float32, device=codes.device)
+    else:
+        o = out
+        _need(o, "out", (torch.float32,), (rows, K), dev)
+    st = load().rfq_hif4_dequant(_ptr(codes), _ptr(meta), rows, K, _ptr(o), _stream(stream, dev))
+    _check("rfq_hif4_dequant", st)
+    return o
+
+
+def rfq_hif4_gemm(q_codes, q_meta, r_codes, r_meta, w_codes, w_meta,
+                  out_dtype=torch.float32, out=None, stream=None):
+    """HiF4 RFQ product Z[M][N] = (V_q + V_r) V_w^T; r_* None: primary only."""
+    M, K = _shape_of_codes(q_codes, "q codes")
+    N, Kw = _shape_of_codes(w_codes, "w codes")
+    if Kw != K:
+        raise ValueError("K mismatch between activation and weight codes")
+    _need(q_codes, "q codes", _U8, (M, K // 2))
+    dev = q_codes.get_device()
+    _need_hif4(q_codes, q_meta, M, K, "q", dev)
+    if (r_codes is None) != (r_meta is None):
+        raise ValueError("r codes and meta must both be given or both be None")
+    if r_codes is not None:
+        _need_hif4(r_codes, r_meta, M, K, "r", dev)
+    _need_hif4(w_codes, w_meta, N, K, "w", dev)
+    z = _z_out(out, out_dtype, M, N, q_codes.device, dev)
+    st = load().rfq_hif4_gemm(_ptr(q_codes), _ptr(q_meta), _ptr(r_codes), _ptr(r_meta),
+                              _ptr(w_codes), _ptr(w_meta), M, N, K, _ptr(z), _dtype_code(z),
+                              _stream(stream, dev))
+    _check("rfq_hif4_gemm", st)
+    return z
 
 
 def interleave_gate_up(gate, up):

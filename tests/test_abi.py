@@ -94,6 +94,46 @@ def test_quantize_act_validation():
     assert q(A, 0, 0, 64, A, A, None, None, None) == OK
 
 
+def test_hif4_validation():
+    lib = _lib()
+    q = lib.rfq_hif4_quantize
+    assert q(None, 1, 4, 128, A, A, A, A, None) == ENULL
+    assert q(A, 1, 4, 128, A, A, A, None, None) == ENULL      # half residual pair
+    assert q(A, 7, 4, 128, A, A, A, A, None) == EDTYPE
+    assert q(A, 1, 4, 96, A, A, A, A, None) == ESHAPE         # K not a multiple of 64
+    assert q(A, 1, 4, 32, A, A, A, A, None) == ESHAPE
+    assert q(A, 1, -1, 64, A, A, A, A, None) == ESHAPE
+    assert q(A, 1, 1 << 40, 1 << 20, A, A, A, A, None) == ESHAPE
+    assert q(MIS, 1, 4, 64, A, A, A, A, None) == EALIGN
+    assert q(A, 1, 4, 64, A, A + 2, A, A, None) == EALIGN     # meta word alignment
+    assert q(None, 1, 0, 64, None, None, None, None, None) == OK
+    d = lib.rfq_hif4_dequant
+    assert d(A, A, 4, 96, A, None) == ESHAPE
+    assert d(None, A, 4, 64, A, None) == ENULL
+    assert d(A, A, 4, 64, MIS, None) == EALIGN
+    assert d(None, None, 0, 64, None, None) == OK
+    g = lib.rfq_hif4_gemm
+    args = [A, A, A, A, A, A, 8, 8, 128, A, 0, None]
+
+    def call(**kw):
+        a = list(args)
+        for k, v in kw.items():
+            a[int(k[1:])] = v
+        return g(*a)
+
+    assert call(a0=None) == ENULL
+    assert call(a3=None) == ENULL                     # half residual pair
+    assert call(a10=2) == EDTYPE
+    assert call(a8=96) == ESHAPE
+    assert call(a7=-1) == ESHAPE
+    assert call(a6=1 << 40) == ESHAPE
+    assert call(a4=MIS) == EALIGN
+    assert call(a1=A + 2) == EALIGN
+    assert call(a9=MIS) == EALIGN
+    assert call(a6=0) == OK
+    assert call(a0=None, a1=None, a2=None, a3=None, a9=None, a6=0) == OK
+
+
 def test_quantize_weight_validation():
     q = _lib().rfq_quantize_weight
     assert q(None, 0, 4, 64, A, A, None) == ENULL
@@ -301,3 +341,5 @@ def test_valid_arguments_without_a_gpu_report_device_error():
     assert _lib().rfq_quantize_act(A, 1, 4, 64, A, A, A, A, None) == EDEVICE
     assert _lib().rfq_gemm(A, A, A, A, A, A, 8, 8, 64, A, 0, None) == EDEVICE
     assert _lib().rfq_gemm_stream(A, 1, 1, A, A, 8, 8, 512, A, 0, None) == EDEVICE
+    assert _lib().rfq_hif4_quantize(A, 1, 4, 64, A, A, A, A, None) == EDEVICE
+    assert _lib().rfq_hif4_gemm(A, A, A, A, A, A, 8, 8, 64, A, 0, None) == EDEVICE

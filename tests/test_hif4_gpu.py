@@ -1,0 +1,216 @@
+"""Parity of the HiF4 path (Sec. 3.2.3, Eq. 5-6, with RFQ's residual) with
+the CPU oracle, through the C ABI.
+
+Quantizer codes and metadata words: bit-exact (the encoder reading is the
+same on both sides; parity of that reading with the paper is unpinned, since
+the paper defines only the decode).  Dequantization: exact.  Product: within
+the tolerance of gpu_util (every product of two HiF4 values is exact in
+fp32, so only the fp32 sums round).  The small cases span several 128 x 256
+tiles with ragged edges; the full-size case uses the shapes of the Qwen-like
+workload with sampled rows and columns.
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2608_26581_amd as rfq
+from paper_2608_26581_amd import workloads as wl
+from gpu_util import assert_gemm_close, dev, dev_bf16, host
+from oracle_pins import padded_bytes, padded_floats, read_golden
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+def _meta_u32(t):
+    return host(t).view(np.uint32)
+
+
+def _x_dev(x32, bf16):
+    if bf16:
+        return dev_bf16(wl.f32_to_bf16_bits(x32))
+    return dev(np.ascontiguousarray(x32, np.float32))
+
+
+def _gpu_quant(x32, bf16, residual=True):
+    q = rfq.rfq_hif4_quantize(_x_dev(x32, bf16), residual=residual)
+    torch.cuda.synchronize()
+    qc, qm, rc, rm = q
+    return (host(qc), _meta_u32(qm), None if rc is None else host(rc),
+            None if rm is None else _meta_u32(rm)), q
+
+
+def _assert_same(g, r, what):
+    for n, a, b in zip(("q_codes", "q_meta", "r_codes", "r_meta"), g, r):
+        if b is None:
+            assert a is None, (what, n)
+            continue
+        if not np.array_equal(a, b):
+            i = tuple(np.argwhere(a != b)[0])
+            raise AssertionError("%s %s differ at %s: gpu %#x oracle %#x (%d differ)" %
+                                 (what, n, i, int(a[i]), int(b[i]), int((a != b).sum())))
+
+
+def _values_bf16_exact(x):
+    return wl.bf16_bits_to_f32(wl.f32_to_bf16_bits(x))
+
+
+def _hard_blocks(rng, rows, K, near_ties):
+    """Blocks built around the format's grid: each 4-element group has one
+    element at 1.75 2^e S (forcing its exponent) and the others at exact
+    rounding ties (2j+1)/8 S 2^e, optionally one fp32 step off; plus zeros,
+    negative zeros, tiny blocks (byte 0) and huge ones (saturating byte 255)."""
+    x = np.zeros((rows, K), np.float64)
+    for r in range(rows):
+        for b0 in range(0, K, 64):
+            kind = rng.integers(0, 8)
+            blk = np.zeros(64)
+            if kind == 0:
+                blk[:] = 0.0
+                blk[rng.integers(0, 64, 5)] = -0.0
+            elif kind == 1:
+                blk[:] = rng.standard_normal(64) * 1e-20
+            elif kind == 2:
+                blk[:] = rng.standard_normal(64) * 1e7
+            else:
+                byte = int(rng.integers(60, 230))
+                S = (4 + (byte & 3)) * 2.0 ** ((byte >> 2) - 50)
+                for j in range(16):
+                    e = int(rng.integers(0, 3))
+                    g = np.array([(2 * int(rng.integers(0, 7)) + 1) / 8.0 * S * 2.0 ** e
+                                  for _ in range(4)])
+                    g[int(rng.integers(0, 4))] = 1.75 * S * 2.0 ** e
+                    blk[4 * j:4 * j + 4] = g * np.where(rng.random(4) < 0.5, -1.0, 1.0)
+            x[r, b0:b0 + 64] = blk
+    x = x.astype(np.float32)
+    if near_ties:
+        sel = rng.random(x.shape) < 0.3
+        up = rng.random(x.shape) < 0.5
+        x = np.where(sel, np.where(up, np.nextafter(x, np.float32(np.inf)),
+                                   np.nextafter(x, np.float32(-np.inf))), x).astype(np.float32)
+    return x
+
+
+# ---------------------------------------------------------------- golden
+def test_golden_encode_block():
+    g = read_golden("h7_hif4_encode.txt")
+    x = padded_floats(g["x"], 64).reshape(1, 64).astype(np.float32)
+    for bf16 in (False, True):
+        (qc, qm, _, _), _ = _gpu_quant(x, bf16, residual=False)
+        assert int(qm[0, 0]) == int(g["meta"][0], 16)
+        assert np.array_equal(qc[0], padded_bytes(g["codes"], 32))
+
+
+def test_golden_decode_block():
+    g = read_golden("h6_hif4_decode.txt")
+    codes = dev(padded_bytes(g["codes"], 32).reshape(1, 32))
+    meta = dev(np.array([[int(g["meta"][0], 16)]], np.uint32).view(np.int32))
+    out = host(rfq.rfq_hif4_dequant(codes, meta))
+    want = padded_floats(g["values"], 64)
+    assert np.array_equal(out[0].astype(np.float64), want)
+    assert np.array_equal(np.signbit(out[0]), np.signbit(want))
+
+
+# ---------------------------------------------------------------- quantizer
+QUANT_SHAPES = [(1, 64), (3, 192), (37, 640), (130, 1088), (257, 2048)]
+
+
+@pytest.mark.parametrize("rows,K", QUANT_SHAPES)
+@pytest.mark.parametrize("bf16", [False, True])
+def test_quantize_random_matches_oracle(orc, rows, K, bf16):
+    _say("hif4 quantize random %dx%d bf16=%s" % (rows, K, bf16))
+    x = wl.generate(wl.WORKLOADS["tiny"].scaled(M=rows, K=K, weights=()), seed=rows + K)["x"]
+    if bf16:
+        x = _values_bf16_exact(x)
+    g, _ = _gpu_quant(x, bf16)
+    _assert_same(g, orc.hif4_quantize(x.astype(np.float64)), "random")
+    gw, _ = _gpu_quant(x, bf16, residual=False)
+    _assert_same(gw, orc.hif4_quantize(x.astype(np.float64), residual=False), "weights")
+
+
+@pytest.mark.parametrize("bf16,near", [(False, False), (False, True), (True, False)])
+def test_quantize_ties_and_edges_match_oracle(orc, bf16, near):
+    _say("hif4 quantize ties bf16=%s near=%s" % (bf16, near))
+    rng = np.random.default_rng(11 + near)
+    x = _hard_blocks(rng, 24, 512, near)
+    if bf16:
+        x = _values_bf16_exact(x)
+    g, _ = _gpu_quant(x, bf16)
+    _assert_same(g, orc.hif4_quantize(x.astype(np.float64)), "ties")
+
+
+def test_quantize_full_size_matches_oracle(orc):
+    _say("hif4 quantize qwen 4096x4096 bf16")
+    data = wl.generate("qwen")
+    g, _ = _gpu_quant(data["x"], True)
+    _assert_same(g, orc.hif4_quantize(data["x"].astype(np.float64)), "qwen")
+
+
+def test_dequant_matches_oracle(orc):
+    rng = np.random.default_rng(5)
+    x = _hard_blocks(rng, 9, 320, True)
+    _, (qc, qm, rc, rm) = _gpu_quant(x, False)
+    for c, m in ((qc, qm), (rc, rm)):
+        out = host(rfq.rfq_hif4_dequant(c, m)).astype(np.float64)
+        want = orc.hif4_dequant(host(c), host(m).view(np.uint32))
+        assert np.array_equal(out, want)
+        assert np.array_equal(np.signbit(out), np.signbit(want))
+
+
+# ---------------------------------------------------------------- product
+GEMM_SHAPES = [(1, 1, 64), (37, 300, 192), (128, 256, 64), (130, 257, 640),
+               (256, 512, 1024), (300, 700, 320)]
+
+
+@pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
+@pytest.mark.parametrize("residual", [True, False])
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
+def test_gemm_matches_oracle(orc, M, N, K, residual, out_dtype):
+    _say("hif4 gemm %dx%dx%d residual=%s %s" % (M, N, K, residual, out_dtype))
+    w = wl.WORKLOADS["tiny"].scaled(M=M, K=K, weights=(("w", K, N),))
+    data = wl.generate(w, seed=M * 7 + N + K)
+    _, q = _gpu_quant(data["x"], False, residual)
+    _, wq = _gpu_quant(data["w"], False, residual=False)
+    z = rfq.rfq_hif4_gemm(q[0], q[1], q[2], q[3], wq[0], wq[1], out_dtype=out_dtype)
+    zh = host(z.float())
+    oq = orc.hif4_quantize(data["x"].astype(np.float64), residual)
+    ow = orc.hif4_quantize(data["w"].astype(np.float64), residual=False)
+    zr, bound = orc.hif4_gemm(oq[0], oq[1], oq[2], oq[3], ow[0], ow[1])
+    assert_gemm_close(zh, zr, bound, out_dtype == torch.bfloat16, "hif4 gemm")
+
+
+def test_gemm_full_size_sampled(orc):
+    """Qwen-like shapes (M 4096, K 4096, N 12288), bf16 activations, in the
+    configuration the benchmark times; 48 sampled rows x 96 sampled columns."""
+    _say("hif4 gemm full size sampled")
+    data = wl.generate("qwen")
+    x, w = data["x"], data["w"]
+    _, q = _gpu_quant(x, True)
+    _, wq = _gpu_quant(w, False, residual=False)
+    z = host(rfq.rfq_hif4_gemm(*q, wq[0], wq[1]))
+    rng = np.random.default_rng(3)
+    rows = np.sort(np.concatenate([[0, 4095], rng.choice(4096, 46, replace=False)]))
+    cols = np.sort(np.concatenate([[0, 12287], rng.choice(12288, 94, replace=False)]))
+    oq = orc.hif4_quantize(x[rows].astype(np.float64))
+    ow = orc.hif4_quantize(w[cols].astype(np.float64), residual=False)
+    zr, bound = orc.hif4_gemm(oq[0], oq[1], oq[2], oq[3], ow[0], ow[1])
+    assert_gemm_close(z[np.ix_(rows, cols)], zr, bound, False, "hif4 full")
+
+
+def test_gemm_hif4_residual_reduces_error(orc):
+    """RFQ's point (Sec. 4.3): with the residual term the product is closer
+    to the unquantized one than with the primary code alone."""
+    data = wl.generate(wl.WORKLOADS["tiny"].scaled(M=128, K=1024, weights=(("w", 1024, 256),)),
+                       seed=9)
+    _, q = _gpu_quant(data["x"], False)
+    _, wq = _gpu_quant(data["w"], False, residual=False)
+    z1 = host(rfq.rfq_hif4_gemm(*q, wq[0], wq[1])).astype(np.float64)
+    z0 = host(rfq.rfq_hif4_gemm(q[0], q[1], None, None, wq[0], wq[1])).astype(np.float64)
+    wd = orc.hif4_dequant(host(wq[0]), _meta_u32(wq[1]))
+    exact = data["x"].astype(np.float64) @ wd.T
+    e1 = np.linalg.norm(z1 - exact) / np.linalg.norm(exact)
+    e0 = np.linalg.norm(z0 - exact) / np.linalg.norm(exact)
+    assert e1 < 0.25 * e0, (e1, e0)
