@@ -32,6 +32,7 @@ if REPO not in sys.path:
 
 PEAK_FP4_TFLOPS = 10100.0     # MI355X dense MXFP4 matrix cores
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 matrix cores
 N_SETS = 3
 Q_SETS = 9                    # 9 x 64 MiB quantizer inputs: over twice the 256 MB last-level cache
 PHI_MARGIN = 4                # scale-threshold phi: median primary scale byte + 4
@@ -359,6 +360,27 @@ def secondary(torch, rfq, wl, x, w, stream):
         "exec_tflops": round((2.0 + 2.0 * on) * M * N * K / ms / 1e9, 1)}
     del q, z, wt, phi
 
+    # HiF4 form (64-element blocks, E6M2 macro scale, micro-exponents): the
+    # quantizer (primary + residual of the bf16 activations) and the product,
+    # which decodes to bf16 and runs the bf16 matrix cores (no HiF4 format
+    # there), so its rate is set against the 2.5 PFLOP/s dense bf16 peak.
+    hq = rfq.rfq_hif4_quantize(x)
+    hw = rfq.rfq_hif4_quantize(w, residual=False)
+    ms = _per_launch_ms(torch, stream, lambda i: rfq.rfq_hif4_quantize(x, out=hq, stream=stream),
+                        20)
+    hbytes = M * K * x.element_size() + 2 * (M * K // 2 + M * K // 64 * 4)
+    out["hif4_quantize_act"] = {"ms": round(ms, 5), "gb_per_s": round(hbytes / ms / 1e6, 1)}
+    z = torch.empty((M, N), dtype=torch.bfloat16, device=x.device)
+    for res in (True, False):
+        ms = _per_launch_ms(torch, stream, lambda i: rfq.rfq_hif4_gemm(
+            hq[0], hq[1], hq[2] if res else None, hq[3] if res else None, hw[0], hw[1], out=z,
+            stream=stream), 10)
+        tf = (4.0 if res else 2.0) * M * N * K / ms / 1e9
+        out["hif4_gemm" if res else "hif4_gemm_plain"] = {
+            "ms": round(ms, 5), "exec_tflops": round(tf, 1),
+            "frac_of_bf16_peak": round(tf / (PEAK_BF16_TFLOPS), 4)}
+    del hq, hw, z
+
     # Decode-sized products on the same weight: few activation rows, codes in
     # (rfq_quantize_act + rfq_gemm, whose few-row kernel streams W) and the
     # streaming form (rfq_gemm_stream, activations quantized inside the
@@ -486,6 +508,11 @@ def accuracy(torch, rfq, x, w, nrows=64):
     thr = int(q[1].float().median().item()) + PHI_MARGIN
     phi = rfq.rfq_fallback_map(None, q[1], rfq.RFQ_PHI_SCALE_AT_LEAST, thr)
     out["rfq_phi_scale_threshold"] = rel(rfq.rfq_gemm_phi(*q, *wq, phi))
+    hq = rfq.rfq_hif4_quantize(x)
+    hw = rfq.rfq_hif4_quantize(w, residual=False)
+    out["plain_hif4"] = rel(rfq.rfq_hif4_gemm(hq[0], hq[1], None, None, hw[0], hw[1]))
+    out["rfq_hif4"] = rel(rfq.rfq_hif4_gemm(*hq, hw[0], hw[1]))
+    del hq, hw
     wdq = rfq.rfq_dequant(*wq).double()
     out["weight_only_floor"] = float(torch.linalg.norm(x64 @ wdq.t() - zt) / nt)
     out["rows"] = int(rows.numel())

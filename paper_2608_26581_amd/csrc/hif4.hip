@@ -46,13 +46,14 @@
 // Product.  gfx950 has no matrix-core format for HiF4, so the product
 // decodes codes to bf16 and runs v_mfma_f32_32x32x16_bf16, whose products are
 // exact; accumulation is fp32.  A workgroup computes a 128 x 256 tile of Z
-// with 8 waves in two roles: four producer waves load the codes and metadata
-// of one K block (64 values) of the tile's 128 activation rows (and 128
-// residual rows) and 256 weight rows, decode them and write bf16 rows into
-// one of two LDS buffers, while four consumer waves (2 x 2, each a 64 x 128
-// sub-tile) multiply the other buffer; one workgroup barrier per K block
-// hands the buffers over.  Each SIMD holds one wave of each role, so
-// decoding (VALU) and multiplication (matrix core) overlap.  16-byte chunks of
+// with waves in two roles: producer waves load the codes and metadata of one
+// K block (64 values) of the tile's 128 activation rows (and 128 residual
+// rows) and 256 weight rows, decode them and write bf16 rows into one of two
+// LDS buffers, while four consumer waves (2 x 2, each a 64 x 128 sub-tile)
+// multiply the other buffer; one workgroup barrier per K block hands the
+// buffers over.  Every SIMD runs one consumer and (with the residual) two
+// producers, so decoding (VALU) and multiplication (matrix core) overlap and
+// the decode has two instruction streams to issue from.  16-byte chunks of
 // an LDS row are XOR-swizzled by row so that fragment reads and row writes
 // are free of bank conflicts.  Rows past M or N are clamped to the last row
 // for loading; their results are not stored.
@@ -244,7 +245,6 @@ __global__ __launch_bounds__(256) void hif4_dequant_kernel(
 // ---------------------------------------------------------------- product
 
 constexpr int kBM = 128, kBN = 256;            // tile: activation rows x weight rows
-constexpr int kGThreads = 512;                 // 4 producer + 4 consumer waves
 constexpr int kRowBytes = kH * 2;              // one decoded bf16 row of a K block
 constexpr int kTM = 64, kTN = 128;             // consumer sub-tile
 constexpr int kFM = kTM / 32, kFN = kTN / 32;
@@ -255,10 +255,23 @@ struct HSmem {
   static constexpr int kRows = kWRow0 + kBN;
   static constexpr int kBufBytes = kRows * kRowBytes;
   static constexpr int kBytes = 2 * kBufBytes;
+  // Producer waves: two per SIMD with the residual (each lane decodes two
+  // half-block rows per step), six without.
+  static constexpr int kProducers = RES ? 8 : 6;
+  static constexpr int kThreads = (kProducers + 4) * 64;
 };
 
 __device__ __forceinline__ int hswz(int row, int chunk) {
-  return row * kRowBytes + 16 * (chunk ^ ((row >> 1) & 7));
+  return row * kRowBytes + 16 * (chunk ^ (row & 7));
+}
+
+// a & m, opaque to the optimizer, so that the byte conversions below stay
+// single v_cvt_f32_ubyte{0..3} instructions instead of a bit-field extract
+// per element followed by a conversion.
+__device__ __forceinline__ uint32_t and_opaque(uint32_t a, uint32_t m) {
+  uint32_t r;
+  asm("v_and_b32 %0, %1, %2" : "=v"(r) : "s"(m), "v"(a));
+  return r;
 }
 
 // bf16 pairs of the 8 elements of code word w (8-element group g of a block
@@ -266,7 +279,8 @@ __device__ __forceinline__ int hswz(int row, int chunk) {
 __device__ __forceinline__ u32x4 decode8_bf16(uint32_t w, uint32_t meta, int g) {
   float ua, ub;
   group_units(meta, g, ua, ub);
-  const uint32_t lo = w & 0x07070707u, hi = (w >> 4) & 0x07070707u, w4 = w << 4;
+  const uint32_t lo = and_opaque(w, 0x07070707u), hi = and_opaque(w >> 4, 0x07070707u);
+  const uint32_t w4 = w << 4;
   uint32_t p[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
@@ -284,7 +298,7 @@ __device__ __forceinline__ u32x4 decode8_bf16(uint32_t w, uint32_t meta, int g) 
 }
 
 template <bool RES, bool ZBF16>
-__global__ __launch_bounds__(kGThreads) void hif4_gemm_kernel(
+__global__ __launch_bounds__(HSmem<RES>::kThreads) void hif4_gemm_kernel(
     const uint8_t *__restrict__ qc, const uint32_t *__restrict__ qm,
     const uint8_t *__restrict__ rc, const uint32_t *__restrict__ rm,
     const uint8_t *__restrict__ wc, const uint32_t *__restrict__ wm, int64_t M, int64_t N,
@@ -299,16 +313,18 @@ __global__ __launch_bounds__(kGThreads) void hif4_gemm_kernel(
   const int nsteps = (int)(K / kH);
   const int64_t kbytes = K / 2, kblocks = K / kH;
 
-  if (wave < 4) {
+  if (wave < S::kProducers) {
     // ---- producer: (row, half) items; a half is 32 elements, 16 code bytes.
-    constexpr int kItems = S::kRows * 2 / 256;
-    const int pt = tid;                         // 0..255
+    constexpr int kPT = S::kProducers * 64;
+    constexpr int kItems = S::kRows * 2 / kPT;
+    static_assert(kItems * kPT == S::kRows * 2, "item split");
+    const int pt = tid;
     const uint8_t *src[kItems];
     const uint32_t *msrc[kItems];
     int lrow[kItems];
 #pragma unroll
     for (int i = 0; i < kItems; ++i) {
-      const int r = pt / 2 + 128 * i;
+      const int r = pt / 2 + (kPT / 2) * i;
       lrow[i] = r;
       int64_t grow;
       if (r >= S::kWRow0) {
@@ -323,14 +339,22 @@ __global__ __launch_bounds__(kGThreads) void hif4_gemm_kernel(
       }
     }
     const int h = pt & 1;
-    u32x4 cw[kItems];
-    uint32_t mw[kItems];
+    // Codes of step s + 1 are loaded while step s is decoded.
+    u32x4 cw[kItems], nw[kItems];
+    uint32_t mw[kItems], nm[kItems];
 #pragma unroll
     for (int i = 0; i < kItems; ++i) {
       cw[i] = *reinterpret_cast<const u32x4 *>(src[i]);
       mw[i] = msrc[i][0];
     }
     for (int s = 0; s < nsteps; ++s) {
+      if (s + 1 < nsteps) {
+#pragma unroll
+        for (int i = 0; i < kItems; ++i) {
+          nw[i] = *reinterpret_cast<const u32x4 *>(src[i] + (int64_t)(s + 1) * 32);
+          nm[i] = msrc[i][s + 1];
+        }
+      }
       uint8_t *buf = smem + (s & 1) * S::kBufBytes;
 #pragma unroll
       for (int i = 0; i < kItems; ++i) {
@@ -340,20 +364,18 @@ __global__ __launch_bounds__(kGThreads) void hif4_gemm_kernel(
           *reinterpret_cast<u32x4 *>(buf + hswz(lrow[i], 4 * h + q)) =
               decode8_bf16(d[q], mw[i], 4 * h + q);
       }
-      if (s + 1 < nsteps) {
-#pragma unroll
-        for (int i = 0; i < kItems; ++i) {
-          cw[i] = *reinterpret_cast<const u32x4 *>(src[i] + (int64_t)(s + 1) * 32);
-          mw[i] = msrc[i][s + 1];
-        }
-      }
       __syncthreads();
+#pragma unroll
+      for (int i = 0; i < kItems; ++i) {
+        cw[i] = nw[i];
+        mw[i] = nm[i];
+      }
     }
     return;
   }
 
   // ---- consumer: 2 x 2 waves, each 64 activation rows x 128 weight rows.
-  const int cw_ = wave - 4, wmi = cw_ >> 1, wni = cw_ & 1;
+  const int cw_ = wave - S::kProducers, wmi = cw_ >> 1, wni = cw_ & 1;
   const int frow = lane & 31, half = lane >> 5;
   v16f acc[kFM][kFN];
 #pragma unroll
@@ -443,7 +465,7 @@ hipError_t launch_hg(const uint8_t *qc, const uint32_t *qm, const uint8_t *rc,
       set_lds_limit(attr_done, reinterpret_cast<const void *>(kern), HSmem<RES>::kBytes);
   if (e != hipSuccess) return e;
   const int64_t tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
-  kern<<<dim3((unsigned)tiles), dim3(kGThreads), HSmem<RES>::kBytes, stream>>>(
+  kern<<<dim3((unsigned)tiles), dim3(HSmem<RES>::kThreads), HSmem<RES>::kBytes, stream>>>(
       qc, qm, rc, rm, wc, wm, M, N, K, z);
   return hipGetLastError();
 }
