@@ -281,12 +281,14 @@ rfq_status rfq_hif4_quantize(const void *x, rfq_dtype x_dtype, int64_t rows, int
                              uint8_t *r_codes, uint32_t *r_meta, void *hip_stream);
 
 /*
- * HiF4 dequantization (Eq. 6): out[r][k] = V of the code, exact in fp32.
- *   codes [rows][K/2], meta [rows][K/64] (4-byte aligned); out [rows][K]
- *   fp32, 16-byte aligned.
+ * HiF4 dequantization (Eq. 6): out[r][k] = V of the code, exact in fp32 and
+ * in bf16 (every HiF4 value has at most 6 significant bits and an exponent
+ * in [-52, 19]).  The bf16 form is the weight operand of rfq_hif4_gemm_wbf16.
+ *   codes [rows][K/2], meta [rows][K/64] (4-byte aligned); out [rows][K] of
+ *   out_dtype (RFQ_F32 or RFQ_BF16), 16-byte aligned.
  */
 rfq_status rfq_hif4_dequant(const uint8_t *codes, const uint32_t *meta, int64_t rows, int64_t K,
-                            float *out, void *hip_stream);
+                            void *out, rfq_dtype out_dtype, void *hip_stream);
 
 /*
  * HiF4 RFQ product (Eq. 11 with HiF4 codes, phi = 1; phi = 0 when r_codes and
@@ -304,6 +306,25 @@ rfq_status rfq_hif4_gemm(const uint8_t *q_codes, const uint32_t *q_meta,
                          const uint8_t *w_codes, const uint32_t *w_meta,
                          int64_t M, int64_t N, int64_t K,
                          void *z, rfq_dtype z_dtype, void *hip_stream);
+
+/*
+ * HiF4 RFQ product with the weights given as bf16 values: Z = sum_k V_q w +
+ * sum_k V_r w (phi = 0 without the residual pair).  Meant for weights that are
+ * decoded once (rfq_hif4_dequant with bf16 output): constant weights at
+ * inference, or weights re-quantized once per training step.  The product then
+ * decodes only the activation codes.  Any bf16 w is accepted; every product
+ * of a HiF4 value and a bf16 value is exact in fp32.  With w the bf16 decode
+ * of HiF4 weight codes the result is bit-identical to rfq_hif4_gemm on those
+ * codes.
+ *   q_codes, q_meta, r_codes, r_meta: as rfq_hif4_gemm.
+ *   w_bf16   [N][K] bf16, 16-byte aligned.
+ *   z        [M][N] row-major, z_dtype; 16-byte aligned.
+ * Shape limits and errors as rfq_hif4_gemm.
+ */
+rfq_status rfq_hif4_gemm_wbf16(const uint8_t *q_codes, const uint32_t *q_meta,
+                               const uint8_t *r_codes, const uint32_t *r_meta,
+                               const void *w_bf16, int64_t M, int64_t N, int64_t K,
+                               void *z, rfq_dtype z_dtype, void *hip_stream);
 
 /* Static, never-NULL description of a status code. */
 const char *rfq_status_str(rfq_status s);

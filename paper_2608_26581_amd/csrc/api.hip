@@ -299,7 +299,8 @@ rfq_status rfq_hif4_quantize(const void *x, rfq_dtype x_dtype, int64_t rows, int
 }
 
 rfq_status rfq_hif4_dequant(const uint8_t *codes, const uint32_t *meta, int64_t rows, int64_t K,
-                            float *out, void *hip_stream) {
+                            void *out, rfq_dtype out_dtype, void *hip_stream) {
+  if (!valid_dtype(out_dtype)) return RFQ_ERR_DTYPE;
   rfq_status s = check_k64(rows, K);
   if (s != RFQ_OK) return s;
   if (exceeds(rows, K, kMaxElements)) return RFQ_ERR_SHAPE;
@@ -307,7 +308,7 @@ rfq_status rfq_hif4_dequant(const uint8_t *codes, const uint32_t *meta, int64_t 
   if (!codes || !meta || !out) return RFQ_ERR_NULL;
   if (!aligned(codes, 4) || !aligned(meta, 4) || !aligned(out, 16)) return RFQ_ERR_ALIGN;
   if ((s = check_device()) != RFQ_OK) return s;
-  return launched(rfq::launch_hif4_dequant(codes, meta, rows * K, out,
+  return launched(rfq::launch_hif4_dequant(codes, meta, rows * K, out, out_dtype == RFQ_BF16,
                                            static_cast<hipStream_t>(hip_stream)));
 }
 
@@ -328,8 +329,29 @@ rfq_status rfq_hif4_gemm(const uint8_t *q_codes, const uint32_t *q_meta,
       !aligned(z, 16))
     return RFQ_ERR_ALIGN;
   if ((s = check_device()) != RFQ_OK) return s;
-  return launched(rfq::launch_hif4_gemm(q_codes, q_meta, r_codes, r_meta, w_codes, w_meta, M, N,
-                                        K, z, z_dtype == RFQ_BF16,
+  return launched(rfq::launch_hif4_gemm(q_codes, q_meta, r_codes, r_meta, w_codes, w_meta,
+                                        nullptr, M, N, K, z, z_dtype == RFQ_BF16,
+                                        static_cast<hipStream_t>(hip_stream)));
+}
+
+rfq_status rfq_hif4_gemm_wbf16(const uint8_t *q_codes, const uint32_t *q_meta,
+                               const uint8_t *r_codes, const uint32_t *r_meta,
+                               const void *w_bf16, int64_t M, int64_t N, int64_t K,
+                               void *z, rfq_dtype z_dtype, void *hip_stream) {
+  if (!valid_dtype(z_dtype)) return RFQ_ERR_DTYPE;
+  rfq_status s = check_k64(M, K);
+  if (s != RFQ_OK) return s;
+  if (N < 0 || !hif4_product_fits(M, N)) return RFQ_ERR_SHAPE;
+  if (M == 0 || N == 0) return RFQ_OK;
+  if (!q_codes || !q_meta || !w_bf16 || !z) return RFQ_ERR_NULL;
+  if ((r_codes == nullptr) != (r_meta == nullptr)) return RFQ_ERR_NULL;
+  if (!aligned(q_codes, 16) || !aligned(q_meta, 4) || !aligned(w_bf16, 16) ||
+      (r_codes && (!aligned(r_codes, 16) || !aligned(r_meta, 4))) || !aligned(z, 16))
+    return RFQ_ERR_ALIGN;
+  if ((s = check_device()) != RFQ_OK) return s;
+  return launched(rfq::launch_hif4_gemm(q_codes, q_meta, r_codes, r_meta, nullptr, nullptr,
+                                        static_cast<const uint16_t *>(w_bf16), M, N, K, z,
+                                        z_dtype == RFQ_BF16,
                                         static_cast<hipStream_t>(hip_stream)));
 }
 

@@ -221,10 +221,12 @@ __device__ __forceinline__ void group_units(uint32_t meta, int g, float &ua, flo
   ub = __uint_as_float(__float_as_uint(base) + (eb << 23));
 }
 
-// One dequantization thread: 8 elements (one code word) to fp32.
+// One dequantization thread: 8 elements (one code word) to fp32 or to bf16
+// (exact either way).
+template <bool BF16_OUT>
 __global__ __launch_bounds__(256) void hif4_dequant_kernel(
     const uint32_t *__restrict__ codes, const uint32_t *__restrict__ meta, int64_t nunits,
-    float4 *__restrict__ out) {
+    void *__restrict__ out) {
   const int64_t stride = (int64_t)gridDim.x * 256;
   for (int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x; u < nunits; u += stride) {
     const uint32_t w = codes[u];
@@ -237,8 +239,17 @@ __global__ __launch_bounds__(256) void hif4_dequant_kernel(
       const float mag = (float)(nib & 7u) * (i < 4 ? ua : ub);
       d[i] = (nib & 8u) ? -mag : mag;
     }
-    out[2 * u] = make_float4(d[0], d[1], d[2], d[3]);
-    out[2 * u + 1] = make_float4(d[4], d[5], d[6], d[7]);
+    if constexpr (BF16_OUT) {
+      reinterpret_cast<u32x4 *>(out)[u] =
+          u32x4{(__float_as_uint(d[0]) >> 16) | (__float_as_uint(d[1]) & 0xFFFF0000u),
+                (__float_as_uint(d[2]) >> 16) | (__float_as_uint(d[3]) & 0xFFFF0000u),
+                (__float_as_uint(d[4]) >> 16) | (__float_as_uint(d[5]) & 0xFFFF0000u),
+                (__float_as_uint(d[6]) >> 16) | (__float_as_uint(d[7]) & 0xFFFF0000u)};
+    } else {
+      float4 *o = reinterpret_cast<float4 *>(out);
+      o[2 * u] = make_float4(d[0], d[1], d[2], d[3]);
+      o[2 * u + 1] = make_float4(d[4], d[5], d[6], d[7]);
+    }
   }
 }
 
@@ -297,12 +308,15 @@ __device__ __forceinline__ u32x4 decode8_bf16(uint32_t w, uint32_t meta, int g) 
   return u32x4{p[0], p[1], p[2], p[3]};
 }
 
-template <bool RES, bool ZBF16>
+// WBF16: the weights come as bf16 values wv[N][K] (for example HiF4 weights
+// decoded once) and are copied into LDS as they are; only the activation
+// codes are decoded.
+template <bool RES, bool ZBF16, bool WBF16>
 __global__ __launch_bounds__(HSmem<RES>::kThreads) void hif4_gemm_kernel(
     const uint8_t *__restrict__ qc, const uint32_t *__restrict__ qm,
     const uint8_t *__restrict__ rc, const uint32_t *__restrict__ rm,
-    const uint8_t *__restrict__ wc, const uint32_t *__restrict__ wm, int64_t M, int64_t N,
-    int64_t K, void *__restrict__ z) {
+    const uint8_t *__restrict__ wc, const uint32_t *__restrict__ wm,
+    const uint16_t *__restrict__ wv, int64_t M, int64_t N, int64_t K, void *__restrict__ z) {
   using S = HSmem<RES>;
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
 
@@ -321,16 +335,26 @@ __global__ __launch_bounds__(HSmem<RES>::kThreads) void hif4_gemm_kernel(
     const int pt = tid;
     const uint8_t *src[kItems];
     const uint32_t *msrc[kItems];
+    const u32x4 *vsrc[kItems];
     int lrow[kItems];
+    bool is_w[kItems];
 #pragma unroll
     for (int i = 0; i < kItems; ++i) {
       const int r = pt / 2 + (kPT / 2) * i;
       lrow[i] = r;
+      is_w[i] = r >= S::kWRow0;
+      vsrc[i] = nullptr;
       int64_t grow;
       if (r >= S::kWRow0) {
         grow = min(n0 + (r - S::kWRow0), N - 1);
-        src[i] = wc + grow * kbytes + 16 * (pt & 1);
-        msrc[i] = wm + grow * kblocks;
+        if constexpr (WBF16) {
+          vsrc[i] = reinterpret_cast<const u32x4 *>(wv + grow * K + 32 * (pt & 1));
+          src[i] = nullptr;
+          msrc[i] = nullptr;
+        } else {
+          src[i] = wc + grow * kbytes + 16 * (pt & 1);
+          msrc[i] = wm + grow * kblocks;
+        }
       } else {
         const bool is_r = RES && r >= kBM;
         grow = min(m0 + (is_r ? r - kBM : r), M - 1);
@@ -339,35 +363,47 @@ __global__ __launch_bounds__(HSmem<RES>::kThreads) void hif4_gemm_kernel(
       }
     }
     const int h = pt & 1;
-    // Codes of step s + 1 are loaded while step s is decoded.
-    u32x4 cw[kItems], nw[kItems];
+    // Codes (or bf16 weight values: four 16-byte pieces per item) of step
+    // s + 1 are loaded while step s is decoded.  Whether an item is a weight
+    // row is uniform over a wave.
+    constexpr int kV = WBF16 ? 4 : 1;
+    u32x4 cw[kItems][kV], nw[kItems][kV];
     uint32_t mw[kItems], nm[kItems];
+    auto load = [&](int s, u32x4 (&c)[kItems][kV], uint32_t (&m)[kItems]) {
 #pragma unroll
-    for (int i = 0; i < kItems; ++i) {
-      cw[i] = *reinterpret_cast<const u32x4 *>(src[i]);
-      mw[i] = msrc[i][0];
-    }
-    for (int s = 0; s < nsteps; ++s) {
-      if (s + 1 < nsteps) {
+      for (int i = 0; i < kItems; ++i) {
+        if (WBF16 && is_w[i]) {
 #pragma unroll
-        for (int i = 0; i < kItems; ++i) {
-          nw[i] = *reinterpret_cast<const u32x4 *>(src[i] + (int64_t)(s + 1) * 32);
-          nm[i] = msrc[i][s + 1];
+          for (int v = 0; v < kV; ++v) c[i][v] = vsrc[i][(int64_t)s * 8 + v];
+        } else {
+          c[i][0] = *reinterpret_cast<const u32x4 *>(src[i] + (int64_t)s * 32);
+          m[i] = msrc[i][s];
         }
       }
+    };
+    load(0, cw, mw);
+    for (int s = 0; s < nsteps; ++s) {
+      if (s + 1 < nsteps) load(s + 1, nw, nm);
       uint8_t *buf = smem + (s & 1) * S::kBufBytes;
 #pragma unroll
       for (int i = 0; i < kItems; ++i) {
-        const uint32_t d[4] = {cw[i].x, cw[i].y, cw[i].z, cw[i].w};
+        if (WBF16 && is_w[i]) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-          *reinterpret_cast<u32x4 *>(buf + hswz(lrow[i], 4 * h + q)) =
-              decode8_bf16(d[q], mw[i], 4 * h + q);
+          for (int q = 0; q < 4; ++q)
+            *reinterpret_cast<u32x4 *>(buf + hswz(lrow[i], 4 * h + q)) = cw[i][q % kV];
+        } else {
+          const uint32_t d[4] = {cw[i][0].x, cw[i][0].y, cw[i][0].z, cw[i][0].w};
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            *reinterpret_cast<u32x4 *>(buf + hswz(lrow[i], 4 * h + q)) =
+                decode8_bf16(d[q], mw[i], 4 * h + q);
+        }
       }
       __syncthreads();
 #pragma unroll
       for (int i = 0; i < kItems; ++i) {
-        cw[i] = nw[i];
+#pragma unroll
+        for (int v = 0; v < kV; ++v) cw[i][v] = nw[i][v];
         mw[i] = nm[i];
       }
     }
@@ -455,18 +491,19 @@ __global__ __launch_bounds__(HSmem<RES>::kThreads) void hif4_gemm_kernel(
   }
 }
 
-template <bool RES, bool ZBF16>
+template <bool RES, bool ZBF16, bool WBF16>
 hipError_t launch_hg(const uint8_t *qc, const uint32_t *qm, const uint8_t *rc,
-                     const uint32_t *rm, const uint8_t *wc, const uint32_t *wm, int64_t M,
-                     int64_t N, int64_t K, void *z, hipStream_t stream) {
-  auto kern = hif4_gemm_kernel<RES, ZBF16>;
+                     const uint32_t *rm, const uint8_t *wc, const uint32_t *wm,
+                     const uint16_t *wv, int64_t M, int64_t N, int64_t K, void *z,
+                     hipStream_t stream) {
+  auto kern = hif4_gemm_kernel<RES, ZBF16, WBF16>;
   static std::atomic<bool> attr_done[kMaxDevices];
   const hipError_t e =
       set_lds_limit(attr_done, reinterpret_cast<const void *>(kern), HSmem<RES>::kBytes);
   if (e != hipSuccess) return e;
   const int64_t tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
   kern<<<dim3((unsigned)tiles), dim3(HSmem<RES>::kThreads), HSmem<RES>::kBytes, stream>>>(
-      qc, qm, rc, rm, wc, wm, M, N, K, z);
+      qc, qm, rc, rm, wc, wm, wv, M, N, K, z);
   return hipGetLastError();
 }
 
@@ -497,30 +534,33 @@ hipError_t launch_hif4_quantize(const void *x, bool bf16_in, int64_t nelem, uint
 }
 
 hipError_t launch_hif4_dequant(const uint8_t *codes, const uint32_t *meta, int64_t nelem,
-                               float *out, hipStream_t stream) {
+                               void *out, bool bf16_out, hipStream_t stream) {
   const int64_t nunits = nelem / 8;
   const int64_t wgs = (nunits + 255) / 256;
-  hif4_dequant_kernel<<<(unsigned)(wgs < kLoopGrid ? wgs : kLoopGrid), 256, 0, stream>>>(
-      reinterpret_cast<const uint32_t *>(codes), meta, nunits, reinterpret_cast<float4 *>(out));
+  const unsigned grid = (unsigned)(wgs < kLoopGrid ? wgs : kLoopGrid);
+  const uint32_t *c = reinterpret_cast<const uint32_t *>(codes);
+  if (bf16_out)
+    hif4_dequant_kernel<true><<<grid, 256, 0, stream>>>(c, meta, nunits, out);
+  else
+    hif4_dequant_kernel<false><<<grid, 256, 0, stream>>>(c, meta, nunits, out);
   return hipGetLastError();
 }
 
 hipError_t launch_hif4_gemm(const uint8_t *q_codes, const uint32_t *q_meta,
                             const uint8_t *r_codes, const uint32_t *r_meta,
-                            const uint8_t *w_codes, const uint32_t *w_meta, int64_t M, int64_t N,
-                            int64_t K, void *z, bool z_bf16, hipStream_t stream) {
-  if (r_codes) {
-    if (z_bf16)
-      return launch_hg<true, true>(q_codes, q_meta, r_codes, r_meta, w_codes, w_meta, M, N, K, z,
-                                   stream);
-    return launch_hg<true, false>(q_codes, q_meta, r_codes, r_meta, w_codes, w_meta, M, N, K, z,
-                                  stream);
-  }
-  if (z_bf16)
-    return launch_hg<false, true>(q_codes, q_meta, nullptr, nullptr, w_codes, w_meta, M, N, K, z,
-                                  stream);
-  return launch_hg<false, false>(q_codes, q_meta, nullptr, nullptr, w_codes, w_meta, M, N, K, z,
-                                 stream);
+                            const uint8_t *w_codes, const uint32_t *w_meta,
+                            const uint16_t *w_bf16, int64_t M, int64_t N, int64_t K, void *z,
+                            bool z_bf16, hipStream_t stream) {
+  const bool res = r_codes != nullptr, wb = w_bf16 != nullptr;
+#define RFQ_HG(R, Z, W) \
+  if (res == R && z_bf16 == Z && wb == W) \
+    return launch_hg<R, Z, W>(q_codes, q_meta, r_codes, r_meta, w_codes, w_meta, w_bf16, M, N, \
+                              K, z, stream);
+  RFQ_HG(true, true, false) RFQ_HG(true, false, false) RFQ_HG(false, true, false)
+  RFQ_HG(false, false, false) RFQ_HG(true, true, true) RFQ_HG(true, false, true)
+  RFQ_HG(false, true, true) RFQ_HG(false, false, true)
+#undef RFQ_HG
+  return hipErrorInvalidValue;
 }
 
 }  // namespace rfq

@@ -123,10 +123,12 @@ hipError_t launch_hif4_quantize(const void *x, bool bf16_in, int64_t nelem, uint
                                 uint32_t *q_meta, uint8_t *r_codes, uint32_t *r_meta,
                                 hipStream_t stream);
 hipError_t launch_hif4_dequant(const uint8_t *codes, const uint32_t *meta, int64_t nelem,
-                               float *out, hipStream_t stream);
+                               void *out, bool bf16_out, hipStream_t stream);
+// w_bf16 != nullptr: weights given as bf16 values [N][K] (w_codes, w_meta unused).
 hipError_t launch_hif4_gemm(const uint8_t *q_codes, const uint32_t *q_meta,
                             const uint8_t *r_codes, const uint32_t *r_meta,
-                            const uint8_t *w_codes, const uint32_t *w_meta, int64_t M, int64_t N,
-                            int64_t K, void *z, bool z_bf16, hipStream_t stream);
+                            const uint8_t *w_codes, const uint32_t *w_meta,
+                            const uint16_t *w_bf16, int64_t M, int64_t N, int64_t K, void *z,
+                            bool z_bf16, hipStream_t stream);
 
 }  // namespace rfq

@@ -30,6 +30,7 @@ EXPORTS = (
     "rfq_quantize_act", "rfq_quantize_weight", "rfq_gemm", "rfq_dequant",
     "rfq_swiglu_quantize_act", "rfq_gemm_phi", "rfq_fallback_map", "rfq_gemm_swiglu_quantize",
     "rfq_gemm_stream", "rfq_hif4_quantize", "rfq_hif4_dequant", "rfq_hif4_gemm",
+    "rfq_hif4_gemm_wbf16",
     "rfq_status_str", "rfq_abi_version",
 )
 
@@ -68,12 +69,13 @@ def load():
     lib.rfq_fallback_map.argtypes = [P, P, I64, I64, I32, I32, P, P]
     lib.rfq_gemm_stream.argtypes = [P, I32, I32, P, P, I64, I64, I64, P, I32, P]
     lib.rfq_hif4_quantize.argtypes = [P, I32, I64, I64, P, P, P, P, P]
-    lib.rfq_hif4_dequant.argtypes = [P, P, I64, I64, P, P]
+    lib.rfq_hif4_dequant.argtypes = [P, P, I64, I64, P, I32, P]
     lib.rfq_hif4_gemm.argtypes = [P, P, P, P, P, P, I64, I64, I64, P, I32, P]
+    lib.rfq_hif4_gemm_wbf16.argtypes = [P, P, P, P, P, I64, I64, I64, P, I32, P]
     for f in ("rfq_quantize_act", "rfq_quantize_weight", "rfq_gemm", "rfq_dequant",
               "rfq_swiglu_quantize_act", "rfq_gemm_swiglu_quantize", "rfq_gemm_phi",
               "rfq_fallback_map", "rfq_gemm_stream", "rfq_hif4_quantize", "rfq_hif4_dequant",
-              "rfq_hif4_gemm"):
+              "rfq_hif4_gemm", "rfq_hif4_gemm_wbf16"):
         getattr(lib, f).restype = I32
     lib.rfq_status_str.argtypes = [I32]
     lib.rfq_status_str.restype = ctypes.c_char_p
@@ -430,17 +432,21 @@ def rfq_hif4_quantize(x, residual=True, out=None, stream=None):
     return qc, qm, rc, rm
 
 
-def rfq_hif4_dequant(codes, meta, out=None, stream=None):
-    """HiF4 codes[rows][K/2], meta[rows][K/64] -> fp32 [rows][K]."""
+def rfq_hif4_dequant(codes, meta, out_dtype=torch.float32, out=None, stream=None):
+    """HiF4 codes[rows][K/2], meta[rows][K/64] -> [rows][K] fp32 or bf16
+    (exact either way)."""
     rows, K = _shape_of_codes(codes, "codes")
     _need_hif4(codes, meta, rows, K, "dequantization input")
     dev = codes.get_device()
     if out is None:
-        o = torch.empty((rows, K), dtype=torch.float32, device=codes.device)
+        if out_dtype not in _FLOAT:
+            raise TypeError("out_dtype must be torch.float32 or torch.bfloat16")
+        o = torch.empty((rows, K), dtype=out_dtype, device=codes.device)
     else:
         o = out
-        _need(o, "out", (torch.float32,), (rows, K), dev)
-    st = load().rfq_hif4_dequant(_ptr(codes), _ptr(meta), rows, K, _ptr(o), _stream(stream, dev))
+        _need(o, "out", _FLOAT, (rows, K), dev)
+    st = load().rfq_hif4_dequant(_ptr(codes), _ptr(meta), rows, K, _ptr(o), _dtype_code(o),
+                                 _stream(stream, dev))
     _check("rfq_hif4_dequant", st)
     return o
 
@@ -465,6 +471,30 @@ def rfq_hif4_gemm(q_codes, q_meta, r_codes, r_meta, w_codes, w_meta,
                               _ptr(w_codes), _ptr(w_meta), M, N, K, _ptr(z), _dtype_code(z),
                               _stream(stream, dev))
     _check("rfq_hif4_gemm", st)
+    return z
+
+
+def rfq_hif4_gemm_wbf16(q_codes, q_meta, r_codes, r_meta, w_bf16, out_dtype=torch.float32,
+                        out=None, stream=None):
+    """HiF4 RFQ product with bf16 weights w[N][K] (e.g. rfq_hif4_dequant of
+    HiF4 weight codes with out_dtype=torch.bfloat16, decoded once)."""
+    M, K = _shape_of_codes(q_codes, "q codes")
+    _need(q_codes, "q codes", _U8, (M, K // 2))
+    dev = q_codes.get_device()
+    _need_hif4(q_codes, q_meta, M, K, "q", dev)
+    if (r_codes is None) != (r_meta is None):
+        raise ValueError("r codes and meta must both be given or both be None")
+    if r_codes is not None:
+        _need_hif4(r_codes, r_meta, M, K, "r", dev)
+    if not isinstance(w_bf16, torch.Tensor) or w_bf16.dim() != 2 or w_bf16.shape[1] != K:
+        raise ValueError("w_bf16 must be a 2-D tensor [N][K] with the activations' K")
+    N = w_bf16.shape[0]
+    _need(w_bf16, "w_bf16", (torch.bfloat16,), (N, K), dev)
+    z = _z_out(out, out_dtype, M, N, q_codes.device, dev)
+    st = load().rfq_hif4_gemm_wbf16(_ptr(q_codes), _ptr(q_meta), _ptr(r_codes), _ptr(r_meta),
+                                    _ptr(w_bf16), M, N, K, _ptr(z), _dtype_code(z),
+                                    _stream(stream, dev))
+    _check("rfq_hif4_gemm_wbf16", st)
     return z
 
 

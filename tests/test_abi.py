@@ -108,10 +108,18 @@ def test_hif4_validation():
     assert q(A, 1, 4, 64, A, A + 2, A, A, None) == EALIGN     # meta word alignment
     assert q(None, 1, 0, 64, None, None, None, None, None) == OK
     d = lib.rfq_hif4_dequant
-    assert d(A, A, 4, 96, A, None) == ESHAPE
-    assert d(None, A, 4, 64, A, None) == ENULL
-    assert d(A, A, 4, 64, MIS, None) == EALIGN
-    assert d(None, None, 0, 64, None, None) == OK
+    assert d(A, A, 4, 96, A, 0, None) == ESHAPE
+    assert d(A, A, 4, 64, A, 5, None) == EDTYPE
+    assert d(None, A, 4, 64, A, 1, None) == ENULL
+    assert d(A, A, 4, 64, MIS, 0, None) == EALIGN
+    assert d(None, None, 0, 64, None, 1, None) == OK
+    gw = lib.rfq_hif4_gemm_wbf16
+    assert gw(A, A, A, A, None, 8, 8, 128, A, 0, None) == ENULL
+    assert gw(A, A, A, None, A, 8, 8, 128, A, 0, None) == ENULL
+    assert gw(A, A, A, A, A, 8, 8, 96, A, 0, None) == ESHAPE
+    assert gw(A, A, A, A, A, 8, 8, 128, A, 4, None) == EDTYPE
+    assert gw(A, A, A, A, MIS, 8, 8, 128, A, 0, None) == EALIGN
+    assert gw(A, A, A, A, A, 0, 8, 128, A, 0, None) == OK
     g = lib.rfq_hif4_gemm
     args = [A, A, A, A, A, A, 8, 8, 128, A, 0, None]
 

@@ -155,3 +155,39 @@ def test_binding_rejects_bad_tensors():
     z = binding.rfq_gemm(*q, *wq)
     torch.cuda.synchronize()
     assert z.shape == (M, N) and torch.isfinite(z).all()
+
+
+@pytest.mark.parametrize("M,N,K", [(131, 97, 192), (1, 1, 64), (257, 300, 640), (37, 515, 128)])
+def test_hif4_outputs_stay_in_bounds(M, N, K):
+    w = wl.WORKLOADS["qwen"].scaled(M=M, K=K, weights=(("w", K, N),))
+    data = wl.generate(w, seed=37)
+    x = torch.from_numpy(data["x"]).cuda()
+    xb = torch.from_numpy(data["x_bf16"].view(np.int16)).cuda().view(torch.bfloat16)
+
+    def hif4(rows):
+        return [Guarded((rows, K // 2), torch.uint8), Guarded((rows, K // 64), torch.int32)]
+
+    for xin, tag in ((x, "fp32"), (xb, "bf16")):
+        qb = hif4(M) + hif4(M)
+        rfq.rfq_hif4_quantize(xin, out=[b.t for b in qb])
+        _check_all(qb, "hif4_quantize %s" % tag)
+    q = [b.t for b in qb]
+    wb = hif4(N)
+    rfq.rfq_hif4_quantize(torch.from_numpy(data["w"]).cuda(), residual=False,
+                          out=[wb[0].t, wb[1].t, None, None])
+    _check_all(wb, "hif4_quantize weight")
+    for dt in (torch.float32, torch.bfloat16):
+        d = Guarded((M, K), dt)
+        rfq.rfq_hif4_dequant(q[0], q[1], out=d.t)
+        d.check("hif4_dequant %s" % dt)
+    wv = rfq.rfq_hif4_dequant(wb[0].t, wb[1].t, out_dtype=torch.bfloat16)
+    for res in (True, False):
+        for dt in (torch.float32, torch.bfloat16):
+            z = Guarded((M, N), dt)
+            rfq.rfq_hif4_gemm(q[0], q[1], q[2] if res else None, q[3] if res else None,
+                              wb[0].t, wb[1].t, out=z.t)
+            z.check("hif4_gemm res=%s %s" % (res, dt))
+            z = Guarded((M, N), dt)
+            rfq.rfq_hif4_gemm_wbf16(q[0], q[1], q[2] if res else None, q[3] if res else None,
+                                    wv, out=z.t)
+            z.check("hif4_gemm_wbf16 res=%s %s" % (res, dt))

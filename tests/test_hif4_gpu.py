@@ -214,3 +214,53 @@ def test_gemm_hif4_residual_reduces_error(orc):
     e1 = np.linalg.norm(z1 - exact) / np.linalg.norm(exact)
     e0 = np.linalg.norm(z0 - exact) / np.linalg.norm(exact)
     assert e1 < 0.25 * e0, (e1, e0)
+
+
+def test_dequant_bf16_is_exact(orc):
+    rng = np.random.default_rng(6)
+    x = _hard_blocks(rng, 7, 384, False)
+    _, (qc, qm, rc, rm) = _gpu_quant(x, False)
+    for c, m in ((qc, qm), (rc, rm)):
+        ob = rfq.rfq_hif4_dequant(c, m, out_dtype=torch.bfloat16)
+        got = host(ob.float()).astype(np.float64)
+        want = orc.hif4_dequant(host(c), host(m).view(np.uint32))
+        assert np.array_equal(got, want)
+        assert np.array_equal(np.signbit(got), np.signbit(want))
+
+
+@pytest.mark.parametrize("M,N,K", [(37, 300, 192), (130, 257, 640), (256, 512, 1024),
+                                   (1, 5, 64)])
+@pytest.mark.parametrize("residual", [True, False])
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
+def test_gemm_wbf16_bit_identical_to_codes(M, N, K, residual, out_dtype):
+    """Weights decoded once to bf16 give the same LDS tiles, hence the same
+    bits, as the product that decodes the weight codes itself."""
+    _say("hif4 gemm wbf16 %dx%dx%d residual=%s %s" % (M, N, K, residual, out_dtype))
+    w = wl.WORKLOADS["tiny"].scaled(M=M, K=K, weights=(("w", K, N),))
+    data = wl.generate(w, seed=M + 3 * N + K)
+    _, q = _gpu_quant(data["x"], False, residual)
+    _, wq = _gpu_quant(data["w"], False, residual=False)
+    wv = rfq.rfq_hif4_dequant(wq[0], wq[1], out_dtype=torch.bfloat16)
+    z1 = rfq.rfq_hif4_gemm(*q, wq[0], wq[1], out_dtype=out_dtype)
+    z2 = rfq.rfq_hif4_gemm_wbf16(*q, wv, out_dtype=out_dtype)
+    torch.cuda.synchronize()
+    assert torch.equal(z1.view(torch.int16) if out_dtype == torch.bfloat16 else z1.view(torch.int32),
+                       z2.view(torch.int16) if out_dtype == torch.bfloat16 else z2.view(torch.int32))
+
+
+def test_gemm_wbf16_any_bf16_weight(orc):
+    """Arbitrary bf16 weights (not HiF4 values): exact products, fp32 sums;
+    the reference multiplies the oracle's decoded activations with the bf16
+    weights in fp64."""
+    M, N, K = 150, 300, 448
+    data = wl.generate(wl.WORKLOADS["tiny"].scaled(M=M, K=K, weights=(("w", K, N),)), seed=8)
+    wb = wl.f32_to_bf16_bits(data["w"] * 10.0)
+    _, q = _gpu_quant(data["x"], False)
+    z = host(rfq.rfq_hif4_gemm_wbf16(*q, dev_bf16(wb))).astype(np.float64)
+    oq = orc.hif4_quantize(data["x"].astype(np.float64))
+    vq = orc.hif4_dequant(oq[0], oq[1])
+    vr = orc.hif4_dequant(oq[2], oq[3])
+    wf = wl.bf16_bits_to_f32(wb).astype(np.float64)
+    zr = vq @ wf.T + vr @ wf.T
+    bound = np.abs(vq) @ np.abs(wf).T + np.abs(vr) @ np.abs(wf).T
+    assert_gemm_close(z, zr, bound, False, "hif4 wbf16")
