@@ -379,7 +379,15 @@ def secondary(torch, rfq, wl, x, w, stream):
         out["hif4_gemm" if res else "hif4_gemm_plain"] = {
             "ms": round(ms, 5), "exec_tflops": round(tf, 1),
             "frac_of_bf16_peak": round(tf / (PEAK_BF16_TFLOPS), 4)}
-    del hq, hw, z
+    # The same product with the weights decoded to bf16 once (exact; constant
+    # weights, or weights re-quantized once per training step).
+    wv = rfq.rfq_hif4_dequant(hw[0], hw[1], out_dtype=torch.bfloat16)
+    ms = _per_launch_ms(torch, stream, lambda i: rfq.rfq_hif4_gemm_wbf16(
+        *hq, wv, out=z, stream=stream), 10)
+    tf = 4.0 * M * N * K / ms / 1e9
+    out["hif4_gemm_bf16_weights"] = {"ms": round(ms, 5), "exec_tflops": round(tf, 1),
+                                     "frac_of_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4)}
+    del hq, hw, z, wv
 
     # Decode-sized products on the same weight: few activation rows, codes in
     # (rfq_quantize_act + rfq_gemm, whose few-row kernel streams W) and the
