@@ -719,3 +719,46 @@ def test_path_replays_from_a_hip_graph(M, N, K):
     torch.cuda.synchronize()
     for a, b in zip(q + [z, zs], want):
         assert torch.equal(a, b), "replay with new inputs differs from the eager result"
+
+
+def test_hif4_path_replays_from_a_hip_graph():
+    """The HiF4 quantizer, product and bf16-weight product capture into a HIP
+    graph; every replay (eager work between) reproduces the eager results."""
+    M, N, K = 300, 700, 640
+    gen = torch.Generator(device="cuda").manual_seed(5)
+    x = torch.randn((M, K), generator=gen, device="cuda").to(torch.bfloat16)
+    hw = rfq.rfq_hif4_quantize(torch.randn((N, K), generator=gen, device="cuda") * 0.02,
+                               residual=False)
+    wv = rfq.rfq_hif4_dequant(hw[0], hw[1], out_dtype=torch.bfloat16)
+    q = [torch.empty((M, K // 2), dtype=torch.uint8, device="cuda"),
+         torch.empty((M, K // 64), dtype=torch.int32, device="cuda"),
+         torch.empty((M, K // 2), dtype=torch.uint8, device="cuda"),
+         torch.empty((M, K // 64), dtype=torch.int32, device="cuda")]
+    z = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    z2 = torch.empty((M, N), dtype=torch.float32, device="cuda")
+
+    def path():
+        rfq.rfq_hif4_quantize(x, out=q)
+        rfq.rfq_hif4_gemm(*q, hw[0], hw[1], out=z)
+        rfq.rfq_hif4_gemm_wbf16(*q, wv, out=z2)
+
+    path()
+    torch.cuda.synchronize()
+    want = [t.clone() for t in q + [z, z2]]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        path()
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        path()
+    _say("hif4 graph replay M=%d N=%d K=%d" % (M, N, K))
+    for i in range(4):
+        for t in q + [z, z2]:
+            t.zero_()
+        torch.randn((1024, 1024), generator=gen, device="cuda").sum()
+        graph.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(q + [z, z2], want):
+            assert torch.equal(a, b), "replay %d differs from the eager result" % i
