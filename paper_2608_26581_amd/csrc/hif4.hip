@@ -27,15 +27,18 @@
 //     E1_16[j] = max(e_j - E1_8[g], 0);
 //   - k is |x| / (S 2^e / 4) rounded to nearest, ties to even, at most 7; the
 //     sign is kept, also for a zero.
-// The rounding is k = rne(b / c) with b = |x| 2^(52 - E - e), an exact
-// scaling.  A quotient from the reciprocal of c, refined once with the exact
-// remainder fma(-y, c, b), is the correctly rounded b/c wherever the integer
-// rounding depends on it: an exact tie j + 1/2 is representable and comes
-// out exactly, and any other b/c lies at least ulp(b)/c > ulp(y)/2 away from
-// j + 1/2, more than the refined quotient's error.  The residual x - V is
-// exact in fp32 (V is the grid value nearest x, so the difference is a
-// multiple of the finer of ulp(x) and the grid's last bit and smaller than a
-// grid unit), so the second encode sees exactly the residual.
+// The rounding is k = rne(|x| / u) with the grid unit u = c 2^(E - 52 + e),
+// c = 4 + M.  A quotient from the reciprocal of u, refined once with the
+// exact remainder fma(-y, u, |x|), is the correctly rounded |x|/u wherever
+// the integer rounding depends on it: an exact tie j + 1/2 is representable
+// and comes out exactly, and any other |x|/u lies at least ulp(|x|)/(c 2^p)
+// > ulp(y)/2 away from j + 1/2 (2^p the power of two in u), more than the
+// refined quotient's error.  Where k could be nonzero, |x| >= u/2 >= 2^-51,
+// so the remainder stays far above the fp32 subnormal range.  The residual
+// x - V is exact in fp32 (V is the grid value nearest x, so the difference is
+// a multiple of the finer of ulp(x) and the grid's last bit and smaller than
+// a grid unit); it is formed as fma(-k, +-u, x), whose exact result rounds to
+// itself, with +0 for x = V, so the second encode sees exactly the residual.
 //
 // Quantizer work decomposition: a lane owns 8 consecutive elements (one
 // 8-element group, 16 bytes of bf16 or 32 of fp32 input); the 8 lanes of a
@@ -75,9 +78,11 @@ constexpr int kQThreads = 256;
 constexpr int kQSteps = 4;             // 8-element units per lane
 constexpr int kLoopGrid = 1 << 16;     // dequantization grid cap (loops over the rest)
 
+// Every lane of these permutations has a source, so the old value never
+// shows; passing v as it lets the compiler fold the move into the operation.
 template <int CTRL>
 __device__ __forceinline__ uint32_t dpp_u(uint32_t v) {
-  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, CTRL, 0xF, 0xF, true);
 }
 
 // Maximum and bitwise OR over aligned groups of 8 lanes (quad_perm 1,0,3,2,
@@ -116,10 +121,11 @@ __device__ __forceinline__ float pow2(int p) { return __uint_as_float((uint32_t)
 
 // Encodes the 8 elements of this lane (8-element group g of its block): the
 // lane's 32 code bits, the block's metadata word (same in all 8 lanes) and,
-// with WANT_V, the values V of the codes.
-template <bool WANT_V>
+// with WANT_R, the residuals x - V (exact: x - V is representable and the
+// fma rounds it once).
+template <bool WANT_R>
 __device__ __forceinline__ uint32_t encode8(const float (&x)[8], int g, uint32_t &meta,
-                                            float (&v)[8]) {
+                                            float (&res)[8]) {
   float ga = fabsf(x[0]), gb = fabsf(x[4]);
 #pragma unroll
   for (int i = 1; i < 4; ++i) {
@@ -136,16 +142,20 @@ __device__ __forceinline__ uint32_t encode8(const float (&x)[8], int g, uint32_t
   const int E = (int)(byte >> 2);
   const float c = (float)(4 + (byte & 3));
   const float rc = __builtin_amdgcn_rcpf(c);
+  // Per 4-element group: the grid unit c 2^(E-52+e) and its reciprocal
+  // (2^(52-E-e) / c, both powers of two exact scalings).
+  const float unit_a = c * pow2(E - 52 + e8 + ea), unit_b = c * pow2(E - 52 + e8 + eb);
+  const float ru_a = rc * pow2(52 - E - e8 - ea), ru_b = rc * pow2(52 - E - e8 - eb);
   uint32_t code = 0;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    const int e = e8 + (i < 4 ? ea : eb);
-    const float b = fabsf(x[i]) * pow2(52 - E - e);
-    const float y = b * rc;
-    const float yq = fmaf(fmaf(-y, c, b), rc, y);
+    const float unit = i < 4 ? unit_a : unit_b, ru = i < 4 ? ru_a : ru_b;
+    const float a = fabsf(x[i]);
+    const float y = a * ru;
+    const float yq = fmaf(fmaf(-y, unit, a), ru, y);
     const float kf = fminf(__builtin_rintf(yq), 7.0f);
     code |= (((__float_as_uint(x[i]) >> 28) & 8u) | (uint32_t)kf) << (4 * i);
-    if constexpr (WANT_V) v[i] = copysignf(kf * (c * pow2(E - 52 + e)), x[i]);
+    if constexpr (WANT_R) res[i] = fmaf(-kf, copysignf(unit, x[i]), x[i]);
   }
   return code;
 }
@@ -188,18 +198,16 @@ __global__ __launch_bounds__(kQThreads) void hif4_quantize_kernel(
 #pragma unroll
   for (int s = 0; s < kQSteps; ++s) {
     const int64_t u = u0 + 64 * s + lane;
-    float v[8], d[8];
+    float v[8], r[8];
     unpack8<BF16_IN>(in[s], v);
     uint32_t meta;
-    const uint32_t code = encode8<RES>(v, g, meta, d);
+    const uint32_t code = encode8<RES>(v, g, meta, r);
     if (u < nunits) {
       reinterpret_cast<uint32_t *>(qc)[u] = code;
       if (g == 0) qm[u >> 3] = meta;
     }
     if constexpr (RES) {
-      float r[8], unused[8];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) r[i] = v[i] - d[i];
+      float unused[8];
       uint32_t rmeta;
       const uint32_t rcode = encode8<false>(r, g, rmeta, unused);
       if (u < nunits) {
