@@ -326,6 +326,8 @@ def test_binding_rejects_host_tensors():
     x = torch.zeros(4, 64)
     c = torch.zeros(4, 32, dtype=torch.uint8)
     s = torch.zeros(4, 2, dtype=torch.uint8)
+    m = torch.zeros(4, 1, dtype=torch.int32)
+    xb = torch.zeros(4, 64, dtype=torch.bfloat16)
     calls = [
         lambda: binding.rfq_quantize_act(x),
         lambda: binding.rfq_quantize_weight(x),
@@ -336,6 +338,10 @@ def test_binding_rejects_host_tensors():
         lambda: binding.rfq_fallback_map(c, s, binding.RFQ_PHI_RESIDUAL_NONZERO),
         lambda: binding.rfq_swiglu_quantize_act(x, x),
         lambda: binding.rfq_gemm_swiglu_quantize(c, s, None, None, c, s),
+        lambda: binding.rfq_hif4_quantize(x),
+        lambda: binding.rfq_hif4_dequant(c, m),
+        lambda: binding.rfq_hif4_gemm(c, m, None, None, c, m),
+        lambda: binding.rfq_hif4_gemm_wbf16(c, m, None, None, xb),
     ]
     for call in calls:
         with pytest.raises(ValueError, match="device tensor"):
