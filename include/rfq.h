@@ -1,12 +1,14 @@
 /*
  * rfq.h -- C ABI of librfq: Residual Fallback Quantization (RFQ) with MXFP4
- * codes on AMD Instinct MI355X (gfx950).
+ * and HiF4 codes on AMD Instinct MI355X (gfx950).
  *
  * The library computes the data-parallel forward path of RFQ (Sec. 4.3 of the
  * paper): an MX activation quantizer that emits a primary MXFP4 code and an
  * MXFP4 code of the residual the primary code lost (Eq. 8-10), and a
  * block-scaled FP4 product that contracts both codes against MXFP4 weights
- * (Eq. 11, Algorithm 1).
+ * (Eq. 11, Algorithm 1).  The rfq_hif4_* calls at the end do the same with
+ * the HiF4 format of Sec. 3.2.3 (64-element blocks); the number format below
+ * is MXFP4's, HiF4's is described with those calls.
  *
  * Number format (Sec. 3.2, Eq. 3-4, element format of Sec. 3.2.2):
  *   - a block is 32 consecutive elements of one row along K (the reduction
