@@ -499,6 +499,175 @@ __global__ __launch_bounds__(HSmem<RES>::kThreads) void hif4_gemm_kernel(
   }
 }
 
+// ---------------------------------------------------------------- few rows
+//
+// Product for at most 16 activation rows (decode): one workgroup per 32
+// weight rows; its 4 waves take interleaved K blocks (wave w: blocks w, w+4,
+// ...), decode the block's weight rows and activation rows into a
+// wave-private LDS area (no workgroup barrier in the loop: LDS serves one
+// wave's accesses in order) and run v_mfma_f32_16x16x32_bf16 with the weights
+// as the first operand; the four partial sums are added in wave order at the
+// end.  Lane l of a 16x16x32 operand holds row l mod 16 and 8 consecutive K
+// values (chunk l / 16 of the 32-value half); the result in lane l is Z[m = l
+// mod 16][n = 4 (l / 16) .. +3] of the fragment.  Only activation rows below
+// M are decoded; the other rows of the area are never written and only feed
+// result columns m >= M, which are not stored.
+constexpr int kFewRows = 16;
+constexpr int kFewN = 32;
+constexpr int kFewWaves = 4;
+
+struct alignas(16) FewArea {
+  uint8_t w[kFewN * kRowBytes];             // 32 weight rows of one K block
+  uint8_t x[2 * kFewRows * kRowBytes];      // primary rows 0..15, residual 16..31
+};
+
+template <bool RES, bool ZBF16, bool WBF16>
+__global__ __launch_bounds__(kFewWaves * 64) void hif4_gemm_few_kernel(
+    const uint8_t *__restrict__ qc, const uint32_t *__restrict__ qm,
+    const uint8_t *__restrict__ rc, const uint32_t *__restrict__ rm,
+    const uint8_t *__restrict__ wc, const uint32_t *__restrict__ wm,
+    const uint16_t *__restrict__ wv, int64_t M, int64_t N, int64_t K, void *__restrict__ z) {
+  __shared__ FewArea area[kFewWaves];
+  __shared__ v4f part[kFewWaves][2][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t n0 = (int64_t)blockIdx.x * kFewN;
+  const int64_t kbytes = K / 2, kblocks = K / kH;
+
+  // Work items are code words (8 elements, one LDS chunk): 256 per K block
+  // for the 32 weight rows (lane l takes words l + 64 i, i < 4: row
+  // (l + 64 i) / 8, word l mod 8), and 8 per activation row for the
+  // 2M activation rows (words l + 64 i below 16 M), so a lane decodes four
+  // weight words and at most four activation words, and with few rows most
+  // lanes decode no activation word at all.
+  constexpr int kWI = 4;
+  const int dw = lane & 7;
+  const uint8_t *wsrc[kWI];
+  const uint32_t *wmsrc[kWI];
+  const u32x4 *wvsrc[kWI];
+  int wlrow[kWI];
+#pragma unroll
+  for (int i = 0; i < kWI; ++i) {
+    const int r = (lane >> 3) + 8 * i;
+    wlrow[i] = r;
+    const int64_t g = min(n0 + r, N - 1);
+    wsrc[i] = WBF16 ? nullptr : wc + g * kbytes + 4 * dw;
+    wmsrc[i] = WBF16 ? nullptr : wm + g * kblocks;
+    wvsrc[i] = WBF16 ? reinterpret_cast<const u32x4 *>(wv + g * K + 8 * dw) : nullptr;
+  }
+  const int nx = (RES ? 2 : 1) * (int)M * 8;              // activation words per block
+  const uint8_t *xsrc[kWI];
+  const uint32_t *xmsrc[kWI];
+  int xlrow[kWI];
+#pragma unroll
+  for (int i = 0; i < kWI; ++i) {
+    const int t = lane + 64 * i;
+    const int j = t >> 3;                                   // activation row index
+    const bool on = t < nx;
+    const bool is_r = RES && j >= M;
+    const int64_t g = on ? (is_r ? j - M : j) : 0;
+    xlrow[i] = is_r ? kFewRows + (j - (int)M) : j;
+    xsrc[i] = (is_r ? rc : qc) + g * kbytes + 4 * dw;
+    xmsrc[i] = (is_r ? rm : qm) + g * kblocks;
+  }
+
+  FewArea &A = area[wave];
+  const int frow = lane & 15, fch = lane >> 4;
+  v4f acc[2] = {v4f{0.f, 0.f, 0.f, 0.f}, v4f{0.f, 0.f, 0.f, 0.f}};
+  // The words of a wave's next K block are loaded while the current one is
+  // decoded and multiplied.
+  struct Words {
+    u32x4 v[WBF16 ? kWI : 1];
+    uint32_t c[kWI], m[kWI], xc[kWI], xm[kWI];
+  };
+  Words cur, nxt;
+  auto load = [&](int64_t b, Words &o) {
+#pragma unroll
+    for (int i = 0; i < kWI; ++i) {
+      if constexpr (WBF16) {
+        o.v[i] = wvsrc[i][b * 8];
+      } else {
+        o.c[i] = *reinterpret_cast<const uint32_t *>(wsrc[i] + b * 32);
+        o.m[i] = wmsrc[i][b];
+      }
+      if (lane + 64 * i < nx) {
+        o.xc[i] = *reinterpret_cast<const uint32_t *>(xsrc[i] + b * 32);
+        o.xm[i] = xmsrc[i][b];
+      }
+    }
+  };
+  if (wave < kblocks) load(wave, cur);
+  for (int64_t b = wave; b < kblocks; b += kFewWaves) {
+    if (b + kFewWaves < kblocks) load(b + kFewWaves, nxt);
+#pragma unroll
+    for (int i = 0; i < kWI; ++i) {
+      u32x4 v;
+      if constexpr (WBF16) v = cur.v[i];
+      else v = decode8_bf16(cur.c[i], cur.m[i], dw);
+      *reinterpret_cast<u32x4 *>(A.w + hswz(wlrow[i], dw)) = v;
+    }
+#pragma unroll
+    for (int i = 0; i < kWI; ++i)
+      if (lane + 64 * i < nx)
+        *reinterpret_cast<u32x4 *>(A.x + hswz(xlrow[i], dw)) = decode8_bf16(cur.xc[i], cur.xm[i], dw);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int sub = 0; sub < 2; ++sub) {
+      const int ch = 4 * sub + fch;
+      const v8bf xq = *reinterpret_cast<const v8bf *>(A.x + hswz(frow, ch));
+      v8bf xr = xq;
+      if constexpr (RES) xr = *reinterpret_cast<const v8bf *>(A.x + hswz(kFewRows + frow, ch));
+#pragma unroll
+      for (int f = 0; f < 2; ++f) {
+        const v8bf wf = *reinterpret_cast<const v8bf *>(A.w + hswz(16 * f + frow, ch));
+        acc[f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, xq, acc[f], 0, 0, 0);
+        if constexpr (RES) acc[f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, xr, acc[f], 0, 0, 0);
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    cur = nxt;
+  }
+  part[wave][0][lane] = acc[0];
+  part[wave][1][lane] = acc[1];
+  __syncthreads();
+  if (wave != 0) return;
+  const int64_t m = frow;
+  if (m >= M) return;
+  const bool vec_ok = (N & 3) == 0;
+#pragma unroll
+  for (int f = 0; f < 2; ++f) {
+    v4f t = part[0][f][lane];
+#pragma unroll
+    for (int w = 1; w < kFewWaves; ++w) t += part[w][f][lane];
+    const int64_t n = n0 + 16 * f + 4 * fch;
+    if constexpr (ZBF16) {
+      uint16_t *zp = reinterpret_cast<uint16_t *>(z) + m * N + n;
+      if (vec_ok && n + 3 < N) {
+        uint2 o;
+        o.x = bf16_rne(t[0]) | (bf16_rne(t[1]) << 16);
+        o.y = bf16_rne(t[2]) | (bf16_rne(t[3]) << 16);
+        *reinterpret_cast<uint2 *>(zp) = o;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (n + e < N) zp[e] = (uint16_t)bf16_rne(t[e]);
+      }
+    } else {
+      float *zp = reinterpret_cast<float *>(z) + m * N + n;
+      if (vec_ok && n + 3 < N) {
+        *reinterpret_cast<float4 *>(zp) = make_float4(t[0], t[1], t[2], t[3]);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (n + e < N) zp[e] = t[e];
+      }
+    }
+  }
+}
+
 template <bool RES, bool ZBF16, bool WBF16>
 hipError_t launch_hg(const uint8_t *qc, const uint32_t *qm, const uint8_t *rc,
                      const uint32_t *rm, const uint8_t *wc, const uint32_t *wm,
@@ -509,6 +678,12 @@ hipError_t launch_hg(const uint8_t *qc, const uint32_t *qm, const uint8_t *rc,
   const hipError_t e =
       set_lds_limit(attr_done, reinterpret_cast<const void *>(kern), HSmem<RES>::kBytes);
   if (e != hipSuccess) return e;
+  if (M <= kFewRows && (N + kFewN - 1) / kFewN <= int64_t(UINT32_MAX / (kFewWaves * 64))) {
+    hif4_gemm_few_kernel<RES, ZBF16, WBF16>
+        <<<dim3((unsigned)((N + kFewN - 1) / kFewN)), dim3(kFewWaves * 64), 0, stream>>>(
+            qc, qm, rc, rm, wc, wm, wv, M, N, K, z);
+    return hipGetLastError();
+  }
   const int64_t tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
   kern<<<dim3((unsigned)tiles), dim3(HSmem<RES>::kThreads), HSmem<RES>::kBytes, stream>>>(
       qc, qm, rc, rm, wc, wm, wv, M, N, K, z);

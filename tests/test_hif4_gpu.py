@@ -264,3 +264,45 @@ def test_gemm_wbf16_any_bf16_weight(orc):
     zr = vq @ wf.T + vr @ wf.T
     bound = np.abs(vq) @ np.abs(wf).T + np.abs(vr) @ np.abs(wf).T
     assert_gemm_close(z, zr, bound, False, "hif4 wbf16")
+
+
+FEW_SHAPES = [(1, 1, 64), (2, 33, 192), (5, 300, 640), (16, 700, 1024), (3, 64, 128)]
+
+
+@pytest.mark.parametrize("M,N,K", FEW_SHAPES)
+@pytest.mark.parametrize("residual", [True, False])
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
+def test_gemm_few_rows_matches_oracle(orc, M, N, K, residual, out_dtype):
+    """At most 16 activation rows run the few-row kernel (K split over four
+    waves, partial sums added in wave order); fewer K blocks than waves
+    included.  The bf16-weight form is bit-identical to it."""
+    _say("hif4 few rows %dx%dx%d residual=%s %s" % (M, N, K, residual, out_dtype))
+    w = wl.WORKLOADS["tiny"].scaled(M=M, K=K, weights=(("w", K, N),))
+    data = wl.generate(w, seed=M * 13 + N + K)
+    _, q = _gpu_quant(data["x"], False, residual)
+    _, wq = _gpu_quant(data["w"], False, residual=False)
+    z = rfq.rfq_hif4_gemm(*q, wq[0], wq[1], out_dtype=out_dtype)
+    wv = rfq.rfq_hif4_dequant(wq[0], wq[1], out_dtype=torch.bfloat16)
+    z2 = rfq.rfq_hif4_gemm_wbf16(*q, wv, out_dtype=out_dtype)
+    torch.cuda.synchronize()
+    assert torch.equal(z.view(torch.int16) if out_dtype == torch.bfloat16 else z.view(torch.int32),
+                       z2.view(torch.int16) if out_dtype == torch.bfloat16 else z2.view(torch.int32))
+    oq = orc.hif4_quantize(data["x"].astype(np.float64), residual)
+    ow = orc.hif4_quantize(data["w"].astype(np.float64), residual=False)
+    zr, bound = orc.hif4_gemm(oq[0], oq[1], oq[2], oq[3], ow[0], ow[1])
+    assert_gemm_close(host(z.float()), zr, bound, out_dtype == torch.bfloat16, "hif4 few")
+
+
+def test_gemm_few_rows_decode_shape(orc):
+    """Decode shape of the Qwen-like layer: 1 and 16 rows x 12288 x 4096."""
+    data = wl.generate("qwen")
+    _, wq = _gpu_quant(data["w"], False, residual=False)
+    ow = orc.hif4_quantize(data["w"].astype(np.float64), residual=False)
+    for M in (1, 16):
+        _say("hif4 few rows decode M=%d" % M)
+        x = data["x"][:M]
+        _, q = _gpu_quant(x, True)
+        z = host(rfq.rfq_hif4_gemm(*q, wq[0], wq[1]))
+        oq = orc.hif4_quantize(x.astype(np.float64))
+        zr, bound = orc.hif4_gemm(oq[0], oq[1], oq[2], oq[3], ow[0], ow[1])
+        assert_gemm_close(z, zr, bound, False, "hif4 decode M=%d" % M)
