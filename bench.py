@@ -421,6 +421,24 @@ def secondary(torch, rfq, wl, x, w, stream):
             "hip_graph_stream_ms": round(gs_ms, 5)}
     del wq, wcs
 
+    # HiF4 at the same decode shapes (few-row HiF4 kernel; codes in).
+    hw = rfq.rfq_hif4_quantize(w, residual=False)
+    hws = [(torch.roll(hw[0], 97 * s, 0), torch.roll(hw[1], 97 * s, 0)) for s in range(10)]
+    for md in (1, 16):
+        xd = x[:md].contiguous()
+        hq = rfq.rfq_hif4_quantize(xd)
+        zd = torch.empty((md, N), dtype=torch.bfloat16, device=x.device)
+
+        def hif4_path(i):
+            rfq.rfq_hif4_quantize(xd, out=hq, stream=stream)
+            rfq.rfq_hif4_gemm(*hq, *hws[i % 10], out=zd, stream=stream)
+
+        ms = _per_launch_ms(torch, stream, hif4_path, 50)
+        out["hif4_decode_%dx%dx%d" % (md, K, N)] = {
+            "quantize_then_gemm_ms": round(ms, 5),
+            "w_gbs": round((N * K // 2 + N * K // 64 * 4) / ms / 1e6, 1)}
+    del hw, hws
+
     # Wan2.2-DiT-like product: X 32768x5120, W 5120x13824.
     d = wl.generate(wl.WORKLOADS["wan"], seed=0)
     xw = torch.from_numpy(d["x_bf16"].view(np.int16)).to(x.device).view(torch.bfloat16)

@@ -75,7 +75,10 @@ typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 
 constexpr int kH = 64;                 // elements per HiF4 block
 constexpr int kQThreads = 256;
-constexpr int kQSteps = 4;             // 8-element units per lane
+constexpr int kQSteps = 4;             // 8-element units per lane (large tensors)
+// Below this many 8-element units a lane takes one unit, so that small
+// (decode-sized) tensors spread over four times as many waves.
+constexpr int64_t kQSmallUnits = int64_t(1) << 18;
 constexpr int kLoopGrid = 1 << 16;     // dequantization grid cap (loops over the rest)
 
 // Every lane of these permutations has a source, so the old value never
@@ -178,25 +181,25 @@ __device__ __forceinline__ void unpack8(const u32x4 (&w)[BF16_IN ? 1 : 2], float
 
 // nunits = elements / 8.  Lanes past the end load the last unit (never out
 // of bounds) and store nothing; a block is wholly inside or past the end.
-template <bool BF16_IN, bool RES>
+template <bool BF16_IN, bool RES, int STEPS>
 __global__ __launch_bounds__(kQThreads) void hif4_quantize_kernel(
     const void *__restrict__ x, int64_t nunits, uint8_t *__restrict__ qc,
     uint32_t *__restrict__ qm, uint8_t *__restrict__ rc, uint32_t *__restrict__ rm) {
   constexpr int kLoads = BF16_IN ? 1 : 2;
   const int lane = threadIdx.x & 63, g = lane & 7;
   const int64_t u0 =
-      ((int64_t)blockIdx.x * (kQThreads / 64) + (threadIdx.x >> 6)) * (64 * kQSteps);
+      ((int64_t)blockIdx.x * (kQThreads / 64) + (threadIdx.x >> 6)) * (64 * STEPS);
   const u32x4 *xin = reinterpret_cast<const u32x4 *>(x);
-  u32x4 in[kQSteps][kLoads];
+  u32x4 in[STEPS][kLoads];
 #pragma unroll
-  for (int s = 0; s < kQSteps; ++s) {
+  for (int s = 0; s < STEPS; ++s) {
     int64_t u = u0 + 64 * s + lane;
     u = u < nunits ? u : nunits - 1;
 #pragma unroll
     for (int l = 0; l < kLoads; ++l) in[s][l] = __builtin_nontemporal_load(xin + kLoads * u + l);
   }
 #pragma unroll
-  for (int s = 0; s < kQSteps; ++s) {
+  for (int s = 0; s < STEPS; ++s) {
     const int64_t u = u0 + 64 * s + lane;
     float v[8], r[8];
     unpack8<BF16_IN>(in[s], v);
@@ -690,30 +693,38 @@ hipError_t launch_hg(const uint8_t *qc, const uint32_t *qm, const uint8_t *rc,
   return hipGetLastError();
 }
 
+
+template <int STEPS>
+hipError_t launch_hq(const void *x, bool bf16_in, int64_t nunits, uint8_t *qc, uint32_t *qm,
+                     uint8_t *rc, uint32_t *rm, hipStream_t stream) {
+  const int64_t per_wg = (kQThreads / 64) * 64 * STEPS;
+  const dim3 grid((unsigned)((nunits + per_wg - 1) / per_wg)), block(kQThreads);
+  if (bf16_in) {
+    if (rc)
+      hif4_quantize_kernel<true, true, STEPS><<<grid, block, 0, stream>>>(x, nunits, qc, qm, rc, rm);
+    else
+      hif4_quantize_kernel<true, false, STEPS><<<grid, block, 0, stream>>>(x, nunits, qc, qm,
+                                                                          nullptr, nullptr);
+  } else {
+    if (rc)
+      hif4_quantize_kernel<false, true, STEPS><<<grid, block, 0, stream>>>(x, nunits, qc, qm, rc,
+                                                                          rm);
+    else
+      hif4_quantize_kernel<false, false, STEPS><<<grid, block, 0, stream>>>(x, nunits, qc, qm,
+                                                                           nullptr, nullptr);
+  }
+  return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_hif4_quantize(const void *x, bool bf16_in, int64_t nelem, uint8_t *q_codes,
                                 uint32_t *q_meta, uint8_t *r_codes, uint32_t *r_meta,
                                 hipStream_t stream) {
   const int64_t nunits = nelem / 8;
-  const int64_t per_wg = (kQThreads / 64) * 64 * kQSteps;
-  const dim3 grid((unsigned)((nunits + per_wg - 1) / per_wg)), block(kQThreads);
-  if (bf16_in) {
-    if (r_codes)
-      hif4_quantize_kernel<true, true><<<grid, block, 0, stream>>>(x, nunits, q_codes, q_meta,
-                                                                  r_codes, r_meta);
-    else
-      hif4_quantize_kernel<true, false><<<grid, block, 0, stream>>>(x, nunits, q_codes, q_meta,
-                                                                   nullptr, nullptr);
-  } else {
-    if (r_codes)
-      hif4_quantize_kernel<false, true><<<grid, block, 0, stream>>>(x, nunits, q_codes, q_meta,
-                                                                   r_codes, r_meta);
-    else
-      hif4_quantize_kernel<false, false><<<grid, block, 0, stream>>>(x, nunits, q_codes, q_meta,
-                                                                    nullptr, nullptr);
-  }
-  return hipGetLastError();
+  if (nunits < kQSmallUnits)
+    return launch_hq<1>(x, bf16_in, nunits, q_codes, q_meta, r_codes, r_meta, stream);
+  return launch_hq<kQSteps>(x, bf16_in, nunits, q_codes, q_meta, r_codes, r_meta, stream);
 }
 
 hipError_t launch_hif4_dequant(const uint8_t *codes, const uint32_t *meta, int64_t nelem,
