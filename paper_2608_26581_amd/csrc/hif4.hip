@@ -524,7 +524,10 @@ struct alignas(16) FewArea {
   uint8_t x[2 * kFewRows * kRowBytes];      // primary rows 0..15, residual 16..31
 };
 
-template <bool RES, bool ZBF16, bool WBF16>
+// NR weight rows per workgroup: 16 for up to 4 activation rows (twice the
+// workgroups, for latency hiding, where activation decoding costs little),
+// else 32.
+template <bool RES, bool ZBF16, bool WBF16, int NR>
 __global__ __launch_bounds__(kFewWaves * 64) void hif4_gemm_few_kernel(
     const uint8_t *__restrict__ qc, const uint32_t *__restrict__ qm,
     const uint8_t *__restrict__ rc, const uint32_t *__restrict__ rm,
@@ -533,16 +536,17 @@ __global__ __launch_bounds__(kFewWaves * 64) void hif4_gemm_few_kernel(
   __shared__ FewArea area[kFewWaves];
   __shared__ v4f part[kFewWaves][2][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int64_t n0 = (int64_t)blockIdx.x * kFewN;
+  static_assert(NR == 16 || NR == 32, "weight rows per workgroup");
+  const int64_t n0 = (int64_t)blockIdx.x * NR;
   const int64_t kbytes = K / 2, kblocks = K / kH;
 
   // Work items are code words (8 elements, one LDS chunk): 256 per K block
-  // for the 32 weight rows (lane l takes words l + 64 i, i < 4: row
+  // for the NR weight rows (lane l takes words l + 64 i, i < NR / 8: row
   // (l + 64 i) / 8, word l mod 8), and 8 per activation row for the
-  // 2M activation rows (words l + 64 i below 16 M), so a lane decodes four
+  // 2M activation rows (words l + 64 i below 16 M), so a lane decodes NR / 8
   // weight words and at most four activation words, and with few rows most
   // lanes decode no activation word at all.
-  constexpr int kWI = 4;
+  constexpr int kWI = NR / 8, kXI = 4;
   const int dw = lane & 7;
   const uint8_t *wsrc[kWI];
   const uint32_t *wmsrc[kWI];
@@ -558,11 +562,11 @@ __global__ __launch_bounds__(kFewWaves * 64) void hif4_gemm_few_kernel(
     wvsrc[i] = WBF16 ? reinterpret_cast<const u32x4 *>(wv + g * K + 8 * dw) : nullptr;
   }
   const int nx = (RES ? 2 : 1) * (int)M * 8;              // activation words per block
-  const uint8_t *xsrc[kWI];
-  const uint32_t *xmsrc[kWI];
-  int xlrow[kWI];
+  const uint8_t *xsrc[kXI];
+  const uint32_t *xmsrc[kXI];
+  int xlrow[kXI];
 #pragma unroll
-  for (int i = 0; i < kWI; ++i) {
+  for (int i = 0; i < kXI; ++i) {
     const int t = lane + 64 * i;
     const int j = t >> 3;                                   // activation row index
     const bool on = t < nx;
@@ -580,7 +584,7 @@ __global__ __launch_bounds__(kFewWaves * 64) void hif4_gemm_few_kernel(
   // decoded and multiplied.
   struct Words {
     u32x4 v[WBF16 ? kWI : 1];
-    uint32_t c[kWI], m[kWI], xc[kWI], xm[kWI];
+    uint32_t c[kWI], m[kWI], xc[kXI], xm[kXI];
   };
   Words cur, nxt;
   auto load = [&](int64_t b, Words &o) {
@@ -592,6 +596,9 @@ __global__ __launch_bounds__(kFewWaves * 64) void hif4_gemm_few_kernel(
         o.c[i] = *reinterpret_cast<const uint32_t *>(wsrc[i] + b * 32);
         o.m[i] = wmsrc[i][b];
       }
+    }
+#pragma unroll
+    for (int i = 0; i < kXI; ++i) {
       if (lane + 64 * i < nx) {
         o.xc[i] = *reinterpret_cast<const uint32_t *>(xsrc[i] + b * 32);
         o.xm[i] = xmsrc[i][b];
@@ -609,7 +616,7 @@ __global__ __launch_bounds__(kFewWaves * 64) void hif4_gemm_few_kernel(
       *reinterpret_cast<u32x4 *>(A.w + hswz(wlrow[i], dw)) = v;
     }
 #pragma unroll
-    for (int i = 0; i < kWI; ++i)
+    for (int i = 0; i < kXI; ++i)
       if (lane + 64 * i < nx)
         *reinterpret_cast<u32x4 *>(A.x + hswz(xlrow[i], dw)) = decode8_bf16(cur.xc[i], cur.xm[i], dw);
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -622,7 +629,7 @@ __global__ __launch_bounds__(kFewWaves * 64) void hif4_gemm_few_kernel(
       v8bf xr = xq;
       if constexpr (RES) xr = *reinterpret_cast<const v8bf *>(A.x + hswz(kFewRows + frow, ch));
 #pragma unroll
-      for (int f = 0; f < 2; ++f) {
+      for (int f = 0; f < NR / 16; ++f) {
         const v8bf wf = *reinterpret_cast<const v8bf *>(A.w + hswz(16 * f + frow, ch));
         acc[f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, xq, acc[f], 0, 0, 0);
         if constexpr (RES) acc[f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, xr, acc[f], 0, 0, 0);
@@ -641,7 +648,7 @@ __global__ __launch_bounds__(kFewWaves * 64) void hif4_gemm_few_kernel(
   if (m >= M) return;
   const bool vec_ok = (N & 3) == 0;
 #pragma unroll
-  for (int f = 0; f < 2; ++f) {
+  for (int f = 0; f < NR / 16; ++f) {
     v4f t = part[0][f][lane];
 #pragma unroll
     for (int w = 1; w < kFewWaves; ++w) t += part[w][f][lane];
@@ -681,10 +688,15 @@ hipError_t launch_hg(const uint8_t *qc, const uint32_t *qm, const uint8_t *rc,
   const hipError_t e =
       set_lds_limit(attr_done, reinterpret_cast<const void *>(kern), HSmem<RES>::kBytes);
   if (e != hipSuccess) return e;
-  if (M <= kFewRows && (N + kFewN - 1) / kFewN <= int64_t(UINT32_MAX / (kFewWaves * 64))) {
-    hif4_gemm_few_kernel<RES, ZBF16, WBF16>
-        <<<dim3((unsigned)((N + kFewN - 1) / kFewN)), dim3(kFewWaves * 64), 0, stream>>>(
-            qc, qm, rc, rm, wc, wm, wv, M, N, K, z);
+  if (M <= kFewRows && (N + 15) / 16 <= int64_t(UINT32_MAX / (kFewWaves * 64))) {
+    if (M <= 4)
+      hif4_gemm_few_kernel<RES, ZBF16, WBF16, 16>
+          <<<dim3((unsigned)((N + 15) / 16)), dim3(kFewWaves * 64), 0, stream>>>(
+              qc, qm, rc, rm, wc, wm, wv, M, N, K, z);
+    else
+      hif4_gemm_few_kernel<RES, ZBF16, WBF16, kFewN>
+          <<<dim3((unsigned)((N + kFewN - 1) / kFewN)), dim3(kFewWaves * 64), 0, stream>>>(
+              qc, qm, rc, rm, wc, wm, wv, M, N, K, z);
     return hipGetLastError();
   }
   const int64_t tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
