@@ -504,8 +504,8 @@ __global__ __launch_bounds__(HSmem<RES>::kThreads) void hif4_gemm_kernel(
 
 // ---------------------------------------------------------------- few rows
 //
-// Product for at most 16 activation rows (decode): one workgroup per 32
-// weight rows; its 4 waves take interleaved K blocks (wave w: blocks w, w+4,
+// Product for at most 16 activation rows (decode): one workgroup per 16 or
+// 32 weight rows; its 4 waves take interleaved K blocks (wave w: blocks w, w+4,
 // ...), decode the block's weight rows and activation rows into a
 // wave-private LDS area (no workgroup barrier in the loop: LDS serves one
 // wave's accesses in order) and run v_mfma_f32_16x16x32_bf16 with the weights
@@ -516,11 +516,11 @@ __global__ __launch_bounds__(HSmem<RES>::kThreads) void hif4_gemm_kernel(
 // M are decoded; the other rows of the area are never written and only feed
 // result columns m >= M, which are not stored.
 constexpr int kFewRows = 16;
-constexpr int kFewN = 32;
+constexpr int kFewN = 32;                   // weight rows per workgroup (at most)
 constexpr int kFewWaves = 4;
 
 struct alignas(16) FewArea {
-  uint8_t w[kFewN * kRowBytes];             // 32 weight rows of one K block
+  uint8_t w[kFewN * kRowBytes];             // up to 32 weight rows of one K block
   uint8_t x[2 * kFewRows * kRowBytes];      // primary rows 0..15, residual 16..31
 };
 
