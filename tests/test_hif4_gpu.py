@@ -306,3 +306,23 @@ def test_gemm_few_rows_decode_shape(orc):
         oq = orc.hif4_quantize(x.astype(np.float64))
         zr, bound = orc.hif4_gemm(oq[0], oq[1], oq[2], oq[3], ow[0], ow[1])
         assert_gemm_close(z, zr, bound, False, "hif4 decode M=%d" % M)
+
+
+def test_gemm_full_size_k12288_sampled(orc):
+    """The down-projection shape of the MLP workload (M 4096, N 4096,
+    K 12288): the largest reduction of the configurations, at the edge of
+    the product tolerance's derivation; 40 sampled rows x 64 columns."""
+    _say("hif4 gemm 4096x4096x12288 sampled")
+    w = wl.WORKLOADS["qwen"].scaled(M=4096, K=12288, weights=(("w", 12288, 4096),))
+    data = wl.generate(w, seed=4)
+    x, wt = data["x"], data["w"]
+    _, q = _gpu_quant(x, True)
+    _, wq = _gpu_quant(wt, False, residual=False)
+    z = host(rfq.rfq_hif4_gemm(*q, wq[0], wq[1]))
+    rng = np.random.default_rng(12)
+    rows = np.sort(np.concatenate([[0, 4095], rng.choice(4096, 38, replace=False)]))
+    cols = np.sort(np.concatenate([[0, 4095], rng.choice(4096, 62, replace=False)]))
+    oq = orc.hif4_quantize(x[rows].astype(np.float64))
+    ow = orc.hif4_quantize(wt[cols].astype(np.float64), residual=False)
+    zr, bound = orc.hif4_gemm(oq[0], oq[1], oq[2], oq[3], ow[0], ow[1])
+    assert_gemm_close(z[np.ix_(rows, cols)], zr, bound, False, "hif4 K=12288")
