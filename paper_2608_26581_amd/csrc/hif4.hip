@@ -266,21 +266,24 @@ __global__ __launch_bounds__(256) void hif4_dequant_kernel(
 
 // ---------------------------------------------------------------- product
 
-constexpr int kBM = 128, kBN = 256;            // tile: activation rows x weight rows
+constexpr int kBM = 128;                       // tile: activation rows x BN weight rows
 constexpr int kRowBytes = kH * 2;              // one decoded bf16 row of a K block
-constexpr int kTM = 64, kTN = 128;             // consumer sub-tile
-constexpr int kFM = kTM / 32, kFN = kTN / 32;
+constexpr int kTM = 64;                        // consumer sub-tile: 64 x BN/2
+constexpr int kFM = kTM / 32;
 
-template <bool RES>
+// BN = 256 weight rows per tile, or 128 where 256-row tiles would leave CUs
+// idle (fewer activation rows).
+template <bool RES, int BN>
 struct HSmem {
   static constexpr int kWRow0 = (RES ? 2 : 1) * kBM;    // q rows, r rows, then w rows
-  static constexpr int kRows = kWRow0 + kBN;
+  static constexpr int kRows = kWRow0 + BN;
   static constexpr int kBufBytes = kRows * kRowBytes;
   static constexpr int kBytes = 2 * kBufBytes;
-  // Producer waves: two per SIMD with the residual (each lane decodes two
-  // half-block rows per step), six without.
-  static constexpr int kProducers = RES ? 8 : 6;
+  // Producer waves: each lane decodes two half-block rows per step (8 waves,
+  // two per SIMD, with the residual and BN = 256).
+  static constexpr int kProducers = kRows / 64;
   static constexpr int kThreads = (kProducers + 4) * 64;
+  static constexpr int kTN = BN / 2, kFN = kTN / 32;
 };
 
 __device__ __forceinline__ int hswz(int row, int chunk) {
@@ -322,18 +325,19 @@ __device__ __forceinline__ u32x4 decode8_bf16(uint32_t w, uint32_t meta, int g) 
 // WBF16: the weights come as bf16 values wv[N][K] (for example HiF4 weights
 // decoded once) and are copied into LDS as they are; only the activation
 // codes are decoded.
-template <bool RES, bool ZBF16, bool WBF16>
-__global__ __launch_bounds__(HSmem<RES>::kThreads) void hif4_gemm_kernel(
+template <bool RES, bool ZBF16, bool WBF16, int BN>
+__global__ __launch_bounds__((HSmem<RES, BN>::kThreads)) void hif4_gemm_kernel(
     const uint8_t *__restrict__ qc, const uint32_t *__restrict__ qm,
     const uint8_t *__restrict__ rc, const uint32_t *__restrict__ rm,
     const uint8_t *__restrict__ wc, const uint32_t *__restrict__ wm,
     const uint16_t *__restrict__ wv, int64_t M, int64_t N, int64_t K, void *__restrict__ z) {
-  using S = HSmem<RES>;
+  using S = HSmem<RES, BN>;
+  constexpr int kTN = S::kTN, kFN = S::kFN;
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
 
   int tm, tn;
-  tile_coords<8>(blockIdx.x, (int)((M + kBM - 1) / kBM), (int)((N + kBN - 1) / kBN), tm, tn);
-  const int64_t m0 = (int64_t)tm * kBM, n0 = (int64_t)tn * kBN;
+  tile_coords<8>(blockIdx.x, (int)((M + kBM - 1) / kBM), (int)((N + BN - 1) / BN), tm, tn);
+  const int64_t m0 = (int64_t)tm * kBM, n0 = (int64_t)tn * BN;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int nsteps = (int)(K / kH);
   const int64_t kbytes = K / 2, kblocks = K / kH;
@@ -678,16 +682,30 @@ __global__ __launch_bounds__(kFewWaves * 64) void hif4_gemm_few_kernel(
   }
 }
 
+template <bool RES, bool ZBF16, bool WBF16, int BN>
+hipError_t launch_tiles(const uint8_t *qc, const uint32_t *qm, const uint8_t *rc,
+                        const uint32_t *rm, const uint8_t *wc, const uint32_t *wm,
+                        const uint16_t *wv, int64_t M, int64_t N, int64_t K, void *z,
+                        hipStream_t stream) {
+  using S = HSmem<RES, BN>;
+  auto kern = hif4_gemm_kernel<RES, ZBF16, WBF16, BN>;
+  static std::atomic<bool> attr_done[kMaxDevices];
+  const hipError_t e = set_lds_limit(attr_done, reinterpret_cast<const void *>(kern), S::kBytes);
+  if (e != hipSuccess) return e;
+  const int64_t tiles = ((M + kBM - 1) / kBM) * ((N + BN - 1) / BN);
+  kern<<<dim3((unsigned)tiles), dim3(S::kThreads), S::kBytes, stream>>>(qc, qm, rc, rm, wc, wm,
+                                                                         wv, M, N, K, z);
+  return hipGetLastError();
+}
+
+// Workgroups that fill the chip once (256 CUs on MI355X).
+constexpr int64_t kFillTiles = 256;
+
 template <bool RES, bool ZBF16, bool WBF16>
 hipError_t launch_hg(const uint8_t *qc, const uint32_t *qm, const uint8_t *rc,
                      const uint32_t *rm, const uint8_t *wc, const uint32_t *wm,
                      const uint16_t *wv, int64_t M, int64_t N, int64_t K, void *z,
                      hipStream_t stream) {
-  auto kern = hif4_gemm_kernel<RES, ZBF16, WBF16>;
-  static std::atomic<bool> attr_done[kMaxDevices];
-  const hipError_t e =
-      set_lds_limit(attr_done, reinterpret_cast<const void *>(kern), HSmem<RES>::kBytes);
-  if (e != hipSuccess) return e;
   if (M <= kFewRows && (N + 15) / 16 <= int64_t(UINT32_MAX / (kFewWaves * 64))) {
     if (M <= 4)
       hif4_gemm_few_kernel<RES, ZBF16, WBF16, 16>
@@ -699,10 +717,9 @@ hipError_t launch_hg(const uint8_t *qc, const uint32_t *qm, const uint8_t *rc,
               qc, qm, rc, rm, wc, wm, wv, M, N, K, z);
     return hipGetLastError();
   }
-  const int64_t tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
-  kern<<<dim3((unsigned)tiles), dim3(HSmem<RES>::kThreads), HSmem<RES>::kBytes, stream>>>(
-      qc, qm, rc, rm, wc, wm, wv, M, N, K, z);
-  return hipGetLastError();
+  if (((M + kBM - 1) / kBM) * ((N + 255) / 256) < kFillTiles)
+    return launch_tiles<RES, ZBF16, WBF16, 128>(qc, qm, rc, rm, wc, wm, wv, M, N, K, z, stream);
+  return launch_tiles<RES, ZBF16, WBF16, 256>(qc, qm, rc, rm, wc, wm, wv, M, N, K, z, stream);
 }
 
 

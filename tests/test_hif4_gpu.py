@@ -326,3 +326,21 @@ def test_gemm_full_size_k12288_sampled(orc):
     ow = orc.hif4_quantize(wt[cols].astype(np.float64), residual=False)
     zr, bound = orc.hif4_gemm(oq[0], oq[1], oq[2], oq[3], ow[0], ow[1])
     assert_gemm_close(z[np.ix_(rows, cols)], zr, bound, False, "hif4 K=12288")
+
+
+@pytest.mark.parametrize("residual", [True, False])
+def test_gemm_wide_tiles_ragged(orc, residual):
+    """A product with enough 128 x 256 tiles to fill the chip (16 x 16, ragged
+    in both directions) runs the 256-wide weight tiles; the smaller shapes
+    above run the 128-wide ones."""
+    M, N, K = 2000, 4000, 128
+    _say("hif4 gemm wide tiles %dx%dx%d residual=%s" % (M, N, K, residual))
+    w = wl.WORKLOADS["tiny"].scaled(M=M, K=K, weights=(("w", K, N),))
+    data = wl.generate(w, seed=21)
+    _, q = _gpu_quant(data["x"], False, residual)
+    _, wq = _gpu_quant(data["w"], False, residual=False)
+    z = host(rfq.rfq_hif4_gemm(*q, wq[0], wq[1]))
+    oq = orc.hif4_quantize(data["x"].astype(np.float64), residual)
+    ow = orc.hif4_quantize(data["w"].astype(np.float64), residual=False)
+    zr, bound = orc.hif4_gemm(oq[0], oq[1], oq[2], oq[3], ow[0], ow[1])
+    assert_gemm_close(z, zr, bound, False, "hif4 wide tiles")
