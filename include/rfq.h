@@ -7,7 +7,7 @@
  * MXFP4 code of the residual the primary code lost (Eq. 8-10), and a
  * block-scaled FP4 product that contracts both codes against MXFP4 weights
  * (Eq. 11, Algorithm 1).  The rfq_hif4_* calls at the end do the same with
- * the HiF4 format of Sec. 3.2.3 (64-element blocks); the number format below
+ * the HiF4 format of Sec. 3.3 (64-element blocks); the number format below
  * is MXFP4's, HiF4's is described with those calls.
  *
  * Number format (Sec. 3.2, Eq. 3-4, element format of Sec. 3.2.2):
@@ -246,7 +246,7 @@ rfq_status rfq_gemm_stream(const void *x, rfq_dtype x_dtype, int residual,
                            void *z, rfq_dtype z_dtype, void *hip_stream);
 
 /*
- * HiF4 form of the path (Sec. 3.2.3, Eq. 5-6).  A block is 64 consecutive
+ * HiF4 form of the path (Sec. 3.3, Eq. 5-6).  A block is 64 consecutive
  * elements of a row along K (K a positive multiple of 64, else
  * RFQ_ERR_SHAPE).  Per block one uint32 metadata word:
  *   bits 0-7   E6M2 macro scale byte E << 2 | M: S = 2^(E-48) (1 + M/4) (Eq. 5);

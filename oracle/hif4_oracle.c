@@ -6,7 +6,7 @@
  * leg of the benchmark use it.  It shares no source, header, table or helper
  * with the GPU library.
  *
- * Format (Sec. 3.2.3, Eq. 5-6): blocks of 64 consecutive elements along K.
+ * Format (Sec. 3.3, Eq. 5-6): blocks of 64 consecutive elements along K.
  * Per block, 32 bits of metadata: a macro scale S in unsigned E6M2 (6
  * exponent bits with bias 48, 2 mantissa bits: S = 2^(E-48) (1 + M/4),
  * Eq. 5), eight 1-bit micro-exponents E1_8 (one per 8 elements) and sixteen

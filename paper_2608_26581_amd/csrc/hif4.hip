@@ -1,4 +1,4 @@
-// HiF4 form of the RFQ path on gfx950 (Sec. 3.2.3, Eq. 5-6, with the RFQ
+// HiF4 form of the RFQ path on gfx950 (Sec. 3.3, Eq. 5-6, with the RFQ
 // steps of Sec. 4.3, Eq. 8-11): the quantizer (primary HiF4 code and, for
 // activations, the HiF4 code of the residual it leaves), dequantization and
 // the RFQ product.

@@ -15,7 +15,7 @@ Sources of truth used here:
     equivariance, idempotence, negation symmetry, monotone improvement, the
     half-error bound of the second stage);
   * closed forms for the SwiGLU intermediate and bf16 rounding;
-  * HiF4 (Sec. 3.2.3): the decode of Eq. 6 worked by hand and implemented
+  * HiF4 (Sec. 3.3): the decode of Eq. 6 worked by hand and implemented
     here independently; the encoder is this build's reading (parity
     unpinned) and is pinned by its defining properties (smallest macro scale
     with no saturation, smallest non-saturating micro-exponents under the
@@ -100,6 +100,84 @@ def bf16_ulp(v):
     return 2.0 ** (math.floor(math.log2(abs(v))) - 7)
 
 
+# Scale bytes swept by the converter-convention tests: the lower clamp and
+# the subnormal range of the scale (0-2), the first byte whose grid is normal
+# (3), unit scale (127), a large scale (200) and the largest byte a finite
+# fp32 or bf16 block can reach (252: amax below 2^128 gives at most
+# exponent field 254, minus the offset 2).
+SWEEP_SCALE_BYTES = (0, 1, 2, 3, 127, 200, 252)
+
+
+def _neighbours(v, bf16):
+    """The two fp32 (or bf16) neighbours of a positive value v of that format
+    (by incrementing its bit pattern, subnormals included)."""
+    shift = 16 if bf16 else 0
+    u = int(np.array([v], np.float32).view(np.uint32)[0])
+    assert (u >> shift) << shift == u, v
+    out = []
+    for d in (-1, 1):
+        w = np.array([((u >> shift) + d) << shift], np.uint32).view(np.float32)[0]
+        out.append(float(w))
+    return out
+
+
+def _below(v, bf16):
+    """The largest fp32 (or bf16) value below v (a power of two up to 2^128,
+    where the bit pattern just below v's is the largest finite value)."""
+    if v == 2.0 ** 128:
+        return float(np.array([0x7F7FFFFF if not bf16 else 0x7F7F0000], np.uint32)
+                     .view(np.float32)[0])
+    return _neighbours(v, bf16)[0]
+
+
+def scale_sweep_blocks(bf16=False):
+    """Blocks that pin the element conversions at the scale bytes of
+    SWEEP_SCALE_BYTES.  Returns x float64 [rows][128]; row i holds four
+    32-element blocks of scale byte SWEEP_SCALE_BYTES[i], S = 2^(byte-127):
+    every E2M1 grid point from 0.5, every midpoint and its two fp32 (bf16)
+    neighbours, zero, and 6.25, 7.5 and the largest value below 8 (which
+    sets the block maximum in [4S, 8S)), all times S, in that order, then
+    negated, with alternating signs, and reversed.  The last row holds
+    clamped blocks at byte 0 (maximum below 2^-125, so x / 2^-127 < 4): the
+    sweep values below 4S, those below 2S (all subnormal), a block of mixed
+    small values with zeros, and the first block with signs flipped on every
+    third element.  Every value is exactly representable in fp32 (in bf16
+    when bf16 is set)."""
+    grid = [v for v in E2M1 if v > 0]
+    mids = [(a + b) / 2 for a, b in zip(E2M1, E2M1[1:])]
+
+    def sweep(S, limit=None):
+        vals = [g * S for g in grid] + [m * S for m in mids]
+        for m in mids:
+            vals += _neighbours(m * S, bf16)
+        vals += [0.0, 6.25 * S, 7.5 * S]
+        if limit is None:
+            vals.append(_below(8.0 * S, bf16))
+        else:
+            vals = [v for v in vals if v < limit * S] + [_below(limit * S, bf16)]
+        assert len(vals) <= 32
+        return np.array(vals + [0.0] * (32 - len(vals)))
+
+    sign_alt = np.where(np.arange(32) % 2 == 0, 1.0, -1.0)
+    rows = []
+    for byte in SWEEP_SCALE_BYTES:
+        b = sweep(2.0 ** (byte - 127))
+        rows.append(np.concatenate([b, -b, b * sign_alt, b[::-1]]))
+    S0 = 2.0 ** -127
+    small, tiny = sweep(S0, 4.0), sweep(S0, 2.0)
+    mixed = [_below(2.0 ** -125, bf16), 1.5 * 2.0 ** -126, 3 * 2.0 ** -128, -(2.0 ** -128),
+             _below(2.0 ** -126, bf16), -1.25 * 2.0 ** -128]
+    mixed = np.array(mixed + [0.0] * (32 - len(mixed)))
+    flip = np.where(np.arange(32) % 3 == 0, -1.0, 1.0)
+    rows.append(np.concatenate([small, -tiny, mixed, small * flip]))
+    x = np.array(rows, np.float64)
+    f = x.astype(np.float32)
+    assert np.array_equal(f.astype(np.float64), x)
+    if bf16:
+        assert ((f.view(np.uint32) & 0xFFFF) == 0).all(), "sweep value not a bf16 value"
+    return x
+
+
 # ---------------------------------------------------------------- pins
 def pin_e2m1_table(o):
     """The 16 code values are the E2M1 magnitudes with the sign bit."""
@@ -134,6 +212,31 @@ def pin_block_exponent(o):
             amax = f * 2.0 ** j
             want = max(-127, min(127, j - 2))
             assert o.block_exponent(amax) == want == brute_exponent(amax), (amax, j)
+
+
+def pin_scale_byte_sweep(o):
+    """The RFQ quantizer (primary and residual) at the scale bytes of
+    SWEEP_SCALE_BYTES, the lower clamp and subnormal elements included, fp32
+    and bf16 values, against brute force: exponent by counting, nearest grid
+    point by exhaustive comparison, residual x - deq(q) exact in Python."""
+    for bf16 in (False, True):
+        x = scale_sweep_blocks(bf16)
+        qc, qs, rc, rs = o.quantize(x)
+        want_bytes = list(SWEEP_SCALE_BYTES) + [0]
+        for i in range(x.shape[0]):
+            for b in range(x.shape[1] // 32):
+                blk = [float(v) for v in x[i, 32 * b:32 * b + 32]]
+                codes, byte = brute_block(blk)
+                assert byte == qs[i, b] and (b != 0 or byte == want_bytes[i]), (i, b, byte)
+                assert pack(codes) == bytes(qc[i, 16 * b:16 * b + 16]), (bf16, i, b)
+                scale = 2.0 ** (byte - 127)
+                res = [v - (-1.0 if c & 8 else 1.0) * E2M1[c & 7] * scale
+                       for v, c in zip(blk, codes)]
+                rcodes, rbyte = brute_block(res)
+                assert rbyte == rs[i, b], (bf16, i, b, rbyte, rs[i, b])
+                assert pack(rcodes) == bytes(rc[i, 16 * b:16 * b + 16]), (bf16, i, b)
+        # The clamped row really is clamped and still has nonzero codes.
+        assert x[-1].max() < 2.0 ** -125 and qc[-1].any() and rc[-1].any()
 
 
 def _check_golden_block(o, name):

@@ -1,4 +1,4 @@
-"""Parity of the HiF4 path (Sec. 3.2.3, Eq. 5-6, with RFQ's residual) with
+"""Parity of the HiF4 path (Sec. 3.3, Eq. 5-6, with RFQ's residual) with
 the CPU oracle, through the C ABI.
 
 Quantizer codes and metadata words: bit-exact (the encoder reading is the

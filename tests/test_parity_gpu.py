@@ -14,7 +14,8 @@ import paper_2608_26581_amd as rfq
 from paper_2608_26581_amd import workloads as wl
 from gpu_util import (assert_gemm_close, dev, dev_bf16, host, host_bf16_as_f32,
                       x_device)
-from oracle_pins import padded_floats, padded_bytes, read_golden
+from oracle_pins import (SWEEP_SCALE_BYTES, padded_floats, padded_bytes, read_golden,
+                         scale_sweep_blocks)
 
 pytestmark = pytest.mark.gpu
 
@@ -139,6 +140,58 @@ def test_quantize_special_values(orc):
             xt = torch.from_numpy(arr).cuda().to(dt)
             g = [host(t) for t in rfq.rfq_quantize_act(xt)]
             _assert_codes_equal(g, orc.quantize(arr.astype(np.float64)), "special %s" % dt)
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_scale_byte_sweep_through_the_converters(orc, dtype):
+    """Pins the conventions of the gfx950 scaled FP4 conversions that
+    bit-exactness rests on (round to nearest even, saturation at 6, sign of
+    zero, the scale operand of every byte) at scale bytes 0, 1, 2, 3, 127,
+    200 and 252: every E2M1 grid point, midpoint and fp32 (bf16) neighbour
+    of a midpoint, both signs, in blocks whose maximum sets that byte, plus
+    clamped blocks at byte 0 (maximum below 2^-125, subnormal elements, and
+    nonzero codes in both the primary and the residual stage).  Sec. 3.2
+    Eq. 3-4 and Sec. 4.3 Eq. 9-10 through the oracle (itself pinned against
+    brute force on the same blocks), bit-exact; dequantization exact; the
+    products of these codes within tolerance (byte 0 reaching the scaled
+    MFMA as 2^-127), on the general, few-row and large-tile kernels."""
+    bf16 = dtype == torch.bfloat16
+    x = scale_sweep_blocks(bf16)
+    _say("scale byte sweep %s rows %d" % (dtype, x.shape[0]))
+    xt = torch.from_numpy(x.astype(np.float32)).cuda().to(dtype)
+    g = [host(t) for t in rfq.rfq_quantize_act(xt)]
+    ref = orc.quantize(x)
+    _assert_codes_equal(g, ref, "sweep %s" % dtype)
+    assert g[1][-1].max() == 0 and g[0][-1].any() and g[3][-1].max() == 0 and g[2][-1].any()
+    w = [host(t) for t in rfq.rfq_quantize_weight(xt)]
+    _assert_codes_equal(w, ref[:2], "sweep weight %s" % dtype)
+    for c, sc in ((g[0], g[1]), (g[2], g[3])):
+        d = host(rfq.rfq_dequant(dev(c), dev(sc)))
+        assert np.array_equal(d.astype(np.float64), orc.dequant(c, sc))
+
+    row_bytes = np.array(list(SWEEP_SCALE_BYTES) + [0])
+    rng = np.random.default_rng(31)
+    # K = 128: general kernel; 8 rows, K = 512: few-row kernel; 320 rows,
+    # K = 512: large-tile kernel.
+    for reps, kreps in ((1, 1), (1, 4), (40, 4)):
+        xs = np.tile(x, (reps, kreps))
+        xst = torch.from_numpy(xs.astype(np.float32)).cuda().to(dtype)
+        q = rfq.rfq_quantize_act(xst)
+        qh = [host(t) for t in q]
+        K = xs.shape[1]
+        for j in (100, 0, -100):
+            # Weights scaled by 2^j; only rows whose products stay far from
+            # fp32 underflow and overflow are compared.
+            wv = (rng.standard_normal((96, K)) * 2.0 ** j).astype(np.float32)
+            wq = rfq.rfq_quantize_weight(dev(wv))
+            _say("sweep product rows=%d K=%d j=%d" % (xs.shape[0], K, j))
+            for out_dtype in (torch.float32, torch.bfloat16):
+                z = rfq.rfq_gemm(*q, *wq, out_dtype=out_dtype)
+                zh = host_bf16_as_f32(z) if out_dtype == torch.bfloat16 else host(z)
+                zr, bound = orc.gemm(*qh, host(wq[0]), host(wq[1]))
+                ok = np.abs(np.tile(row_bytes, reps) - 127 + j) <= 100
+                assert_gemm_close(zh[ok], zr[ok], bound[ok], out_dtype == torch.bfloat16,
+                                  "sweep product K=%d j=%d" % (K, j))
 
 
 @pytest.mark.parametrize("M,K", [(64, 4096), (5, 96), (3, 2080)])
