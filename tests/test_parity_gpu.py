@@ -327,6 +327,17 @@ def test_gemm_small(orc, name, M, N, K, residual, out_dtype):
     assert_gemm_close(zh, zr, bound, out_dtype == torch.bfloat16, "gemm %s" % name)
 
 
+def _tile_samples(M, N, T, rng):
+    """One output at a random position inside every T x T tile of an M x N
+    product (tiles cut at the edges), so that every output tile of the
+    product kernels (256 x 256 and 128 x 128) holds a sampled output."""
+    tm, tn = np.meshgrid(np.arange(0, M, T), np.arange(0, N, T), indexing="ij")
+    tm, tn = tm.ravel(), tn.ravel()
+    rows = tm + (rng.random(tm.size) * np.minimum(T, M - tm)).astype(np.int64)
+    cols = tn + (rng.random(tn.size) * np.minimum(T, N - tn)).astype(np.int64)
+    return rows, cols
+
+
 @pytest.mark.parametrize("name", ["qwen", "wan"])
 def test_gemm_full_size_sampled(orc, name):
     data = wl.generate(wl.WORKLOADS[name], seed=0)
@@ -340,8 +351,9 @@ def test_gemm_full_size_sampled(orc, name):
     hq = [host(t) for t in q]
     hw = [host(t) for t in w]
     rng = np.random.default_rng(1)
-    rows = np.concatenate([rng.integers(0, M, 4000), np.repeat([0, M - 1], N)])
-    cols = np.concatenate([rng.integers(0, N, 4000), np.tile(np.arange(N), 2)])
+    tr, tc = _tile_samples(M, N, 128, rng)
+    rows = np.concatenate([rng.integers(0, M, 4000), np.repeat([0, M - 1], N), tr])
+    cols = np.concatenate([rng.integers(0, N, 4000), np.tile(np.arange(N), 2), tc])
     zr, bound = orc.gemm_sampled(*hq, *hw, rows, cols)
     assert_gemm_close(z32[rows, cols], zr, bound, False, "full fp32")
     assert_gemm_close(zbf[rows, cols], zr, bound, True, "full bf16")
@@ -611,15 +623,22 @@ def test_fallback_map_beyond_one_grid_pass():
 
 
 # --------------------------------------------------- fused SwiGLU epilogue
-def _fused_and_unfused(data, K, Nh, res_in, res_out):
+def _fused_and_unfused(data, K, Nh, res_in, res_out, stages=None):
     """The chained path (gate and up products with bf16 Z, then the SwiGLU
-    quantizer) and the fused one on the same codes."""
+    quantizer) and the fused one on the same codes.  With a dict `stages`,
+    the chained path's intermediates are returned in it as host arrays:
+    q (activation codes), wg and wu (weight codes), g and u (fp32 values of
+    the bf16 products)."""
     q = rfq.rfq_quantize_act(x_device(data), residual=res_in)
     wg = rfq.rfq_quantize_weight(dev(data["w_gate"]))
     wu = rfq.rfq_quantize_weight(dev(data["w_up"]))
     g = rfq.rfq_gemm(*q, *wg, out_dtype=torch.bfloat16)
     u = rfq.rfq_gemm(*q, *wu, out_dtype=torch.bfloat16)
     ref = rfq.rfq_swiglu_quantize_act(g, u, residual=res_out, return_h=True)
+    if stages is not None:
+        stages.update(q=[None if t is None else host(t) for t in q],
+                      wg=[host(t) for t in wg], wu=[host(t) for t in wu],
+                      g=host_bf16_as_f32(g), u=host_bf16_as_f32(u))
     wgu = (rfq.interleave_gate_up(wg[0], wu[0]), rfq.interleave_gate_up(wg[1], wu[1]))
     got = rfq.rfq_gemm_swiglu_quantize(*q, *wgu, residual=res_out, return_h=True)
     return got, ref
@@ -647,20 +666,46 @@ def test_gemm_swiglu_fused_matches_chained(M, Nh, K, res_in, res_out):
 
 
 def test_gemm_swiglu_fused_full_size_and_down_product(orc):
-    """Config-5 shape: fused gate/up epilogue equals the chained path bit for
+    """Config-5 shape (4096 x 4096 -> 2 x 12288 -> 4096), every stage of the
+    chained path against the oracle on the GPU's own input to that stage
+    (Sec. 4.3 Eq. 8-11 applied twice): the gate and up products sampled in
+    every 128 x 128 output tile, all 4096 x 12288 elements of h within one
+    bf16 ulp of the oracle's SwiGLU of the GPU's g and u, all codes and
+    scales of h (primary and residual) bit-exact against the oracle's
+    quantizer; the fused gate/up epilogue equals the chained path bit for
     bit; the down product on the fused codes is checked against the oracle
-    on sampled rows."""
+    on sampled rows and in every output tile."""
     data = wl.generate(wl.WORKLOADS["swiglu"], seed=0)
     _say("fused swiglu full size")
-    got, ref = _fused_and_unfused(data, 4096, 12288, True, True)
+    st = {}
+    got, ref = _fused_and_unfused(data, 4096, 12288, True, True, stages=st)
     for n, a, b in zip(("hq_codes", "hq_scales", "hr_codes", "hr_scales", "h"), got, ref):
         assert torch.equal(a, b), n
+    # Stages of the chained path, each on the GPU's own input to it.
+    M, K, Nh = 4096, 4096, 12288
+    rng = np.random.default_rng(12)
+    for zname, wname in (("g", "wg"), ("u", "wu")):
+        rows, cols = _tile_samples(M, Nh, 128, rng)
+        zr, bound = orc.gemm_sampled(*st["q"], *st[wname], rows, cols)
+        assert_gemm_close(st[zname][rows, cols], zr, bound, True, "full-size %s product" % zname)
+    _say("swiglu stage full size")
+    hg = host_bf16_as_f32(ref[4])
+    href = orc.swiglu(st["g"], st["u"])
+    del st
+    ulp = np.exp2(np.floor(np.log2(np.maximum(np.abs(href), 2.0 ** -126))) - 7)
+    assert np.all(np.abs(hg - href) <= ulp)
+    del href, ulp
+    _assert_codes_equal([host(t) for t in ref[:4]], orc.quantize(hg), "h full size")
+    del hg
     wd = rfq.rfq_quantize_weight(dev(data["w_down"]))
     z = host(rfq.rfq_gemm(*got[:4], *wd))
     rows = np.arange(0, 4096, 97)
     hq = [host(t)[rows] for t in got[:4]]
     zr, bound = orc.gemm(*hq, host(wd[0]), host(wd[1]))
     assert_gemm_close(z[rows], zr, bound, False, "down on fused codes")
+    tr, tc = _tile_samples(M, K, 128, rng)
+    zr, bound = orc.gemm_sampled(*[host(t) for t in got[:4]], host(wd[0]), host(wd[1]), tr, tc)
+    assert_gemm_close(z[tr, tc], zr, bound, False, "down on fused codes, every tile")
 
 
 # ---------------------------------------------------------------- edges
