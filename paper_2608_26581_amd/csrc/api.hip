@@ -59,8 +59,10 @@ bool product_fits(int64_t M, int64_t N) {
 }
 
 // HiF4 calls: K a positive multiple of 64 (one metadata word per 64-element
-// block).  The quantizer runs 256 work items per 128 blocks; the product one
-// 512-work-item workgroup per 128 x 256 output tile.
+// block).  The quantizer runs 256 work items per 128 blocks.  The product
+// runs one workgroup per 128 x 256 output tile (up to 768 work items: eight
+// producer waves with the residual, four consumers) or per 128 x 128 tile
+// (up to 640); both grids must fit, whichever the dispatch picks.
 rfq_status check_k64(int64_t rows, int64_t K) {
   if (rows < 0 || K < 64 || (K % 64) != 0 || K > kMaxK) return RFQ_ERR_SHAPE;
   return RFQ_OK;
@@ -70,7 +72,9 @@ bool hif4_quantizer_fits(int64_t rows, int64_t K) {
 }
 bool hif4_product_fits(int64_t M, int64_t N) {
   if (M > INT32_MAX || N > INT32_MAX) return false;
-  return ((M + 127) / 128) * ((N + 255) / 256) * 512 <= kMaxWorkItems;
+  const int64_t rows = (M + 127) / 128;
+  return rows * ((N + 255) / 256) * 768 <= kMaxWorkItems &&
+         rows * ((N + 127) / 128) * 640 <= kMaxWorkItems;
 }
 
 // Confirms that the current device is a gfx950 GPU (cached per device).

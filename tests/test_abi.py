@@ -357,3 +357,11 @@ def test_valid_arguments_without_a_gpu_report_device_error():
     assert _lib().rfq_gemm_stream(A, 1, 1, A, A, 8, 8, 512, A, 0, None) == EDEVICE
     assert _lib().rfq_hif4_quantize(A, 1, 4, 64, A, A, A, A, None) == EDEVICE
     assert _lib().rfq_hif4_gemm(A, A, A, A, A, A, 8, 8, 64, A, 0, None) == EDEVICE
+    # The HiF4 product's launch-size limit sits at the largest grid it may
+    # launch: 128-row tiles of 256 weight rows with 768 work items or of 128
+    # weight rows with 640, whichever the dispatch picks (N = 256: two
+    # 128-wide tiles, 1280 work items per 128 activation rows).
+    tile_rows = 0xFFFFFFFF // 1280
+    g = _lib().rfq_hif4_gemm
+    assert g(A, A, A, A, A, A, tile_rows * 128, 256, 64, A, 0, None) == EDEVICE
+    assert g(A, A, A, A, A, A, (tile_rows + 1) * 128, 256, 64, A, 0, None) == ESHAPE

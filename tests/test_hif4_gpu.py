@@ -15,7 +15,7 @@ import torch
 
 import paper_2608_26581_amd as rfq
 from paper_2608_26581_amd import workloads as wl
-from gpu_util import assert_gemm_close, dev, dev_bf16, host
+from gpu_util import assert_gemm_close, dev, dev_bf16, host, host_bf16_as_f32
 from oracle_pins import padded_bytes, padded_floats, read_golden
 
 pytestmark = pytest.mark.gpu
@@ -329,18 +329,40 @@ def test_gemm_full_size_k12288_sampled(orc):
 
 
 @pytest.mark.parametrize("residual", [True, False])
-def test_gemm_wide_tiles_ragged(orc, residual):
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
+def test_gemm_wide_tiles_ragged(orc, residual, out_dtype):
     """A product with enough 128 x 256 tiles to fill the chip (16 x 16, ragged
     in both directions) runs the 256-wide weight tiles; the smaller shapes
-    above run the 128-wide ones."""
-    M, N, K = 2000, 4000, 128
-    _say("hif4 gemm wide tiles %dx%dx%d residual=%s" % (M, N, K, residual))
+    above run the 128-wide ones.  K = 640 (ten blocks) passes the LDS
+    double buffer back and forth.  Checked: against the oracle in fp32 and
+    bf16 output, bit-identity of the bf16-weight form with the codes form,
+    and guard bytes around both outputs."""
+    M, N, K = 2000, 4000, 640
+    _say("hif4 gemm wide tiles %dx%dx%d residual=%s %s" % (M, N, K, residual, out_dtype))
     w = wl.WORKLOADS["tiny"].scaled(M=M, K=K, weights=(("w", K, N),))
     data = wl.generate(w, seed=21)
     _, q = _gpu_quant(data["x"], False, residual)
     _, wq = _gpu_quant(data["w"], False, residual=False)
-    z = host(rfq.rfq_hif4_gemm(*q, wq[0], wq[1]))
+    esize = 4 if out_dtype == torch.float32 else 2
+    guard = 4096
+
+    def guarded():
+        raw = torch.full((M * N * esize + 2 * guard,), 0xA5, dtype=torch.uint8, device="cuda")
+        return raw, raw[guard:guard + M * N * esize].view(out_dtype).view(M, N)
+
+    raw1, z1 = guarded()
+    raw2, z2 = guarded()
+    rfq.rfq_hif4_gemm(*q, wq[0], wq[1], out=z1)
+    wv = rfq.rfq_hif4_dequant(wq[0], wq[1], out_dtype=torch.bfloat16)
+    rfq.rfq_hif4_gemm_wbf16(*q, wv, out=z2)
+    torch.cuda.synchronize()
+    for raw in (raw1, raw2):
+        r = host(raw)
+        assert np.all(r[:guard] == 0xA5) and np.all(r[-guard:] == 0xA5), "write outside Z"
+    iv = torch.int32 if out_dtype == torch.float32 else torch.int16
+    assert torch.equal(z1.view(iv), z2.view(iv)), "bf16-weight form differs from codes form"
+    z = host(z1) if out_dtype == torch.float32 else host_bf16_as_f32(z1)
     oq = orc.hif4_quantize(data["x"].astype(np.float64), residual)
     ow = orc.hif4_quantize(data["w"].astype(np.float64), residual=False)
     zr, bound = orc.hif4_gemm(oq[0], oq[1], oq[2], oq[3], ow[0], ow[1])
-    assert_gemm_close(z, zr, bound, False, "hif4 wide tiles")
+    assert_gemm_close(z, zr, bound, out_dtype == torch.bfloat16, "hif4 wide tiles")
