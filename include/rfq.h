@@ -55,7 +55,11 @@
 extern "C" {
 #endif
 
-typedef enum {
+/* Status codes and dtype codes are 32-bit integers with named values (not
+ * enum types), so that every value a caller passes or receives is defined
+ * behaviour in C and in C++; unknown values are rejected or named as such. */
+typedef int32_t rfq_status;
+enum {
     RFQ_OK = 0,
     RFQ_ERR_NULL = 1,    /* a required pointer is NULL, or an optional pair is half given */
     RFQ_ERR_SHAPE = 2,   /* negative size, K < 32 or not a multiple of 32, or a size limit */
@@ -63,19 +67,20 @@ typedef enum {
     RFQ_ERR_ALIGN = 4,   /* a pointer violates the alignment stated for it */
     RFQ_ERR_DEVICE = 5,  /* no current HIP device, or it is not gfx950 */
     RFQ_ERR_LAUNCH = 6   /* a kernel launch failed */
-} rfq_status;
+};
 
-typedef enum {
+typedef int32_t rfq_dtype;
+enum {
     RFQ_F32 = 0,   /* IEEE binary32 */
     RFQ_BF16 = 1   /* bfloat16 (upper half of a binary32) */
-} rfq_dtype;
+};
 
 /* Rules that build a fallback-indicator map (the paper defines phi(p, r) as
  * an input of Algorithm 1 but gives no rule; these two are this library's). */
-typedef enum {
+enum {
     RFQ_PHI_RESIDUAL_NONZERO = 0,   /* phi = 1 where a residual code of the tile is nonzero */
     RFQ_PHI_SCALE_AT_LEAST = 1      /* phi = 1 where a primary scale byte of the tile >= threshold */
-} rfq_phi_rule;
+};
 
 /*
  * RFQ activation quantizer: primary code Q(X) (Eq. 8) and, when r_codes and

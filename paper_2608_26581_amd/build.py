@@ -20,9 +20,10 @@ def sources():
     return sorted(glob.glob(os.path.join(PKG_DIR, "csrc", "*.hip")))
 
 
-def build(verbose=False, extra_flags=()):
-    """Compile every source under csrc/ into librfq.so (always recompiles)."""
-    tmp = LIB_PATH + ".tmp"
+def build(verbose=False, extra_flags=(), out=LIB_PATH):
+    """Compile every source under csrc/ into librfq.so, or into `out` with
+    extra compiler flags (always recompiles)."""
+    tmp = out + ".tmp"
     cmd = [HIPCC, *FLAGS, *extra_flags,
            "-I", os.path.join(REPO_DIR, "include"),
            "-I", os.path.join(PKG_DIR, "csrc"),
@@ -36,8 +37,8 @@ def build(verbose=False, extra_flags=()):
         raise RuntimeError("librfq build failed:\n" + err)
     if verbose and err.strip():
         print(err)
-    os.replace(tmp, LIB_PATH)
-    return LIB_PATH
+    os.replace(tmp, out)
+    return out
 
 
 if __name__ == "__main__":
