@@ -35,7 +35,7 @@ PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 matrix cores
 N_SETS = 3
 Q_SETS = 9                    # 9 x 64 MiB quantizer inputs: over twice the 256 MB last-level cache
-PHI_MARGIN = 4                # scale-threshold phi: median primary scale byte + 4
+PHI_MARGINS = (2, 4, 6)       # scale-threshold phi: median primary scale byte + margin
 METRIC = "RFQ-MXFP4 GEMM TFLOP/s + quantizer GB/s (Qwen3-VL-like 4096×4096×12288)"
 
 
@@ -348,17 +348,22 @@ def secondary(torch, rfq, wl, x, w, stream):
     except (AttributeError, RuntimeError, ValueError, NotImplementedError) as e:
         out["hipblaslt_mxfp4_scaled_mm"] = {"unavailable": str(e)[:120]}
     # Fallback indicator by the scale-threshold rule (phi = 1 on tiles holding
-    # a primary scale byte >= the median + PHI_MARGIN): residual MFMAs only
-    # where outliers are.
-    thr = int(q[1].float().median().item()) + PHI_MARGIN
-    phi = rfq.rfq_fallback_map(None, q[1], rfq.RFQ_PHI_SCALE_AT_LEAST, thr)
-    ms = _per_launch_ms(torch, stream, lambda i: rfq.rfq_gemm_phi(
-        *q, *wq, phi, out=z, stream=stream), 20)
-    on = float(phi.float().mean().item())
-    out["rfq_gemm_phi_scale_threshold"] = {
-        "ms": round(ms, 5), "threshold_byte": thr, "tiles_on": round(on, 4),
-        "exec_tflops": round((2.0 + 2.0 * on) * M * N * K / ms / 1e9, 1)}
-    del q, z, wt, phi
+    # a primary scale byte >= the median + margin): residual work only where
+    # outliers are, at three thresholds; exec_tflops counts the MFMA work
+    # done (2MNK plus 2MNK times the fraction of tiles on).
+    med = int(q[1].float().median().item())
+    sweep = []
+    for margin in PHI_MARGINS:
+        phi = rfq.rfq_fallback_map(None, q[1], rfq.RFQ_PHI_SCALE_AT_LEAST, med + margin)
+        ms = _per_launch_ms(torch, stream, lambda i: rfq.rfq_gemm_phi(
+            *q, *wq, phi, out=z, stream=stream), 20)
+        on = float(phi.float().mean().item())
+        sweep.append({"margin": margin, "threshold_byte": med + margin, "tiles_on": round(on, 4),
+                      "ms": round(ms, 5),
+                      "exec_tflops": round((2.0 + 2.0 * on) * M * N * K / ms / 1e9, 1)})
+        del phi
+    out["rfq_gemm_phi_scale_threshold"] = sweep
+    del q, z, wt
 
     # HiF4 form (64-element blocks, E6M2 macro scale, micro-exponents): the
     # quantizer (primary + residual of the bf16 activations) and the product,
@@ -531,9 +536,10 @@ def accuracy(torch, rfq, x, w, nrows=64):
         "plain_mxfp4": rel(rfq.rfq_gemm(q[0], q[1], None, None, *wq)),
         "rfq": rel(rfq.rfq_gemm(*q, *wq)),
     }
-    thr = int(q[1].float().median().item()) + PHI_MARGIN
-    phi = rfq.rfq_fallback_map(None, q[1], rfq.RFQ_PHI_SCALE_AT_LEAST, thr)
-    out["rfq_phi_scale_threshold"] = rel(rfq.rfq_gemm_phi(*q, *wq, phi))
+    med = int(q[1].float().median().item())
+    for margin in PHI_MARGINS:
+        phi = rfq.rfq_fallback_map(None, q[1], rfq.RFQ_PHI_SCALE_AT_LEAST, med + margin)
+        out["rfq_phi_scale_threshold_margin%d" % margin] = rel(rfq.rfq_gemm_phi(*q, *wq, phi))
     hq = rfq.rfq_hif4_quantize(x)
     hw = rfq.rfq_hif4_quantize(w, residual=False)
     out["plain_hif4"] = rel(rfq.rfq_hif4_gemm(hq[0], hq[1], None, None, hw[0], hw[1]))

@@ -297,11 +297,22 @@ __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
   // stages) of this thread's scale rows.
   u32x4 pf[L::kLoads];
   u32x4 grp[L::kScaleLoads];
-  auto load_stage = [&](int st) {
+  // Offset of a skipped load: at or past the end of any operand below
+  // 2 GiB of codes (for larger operands it may land inside the buffer,
+  // which only costs the fetch: the data is never read).
+  constexpr uint32_t kSkipOffset = 0x80000000u;
+  // Residual row block b of a stage is fetched only where bit b of rmask
+  // is set (fallback-indicator path); otherwise its load gets an offset
+  // past the end of the buffer, which the buffer range check turns into
+  // zeros without a memory access (the block's LDS rows are then never
+  // read).
+  auto load_stage = [&](int st, int rmask) {
 #pragma unroll
     for (int u = 0; u < L::kLoads; ++u) {
       const int o = op_of(u);
-      const uint32_t off = o == 2 ? w_off[u - L::kWRow / kRPL] : a_off[u % (kBM / kRPL)];
+      uint32_t off = o == 2 ? w_off[u - L::kWRow / kRPL] : a_off[u % (kBM / kRPL)];
+      if constexpr (PHI && RES)
+        if (o == 1) off = ((rmask >> (u - kBM / kRPL)) & 1) ? off : kSkipOffset;
       pf[u] = __builtin_amdgcn_raw_buffer_load_b128(o == 0 ? cq : (o == 1 ? cr : cw), off,
                                                     st * kRowBytes, 0);
     }
@@ -336,10 +347,16 @@ __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
     for (int j = 0; j < kFN; ++j)
       f.w[j] = *reinterpret_cast<const u32x4 *>(lds(buf) + chunk_off(wrow(j), 2 * h + s));
   };
-  auto read_a = [&](int buf, int s, int i, AFrag &f) {
+  auto read_q = [&](int buf, int s, int i, AFrag &f) {
     f.q = *reinterpret_cast<const u32x4 *>(lds(buf) + chunk_off(qrow(i), 2 * h + s));
+  };
+  auto read_r = [&](int buf, int s, int i, AFrag &f) {
     if constexpr (RES)
       f.r = *reinterpret_cast<const u32x4 *>(lds(buf) + chunk_off(kBM + qrow(i), 2 * h + s));
+  };
+  auto read_a = [&](int buf, int s, int i, AFrag &f) {
+    read_q(buf, s, i, f);
+    read_r(buf, s, i, f);
   };
   auto read_scales = [&](int buf, Scales<RES> &sc) {
     const uint8_t *b = lds(buf) + L::kDataBytes + 2 * h;
@@ -392,25 +409,38 @@ __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
   using Rl = std::integral_constant<bool, true>;
   using NoRl = std::integral_constant<bool, false>;
 
-  // The fallback-indicator rows of this workgroup's wave rows, copied
-  // to LDS behind the stage buffers (the prologue's barrier publishes them).
+  // The fallback-indicator bytes of this workgroup's four wave rows, copied
+  // to LDS behind the stage buffers, four per reduction tile (one 32-bit
+  // word per tile; the prologue's barrier publishes them).
   const int pcols = (int)((K + kPhiK - 1) / kPhiK);
   uint8_t *phi_lds = smem + L::kBytes;
   if constexpr (PHI) {
     const int64_t prow0 = m0 / kPhiRows, prows = (M + kPhiRows - 1) / kPhiRows;
     for (int i = tid; i < kWaveRows * pcols; i += kThreads) {
-      const int64_t pr = prow0 + i / pcols;
-      phi_lds[i] = pr < prows ? phi[pr * pcols + i % pcols] : (uint8_t)0;
+      const int64_t pr = prow0 + i % kWaveRows;
+      phi_lds[i] = pr < prows ? phi[pr * pcols + i / kWaveRows] : (uint8_t)0;
     }
   }
   const int wm_u = __builtin_amdgcn_readfirstlane(wm);
-
+  // This thread's residual row blocks (u = kBM / kRPL + b) belong to wave
+  // rows lw and lw + 2, b = 0, 1: rows 16 wave + 128 b of the residual tile.
+  const int lw = __builtin_amdgcn_readfirstlane(wave >> 2);
+  auto phi_word = [&](int st) -> uint32_t {
+    return __builtin_amdgcn_readfirstlane(
+        *reinterpret_cast<const uint32_t *>(phi_lds + kWaveRows * (st / 2)));
+  };
+  // Bit b: the residual row block b of stage st is needed.
+  auto res_mask = [&](int st) -> int {
+    const uint32_t w = phi_word(st);
+    return (((w >> (8 * lw)) & 0xFFu) ? 1 : 0) | (((w >> (8 * (lw + 2))) & 0xFFu) ? 2 : 0);
+  };
   // ---- prologue: stage 0 into buffer 0, stage 1 in registers.
+  if constexpr (PHI) __syncthreads();   // the indicator words
   load_group(0);
-  load_stage(0);
+  load_stage(0, PHI ? res_mask(0) : 3);
   store_stage(0, W0{});
   __builtin_amdgcn_sched_barrier(0);
-  load_stage(min(1, nstages - 1));
+  load_stage(min(1, nstages - 1), PHI ? res_mask(min(1, nstages - 1)) : 3);
   asm volatile("" ::: "memory");
   __syncthreads();
 
@@ -428,15 +458,19 @@ __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
   // barrier that ended stage st-1; then fetch stage st+2.  With a
   // fallback-indicator map, each k-step issues the primary MFMAs of both
   // rows (the writes and loads spread between them) and then, where the
-  // wave's indicator `on` is set, the residual MFMAs.
+  // wave's indicator `on` is set, the residual MFMAs; residual row blocks
+  // that no wave row of the workgroup needs are not fetched.
   auto stage = [&](int st, auto handover_tag, auto word_tag, auto reload_tag) {
     constexpr bool HANDOVER = decltype(handover_tag)::value;
     constexpr bool RELOAD = decltype(reload_tag)::value;
     const int buf = st & 1, nbuf = buf ^ 1;
     constexpr int kW = HANDOVER ? L::kLoads + L::kScaleLoads : 0;
     constexpr int kV = (HANDOVER ? L::kLoads : 0) + (RELOAD ? L::kScaleLoads : 0);
-    int on = 1;
-    if constexpr (PHI) on = __builtin_amdgcn_readfirstlane((int)phi_lds[wm_u * pcols + st / 2]);
+    int on = 1, lmask = 3;
+    if constexpr (PHI) {
+      on = (phi_word(st) >> (8 * wm_u)) & 0xFFu;
+      if constexpr (HANDOVER) lmask = res_mask(min(st + 2, nstages - 1));
+    }
     WFrag w;
     AFrag a0, a1;
     Scales<RES> sc;
@@ -464,7 +498,7 @@ __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
     region_end();
 
     if constexpr (RELOAD) load_group((st + 2) / kGroup);
-    if constexpr (HANDOVER) load_stage(min(st + 2, nstages - 1));
+    if constexpr (HANDOVER) load_stage(min(st + 2, nstages - 1), lmask);
     WFrag w1;
     AFrag b0, b1;
     read_w(buf, 1, w1);

@@ -522,6 +522,7 @@ def test_plain_mxfp4_agrees_with_hipblaslt(orc):
 PHI_SHAPES = [
     ("qwen", 200, 328, 1024),       # large-tile kernel, ragged M and N
     ("qwen", 129, 257, 2560),       # large-tile kernel, ragged indicator rows
+    ("qwen", 512, 300, 2048),       # large-tile kernel, two full workgroup rows
     ("qwen", 200, 328, 1056),       # general kernel, K not a multiple of 256
     ("wan", 64, 96, 640),           # general kernel
 ]
@@ -538,15 +539,22 @@ def _phi_case(name, M, N, K, seed):
 @pytest.mark.parametrize("name,M,N,K", PHI_SHAPES)
 @pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
 def test_gemm_phi_random_maps(orc, name, M, N, K, out_dtype):
-    """Eq. 11 with a given phi map against the oracle; phi = 1 and phi = 0
-    give exactly the RFQ and the plain products."""
+    """Eq. 11 with a given phi map against the oracle: random maps at three
+    densities, maps constant along rows or along columns (whole residual row
+    blocks of a stage skipped, or whole stages), and arbitrary nonzero bytes
+    (any nonzero byte means on); phi = 1 and phi = 0 give exactly the RFQ
+    and the plain products."""
     q, wq = _phi_case(name, M, N, K, 21)
     hq = [host(t) for t in q] + [host(t) for t in wq]
     rng = np.random.default_rng(M + K)
     shape = ((M + 63) // 64, (K + 255) // 256)
     _say("phi %s M=%d N=%d K=%d %s" % (name, M, N, K, out_dtype))
-    for trial in range(3):
-        phi = rng.integers(0, 2, shape).astype(np.uint8)
+    maps = [rng.random(shape) < p for p in (0.25, 0.5, 0.75)]
+    maps.append(np.repeat(rng.integers(0, 2, (1, shape[1])), shape[0], 0))
+    maps.append(np.repeat(rng.integers(0, 2, (shape[0], 1)), shape[1], 1))
+    maps.append(rng.integers(0, 256, shape))
+    for trial, phi in enumerate(maps):
+        phi = np.ascontiguousarray(phi).astype(np.uint8)
         z = rfq.rfq_gemm_phi(*q, *wq, torch.from_numpy(phi).cuda(), out_dtype=out_dtype)
         zr, bound = orc.gemm_phi(*hq, phi)
         zg = host_bf16_as_f32(z) if out_dtype == torch.bfloat16 else host(z)
