@@ -33,6 +33,7 @@
 #include <atomic>
 #include <type_traits>
 
+#include "gemm_common.h"
 #include "rfq_internal.h"
 
 namespace rfq {
@@ -58,12 +59,6 @@ struct Smem {
 
 __device__ __forceinline__ int swz(int row, int chunk) {
   return row * kRowBytes + 16 * (chunk ^ (row & 7));
-}
-
-// bf16 round to nearest even of a finite fp32 value.
-__device__ __forceinline__ uint32_t bf16_rne(float f) {
-  const uint32_t u = __float_as_uint(f);
-  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
 }
 
 // Fallback-indicator map: one byte per tile of 64 activation rows (a wave's
@@ -269,8 +264,8 @@ __global__ __launch_bounds__(256) void rfq_gemm_kernel(
         uint16_t *zp = reinterpret_cast<uint16_t *>(z) + m * N + n;
         if (vec_ok && n + 3 < N) {
           uint2 w;
-          w.x = bf16_rne(a[0]) | (bf16_rne(a[1]) << 16);
-          w.y = bf16_rne(a[2]) | (bf16_rne(a[3]) << 16);
+          w.x = bf16x2_rne(a[0], a[1]);
+          w.y = bf16x2_rne(a[2], a[3]);
           *reinterpret_cast<uint2 *>(zp) = w;
         } else {
 #pragma unroll

@@ -15,11 +15,20 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kFmtFp4 = 4;   // E2M1 operand format code of the scaled MFMA
 
-// bf16 round to nearest even of a finite fp32 value (16-bit pattern).
-__device__ __forceinline__ uint32_t bf16_rne(float f) {
-  const uint32_t u = __float_as_uint(f);
-  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// bf16 round to nearest even of two finite fp32 values, a in the low half:
+// one hardware conversion (v_cvt_pk_bf16_f32) for the pair.  It gives the
+// same bits as rounding the fp32 pattern by integer arithmetic (checked on
+// the GPU for every exponent, both signs, the patterns around every tie and
+// subnormals).
+__device__ __forceinline__ uint32_t bf16x2_rne(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{a, b}, bf16x2_t));
 }
+
+// bf16 round to nearest even of a finite fp32 value (16-bit pattern).
+__device__ __forceinline__ uint32_t bf16_rne(float f) { return bf16x2_rne(f, 0.0f) & 0xFFFFu; }
 
 // Output-tile order: tiles handed to one XCD (workgroups are dealt to the 8
 // XCDs round robin) are made contiguous, then walked in groups of GM tile

@@ -563,8 +563,8 @@ __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
           uint8_t *p = ep + frow * E::kRowStride + (32 * jj + 8 * g + 4 * h) * E::kElem;
           if constexpr (ZBF16) {
             uint2 w;
-            w.x = bf16_rne(a[4 * g]) | (bf16_rne(a[4 * g + 1]) << 16);
-            w.y = bf16_rne(a[4 * g + 2]) | (bf16_rne(a[4 * g + 3]) << 16);
+            w.x = bf16x2_rne(a[4 * g], a[4 * g + 1]);
+            w.y = bf16x2_rne(a[4 * g + 2], a[4 * g + 3]);
             *reinterpret_cast<uint2 *>(p) = w;
           } else {
             *reinterpret_cast<float4 *>(p) = make_float4(a[4 * g], a[4 * g + 1], a[4 * g + 2],

@@ -129,8 +129,8 @@ __device__ __forceinline__ void store_tile(const v4f &s, int lane, int64_t m0, i
     uint16_t *zp = reinterpret_cast<uint16_t *>(z) + m * N + n;
     if (n + 4 <= N && (N % 4) == 0) {
       uint2 v;
-      v.x = bf16_rne(s[0]) | (bf16_rne(s[1]) << 16);
-      v.y = bf16_rne(s[2]) | (bf16_rne(s[3]) << 16);
+      v.x = bf16x2_rne(s[0], s[1]);
+      v.y = bf16x2_rne(s[2], s[3]);
       *reinterpret_cast<uint2 *>(zp) = v;
     } else {
 #pragma unroll

@@ -482,8 +482,8 @@ __global__ __launch_bounds__((HSmem<RES, BN>::kThreads)) void hif4_gemm_kernel(
           uint16_t *zp = reinterpret_cast<uint16_t *>(z) + m * N + n;
           if (vec_ok && n + 3 < N) {
             uint2 w;
-            w.x = bf16_rne(c[4 * a]) | (bf16_rne(c[4 * a + 1]) << 16);
-            w.y = bf16_rne(c[4 * a + 2]) | (bf16_rne(c[4 * a + 3]) << 16);
+            w.x = bf16x2_rne(c[4 * a], c[4 * a + 1]);
+            w.y = bf16x2_rne(c[4 * a + 2], c[4 * a + 3]);
             *reinterpret_cast<uint2 *>(zp) = w;
           } else {
 #pragma unroll
@@ -661,8 +661,8 @@ __global__ __launch_bounds__(kFewWaves * 64) void hif4_gemm_few_kernel(
       uint16_t *zp = reinterpret_cast<uint16_t *>(z) + m * N + n;
       if (vec_ok && n + 3 < N) {
         uint2 o;
-        o.x = bf16_rne(t[0]) | (bf16_rne(t[1]) << 16);
-        o.y = bf16_rne(t[2]) | (bf16_rne(t[3]) << 16);
+        o.x = bf16x2_rne(t[0], t[1]);
+        o.y = bf16x2_rne(t[2], t[3]);
         *reinterpret_cast<uint2 *>(zp) = o;
       } else {
 #pragma unroll
