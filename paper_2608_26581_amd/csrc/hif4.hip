@@ -466,17 +466,23 @@ __global__ __launch_bounds__((HSmem<RES, BN>::kThreads)) void hif4_gemm_kernel(
   }
 
   // ---- epilogue: lane holds Z[m][n .. n+3] for n = 8a + 4 half (a = 0..3)
-  // of each fragment (weights are the first MFMA operand).
+  // of each fragment (weights are the first MFMA operand).  The lane's row
+  // and column origins are formed here from the thread index rather than
+  // kept from before the loop (that value is otherwise held across the
+  // loop at the register limit).
   const bool vec_ok = (N & 3) == 0;
+  const int elane = __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+  const int64_t erow0 = m0 + wmi * kTM + (elane & 31);
+  const int64_t ecol0 = n0 + wni * kTN + 4 * (elane >> 5);
 #pragma unroll
   for (int i = 0; i < kFM; ++i) {
-    const int64_t m = m0 + wmi * kTM + 32 * i + frow;
+    const int64_t m = erow0 + 32 * i;
     if (m >= M) continue;
 #pragma unroll
     for (int j = 0; j < kFN; ++j) {
 #pragma unroll
       for (int a = 0; a < 4; ++a) {
-        const int64_t n = n0 + wni * kTN + 32 * j + 8 * a + 4 * half;
+        const int64_t n = ecol0 + 32 * j + 8 * a;
         const v16f &c = acc[i][j];
         if constexpr (ZBF16) {
           uint16_t *zp = reinterpret_cast<uint16_t *>(z) + m * N + n;
