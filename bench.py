@@ -272,11 +272,25 @@ def recorded_traffic(path=TRAFFIC_RECORD):
     return rec
 
 
-def _per_launch_ms(torch, stream, fn, reps):
-    """Mean time of `reps` back-to-back launches between one pair of events."""
-    for i in range(2):
-        fn(i)
-    torch.cuda.synchronize()
+# Seconds of back-to-back launches before a secondary measurement: on MI355X
+# the clock drops a few milliseconds into sustained matrix-core load and
+# settles again over the following ~100 ms, so every variant is timed in the
+# settled state (the headline steps get their own --warmup instead).
+SETTLE_S = 0.12
+
+
+def _per_launch_ms(torch, stream, fn, reps, settle_s=SETTLE_S):
+    """Mean time of `reps` back-to-back launches between one pair of events,
+    after the same launches have run back to back for settle_s seconds."""
+    t0 = time.perf_counter()
+    i = 0
+    while True:
+        for _ in range(8):
+            fn(i)
+            i += 1
+        torch.cuda.synchronize()
+        if time.perf_counter() - t0 >= settle_s:
+            break
     a = torch.cuda.Event(enable_timing=True)
     b = torch.cuda.Event(enable_timing=True)
     a.record(stream)
