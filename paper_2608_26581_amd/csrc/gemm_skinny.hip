@@ -10,8 +10,9 @@
 //
 // With few rows the product is bound by streaming W's codes from memory, and
 // the large-tile kernels (256 activation rows per tile) would leave most of the
-// chip idle.  Here a workgroup owns 32 rows of W (two fragments; one in the
-// streaming form) and up to four 16-row activation slices, and its four waves
+// chip idle.  Here a workgroup owns 32 rows of W (two fragments; one where
+// that gives too few workgroups or for up to 4 activation rows, and one in
+// the streaming form) and up to four 16-row activation slices, and its four waves
 // split K into four contiguous ranges; the partial 16 x 16 results of the
 // waves are summed in a fixed order through LDS.  W is read once per 64
 // activation rows.
@@ -166,29 +167,29 @@ __device__ __forceinline__ void reduce_store(v4f (&partial)[kSkThreads / 64][64]
   store_tile<ZBF16>(s, lane, m0, n0, M, N, z);
 }
 
-// Codes in: a workgroup owns kSkFrags fragments of W (32 rows) and up to S
+// Codes in: a workgroup owns F fragments of W (16 F rows) and up to S
 // activation slices of 16 rows.  Each wave holds a group of W in registers
 // while it multiplies every slice against it, so W is read once per launch
-// (for M <= 16 S) and the activation codes once per 32 W rows.  The next
+// (for M <= 16 S) and the activation codes once per 16 F W rows.  The next
 // slice's codes (or the next group's first slice) are loaded while the
 // current one is multiplied.  Per output the accumulation order is that of
 // a single slice: groups, k-steps, primary then residual, then the
 // fixed-order sum over the four waves.
-constexpr int kSkFrags = 2;
-struct WPair { WGroup f[kSkFrags]; };
+template <int F>
+struct WPair { WGroup f[F]; };
 
-template <bool RES, bool ZBF16, int S>
-__global__ __launch_bounds__(kSkThreads, 2) void rfq_gemm_skinny_kernel(
+template <bool RES, bool ZBF16, int S, int F>
+__global__ __launch_bounds__(kSkThreads, F == 1 ? 3 : 2) void rfq_gemm_skinny_kernel(
     const uint8_t *__restrict__ qc, const uint8_t *__restrict__ qs,
     const uint8_t *__restrict__ rc, const uint8_t *__restrict__ rs,
     const uint8_t *__restrict__ wc, const uint8_t *__restrict__ ws, int64_t M, int64_t N,
     int64_t K, void *__restrict__ z) {
-  __shared__ v4f partial[kSkThreads / 64][kSkFrags * S][64];
+  __shared__ v4f partial[kSkThreads / 64][F * S][64];
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int row = lane & 15, g = lane >> 4;
-  const int64_t n0 = (int64_t)blockIdx.x * (kSkFrags * kSkRows);
+  const int64_t n0 = (int64_t)blockIdx.x * (F * kSkRows);
   const int64_t m0 = (int64_t)blockIdx.y * (S * kSkRows);
   const int slices = (int)min<int64_t>(S, (M - m0 + kSkRows - 1) / kSkRows);
   const int64_t kbytes = K / 2, kblocks = K / 32;
@@ -198,16 +199,16 @@ __global__ __launch_bounds__(kSkThreads, 2) void rfq_gemm_skinny_kernel(
   const int gb = (ngroups * wave) / 4, ge = (ngroups * (wave + 1)) / 4;
 
   const __amdgpu_buffer_rsrc_t rwc = rsrc(wc, N * kbytes), rws = rsrc(ws, N * kblocks);
-  uint32_t w_off[kSkFrags], ws_off[kSkFrags];
+  uint32_t w_off[F], ws_off[F];
 #pragma unroll
-  for (int f = 0; f < kSkFrags; ++f) {
+  for (int f = 0; f < F; ++f) {
     const int64_t wn = min(n0 + kSkRows * f + row, N - 1);
     w_off[f] = (uint32_t)wn * (uint32_t)kbytes + 16 * g;
     ws_off[f] = (uint32_t)wn * (uint32_t)kblocks;
   }
-  auto load_w = [&](WPair &w, int gi) {
+  auto load_w = [&](WPair<F> &w, int gi) {
 #pragma unroll
-    for (int f = 0; f < kSkFrags; ++f) {
+    for (int f = 0; f < F; ++f) {
 #pragma unroll
       for (int j = 0; j < 4; ++j)
         w.f[f].c[j] = __builtin_amdgcn_raw_buffer_load_b128(rwc, w_off[f],
@@ -235,17 +236,17 @@ __global__ __launch_bounds__(kSkThreads, 2) void rfq_gemm_skinny_kernel(
       xg.rs = __builtin_amdgcn_raw_buffer_load_b128(rxt, xs_off, gi * (kSkGroupK / 32), 0);
   };
 
-  v4f acc[S][kSkFrags];
+  v4f acc[S][F];
 #pragma unroll
   for (int sl = 0; sl < S; ++sl)
 #pragma unroll
-    for (int f = 0; f < kSkFrags; ++f) acc[sl][f] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+    for (int f = 0; f < F; ++f) acc[sl][f] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
 
-  auto compute = [&](const WPair &w, const XGroup &xg, v4f (&a)[kSkFrags]) {
+  auto compute = [&](const WPair<F> &w, const XGroup &xg, v4f (&a)[F]) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
 #pragma unroll
-      for (int f = 0; f < kSkFrags; ++f) {
+      for (int f = 0; f < F; ++f) {
         const uint32_t wsc = scale_of(w.f[f].s, j, g);
         a[f] = mma16(w.f[f].c[j], wsc, xg.q[j], scale_of(xg.qs, j, g), a[f]);
         if constexpr (RES) a[f] = mma16(w.f[f].c[j], wsc, xg.r[j], scale_of(xg.rs, j, g), a[f]);
@@ -258,7 +259,7 @@ __global__ __launch_bounds__(kSkThreads, 2) void rfq_gemm_skinny_kernel(
   // the other buffer before the current one is waited for.  Slices past M
   // load zeros without touching memory and skip their MFMAs.  With S even
   // the next group again starts in xa; with S = 1 the buffers swap roles.
-  auto group = [&](const WPair &w, int gi, XGroup &xa, XGroup &xb) {
+  auto group = [&](const WPair<F> &w, int gi, XGroup &xa, XGroup &xb) {
 #pragma unroll
     for (int sl = 0; sl < S; ++sl) {
       XGroup &cur = (sl & 1) ? xb : xa;
@@ -269,7 +270,7 @@ __global__ __launch_bounds__(kSkThreads, 2) void rfq_gemm_skinny_kernel(
     }
   };
   if (gb < ge) {
-    WPair w0, w1;
+    WPair<F> w0, w1;
     XGroup xa, xb;
     load_w(w0, gb);
     load_x(xa, gb, 0);
@@ -287,11 +288,11 @@ __global__ __launch_bounds__(kSkThreads, 2) void rfq_gemm_skinny_kernel(
   // Fixed-order sum over the four waves; output (fragment f, slice sl) is
   // summed and stored by wave (f S + sl) mod 4.
 #pragma unroll
-  for (int f = 0; f < kSkFrags; ++f)
+  for (int f = 0; f < F; ++f)
 #pragma unroll
     for (int sl = 0; sl < S; ++sl) partial[wave][f * S + sl][lane] = acc[sl][f];
   __syncthreads();
-  for (int p = wave; p < kSkFrags * S; p += kSkThreads / 64) {
+  for (int p = wave; p < F * S; p += kSkThreads / 64) {
     const int f = p / S, sl = p % S;
     if (sl >= slices) continue;
     v4f s = partial[0][p][lane];
@@ -496,26 +497,38 @@ __global__ __launch_bounds__(kSkThreads, XF32 ? 1 : 2) void rfq_gemm_stream_kern
   }
 }
 
-template <bool RES, bool ZBF16, int S>
+template <bool RES, bool ZBF16, int S, int F = 2>
 hipError_t launch_sk_s(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc, const uint8_t *rs,
                        const uint8_t *wc, const uint8_t *ws, int64_t M, int64_t N, int64_t K,
                        void *z, hipStream_t stream) {
-  const dim3 grid((unsigned)((N + kSkFrags * kSkRows - 1) / (kSkFrags * kSkRows)),
+  const dim3 grid((unsigned)((N + F * kSkRows - 1) / (F * kSkRows)),
                   (unsigned)((M + S * kSkRows - 1) / (S * kSkRows)));
-  rfq_gemm_skinny_kernel<RES, ZBF16, S><<<grid, dim3(kSkThreads), 0, stream>>>(
+  rfq_gemm_skinny_kernel<RES, ZBF16, S, F><<<grid, dim3(kSkThreads), 0, stream>>>(
       qc, qs, rc, rs, wc, ws, M, N, K, z);
   return hipGetLastError();
 }
 
 // Slices per workgroup: the fewest of 1, 2 or 4 that cover M's rows, at most
 // 4 (more slices per workgroup make the kernel spill, measured slower).
+// Weight fragments per workgroup: one (16 rows, twice the workgroups) for up
+// to 4 activation rows (whose loads are then negligible) and where two would
+// leave CUs without a workgroup; else two (the activation codes are then
+// loaded once per 32 weight rows).  Measured on MI355X at 12288 x 4096 and
+// 4096 x 12288 weights: 8 - 26% faster where chosen, slower elsewhere.
+constexpr int64_t kFillWorkgroups = 256;    // one per CU on MI355X
 template <bool RES, bool ZBF16>
 hipError_t launch_sk(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc, const uint8_t *rs,
                      const uint8_t *wc, const uint8_t *ws, int64_t M, int64_t N, int64_t K,
                      void *z, hipStream_t stream) {
-  if (M <= kSkRows) return launch_sk_s<RES, ZBF16, 1>(qc, qs, rc, rs, wc, ws, M, N, K, z, stream);
-  if (M <= 2 * kSkRows) return launch_sk_s<RES, ZBF16, 2>(qc, qs, rc, rs, wc, ws, M, N, K, z, stream);
-  return launch_sk_s<RES, ZBF16, 4>(qc, qs, rc, rs, wc, ws, M, N, K, z, stream);
+  auto narrow = [&](int64_t S) {
+    const int64_t wgs = ((N + 2 * kSkRows - 1) / (2 * kSkRows)) * ((M + S * kSkRows - 1) / (S * kSkRows));
+    return M <= 4 || wgs < kFillWorkgroups;
+  };
+#define RFQ_SK(S, F) launch_sk_s<RES, ZBF16, S, F>(qc, qs, rc, rs, wc, ws, M, N, K, z, stream)
+  if (M <= kSkRows) return narrow(1) ? RFQ_SK(1, 1) : RFQ_SK(1, 2);
+  if (M <= 2 * kSkRows) return narrow(2) ? RFQ_SK(2, 1) : RFQ_SK(2, 2);
+  return narrow(4) ? RFQ_SK(4, 1) : RFQ_SK(4, 2);
+#undef RFQ_SK
 }
 
 template <bool RES, bool ZBF16, bool XF32, int S>

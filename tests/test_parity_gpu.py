@@ -303,6 +303,9 @@ GEMM_SMALL = [
     ("qwen", 128, 260, 512),          # the few-row kernel's largest M
     ("wan", 64, 200, 5120),           # K range split unevenly over the waves
     ("qwen", 5, 1, 512),
+    # enough weight rows for 32 per workgroup (16 elsewhere), ragged
+    ("qwen", 16, 8200, 512),
+    ("qwen", 40, 8200, 512),
 ]
 
 
@@ -411,7 +414,7 @@ def test_gemm_stream_bit_identical_to_quantize_then_gemm(M, N, K, residual):
 
 
 @pytest.mark.parametrize("M,N,K", [(1, 12288, 4096), (16, 12288, 4096), (8, 4096, 12288),
-                                   (100, 4096, 4096)])
+                                   (100, 4096, 4096), (64, 4096, 12288)])
 def test_decode_shapes_full(orc, M, N, K):
     """Decode-sized products at the workloads' weight shapes, every output
     checked, in both forms (codes in and streaming)."""
