@@ -195,8 +195,12 @@ rfq_status rfq_fallback_map(const uint8_t *r_codes, const uint8_t *q_scales, int
  * per 32 hidden units, g and u are the bf16 roundings of Z's gate and up
  * columns, h = bf16(silu(g) * u) as in rfq_swiglu_quantize_act, and Q(h),
  * Q(h - deq Q(h)) (Eq. 8-10) are written.  Neither Z nor g and u reach
- * memory.  The codes are bit-identical to rfq_gemm with bf16 Z (gate and up
- * columns) followed by rfq_swiglu_quantize_act.
+ * memory.  For M > 128 the codes are bit-identical to rfq_gemm with bf16 Z
+ * (gate and up columns) followed by rfq_swiglu_quantize_act, which then runs
+ * the same product kernel; with up to 128 rows rfq_gemm runs its few-row
+ * kernel, whose fp32 summation order differs, so g or u, and through them h
+ * and its codes, can differ where a bf16 rounding boundary lies between the
+ * two sums (both stay within the product's tolerance).
  *   q_codes, q_scales, r_codes, r_scales: activation codes as for rfq_gemm
  *            ([M][K/2], [M][K/32]; residual pair optional, NULL gives phi = 0).
  *   wgu_codes [2 Nh][K/2], wgu_scales [2 Nh][K/32]: quantized weights whose

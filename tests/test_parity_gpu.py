@@ -643,8 +643,17 @@ def _fused_and_unfused(data, K, Nh, res_in, res_out, stages=None):
     q = rfq.rfq_quantize_act(x_device(data), residual=res_in)
     wg = rfq.rfq_quantize_weight(dev(data["w_gate"]))
     wu = rfq.rfq_quantize_weight(dev(data["w_up"]))
-    g = rfq.rfq_gemm(*q, *wg, out_dtype=torch.bfloat16)
-    u = rfq.rfq_gemm(*q, *wu, out_dtype=torch.bfloat16)
+    # The fused path runs the large-tile product; rfq_gemm does so above 128
+    # rows.  Below, its reference runs on codes zero-padded to 129 rows (rows
+    # are independent: padding changes no output of the real rows).
+    M = q[0].shape[0]
+    qg = q
+    if M <= 128:
+        qg = [None if t is None else torch.cat([t, torch.zeros((129 - M, t.shape[1]),
+                                                               dtype=t.dtype, device=t.device)])
+              for t in q]
+    g = rfq.rfq_gemm(*qg, *wg, out_dtype=torch.bfloat16)[:M].contiguous()
+    u = rfq.rfq_gemm(*qg, *wu, out_dtype=torch.bfloat16)[:M].contiguous()
     ref = rfq.rfq_swiglu_quantize_act(g, u, residual=res_out, return_h=True)
     if stages is not None:
         stages.update(q=[None if t is None else host(t) for t in q],
