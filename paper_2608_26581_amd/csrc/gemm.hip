@@ -57,8 +57,13 @@ struct Smem {
   static constexpr int kBytes = 2 * kStageBytes;
 };
 
+// LDS serves a 16-byte access of 16 lanes at a time across 256 bytes of
+// banks (two 128-byte rows): the XOR with (row >> 1) & 7 gives the 16
+// consecutive rows of a fragment read 16 distinct slots (row & 7 let rows r
+// and r + 8 collide); the stores (2 rows x 8 chunks per 16 lanes) stay
+// conflict-free.
 __device__ __forceinline__ int swz(int row, int chunk) {
-  return row * kRowBytes + 16 * (chunk ^ (row & 7));
+  return row * kRowBytes + 16 * (chunk ^ ((row >> 1) & 7));
 }
 
 // Fallback-indicator map: one byte per tile of 64 activation rows (a wave's

@@ -36,7 +36,7 @@
 // descriptors (scalar base and size, a 32-bit offset per load).  Scale bytes
 // arrive 16 per row every four stages (a 4-byte fetch per row and stage costs
 // a whole L2 request for 4 useful bytes).  Inside LDS the 16-byte chunks of a
-// row are XOR-swizzled by row, so the 8 rows served together by one 16-byte
+// row are XOR-swizzled by row, so the 16 rows served together by one 16-byte
 // read hit distinct banks.
 //
 // Epilogue: each wave stages its results through LDS (padded rows) and
@@ -88,9 +88,16 @@ struct Layout {
   static constexpr int kScaleLoads = (kRows + kThreads - 1) / kThreads;
 };
 
-// Byte offset of 16-byte chunk c of buffer row r.
+// Byte offset of 16-byte chunk c of buffer row r.  LDS serves a 16-byte
+// access of 16 lanes at a time across 256 bytes of banks, so the 16
+// consecutive rows that one fragment read touches (same chunk) must land in
+// 16 distinct 16-byte slots: a row is 4 slots wide, and the XOR with
+// (r >> 2) & 3 separates the four rows that share a slot column (with
+// (r >> 1) & 3, rows r and r + 8 collided: 2-way conflicts measured as a
+// third of the LDS's active cycles).  The stores (4 rows x 4 chunks per 16
+// lanes) stay conflict-free.
 __device__ __forceinline__ int chunk_off(int r, int c) {
-  return r * kRowBytes + 16 * (c ^ ((r >> 1) & 3));
+  return r * kRowBytes + 16 * (c ^ ((r >> 2) & 3));
 }
 
 __device__ __forceinline__ v8i as_v8i(const u32x4 &d) {

@@ -286,8 +286,13 @@ struct HSmem {
   static constexpr int kTN = BN / 2, kFN = kTN / 32;
 };
 
+// LDS serves a 16-byte access of 16 lanes at a time across 256 bytes of
+// banks (two 128-byte rows): with the XOR by (row >> 1) & 7 the 16
+// consecutive rows of a fragment read, and the producers' stores (8 rows x
+// two chunk halves per 16 lanes), land in 16 distinct slots (row & 7 let
+// rows r and r + 8 collide).
 __device__ __forceinline__ int hswz(int row, int chunk) {
-  return row * kRowBytes + 16 * (chunk ^ (row & 7));
+  return row * kRowBytes + 16 * (chunk ^ ((row >> 1) & 7));
 }
 
 // a & m, opaque to the optimizer, so that the byte conversions below stay
