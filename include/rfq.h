@@ -197,7 +197,8 @@ rfq_status rfq_fallback_map(const uint8_t *r_codes, const uint8_t *q_scales, int
  * Q(h - deq Q(h)) (Eq. 8-10) are written.  Neither Z nor g and u reach
  * memory.  For M > 128 the codes are bit-identical to rfq_gemm with bf16 Z
  * (gate and up columns) followed by rfq_swiglu_quantize_act, which then runs
- * the same product kernel; with up to 128 rows rfq_gemm runs its few-row
+ * the same product kernel (with 256- or 128-wide tiles, which accumulate
+ * each output in the same order); with up to 128 rows rfq_gemm runs its few-row
  * kernel, whose fp32 summation order differs, so g or u, and through them h
  * and its codes, can differ where a bf16 rounding boundary lies between the
  * two sums (both stay within the product's tolerance).

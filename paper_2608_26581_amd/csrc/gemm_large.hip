@@ -10,7 +10,10 @@
 // which loads a quarter fewer operand bytes per output than the two
 // workgroups, is another 4% faster.  The cost of the global loads lies in the
 // load instructions themselves: pointing them at always-cached data does not
-// change the time.)
+// change the time.)  Where the 256 x 256 tiles would leave CUs idle, the same
+// code runs 128 x 128 tiles (4 waves of 64 x 64, up to three workgroups per
+// CU); each output is accumulated in the same order in both shapes, so they
+// give the same bits.
 //
 // Instruction: v_mfma_scale_f32_32x32x64_f8f6f4 with E2M1 operands: lane l
 // of an operand holds row (l mod 32) and 32 consecutive K values (one MX
@@ -63,29 +66,42 @@
 namespace rfq {
 namespace {
 
-constexpr int kBM = 256, kBN = 256;
-constexpr int kThreads = 512;                   // 8 waves, two per SIMD
-constexpr int kTM = 64, kTN = 128;              // wave sub-tile (2 x 2 waves)
-constexpr int kFM = kTM / 32, kFN = kTN / 32;   // 2 x 4 fragments of 32 x 32
-constexpr int kRPL = kThreads / 4;              // buffer rows per load step (4 chunks a row)
-constexpr int kWaveRows = kBM / kTM;            // waves along M
+// Workgroup tile: WM x WN waves, each 64 rows x 32 FN columns (2 x FN
+// fragments of 32 x 32).
+template <int WM, int WN, int FN>
+struct Tile {
+  static constexpr int kThreads = 64 * WM * WN;
+  static constexpr int kFM = 2, kFN = FN;
+  static constexpr int kTM = 32 * kFM, kTN = 32 * FN;   // wave sub-tile
+  static constexpr int kBM = kTM * WM, kBN = kTN * WN;  // workgroup tile
+  static constexpr int kWaveRows = WM;                  // waves along M
+  static constexpr int kWaveCols = WN;
+  static constexpr int kRPL = kThreads / 4;             // buffer rows per load step (4 chunks a row)
+};
+// 256 x 256, 8 waves of 64 x 128, one workgroup per CU, two waves per SIMD.
+using Big = Tile<4, 2, 4>;
+// 128 x 128, 4 waves of 64 x 64, for products whose 256 x 256 tiles would
+// leave CUs idle; up to three workgroups per CU.
+using Mid = Tile<2, 2, 2>;
+
 constexpr int kStageK = 128;
 constexpr int kRowBytes = kStageK / 2;
 constexpr int kGroup = 4;
 
 // LDS stage buffer: rows [0, kBM) q, (RES) [kBM, 2 kBM) r, then kBN weight
 // rows, 64 code bytes each; then one 4-byte scale word per row.
-template <bool RES>
+template <class C, bool RES>
 struct Layout {
-  static constexpr int kARows = RES ? 2 * kBM : kBM;       // q rows, then r rows
-  static constexpr int kRows = kARows + kBN;
+  static constexpr int kARows = RES ? 2 * C::kBM : C::kBM;   // q rows, then r rows
+  static constexpr int kRows = kARows + C::kBN;
   static constexpr int kWRow = kARows;
   static constexpr int kDataBytes = kRows * kRowBytes;
   static constexpr int kScaleBytes = kRows * 4;
   static constexpr int kStageBytes = kDataBytes + kScaleBytes;
   static constexpr int kBytes = 2 * kStageBytes;
-  static constexpr int kLoads = kRows * 4 / kThreads;
-  static constexpr int kScaleLoads = (kRows + kThreads - 1) / kThreads;
+  static constexpr int kLoads = kRows * 4 / C::kThreads;
+  static constexpr int kScaleLoads = (kRows + C::kThreads - 1) / C::kThreads;
+  static_assert(kRows * 4 % C::kThreads == 0, "whole load steps");
 };
 
 // Byte offset of 16-byte chunk c of buffer row r.  LDS serves a 16-byte
@@ -124,9 +140,9 @@ struct SwigluOut {
 };
 
 // Scale pairs of one stage (both k-steps) for the wave's fragments.
-template <bool RES>
+template <class C, bool RES>
 struct Scales {
-  int w[kFN], q[kFM], r[RES ? kFM : 1];
+  int w[C::kFN], q[C::kFM], r[RES ? C::kFM : 1];
 };
 
 // Instruction classes of the scheduling masks.
@@ -158,15 +174,15 @@ __device__ __forceinline__ void reads_first() {
 // 8a + 4(l/32) + v for accumulator element 4a + v; the other 16 are in lane
 // l ^ 32.  The block maximum and the 16-bit code pieces are exchanged with
 // that lane; the lower lane stores the primary codes, the upper the residual.
-template <bool HRES>
-__device__ __forceinline__ void swiglu_epilogue(const v16f (&acc)[kFM][kFN], const SwigluOut &so,
-                                                int64_t M, int64_t m_base, int64_t n_base,
-                                                int h) {
+template <class C, bool HRES>
+__device__ __forceinline__ void swiglu_epilogue(const v16f (&acc)[C::kFM][C::kFN],
+                                                const SwigluOut &so, int64_t M, int64_t m_base,
+                                                int64_t n_base, int h) {
   const int64_t nblk = so.nh / 32;
 #pragma unroll
-  for (int i = 0; i < kFM; ++i) {
+  for (int i = 0; i < C::kFM; ++i) {
 #pragma unroll
-    for (int p = 0; p < kFN / 2; ++p) {
+    for (int p = 0; p < C::kFN / 2; ++p) {
       const v16f &ag = acc[i][2 * p], &au = acc[i][2 * p + 1];
       const int64_t m = m_base + 32 * i;
       const int64_t blk = (n_base + 64 * p) / 64;
@@ -240,19 +256,25 @@ __device__ __forceinline__ void swiglu_epilogue(const v16f (&acc)[kFM][kFN], con
 }
 
 // Fallback-indicator map: one byte per tile of kPhiRows activation rows by
-// kPhiK reduction columns (a wave's rows by two stages).
+// kPhiK reduction columns (a wave's rows by two stages); 256 x 256 tiles only.
 constexpr int kPhiRows = 64, kPhiK = 256;
-// LDS reserved for the two map rows of a workgroup (K up to 2^20).
-constexpr int kPhiMapMaxBytes = kWaveRows * ((1 << 20) / kPhiK);
+// LDS reserved for the map rows of a workgroup (K up to 2^20).
+constexpr int kPhiMapMaxBytes = Big::kWaveRows * ((1 << 20) / kPhiK);
 
-template <bool RES, bool ZBF16, bool SWIGLU = false, bool HRES = false, bool PHI = false>
-__global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
+// The product of one workgroup tile (both tile shapes; the kernels below
+// fix the shape and the occupancy).
+template <class C, bool RES, bool ZBF16, bool SWIGLU, bool HRES, bool PHI>
+__device__ __forceinline__ void gemm_tile(
     const uint8_t *__restrict__ qc, const uint8_t *__restrict__ qs,
     const uint8_t *__restrict__ rc, const uint8_t *__restrict__ rs,
     const uint8_t *__restrict__ wc, const uint8_t *__restrict__ ws,
-    int64_t M, int64_t N, int64_t K, void *__restrict__ z, SwigluOut so,
+    int64_t M, int64_t N, int64_t K, void *__restrict__ z, const SwigluOut &so,
     const uint8_t *__restrict__ phi) {
-  using L = Layout<RES>;
+  static_assert(!PHI || std::is_same<C, Big>::value, "fallback-indicator maps use 256 x 256 tiles");
+  using L = Layout<C, RES>;
+  constexpr int kBM = C::kBM, kBN = C::kBN, kTM = C::kTM, kTN = C::kTN;
+  constexpr int kFM = C::kFM, kFN = C::kFN, kRPL = C::kRPL, kThreads = C::kThreads;
+  constexpr int kWaveRows = C::kWaveRows;
   extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
 
   int tm, tn;
@@ -261,7 +283,7 @@ __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / C::kWaveCols, wn = wave % C::kWaveCols;
   const int64_t kbytes = K / 2, kblocks = K / 32;
   const int nstages = (int)(K / kStageK);
 
@@ -365,7 +387,7 @@ __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
     read_q(buf, s, i, f);
     read_r(buf, s, i, f);
   };
-  auto read_scales = [&](int buf, Scales<RES> &sc) {
+  auto read_scales = [&](int buf, Scales<C, RES> &sc) {
     const uint8_t *b = lds(buf) + L::kDataBytes + 2 * h;
 #pragma unroll
     for (int j = 0; j < kFN; ++j) sc.w[j] = *reinterpret_cast<const uint16_t *>(b + 4 * wrow(j));
@@ -382,7 +404,7 @@ __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
 #pragma unroll
     for (int j = 0; j < kFN; ++j) acc[i][j] = v16f{};
 
-  auto mma_row = [&](const WFrag &w, const AFrag &a, const Scales<RES> &sc, int i, auto s_tag) {
+  auto mma_row = [&](const WFrag &w, const AFrag &a, const Scales<C, RES> &sc, int i, auto s_tag) {
     constexpr int S = decltype(s_tag)::value;
 #pragma unroll
     for (int j = 0; j < kFN; ++j) {
@@ -395,7 +417,7 @@ __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
   };
   // The primary (R false) or the residual (R true) MFMAs of fragment row i,
   // for the fallback-indicator path, which issues them in two groups.
-  auto mma_part = [&](const WFrag &w, const AFrag &a, const Scales<RES> &sc, int i, auto s_tag,
+  auto mma_part = [&](const WFrag &w, const AFrag &a, const Scales<C, RES> &sc, int i, auto s_tag,
                       auto r_tag) {
     constexpr int S = decltype(s_tag)::value;
     constexpr bool R = decltype(r_tag)::value;
@@ -455,7 +477,7 @@ __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
     __builtin_amdgcn_sched_barrier(0);
     asm volatile("" ::: "memory");
   };
-  constexpr int kRowMfma = RES ? 8 : 4;
+  constexpr int kRowMfma = RES ? 2 * kFN : kFN;
   constexpr int kAR = RES ? 2 : 1;
   constexpr int kSR = kFN + kFM * (RES ? 2 : 1);
   using Prim = std::integral_constant<bool, false>;
@@ -480,7 +502,7 @@ __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
     }
     WFrag w;
     AFrag a0, a1;
-    Scales<RES> sc;
+    Scales<C, RES> sc;
     read_w(buf, 0, w);
     read_scales(buf, sc);
     read_a(buf, 0, 0, a0);
@@ -549,7 +571,7 @@ __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
   stage(nstages - 1, NoHO{}, W0{}, NoRl{});
 
   if constexpr (SWIGLU) {
-    swiglu_epilogue<HRES>(acc, so, M, m0 + wm * kTM + frow, n0 + wn * kTN, h);
+    swiglu_epilogue<C, HRES>(acc, so, M, m0 + wm * kTM + frow, n0 + wn * kTN, h);
     return;
   }
 
@@ -610,24 +632,59 @@ __global__ __launch_bounds__(kThreads, 2) void rfq_gemm_large_kernel(
   }
 }
 
+#define RFQ_TILE_ARGS                                                                      \
+  const uint8_t *__restrict__ qc, const uint8_t *__restrict__ qs,                          \
+      const uint8_t *__restrict__ rc, const uint8_t *__restrict__ rs,                      \
+      const uint8_t *__restrict__ wc, const uint8_t *__restrict__ ws, int64_t M, int64_t N, \
+      int64_t K, void *__restrict__ z, SwigluOut so, const uint8_t *__restrict__ phi
+
 template <bool RES, bool ZBF16, bool SWIGLU = false, bool HRES = false, bool PHI = false>
+__global__ __launch_bounds__(Big::kThreads, 2) void rfq_gemm_large_kernel(RFQ_TILE_ARGS) {
+  gemm_tile<Big, RES, ZBF16, SWIGLU, HRES, PHI>(qc, qs, rc, rs, wc, ws, M, N, K, z, so, phi);
+}
+
+template <bool RES, bool ZBF16, bool SWIGLU = false, bool HRES = false>
+__global__ __launch_bounds__(Mid::kThreads, 3) void rfq_gemm_mid_kernel(RFQ_TILE_ARGS) {
+  gemm_tile<Mid, RES, ZBF16, SWIGLU, HRES, false>(qc, qs, rc, rs, wc, ws, M, N, K, z, so, phi);
+}
+#undef RFQ_TILE_ARGS
+
+template <class C, bool RES, bool ZBF16, bool SWIGLU = false, bool HRES = false, bool PHI = false>
 hipError_t launch(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc,
                   const uint8_t *rs, const uint8_t *wc, const uint8_t *ws,
                   int64_t M, int64_t N, int64_t K, void *z, hipStream_t stream,
                   const SwigluOut &so = SwigluOut{}, const uint8_t *phi = nullptr) {
-  using L = Layout<RES>;
-  static_assert((kThreads / 64) * Epi<ZBF16>::kWaveBytes <= L::kBytes, "epilogue staging fits");
-  auto kern = rfq_gemm_large_kernel<RES, ZBF16, SWIGLU, HRES, PHI>;
-  // LDS: the two stage buffers, then (PHI) two rows of the indicator map.
+  using L = Layout<C, RES>;
+  static_assert((C::kThreads / 64) * Epi<ZBF16>::kWaveBytes <= L::kBytes, "epilogue staging fits");
+  void (*kern)(const uint8_t *, const uint8_t *, const uint8_t *, const uint8_t *,
+               const uint8_t *, const uint8_t *, int64_t, int64_t, int64_t, void *, SwigluOut,
+               const uint8_t *);
+  if constexpr (std::is_same<C, Big>::value)
+    kern = rfq_gemm_large_kernel<RES, ZBF16, SWIGLU, HRES, PHI>;
+  else
+    kern = rfq_gemm_mid_kernel<RES, ZBF16, SWIGLU, HRES>;
+  // LDS: the two stage buffers, then (PHI) the rows of the indicator map.
   constexpr int kMaxBytes = L::kBytes + (PHI ? kPhiMapMaxBytes : 0);
-  const int phi_bytes = PHI ? (int)(((kWaveRows * ((K + kPhiK - 1) / kPhiK)) + 15) / 16 * 16) : 0;
+  const int phi_bytes =
+      PHI ? (int)(((C::kWaveRows * ((K + kPhiK - 1) / kPhiK)) + 15) / 16 * 16) : 0;
   static std::atomic<bool> attr_done[kMaxDevices];
   const hipError_t e = set_lds_limit(attr_done, reinterpret_cast<const void *>(kern), kMaxBytes);
   if (e != hipSuccess) return e;
-  const int64_t ntiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
-  kern<<<dim3((unsigned)ntiles), dim3(kThreads), L::kBytes + phi_bytes, stream>>>(
+  const int64_t ntiles = ((M + C::kBM - 1) / C::kBM) * ((N + C::kBN - 1) / C::kBN);
+  kern<<<dim3((unsigned)ntiles), dim3(C::kThreads), L::kBytes + phi_bytes, stream>>>(
       qc, qs, rc, rs, wc, ws, M, N, K, z, so, phi);
   return hipGetLastError();
+}
+
+// 128 x 128 tiles while they number fewer than two per CU of the 256 (up to
+// three run on a CU at once).  Measured, same outputs either way: 0.53-0.58
+// of the 256 x 256 time where those tiles fill at most a quarter of the CUs
+// (129-256 rows x 12288 x 4096: 22-25 us against 40-43 us; 129-768 rows x
+// 4096 x 12288: 60-67 us against 108-117 us), 0.8-0.96 at 384-480 tiles,
+// 1.06-1.23 at 512-576.
+bool use_mid_tiles(int64_t M, int64_t N) {
+  const int64_t mid = ((M + Mid::kBM - 1) / Mid::kBM) * ((N + Mid::kBN - 1) / Mid::kBN);
+  return mid < 2 * 256;
 }
 
 }  // namespace
@@ -648,14 +705,18 @@ hipError_t launch_gemm_large(const uint8_t *q_codes, const uint8_t *q_scales,
                              const uint8_t *w_codes, const uint8_t *w_scales,
                              int64_t M, int64_t N, int64_t K, void *z, bool z_bf16,
                              hipStream_t stream) {
-  if (r_codes) {
+  auto go = [&](auto tile) {
+    using C = decltype(tile);
+    if (r_codes) {
+      if (z_bf16)
+        return launch<C, true, true>(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K, z, stream);
+      return launch<C, true, false>(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K, z, stream);
+    }
     if (z_bf16)
-      return launch<true, true>(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K, z, stream);
-    return launch<true, false>(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K, z, stream);
-  }
-  if (z_bf16)
-    return launch<false, true>(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K, z, stream);
-  return launch<false, false>(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K, z, stream);
+      return launch<C, false, true>(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K, z, stream);
+    return launch<C, false, false>(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K, z, stream);
+  };
+  return use_mid_tiles(M, N) ? go(Mid{}) : go(Big{});
 }
 
 hipError_t launch_gemm_large_phi(const uint8_t *q_codes, const uint8_t *q_scales,
@@ -664,10 +725,12 @@ hipError_t launch_gemm_large_phi(const uint8_t *q_codes, const uint8_t *q_scales
                                  const uint8_t *phi, int64_t M, int64_t N, int64_t K, void *z,
                                  bool z_bf16, hipStream_t stream) {
   if (z_bf16)
-    return launch<true, true, false, false, true>(q_codes, q_scales, r_codes, r_scales, w_codes,
-                                                  w_scales, M, N, K, z, stream, SwigluOut{}, phi);
-  return launch<true, false, false, false, true>(q_codes, q_scales, r_codes, r_scales, w_codes,
-                                                 w_scales, M, N, K, z, stream, SwigluOut{}, phi);
+    return launch<Big, true, true, false, false, true>(q_codes, q_scales, r_codes, r_scales,
+                                                       w_codes, w_scales, M, N, K, z, stream,
+                                                       SwigluOut{}, phi);
+  return launch<Big, true, false, false, false, true>(q_codes, q_scales, r_codes, r_scales,
+                                                      w_codes, w_scales, M, N, K, z, stream,
+                                                      SwigluOut{}, phi);
 }
 
 hipError_t launch_gemm_swiglu(const uint8_t *q_codes, const uint8_t *q_scales,
@@ -678,18 +741,22 @@ hipError_t launch_gemm_swiglu(const uint8_t *q_codes, const uint8_t *q_scales,
                               uint16_t *h_out, hipStream_t stream) {
   const SwigluOut so{hq_codes, hq_scales, hr_codes, hr_scales, h_out, Nh};
   const int64_t N = 2 * Nh;
-  if (r_codes) {
+  auto go = [&](auto tile) {
+    using C = decltype(tile);
+    if (r_codes) {
+      if (hr_codes)
+        return launch<C, true, true, true, true>(q_codes, q_scales, r_codes, r_scales, wgu_codes,
+                                                 wgu_scales, M, N, K, nullptr, stream, so);
+      return launch<C, true, true, true, false>(q_codes, q_scales, r_codes, r_scales, wgu_codes,
+                                                wgu_scales, M, N, K, nullptr, stream, so);
+    }
     if (hr_codes)
-      return launch<true, true, true, true>(q_codes, q_scales, r_codes, r_scales, wgu_codes,
-                                            wgu_scales, M, N, K, nullptr, stream, so);
-    return launch<true, true, true, false>(q_codes, q_scales, r_codes, r_scales, wgu_codes,
-                                           wgu_scales, M, N, K, nullptr, stream, so);
-  }
-  if (hr_codes)
-    return launch<false, true, true, true>(q_codes, q_scales, r_codes, r_scales, wgu_codes,
-                                           wgu_scales, M, N, K, nullptr, stream, so);
-  return launch<false, true, true, false>(q_codes, q_scales, r_codes, r_scales, wgu_codes,
-                                          wgu_scales, M, N, K, nullptr, stream, so);
+      return launch<C, false, true, true, true>(q_codes, q_scales, r_codes, r_scales, wgu_codes,
+                                                wgu_scales, M, N, K, nullptr, stream, so);
+    return launch<C, false, true, true, false>(q_codes, q_scales, r_codes, r_scales, wgu_codes,
+                                               wgu_scales, M, N, K, nullptr, stream, so);
+  };
+  return use_mid_tiles(M, N) ? go(Mid{}) : go(Big{});
 }
 
 }  // namespace rfq

@@ -43,7 +43,7 @@ def _check_all(bufs, what):
 
 
 @pytest.mark.parametrize("M,N,K", [(131, 97, 512), (131, 97, 96), (1, 1, 1024), (257, 300, 1536),
-                                   (37, 77, 1024)])
+                                   (37, 77, 1024), (1300, 6500, 512)])
 def test_outputs_stay_in_bounds(M, N, K):
     w = wl.WORKLOADS["qwen"].scaled(M=M, K=K, weights=(("w", K, N),))
     data = wl.generate(w, seed=31)

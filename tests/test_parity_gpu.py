@@ -362,6 +362,63 @@ def test_gemm_full_size_sampled(orc, name):
     assert_gemm_close(zbf[rows, cols], zr, bound, True, "full bf16")
 
 
+def _gemm_bits(z):
+    return z.view(torch.int16) if z.dtype == torch.bfloat16 else z.view(torch.int32)
+
+
+@pytest.mark.parametrize("residual", [True, False])
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
+def test_gemm_tile_shapes_agree(orc, residual, out_dtype):
+    """The large-tile product runs 256 x 256 tiles, or 128 x 128 ones while
+    those number fewer than 512.  1300 x 6500 (ragged both ways, 8 stages,
+    two scale groups) takes the 256-wide tiles: sampled against the oracle in
+    every 64 x 64 tile, the last row and the last column in full.  Row and
+    column slices of the same operands take the 128-wide tiles and must give
+    the same bits (rows and columns are independent; both tile shapes
+    accumulate each output in the same order)."""
+    M, N, K = 1300, 6500, 1024
+    data = _gemm_case("qwen", M, N, K, seed=77)
+    _say("gemm tile shapes M=%d N=%d K=%d residual=%s out=%s" % (M, N, K, residual, out_dtype))
+    q = rfq.rfq_quantize_act(x_device(data), residual=residual)
+    w = rfq.rfq_quantize_weight(dev(data["w"]))
+    z = rfq.rfq_gemm(*q, *w, out_dtype=out_dtype)
+    zh = host(z) if out_dtype == torch.float32 else host_bf16_as_f32(z)
+    rng = np.random.default_rng(5)
+    tr, tc = _tile_samples(M, N, 64, rng)
+    rows = np.concatenate([tr, np.full(N, M - 1), np.arange(M)])
+    cols = np.concatenate([tc, np.arange(N), np.full(M, N - 1)])
+    hq = [None if t is None else host(t) for t in q]
+    zr, bound = orc.gemm_sampled(*hq, host(w[0]), host(w[1]), rows, cols)
+    assert_gemm_close(zh[rows, cols], zr, bound, out_dtype == torch.bfloat16, "256-wide tiles")
+    for a, b in ((0, 300), (1000, 1300), (129, 387)):
+        qs = [None if t is None else t[a:b] for t in q]
+        zs = rfq.rfq_gemm(*qs, *w, out_dtype=out_dtype)
+        assert torch.equal(_gemm_bits(zs), _gemm_bits(z[a:b])), "rows %d:%d" % (a, b)
+    for a, b in ((0, 1000), (5500, 6500)):
+        zs = rfq.rfq_gemm(*q, w[0][a:b], w[1][a:b], out_dtype=out_dtype)
+        assert torch.equal(_gemm_bits(zs), _gemm_bits(z[:, a:b].contiguous())), "cols %d:%d" % (a, b)
+
+
+@pytest.mark.parametrize("M,N,K", [(256, 12288, 4096), (300, 4096, 12288), (129, 12288, 4096)])
+def test_gemm_mid_rows_full_width(orc, M, N, K):
+    """Between 129 and a few hundred activation rows at the workloads' weight
+    shapes (128 x 128 tiles), sampled in every 64 x 64 output tile, plus the
+    first and last rows in full."""
+    data = _gemm_case("qwen", M, N, K, seed=M + 3)
+    _say("gemm mid rows M=%d N=%d K=%d" % (M, N, K))
+    q = rfq.rfq_quantize_act(x_device(data))
+    w = rfq.rfq_quantize_weight(dev(data["w"]))
+    z32 = host(rfq.rfq_gemm(*q, *w))
+    zbf = host_bf16_as_f32(rfq.rfq_gemm(*q, *w, out_dtype=torch.bfloat16))
+    rng = np.random.default_rng(M)
+    tr, tc = _tile_samples(M, N, 64, rng)
+    rows = np.concatenate([tr, np.repeat([0, M - 1], N)])
+    cols = np.concatenate([tc, np.tile(np.arange(N), 2)])
+    zr, bound = orc.gemm_sampled(*[host(t) for t in q], *[host(t) for t in w], rows, cols)
+    assert_gemm_close(z32[rows, cols], zr, bound, False, "mid rows fp32")
+    assert_gemm_close(zbf[rows, cols], zr, bound, True, "mid rows bf16")
+
+
 # ---------------------------------------------------- streaming form
 STREAM = [
     ("qwen", 1, 300, 512),
@@ -664,7 +721,9 @@ def _fused_and_unfused(data, K, Nh, res_in, res_out, stages=None):
     return got, ref
 
 
-FUSED = [(200, 640, 512), (64, 96, 1024), (300, 1280, 1536), (1, 32, 512)]
+# (1300, 3296, 512): the fused product (N = 6592) runs 256 x 256 tiles, the
+# chained gate and up products (N = 3296) 128 x 128 ones.
+FUSED = [(200, 640, 512), (64, 96, 1024), (300, 1280, 1536), (1, 32, 512), (1300, 3296, 512)]
 
 
 @pytest.mark.parametrize("M,Nh,K", FUSED)
