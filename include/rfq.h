@@ -244,8 +244,9 @@ rfq_status rfq_gemm_swiglu_quantize(const uint8_t *q_codes, const uint8_t *q_sca
  *            (2^24 - 1 column slices of 16); X and the weight codes below
  *            2 GiB each.
  *   z        [M][N] row-major, z_dtype; 16-byte aligned.
- * For M <= 128 the result is bit-identical to rfq_quantize_act followed by
- * rfq_gemm (which multiplies such few rows in the same accumulation order);
+ * For M <= 64, and for M <= 128 with N <= 12160, the result is
+ * bit-identical to rfq_quantize_act followed by rfq_gemm (which multiplies
+ * such few rows with its few-row kernel, in the same accumulation order);
  * otherwise it agrees within the product's rounding (fp32 accumulation in an
  * unspecified order).  Errors: RFQ_ERR_SHAPE for the shape conditions above,
  * otherwise as rfq_gemm.  Asynchronous on hip_stream.

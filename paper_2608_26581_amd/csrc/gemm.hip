@@ -318,10 +318,12 @@ hipError_t launch_gemm(const uint8_t *q_codes, const uint8_t *q_scales,
                        const uint8_t *w_codes, const uint8_t *w_scales,
                        int64_t M, int64_t N, int64_t K, void *z, bool z_bf16,
                        hipStream_t stream) {
-  if (gemm_skinny_applies(q_scales, r_scales, w_scales, M, N, K))
+  const bool large = gemm_large_applies(q_scales, r_scales, w_scales, M, N, K);
+  if (gemm_skinny_applies(q_scales, r_scales, w_scales, M, N, K) &&
+      !(large && large_tiles_beat_few_rows(M, N)))
     return launch_gemm_skinny(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K,
                               z, z_bf16, stream);
-  if (gemm_large_applies(q_scales, r_scales, w_scales, M, N, K))
+  if (large)
     return launch_gemm_large(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K,
                              z, z_bf16, stream);
   constexpr int BM = 128, BN = 128;

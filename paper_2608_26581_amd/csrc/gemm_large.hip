@@ -689,6 +689,10 @@ bool use_mid_tiles(int64_t M, int64_t N) {
 
 }  // namespace
 
+bool large_tiles_beat_few_rows(int64_t M, int64_t N) {
+  return M > 64 && (N + Mid::kBN - 1) / Mid::kBN >= 96;
+}
+
 bool gemm_large_applies(const uint8_t *q_scales, const uint8_t *r_scales,
                         const uint8_t *w_scales, int64_t M, int64_t N, int64_t K) {
   const uintptr_t a = reinterpret_cast<uintptr_t>(q_scales) |

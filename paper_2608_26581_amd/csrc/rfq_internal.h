@@ -68,6 +68,13 @@ hipError_t launch_gemm_large(const uint8_t *q_codes, const uint8_t *q_scales,
                              int64_t M, int64_t N, int64_t K, void *z, bool z_bf16,
                              hipStream_t stream);
 
+// Between 65 and kSkinnyMaxRows rows the large-tile kernel's 128-wide tiles
+// are faster than the few-row kernel once there are at least 96 column tiles
+// (N > 12160): measured 0.45-0.77 of its time at 80-128 rows and N = 12288,
+// 13824 and 24576; 1.3-3x slower at N = 4096-5120, where one row of tiles
+// occupies 32-40 CUs.
+bool large_tiles_beat_few_rows(int64_t M, int64_t N);
+
 // Product for few activation rows (M <= kSkinnyMaxRows, K a multiple of 512,
 // 16-byte aligned scale tensors, code tensors below 2 GiB): one workgroup per
 // 32 weight rows and up to 64 activation rows.

@@ -306,6 +306,8 @@ GEMM_SMALL = [
     # enough weight rows for 32 per workgroup (16 elsewhere), ragged
     ("qwen", 16, 8200, 512),
     ("qwen", 40, 8200, 512),
+    # 65-128 rows with 96 or more 128-wide column tiles: the large-tile kernel
+    ("qwen", 100, 12300, 512),
 ]
 
 
@@ -454,7 +456,8 @@ def test_gemm_stream_matches_oracle(orc, name, M, N, K, xdt, residual, out_dtype
                                    (65, 97, 1536), (128, 300, 512), (100, 33, 2048)])
 @pytest.mark.parametrize("residual", [True, False])
 def test_gemm_stream_bit_identical_to_quantize_then_gemm(M, N, K, residual):
-    """Up to 128 rows both forms accumulate every output in the same order
+    """Where rfq_gemm runs its few-row kernel (up to 64 rows, and up to 128
+    where N <= 12160) both forms accumulate every output in the same order
     (groups, k-steps, primary then residual, the same four-wave sum) on the
     same codes: the streaming form must reproduce quantize + product bit for
     bit."""
@@ -701,8 +704,9 @@ def _fused_and_unfused(data, K, Nh, res_in, res_out, stages=None):
     wg = rfq.rfq_quantize_weight(dev(data["w_gate"]))
     wu = rfq.rfq_quantize_weight(dev(data["w_up"]))
     # The fused path runs the large-tile product; rfq_gemm does so above 128
-    # rows.  Below, its reference runs on codes zero-padded to 129 rows (rows
-    # are independent: padding changes no output of the real rows).
+    # rows (and from 65 where N > 12160).  With up to 128 rows the reference
+    # runs on codes zero-padded to 129 rows (rows are independent: padding
+    # changes no output of the real rows).
     M = q[0].shape[0]
     qg = q
     if M <= 128:
