@@ -36,6 +36,7 @@ PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 matrix cores
 N_SETS = 3
 Q_SETS = 9                    # 9 x 64 MiB quantizer inputs: over twice the 256 MB last-level cache
 PHI_MARGINS = (2, 4, 6)       # scale-threshold phi: median primary scale byte + margin
+MFMA_LOOP_ITERS = 512         # register-only MFMA loop: iterations per launch (2.1 GFLOP each)
 METRIC = "RFQ-MXFP4 GEMM TFLOP/s + quantizer GB/s (Qwen3-VL-like 4096×4096×12288)"
 
 
@@ -361,6 +362,18 @@ def secondary(torch, rfq, wl, x, w, stream):
             "ms": round(ms, 5), "exec_tflops": round(2.0 * M * N * K / ms / 1e9, 1)}
     except (AttributeError, RuntimeError, ValueError, NotImplementedError) as e:
         out["hipblaslt_mxfp4_scaled_mm"] = {"unavailable": str(e)[:120]}
+    # The FP4 matrix cores' sustained rate without memory traffic: the
+    # register-only MFMA loop of the library (the product's instruction,
+    # workgroup shape and accumulator pattern), with random and with
+    # constant operand bits; about 0.2 ms per launch.
+    loop = {}
+    sink = torch.empty(rfq.MFMA_LOOP_ITEMS, dtype=torch.float32, device=x.device)
+    for mode, rnd in (("random_operands", True), ("constant_operands", False)):
+        ms = _per_launch_ms(torch, stream, lambda i: rfq.rfq_mfma_fp4_loop(
+            MFMA_LOOP_ITERS, random_operands=rnd, sink=sink, stream=stream), 20)
+        loop[mode] = {"ms": round(ms, 5), "tflops": round(
+            MFMA_LOOP_ITERS * rfq.MFMA_LOOP_FLOPS_PER_ITER / ms / 1e9, 1)}
+    out["mfma_fp4_register_loop"] = loop
     # Fallback indicator by the scale-threshold rule (phi = 1 on tiles holding
     # a primary scale byte >= the median + margin): residual work only where
     # outliers are, at three thresholds; exec_tflops counts the MFMA work

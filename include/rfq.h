@@ -339,6 +339,27 @@ rfq_status rfq_hif4_gemm_wbf16(const uint8_t *q_codes, const uint32_t *q_meta,
                                const void *w_bf16, int64_t M, int64_t N, int64_t K,
                                void *z, rfq_dtype z_dtype, void *hip_stream);
 
+/*
+ * Measurement support, not a step of the method: the sustained rate of the
+ * FP4 matrix cores that the product (Eq. 11) runs on, without memory
+ * traffic.  256 workgroups of 8 waves (one per CU of the MI355X, two waves
+ * per SIMD); each wave holds two activation and four weight fragments of
+ * E2M1 codes in registers and issues 8 * iters MFMAs
+ * (v_mfma_scale_f32_32x32x64_f8f6f4, 2 * 32 * 32 * 64 flops each, scale 1.0)
+ * into eight 32 x 32 fp32 accumulators.  The operand bits are random
+ * (random_operands nonzero; fixed per work item) or the constant code 0x2
+ * (1.0), since the clock the chip holds depends on them.  One launch is
+ * 256 * 8 * 8 * iters * 131072 flops.
+ *   iters    1 .. 2^24.
+ *   sink     [256 * 512] fp32, 16-byte aligned, device memory owned by the
+ *            caller: work item t writes the sum of its accumulator elements
+ *            to sink[t] (with constant operands 8192 * iters, exact up to
+ *            iters = 2048).
+ * Errors: RFQ_ERR_SHAPE for iters out of range, RFQ_ERR_NULL, RFQ_ERR_ALIGN,
+ * RFQ_ERR_DEVICE, RFQ_ERR_LAUNCH.  Asynchronous on hip_stream.
+ */
+rfq_status rfq_mfma_fp4_loop(int64_t iters, int random_operands, float *sink, void *hip_stream);
+
 /* Static, never-NULL description of a status code. */
 const char *rfq_status_str(rfq_status s);
 

@@ -138,4 +138,11 @@ hipError_t launch_hif4_gemm(const uint8_t *q_codes, const uint32_t *q_meta,
                             const uint16_t *w_bf16, int64_t M, int64_t N, int64_t K, void *z,
                             bool z_bf16, hipStream_t stream);
 
+// Register-only loop of FP4 scaled MFMAs (measurement support):
+// kMfmaLoopWorkgroups workgroups of 512 work items, each wave issuing
+// 8 * iters 32x32x64 MFMAs; sink receives one float per work item.
+constexpr int kMfmaLoopWorkgroups = 256;
+hipError_t launch_mfma_fp4_loop(int64_t iters, bool random_operands, float *sink,
+                                hipStream_t stream);
+
 }  // namespace rfq

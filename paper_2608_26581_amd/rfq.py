@@ -30,9 +30,14 @@ EXPORTS = (
     "rfq_quantize_act", "rfq_quantize_weight", "rfq_gemm", "rfq_dequant",
     "rfq_swiglu_quantize_act", "rfq_gemm_phi", "rfq_fallback_map", "rfq_gemm_swiglu_quantize",
     "rfq_gemm_stream", "rfq_hif4_quantize", "rfq_hif4_dequant", "rfq_hif4_gemm",
-    "rfq_hif4_gemm_wbf16",
+    "rfq_hif4_gemm_wbf16", "rfq_mfma_fp4_loop",
     "rfq_status_str", "rfq_abi_version",
 )
+
+# Work items of rfq_mfma_fp4_loop (256 workgroups of 512) and its flops per
+# iteration (each of the 2048 waves issues 8 MFMAs of 32 x 32 x 64).
+MFMA_LOOP_ITEMS = 256 * 512
+MFMA_LOOP_FLOPS_PER_ITER = 256 * 8 * 8 * 2 * 32 * 32 * 64
 
 RFQ_PHI_RESIDUAL_NONZERO = 0
 RFQ_PHI_SCALE_AT_LEAST = 1
@@ -72,10 +77,11 @@ def load():
     lib.rfq_hif4_dequant.argtypes = [P, P, I64, I64, P, I32, P]
     lib.rfq_hif4_gemm.argtypes = [P, P, P, P, P, P, I64, I64, I64, P, I32, P]
     lib.rfq_hif4_gemm_wbf16.argtypes = [P, P, P, P, P, I64, I64, I64, P, I32, P]
+    lib.rfq_mfma_fp4_loop.argtypes = [I64, I32, P, P]
     for f in ("rfq_quantize_act", "rfq_quantize_weight", "rfq_gemm", "rfq_dequant",
               "rfq_swiglu_quantize_act", "rfq_gemm_swiglu_quantize", "rfq_gemm_phi",
               "rfq_fallback_map", "rfq_gemm_stream", "rfq_hif4_quantize", "rfq_hif4_dequant",
-              "rfq_hif4_gemm", "rfq_hif4_gemm_wbf16"):
+              "rfq_hif4_gemm", "rfq_hif4_gemm_wbf16", "rfq_mfma_fp4_loop"):
         getattr(lib, f).restype = I32
     lib.rfq_status_str.argtypes = [I32]
     lib.rfq_status_str.restype = ctypes.c_char_p
@@ -331,6 +337,20 @@ def rfq_fallback_map(r_codes, q_scales, rule, threshold=0, out=None, stream=None
                                  _ptr(phi), _stream(stream))
     _check("rfq_fallback_map", st)
     return phi
+
+
+def rfq_mfma_fp4_loop(iters, random_operands=True, sink=None, stream=None):
+    """Measurement support: a register-only loop of FP4 scaled MFMAs on every
+    CU (MFMA_LOOP_FLOPS_PER_ITER flops per iteration); returns the sink of
+    one fp32 checksum per work item."""
+    if sink is None:
+        sink = torch.empty(MFMA_LOOP_ITEMS, dtype=torch.float32, device="cuda")
+    else:
+        _need(sink, "sink", (torch.float32,), (MFMA_LOOP_ITEMS,))
+    st = load().rfq_mfma_fp4_loop(int(iters), 1 if random_operands else 0, _ptr(sink),
+                                  _stream(stream, sink.get_device()))
+    _check("rfq_mfma_fp4_loop", st)
+    return sink
 
 
 def rfq_dequant(codes, scales, out=None, stream=None):

@@ -319,6 +319,17 @@ def test_size_limits():
     assert sw(A, A, A, A, A, A, 64, 1 << 31, 512, A, A, A, A, None, None) == ESHAPE
 
 
+def test_mfma_loop_validation():
+    """The measurement loop: iteration count 1 .. 2^24, a 16-byte aligned
+    sink."""
+    f = _lib().rfq_mfma_fp4_loop
+    assert f(0, 1, A, None) == ESHAPE
+    assert f(-5, 1, A, None) == ESHAPE
+    assert f((1 << 24) + 1, 0, A, None) == ESHAPE
+    assert f(4, 1, None, None) == ENULL
+    assert f(4, 1, MIS, None) == EALIGN
+
+
 def test_binding_rejects_host_tensors():
     """The binding passes only device pointers on: host tensors are refused
     before any library call (a host pointer would fault in a kernel)."""
@@ -342,6 +353,7 @@ def test_binding_rejects_host_tensors():
         lambda: binding.rfq_hif4_dequant(c, m),
         lambda: binding.rfq_hif4_gemm(c, m, None, None, c, m),
         lambda: binding.rfq_hif4_gemm_wbf16(c, m, None, None, xb),
+        lambda: binding.rfq_mfma_fp4_loop(4, sink=torch.zeros(binding.MFMA_LOOP_ITEMS)),
     ]
     for call in calls:
         with pytest.raises(ValueError, match="device tensor"):
@@ -357,6 +369,7 @@ def test_valid_arguments_without_a_gpu_report_device_error():
     assert _lib().rfq_gemm_stream(A, 1, 1, A, A, 8, 8, 512, A, 0, None) == EDEVICE
     assert _lib().rfq_hif4_quantize(A, 1, 4, 64, A, A, A, A, None) == EDEVICE
     assert _lib().rfq_hif4_gemm(A, A, A, A, A, A, 8, 8, 64, A, 0, None) == EDEVICE
+    assert _lib().rfq_mfma_fp4_loop(4, 1, A, None) == EDEVICE
     # The HiF4 product's launch-size limit sits at the largest grid it may
     # launch: 128-row tiles of 256 weight rows with 768 work items or of 128
     # weight rows with 640, whichever the dispatch picks (N = 256: two
