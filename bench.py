@@ -538,6 +538,30 @@ def secondary(torch, rfq, wl, x, w, stream):
         "ms": round(ms, 5), "exec_tflops": round(flops / ms / 1e9, 1),
         "stages": "quantize X; RFQ gate/up product (N=24576) with SwiGLU + RFQ quantize "
                   "in its epilogue; RFQ down product; bf16 output"}
+
+    # Prefill-sized token counts through the block's products: the gate
+    # product (12288 x 4096 weights; 128-wide tiles) and the down product
+    # (4096 x 12288 weights), the latter with K unsplit (rfq_gemm) and split
+    # over workgroups (rfq_gemm_split).
+    for mp in (256, 512):
+        qp = [t[:mp] for t in q]
+        hp = [t[:mp] for t in h]
+        gp = torch.empty((mp, Nh), dtype=torch.bfloat16, device=dev)
+        yp = torch.empty((mp, Ks), dtype=torch.bfloat16, device=dev)
+        ms_g = _per_launch_ms(torch, stream, lambda i: rfq.rfq_gemm(
+            *qp, *wg, out=gp, stream=stream), 20)
+        ms_d = _per_launch_ms(torch, stream, lambda i: rfq.rfq_gemm(
+            *hp, *wd, out=yp, stream=stream), 20)
+        nb = rfq.rfq_gemm_workspace_bytes(mp, Ks, Nh)
+        ws = torch.empty(max(nb, 16), dtype=torch.uint8, device=dev)
+        ms_s = _per_launch_ms(torch, stream, lambda i: rfq.rfq_gemm_split(
+            *hp, *wd, ws, out=yp, stream=stream), 20)
+        fl = 4.0 * mp * Ks * Nh
+        out["prefill_%d_rows" % mp] = {
+            "gate_ms": round(ms_g, 5), "gate_exec_tflops": round(fl / ms_g / 1e9, 1),
+            "down_ms": round(ms_d, 5), "down_exec_tflops": round(fl / ms_d / 1e9, 1),
+            "down_split_ms": round(ms_s, 5), "down_split_exec_tflops": round(fl / ms_s / 1e9, 1),
+            "down_split_workspace_bytes": nb}
     return out
 
 

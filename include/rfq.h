@@ -126,6 +126,38 @@ rfq_status rfq_gemm(const uint8_t *q_codes, const uint8_t *q_scales,
                     void *z, rfq_dtype z_dtype, void *hip_stream);
 
 /*
+ * The RFQ product of rfq_gemm with the reduction over K split across
+ * several workgroups per output tile where that is faster: products with few
+ * output tiles and a long K (at most 192 tiles of 128 x 128 and K >= 8192,
+ * e.g. an MLP down projection with up to a few hundred activation rows).
+ * Each part of K writes its fp32 partial sums to the workspace; one pass then
+ * adds the parts in a fixed order and rounds to z_dtype, so the result is
+ * deterministic but its fp32 summation order differs from rfq_gemm's (both
+ * agree within the product's rounding).  Where the shape does not split, or
+ * workspace_bytes is below rfq_gemm_workspace_bytes(M, N, K), it is rfq_gemm.
+ *   workspace: device memory owned by the caller, 16-byte aligned, not read
+ *            before it is written; NULL only with workspace_bytes == 0.
+ *   workspace_bytes: its size, >= 0.
+ * Other arguments and errors as rfq_gemm.  Calls that share a workspace must
+ * be ordered (one stream, or events).  Asynchronous on hip_stream.
+ */
+rfq_status rfq_gemm_split(const uint8_t *q_codes, const uint8_t *q_scales,
+                          const uint8_t *r_codes, const uint8_t *r_scales,
+                          const uint8_t *w_codes, const uint8_t *w_scales,
+                          int64_t M, int64_t N, int64_t K,
+                          void *z, rfq_dtype z_dtype, void *workspace,
+                          int64_t workspace_bytes, void *hip_stream);
+
+/*
+ * Workspace rfq_gemm_split uses for this shape: parts * M * N * 4 bytes for
+ * the fp32 partials (at most 32 MiB), or 0 where it does not split (few
+ * rows, K not a multiple of 512, many tiles, K < 8192, or sizes that
+ * rfq_gemm rejects).  Assumes 16-byte aligned scale tensors (with others the
+ * product runs unsplit).  Host-only; no device call.
+ */
+int64_t rfq_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K);
+
+/*
  * Dequantization, one term of Eq. (12): out[r][k] = value(code) * 2^(scale-127),
  * exact in fp32 (scale byte 0xFF gives NaN).
  *   codes [rows][K/2] 16-byte aligned; scales [rows][K/32]; out [rows][K]

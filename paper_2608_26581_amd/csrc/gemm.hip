@@ -313,19 +313,38 @@ hipError_t launch_tile(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc,
 
 }  // namespace
 
+// The few-row kernel takes the product (shape conditions only; alignment and
+// size conditions of the kernels are checked where they are dispatched).
+static bool few_rows_chosen(int64_t M, int64_t N, int64_t K) {
+  return M <= kSkinnyMaxRows && (K % 512) == 0 && !large_tiles_beat_few_rows(M, N);
+}
+
+int64_t gemm_split_bytes(int64_t M, int64_t N, int64_t K) {
+  if (M <= 0 || N <= 0 || (K % 512) != 0 || few_rows_chosen(M, N, K)) return 0;
+  const SplitPlan p = splitk_plan(M, N, K);
+  return p.parts > 1 ? p.work_bytes : 0;
+}
+
 hipError_t launch_gemm(const uint8_t *q_codes, const uint8_t *q_scales,
                        const uint8_t *r_codes, const uint8_t *r_scales,
                        const uint8_t *w_codes, const uint8_t *w_scales,
                        int64_t M, int64_t N, int64_t K, void *z, bool z_bf16,
-                       hipStream_t stream) {
+                       hipStream_t stream, float *work, int64_t work_bytes) {
   const bool large = gemm_large_applies(q_scales, r_scales, w_scales, M, N, K);
   if (gemm_skinny_applies(q_scales, r_scales, w_scales, M, N, K) &&
       !(large && large_tiles_beat_few_rows(M, N)))
     return launch_gemm_skinny(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K,
                               z, z_bf16, stream);
-  if (large)
+  if (large) {
+    if (work) {
+      const SplitPlan plan = splitk_plan(M, N, K);
+      if (plan.parts > 1 && plan.work_bytes <= work_bytes)
+        return launch_gemm_large_split(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales,
+                                       M, N, K, z, z_bf16, plan, work, stream);
+    }
     return launch_gemm_large(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K,
                              z, z_bf16, stream);
+  }
   constexpr int BM = 128, BN = 128;
   if (r_codes) {
     if (z_bf16)

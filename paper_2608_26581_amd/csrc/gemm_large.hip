@@ -56,6 +56,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
 #include <atomic>
 #include <type_traits>
 
@@ -262,30 +263,44 @@ constexpr int kPhiRows = 64, kPhiK = 256;
 constexpr int kPhiMapMaxBytes = Big::kWaveRows * ((1 << 20) / kPhiK);
 
 // The product of one workgroup tile (both tile shapes; the kernels below
-// fix the shape and the occupancy).
-template <class C, bool RES, bool ZBF16, bool SWIGLU, bool HRES, bool PHI>
+// fix the shape and the occupancy).  SPLIT: the grid holds ceil(K / ksplit)
+// copies of the tile grid, copy s multiplying K columns [s ksplit, (s + 1)
+// ksplit) (ksplit a multiple of 512) and writing its fp32 partial product to
+// z + s M N.
+template <class C, bool RES, bool ZBF16, bool SWIGLU, bool HRES, bool PHI, bool SPLIT = false>
 __device__ __forceinline__ void gemm_tile(
     const uint8_t *__restrict__ qc, const uint8_t *__restrict__ qs,
     const uint8_t *__restrict__ rc, const uint8_t *__restrict__ rs,
     const uint8_t *__restrict__ wc, const uint8_t *__restrict__ ws,
     int64_t M, int64_t N, int64_t K, void *__restrict__ z, const SwigluOut &so,
-    const uint8_t *__restrict__ phi) {
+    const uint8_t *__restrict__ phi, int64_t ksplit) {
   static_assert(!PHI || std::is_same<C, Big>::value, "fallback-indicator maps use 256 x 256 tiles");
+  static_assert(!SPLIT || (!ZBF16 && !SWIGLU && !PHI), "split partials are fp32 products");
   using L = Layout<C, RES>;
   constexpr int kBM = C::kBM, kBN = C::kBN, kTM = C::kTM, kTN = C::kTN;
   constexpr int kFM = C::kFM, kFN = C::kFN, kRPL = C::kRPL, kThreads = C::kThreads;
   constexpr int kWaveRows = C::kWaveRows;
   extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
 
+  const int ntm = (int)((M + kBM - 1) / kBM), ntn = (int)((N + kBN - 1) / kBN);
+  int bid = blockIdx.x, split = 0;
+  if constexpr (SPLIT) {
+    split = bid / (ntm * ntn);
+    bid -= split * ntm * ntn;
+    z = reinterpret_cast<float *>(z) + (int64_t)split * M * N;
+  }
   int tm, tn;
-  tile_coords<1024 / kBM>(blockIdx.x, (int)((M + kBM - 1) / kBM), (int)((N + kBN - 1) / kBN), tm, tn);
+  tile_coords<1024 / kBM>(bid, ntm, ntn, tm, tn);
   const int64_t m0 = (int64_t)tm * kBM, n0 = (int64_t)tn * kBN;
+  // First K column of this workgroup's range, as code and scale byte offsets.
+  const int64_t kb = SPLIT ? (int64_t)split * ksplit : 0;
+  const int kb_code = (int)(kb / 2), kb_scale = (int)(kb / 32);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int wm = wave / C::kWaveCols, wn = wave % C::kWaveCols;
   const int64_t kbytes = K / 2, kblocks = K / 32;
-  const int nstages = (int)(K / kStageK);
+  const int nstages = (int)((SPLIT ? min(ksplit, K - kb) : K) / kStageK);
 
   const int trow = tid / 4, tcol = 16 * (tid & 3);
   auto rsrc = [](const uint8_t *p, int64_t bytes) {
@@ -343,14 +358,14 @@ __device__ __forceinline__ void gemm_tile(
       if constexpr (PHI && RES)
         if (o == 1) off = ((rmask >> (u - kBM / kRPL)) & 1) ? off : kSkipOffset;
       pf[u] = __builtin_amdgcn_raw_buffer_load_b128(o == 0 ? cq : (o == 1 ? cr : cw), off,
-                                                    st * kRowBytes, 0);
+                                                    kb_code + st * kRowBytes, 0);
     }
   };
   auto load_group = [&](int gi) {
 #pragma unroll
     for (int v = 0; v < L::kScaleLoads; ++v)
       grp[v] = __builtin_amdgcn_raw_buffer_load_b128(s_op[v] == 0 ? sq : (s_op[v] == 1 ? sr : sw),
-                                                     s_off[v], 16 * gi, 0);
+                                                     s_off[v], kb_scale + 16 * gi, 0);
   };
   // Writes the register stage and word `word` of the scale group to LDS.
   auto store_stage = [&](int buf, auto word_tag) {
@@ -636,18 +651,61 @@ __device__ __forceinline__ void gemm_tile(
   const uint8_t *__restrict__ qc, const uint8_t *__restrict__ qs,                          \
       const uint8_t *__restrict__ rc, const uint8_t *__restrict__ rs,                      \
       const uint8_t *__restrict__ wc, const uint8_t *__restrict__ ws, int64_t M, int64_t N, \
-      int64_t K, void *__restrict__ z, SwigluOut so, const uint8_t *__restrict__ phi
+      int64_t K, void *__restrict__ z, SwigluOut so, const uint8_t *__restrict__ phi,      \
+      int64_t ksplit
 
 template <bool RES, bool ZBF16, bool SWIGLU = false, bool HRES = false, bool PHI = false>
 __global__ __launch_bounds__(Big::kThreads, 2) void rfq_gemm_large_kernel(RFQ_TILE_ARGS) {
-  gemm_tile<Big, RES, ZBF16, SWIGLU, HRES, PHI>(qc, qs, rc, rs, wc, ws, M, N, K, z, so, phi);
+  gemm_tile<Big, RES, ZBF16, SWIGLU, HRES, PHI>(qc, qs, rc, rs, wc, ws, M, N, K, z, so, phi,
+                                                ksplit);
 }
 
 template <bool RES, bool ZBF16, bool SWIGLU = false, bool HRES = false>
 __global__ __launch_bounds__(Mid::kThreads, 3) void rfq_gemm_mid_kernel(RFQ_TILE_ARGS) {
-  gemm_tile<Mid, RES, ZBF16, SWIGLU, HRES, false>(qc, qs, rc, rs, wc, ws, M, N, K, z, so, phi);
+  gemm_tile<Mid, RES, ZBF16, SWIGLU, HRES, false>(qc, qs, rc, rs, wc, ws, M, N, K, z, so, phi,
+                                                  ksplit);
+}
+
+// K split over several workgroups per 128 x 128 tile: fp32 partial products.
+template <bool RES>
+__global__ __launch_bounds__(Mid::kThreads, 3) void rfq_gemm_split_kernel(RFQ_TILE_ARGS) {
+  gemm_tile<Mid, RES, false, false, false, false, true>(qc, qs, rc, rs, wc, ws, M, N, K, z, so,
+                                                        phi, ksplit);
 }
 #undef RFQ_TILE_ARGS
+
+// Z = sum of the S partial products p[s][M N], added in the order s = 0, 1,
+// ...; four outputs per work item (V4: M N a multiple of 4), fp32 or bf16.
+template <bool ZBF16, bool V4>
+__global__ __launch_bounds__(256) void splitk_sum_kernel(const float *__restrict__ p, int S,
+                                                         int64_t mn, void *__restrict__ z) {
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  if constexpr (V4) {
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < mn / 4; i += stride) {
+      float4 a = reinterpret_cast<const float4 *>(p)[i];
+      for (int s = 1; s < S; ++s) {
+        const float4 b = reinterpret_cast<const float4 *>(p + s * mn)[i];
+        a.x += b.x;
+        a.y += b.y;
+        a.z += b.z;
+        a.w += b.w;
+      }
+      if constexpr (ZBF16)
+        reinterpret_cast<uint2 *>(z)[i] = uint2{bf16x2_rne(a.x, a.y), bf16x2_rne(a.z, a.w)};
+      else
+        reinterpret_cast<float4 *>(z)[i] = a;
+    }
+  } else {
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < mn; i += stride) {
+      float a = p[i];
+      for (int s = 1; s < S; ++s) a += p[s * mn + i];
+      if constexpr (ZBF16)
+        reinterpret_cast<uint16_t *>(z)[i] = (uint16_t)bf16_rne(a);
+      else
+        reinterpret_cast<float *>(z)[i] = a;
+    }
+  }
+}
 
 template <class C, bool RES, bool ZBF16, bool SWIGLU = false, bool HRES = false, bool PHI = false>
 hipError_t launch(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc,
@@ -658,7 +716,7 @@ hipError_t launch(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc,
   static_assert((C::kThreads / 64) * Epi<ZBF16>::kWaveBytes <= L::kBytes, "epilogue staging fits");
   void (*kern)(const uint8_t *, const uint8_t *, const uint8_t *, const uint8_t *,
                const uint8_t *, const uint8_t *, int64_t, int64_t, int64_t, void *, SwigluOut,
-               const uint8_t *);
+               const uint8_t *, int64_t);
   if constexpr (std::is_same<C, Big>::value)
     kern = rfq_gemm_large_kernel<RES, ZBF16, SWIGLU, HRES, PHI>;
   else
@@ -672,8 +730,53 @@ hipError_t launch(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc,
   if (e != hipSuccess) return e;
   const int64_t ntiles = ((M + C::kBM - 1) / C::kBM) * ((N + C::kBN - 1) / C::kBN);
   kern<<<dim3((unsigned)ntiles), dim3(C::kThreads), L::kBytes + phi_bytes, stream>>>(
-      qc, qs, rc, rs, wc, ws, M, N, K, z, so, phi);
+      qc, qs, rc, rs, wc, ws, M, N, K, z, so, phi, K);
   return hipGetLastError();
+}
+
+// K split into `parts` ranges of ksplit columns (a multiple of 512): the
+// partial products go to work[parts][M][N] (fp32), then one pass adds them.
+template <bool RES>
+hipError_t launch_split(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc,
+                        const uint8_t *rs, const uint8_t *wc, const uint8_t *ws, int64_t M,
+                        int64_t N, int64_t K, void *z, bool z_bf16, float *work, int parts,
+                        int64_t ksplit, hipStream_t stream) {
+  using L = Layout<Mid, RES>;
+  auto kern = rfq_gemm_split_kernel<RES>;
+  static std::atomic<bool> attr_done[kMaxDevices];
+  hipError_t e = set_lds_limit(attr_done, reinterpret_cast<const void *>(kern), L::kBytes);
+  if (e != hipSuccess) return e;
+  const int64_t ntiles = ((M + Mid::kBM - 1) / Mid::kBM) * ((N + Mid::kBN - 1) / Mid::kBN);
+  kern<<<dim3((unsigned)(ntiles * parts)), dim3(Mid::kThreads), L::kBytes, stream>>>(
+      qc, qs, rc, rs, wc, ws, M, N, K, work, SwigluOut{}, nullptr, ksplit);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  const int64_t mn = M * N;
+  const bool v4 = (mn % 4) == 0;
+  const int64_t items = v4 ? mn / 4 : mn;
+  const unsigned blocks = (unsigned)std::min<int64_t>((items + 255) / 256, 4096);
+  if (z_bf16) {
+    if (v4) splitk_sum_kernel<true, true><<<blocks, 256, 0, stream>>>(work, parts, mn, z);
+    else splitk_sum_kernel<true, false><<<blocks, 256, 0, stream>>>(work, parts, mn, z);
+  } else {
+    if (v4) splitk_sum_kernel<false, true><<<blocks, 256, 0, stream>>>(work, parts, mn, z);
+    else splitk_sum_kernel<false, false><<<blocks, 256, 0, stream>>>(work, parts, mn, z);
+  }
+  return hipGetLastError();
+}
+
+// Parts of K for the split product (1: no split): only for K >= 8192 and at
+// most 192 tiles of 128 x 128, 256 / tiles parts up to 128 tiles and
+// 512 / tiles above, at most 4 (parts x tiles <= 512, so the partials take
+// at most 32 MiB).  Measured against the unsplit 128-wide tiles (random
+// codes, bf16 Z): 129 rows x 4096 x 12288 60.3 -> 23.9 us (4 parts); 256
+// rows 61.9 -> 28.5 (4); 512 rows 63.2 -> 44.3 (2); 768 rows 64.2 -> 63.5
+// (2); 129 and 256 rows x 5120 x 13824 69.6 -> 30.3 and 71.8 -> 34.2 (3);
+// 512 rows 72.5 -> 57.5 (3).  With K = 4096 at 12288 columns the partial
+// sums cost more than the split saves (21.3 -> 25.5 us with 2 parts).
+int splitk_default_parts(int64_t M, int64_t N, int64_t K) {
+  const int64_t tiles = ((M + Mid::kBM - 1) / Mid::kBM) * ((N + Mid::kBN - 1) / Mid::kBN);
+  if (K < 8192 || tiles > 192) return 1;
+  return (int)std::min<int64_t>(4, (tiles <= 128 ? 256 : 512) / tiles);
 }
 
 // 128 x 128 tiles while they number fewer than two per CU of the 256 (up to
@@ -688,6 +791,36 @@ bool use_mid_tiles(int64_t M, int64_t N) {
 }
 
 }  // namespace
+
+SplitPlan splitk_plan(int64_t M, int64_t N, int64_t K, int parts_wanted) {
+  SplitPlan p{1, K, 0};
+  const int64_t units = K / (kStageK * kGroup);
+  if (!use_mid_tiles(M, N) || units < 2) return p;
+  int want = parts_wanted;
+  if (want <= 0) want = splitk_default_parts(M, N, K);
+  if (want < 2) return p;
+  const int64_t per = (units + want - 1) / want;
+  p.parts = (int)((units + per - 1) / per);
+  if (p.parts < 2) return SplitPlan{1, K, 0};
+  p.ksplit = per * kStageK * kGroup;
+  p.work_bytes = (int64_t)p.parts * M * N * 4;
+  return p;
+}
+
+hipError_t launch_gemm_large_split(const uint8_t *q_codes, const uint8_t *q_scales,
+                                   const uint8_t *r_codes, const uint8_t *r_scales,
+                                   const uint8_t *w_codes, const uint8_t *w_scales, int64_t M,
+                                   int64_t N, int64_t K, void *z, bool z_bf16,
+                                   const SplitPlan &plan, float *work, hipStream_t stream) {
+  if (plan.parts < 2)
+    return launch_gemm_large(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K,
+                             z, z_bf16, stream);
+  if (r_codes)
+    return launch_split<true>(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K,
+                              z, z_bf16, work, plan.parts, plan.ksplit, stream);
+  return launch_split<false>(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K, z,
+                             z_bf16, work, plan.parts, plan.ksplit, stream);
+}
 
 bool large_tiles_beat_few_rows(int64_t M, int64_t N) {
   return M > 64 && (N + Mid::kBN - 1) / Mid::kBN >= 96;

@@ -51,12 +51,17 @@ hipError_t launch_dequant(const uint8_t *codes, const uint8_t *scales,
                           int64_t nelem, float *out, hipStream_t stream);
 
 // RFQ product (r_codes == nullptr: primary contraction only).  Picks the
-// large-tile kernel when gemm_large_applies(), else the general one.
+// few-row, large-tile or general kernel; with a workspace (work, 16-byte
+// aligned, work_bytes long) the large-tile kernel splits K where
+// splitk_plan() says so and the workspace holds the partials.
 hipError_t launch_gemm(const uint8_t *q_codes, const uint8_t *q_scales,
                        const uint8_t *r_codes, const uint8_t *r_scales,
                        const uint8_t *w_codes, const uint8_t *w_scales,
                        int64_t M, int64_t N, int64_t K, void *z, bool z_bf16,
-                       hipStream_t stream);
+                       hipStream_t stream, float *work = nullptr, int64_t work_bytes = 0);
+// Workspace bytes launch_gemm splits K with for this shape (0: no split),
+// assuming 16-byte aligned scale tensors.
+int64_t gemm_split_bytes(int64_t M, int64_t N, int64_t K);
 
 // Large-tile product: K a multiple of 512, 16-byte aligned scale tensors and
 // code tensors below 4 GiB.
@@ -67,6 +72,24 @@ hipError_t launch_gemm_large(const uint8_t *q_codes, const uint8_t *q_scales,
                              const uint8_t *w_codes, const uint8_t *w_scales,
                              int64_t M, int64_t N, int64_t K, void *z, bool z_bf16,
                              hipStream_t stream);
+
+// Split of K for the large-tile product's 128-wide tiles: `parts` ranges of
+// ksplit columns (a multiple of 512), fp32 partials in work_bytes of
+// workspace; parts == 1: no split.  parts_wanted <= 0 takes the library's
+// choice for the shape.
+struct SplitPlan {
+  int parts;
+  int64_t ksplit;
+  int64_t work_bytes;
+};
+SplitPlan splitk_plan(int64_t M, int64_t N, int64_t K, int parts_wanted = 0);
+// The product with the plan's split (work: plan.work_bytes of device memory,
+// 16-byte aligned); with parts == 1 the same as launch_gemm_large.
+hipError_t launch_gemm_large_split(const uint8_t *q_codes, const uint8_t *q_scales,
+                                   const uint8_t *r_codes, const uint8_t *r_scales,
+                                   const uint8_t *w_codes, const uint8_t *w_scales, int64_t M,
+                                   int64_t N, int64_t K, void *z, bool z_bf16,
+                                   const SplitPlan &plan, float *work, hipStream_t stream);
 
 // Between 65 and kSkinnyMaxRows rows the large-tile kernel's 128-wide tiles
 // are faster than the few-row kernel once there are at least 96 column tiles

@@ -30,7 +30,7 @@ EXPORTS = (
     "rfq_quantize_act", "rfq_quantize_weight", "rfq_gemm", "rfq_dequant",
     "rfq_swiglu_quantize_act", "rfq_gemm_phi", "rfq_fallback_map", "rfq_gemm_swiglu_quantize",
     "rfq_gemm_stream", "rfq_hif4_quantize", "rfq_hif4_dequant", "rfq_hif4_gemm",
-    "rfq_hif4_gemm_wbf16", "rfq_mfma_fp4_loop",
+    "rfq_hif4_gemm_wbf16", "rfq_mfma_fp4_loop", "rfq_gemm_split", "rfq_gemm_workspace_bytes",
     "rfq_status_str", "rfq_abi_version",
 )
 
@@ -78,10 +78,13 @@ def load():
     lib.rfq_hif4_gemm.argtypes = [P, P, P, P, P, P, I64, I64, I64, P, I32, P]
     lib.rfq_hif4_gemm_wbf16.argtypes = [P, P, P, P, P, I64, I64, I64, P, I32, P]
     lib.rfq_mfma_fp4_loop.argtypes = [I64, I32, P, P]
+    lib.rfq_gemm_split.argtypes = [P, P, P, P, P, P, I64, I64, I64, P, I32, P, I64, P]
+    lib.rfq_gemm_workspace_bytes.argtypes = [I64, I64, I64]
+    lib.rfq_gemm_workspace_bytes.restype = I64
     for f in ("rfq_quantize_act", "rfq_quantize_weight", "rfq_gemm", "rfq_dequant",
               "rfq_swiglu_quantize_act", "rfq_gemm_swiglu_quantize", "rfq_gemm_phi",
               "rfq_fallback_map", "rfq_gemm_stream", "rfq_hif4_quantize", "rfq_hif4_dequant",
-              "rfq_hif4_gemm", "rfq_hif4_gemm_wbf16", "rfq_mfma_fp4_loop"):
+              "rfq_hif4_gemm", "rfq_hif4_gemm_wbf16", "rfq_mfma_fp4_loop", "rfq_gemm_split"):
         getattr(lib, f).restype = I32
     lib.rfq_status_str.argtypes = [I32]
     lib.rfq_status_str.restype = ctypes.c_char_p
@@ -254,9 +257,16 @@ def rfq_quantize_weight(w, out=None, stream=None):
     return wc, ws
 
 
+def rfq_gemm_workspace_bytes(M, N, K):
+    """Workspace rfq_gemm_split splits K with for this shape (0: no split)."""
+    return int(load().rfq_gemm_workspace_bytes(int(M), int(N), int(K)))
+
+
 def rfq_gemm(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales,
-             out_dtype=torch.float32, out=None, stream=None):
-    """Z[M][N] = (deq q + deq r) deq(w)^T; r_* None gives plain MXFP4."""
+             out_dtype=torch.float32, out=None, stream=None, split=False):
+    """Z[M][N] = (deq q + deq r) deq(w)^T; r_* None gives plain MXFP4.
+    split=True: rfq_gemm_split with a workspace from torch's allocator where
+    the shape splits K (a different fp32 summation order)."""
     M, K = _shape_of_codes(q_codes, "q codes")
     N, Kw = _shape_of_codes(w_codes, "w codes")
     if Kw != K:
@@ -267,10 +277,46 @@ def rfq_gemm(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales,
     _need_pair(r_codes, r_scales, M, K, "r", dev)
     _need_codes(w_codes, w_scales, N, K, "w", dev)
     z = _z_out(out, out_dtype, M, N, q_codes.device, dev)
+    if split:
+        nbytes = load().rfq_gemm_workspace_bytes(M, N, K)
+        if nbytes > 0:
+            ws = torch.empty(nbytes, dtype=torch.uint8, device=q_codes.device)
+            st = load().rfq_gemm_split(_ptr(q_codes), _ptr(q_scales), _ptr(r_codes),
+                                       _ptr(r_scales), _ptr(w_codes), _ptr(w_scales), M, N, K,
+                                       _ptr(z), _dtype_code(z), _ptr(ws), nbytes,
+                                       _stream(stream, dev))
+            _check("rfq_gemm_split", st)
+            return z
     st = load().rfq_gemm(_ptr(q_codes), _ptr(q_scales), _ptr(r_codes), _ptr(r_scales),
                          _ptr(w_codes), _ptr(w_scales), M, N, K, _ptr(z), _dtype_code(z),
                          _stream(stream, dev))
     _check("rfq_gemm", st)
+    return z
+
+
+def rfq_gemm_split(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, workspace,
+                   out_dtype=torch.float32, out=None, stream=None):
+    """rfq_gemm with K split over workgroups where the shape calls for it;
+    workspace: a contiguous device uint8 tensor (rfq_gemm_workspace_bytes
+    long, or shorter to run unsplit) or None."""
+    M, K = _shape_of_codes(q_codes, "q codes")
+    N, Kw = _shape_of_codes(w_codes, "w codes")
+    if Kw != K:
+        raise ValueError("K mismatch between activation and weight codes")
+    _need(q_codes, "q codes", _U8, (M, K // 2))
+    dev = q_codes.get_device()
+    _need_codes(q_codes, q_scales, M, K, "q", dev)
+    _need_pair(r_codes, r_scales, M, K, "r", dev)
+    _need_codes(w_codes, w_scales, N, K, "w", dev)
+    nbytes = 0
+    if workspace is not None:
+        _need(workspace, "workspace", _U8, None, dev)
+        nbytes = workspace.numel()
+    z = _z_out(out, out_dtype, M, N, q_codes.device, dev)
+    st = load().rfq_gemm_split(_ptr(q_codes), _ptr(q_scales), _ptr(r_codes), _ptr(r_scales),
+                               _ptr(w_codes), _ptr(w_scales), M, N, K, _ptr(z), _dtype_code(z),
+                               _ptr(workspace), nbytes, _stream(stream, dev))
+    _check("rfq_gemm_split", st)
     return z
 
 

@@ -319,6 +319,27 @@ def test_size_limits():
     assert sw(A, A, A, A, A, A, 64, 1 << 31, 512, A, A, A, A, None, None) == ESHAPE
 
 
+def test_gemm_split_validation_and_workspace_sizes():
+    """rfq_gemm_split checks what rfq_gemm checks plus its workspace; the
+    workspace query is host-only: parts x M x N x 4 bytes where K splits."""
+    f = _lib().rfq_gemm_split
+    assert f(A, A, A, A, A, A, 8, 8, 512, A, 7, A, 64, None) == EDTYPE
+    assert f(A, A, A, A, A, A, 8, 8, 100, A, 0, A, 64, None) == ESHAPE
+    assert f(A, A, A, A, A, A, 8, 8, 512, A, 0, A, -1, None) == ESHAPE
+    assert f(A, A, A, A, A, A, 8, 8, 512, A, 0, None, 64, None) == ENULL
+    assert f(A, A, A, A, A, A, 8, 8, 512, A, 0, MIS, 64, None) == EALIGN
+    assert f(A, A, A, A, A, A, 0, 8, 512, None, 0, None, 0, None) == OK
+    w = _lib().rfq_gemm_workspace_bytes
+    assert w(129, 4096, 12288) == 4 * 129 * 4096 * 4       # 64 tiles: 4 parts
+    assert w(512, 4096, 12288) == 2 * 512 * 4096 * 4       # 128 tiles: 2 parts
+    assert w(512, 5120, 13824) == 3 * 512 * 5120 * 4       # 160 tiles: 3 parts
+    assert w(1024, 4096, 12288) == 0                       # 256 tiles
+    assert w(129, 12288, 4096) == 0                        # K below 8192
+    assert w(64, 4096, 12288) == 0                         # few-row kernel
+    assert w(129, 4096, 12300) == 0                        # K not a multiple of 512
+    assert w(-1, 4096, 12288) == 0 and w(129, 4096, 100) == 0
+
+
 def test_mfma_loop_validation():
     """The measurement loop: iteration count 1 .. 2^24, a 16-byte aligned
     sink."""
@@ -354,6 +375,7 @@ def test_binding_rejects_host_tensors():
         lambda: binding.rfq_hif4_gemm(c, m, None, None, c, m),
         lambda: binding.rfq_hif4_gemm_wbf16(c, m, None, None, xb),
         lambda: binding.rfq_mfma_fp4_loop(4, sink=torch.zeros(binding.MFMA_LOOP_ITEMS)),
+        lambda: binding.rfq_gemm_split(c, s, None, None, c, s, None),
     ]
     for call in calls:
         with pytest.raises(ValueError, match="device tensor"):
@@ -370,6 +392,7 @@ def test_valid_arguments_without_a_gpu_report_device_error():
     assert _lib().rfq_hif4_quantize(A, 1, 4, 64, A, A, A, A, None) == EDEVICE
     assert _lib().rfq_hif4_gemm(A, A, A, A, A, A, 8, 8, 64, A, 0, None) == EDEVICE
     assert _lib().rfq_mfma_fp4_loop(4, 1, A, None) == EDEVICE
+    assert _lib().rfq_gemm_split(A, A, A, A, A, A, 8, 8, 512, A, 0, A, 64, None) == EDEVICE
     # The HiF4 product's launch-size limit sits at the largest grid it may
     # launch: 128-row tiles of 256 weight rows with 768 work items or of 128
     # weight rows with 640, whichever the dispatch picks (N = 256: two

@@ -43,7 +43,7 @@ def _check_all(bufs, what):
 
 
 @pytest.mark.parametrize("M,N,K", [(131, 97, 512), (131, 97, 96), (1, 1, 1024), (257, 300, 1536),
-                                   (37, 77, 1024), (1300, 6500, 512)])
+                                   (37, 77, 1024), (1300, 6500, 512), (131, 301, 8704)])
 def test_outputs_stay_in_bounds(M, N, K):
     w = wl.WORKLOADS["qwen"].scaled(M=M, K=K, weights=(("w", K, N),))
     data = wl.generate(w, seed=31)
@@ -65,6 +65,14 @@ def test_outputs_stay_in_bounds(M, N, K):
         zb = Guarded((M, N), dt)
         rfq.rfq_gemm(q[0], q[1], None, None, *wq, out=zb.t)
         zb.check("gemm plain %s" % dt)
+        nbytes = rfq.rfq_gemm_workspace_bytes(M, N, K)
+        if nbytes:
+            # K split over workgroups: the partials stay inside the workspace.
+            wsb = Guarded((nbytes,), torch.uint8)
+            zb = Guarded((M, N), dt)
+            rfq.rfq_gemm_split(*q, *wq, wsb.t, out=zb.t)
+            zb.check("gemm split %s" % dt)
+            wsb.check("gemm split workspace %s" % dt)
     phi_shape = ((M + 63) // 64, (K + 255) // 256)
     pb = Guarded(phi_shape, torch.uint8)
     rfq.rfq_fallback_map(None, q[1], rfq.RFQ_PHI_SCALE_AT_LEAST, 128, out=pb.t)

@@ -421,6 +421,55 @@ def test_gemm_mid_rows_full_width(orc, M, N, K):
     assert_gemm_close(zbf[rows, cols], zr, bound, True, "mid rows bf16")
 
 
+# K = 8192 (4 parts of 2048), 8704 (parts of 2560 and a last one of 1024),
+# 9216 at a ragged shape; M x N not a multiple of 4 for the scalar sum.
+SPLIT = [(130, 300, 8192), (131, 301, 8704), (200, 257, 9216)]
+
+
+@pytest.mark.parametrize("M,N,K", SPLIT)
+@pytest.mark.parametrize("residual", [True, False])
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
+def test_gemm_split_matches_oracle(orc, M, N, K, residual, out_dtype):
+    """K split over workgroups: every output against the oracle; with a
+    workspace one byte short of the plan's it runs unsplit and gives
+    rfq_gemm's bits."""
+    data = _gemm_case("qwen", M, N, K, seed=K + M)
+    _say("gemm split M=%d N=%d K=%d residual=%s out=%s" % (M, N, K, residual, out_dtype))
+    q = rfq.rfq_quantize_act(x_device(data), residual=residual)
+    w = rfq.rfq_quantize_weight(dev(data["w"]))
+    nbytes = rfq.rfq_gemm_workspace_bytes(M, N, K)
+    assert nbytes > 0
+    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    z = rfq.rfq_gemm_split(*q, *w, ws, out_dtype=out_dtype)
+    zh = host(z) if out_dtype == torch.float32 else host_bf16_as_f32(z)
+    hq = [None if t is None else host(t) for t in q]
+    zr, bound = orc.gemm(*hq, host(w[0]), host(w[1]))
+    assert_gemm_close(zh, zr, bound, out_dtype == torch.bfloat16, "gemm split")
+    short = rfq.rfq_gemm_split(*q, *w, ws[:nbytes - 16], out_dtype=out_dtype)
+    assert torch.equal(_gemm_bits(short), _gemm_bits(rfq.rfq_gemm(*q, *w, out_dtype=out_dtype)))
+
+
+@pytest.mark.parametrize("M,N,K", [(256, 4096, 12288), (129, 5120, 13824), (100, 12288, 12288)])
+def test_gemm_split_full_width(orc, M, N, K):
+    """Down-projection shapes with few activation rows (K split in 4, 3 and
+    2 parts), sampled in every 64 x 64 output tile plus the last row and
+    column in full."""
+    data = _gemm_case("qwen", M, N, K, seed=M + 5)
+    _say("gemm split full M=%d N=%d K=%d" % (M, N, K))
+    q = rfq.rfq_quantize_act(x_device(data))
+    w = rfq.rfq_quantize_weight(dev(data["w"]))
+    assert rfq.rfq_gemm_workspace_bytes(M, N, K) > 0
+    z32 = host(rfq.rfq_gemm(*q, *w, split=True))
+    zbf = host_bf16_as_f32(rfq.rfq_gemm(*q, *w, out_dtype=torch.bfloat16, split=True))
+    rng = np.random.default_rng(M)
+    tr, tc = _tile_samples(M, N, 64, rng)
+    rows = np.concatenate([tr, np.full(N, M - 1), np.arange(M)])
+    cols = np.concatenate([tc, np.arange(N), np.full(M, N - 1)])
+    zr, bound = orc.gemm_sampled(*[host(t) for t in q], *[host(t) for t in w], rows, cols)
+    assert_gemm_close(z32[rows, cols], zr, bound, False, "split fp32")
+    assert_gemm_close(zbf[rows, cols], zr, bound, True, "split bf16")
+
+
 # ---------------------------------------------------- streaming form
 STREAM = [
     ("qwen", 1, 300, 512),
