@@ -149,6 +149,26 @@ rfq_status rfq_gemm_split(const uint8_t *q_codes, const uint8_t *q_scales,
                           int64_t workspace_bytes, void *hip_stream);
 
 /*
+ * rfq_gemm_split without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  The split product's partials go to a
+ * static device array of 32 MiB held by every GPU the library runs on until
+ * the process ends; no call allocates, frees or calls an allocating routine.
+ * Results are those of rfq_gemm_split with a large enough workspace.  Calls
+ * that overlap on one GPU (other streams or host threads) share the array
+ * and race; order them (one stream, or events).
+ * Arguments as rfq_gemm.  Errors as rfq_gemm, plus RFQ_ERR_SHAPE where the
+ * split would need more than the 32 MiB (rfq_gemm_workspace_bytes above
+ * 33554432; the library's split plan stays within it) and RFQ_ERR_DEVICE if
+ * the array's device address cannot be obtained.  Asynchronous on hip_stream.
+ */
+rfq_status rfq_gemm_split_noalloc(const uint8_t *q_codes, const uint8_t *q_scales,
+                                  const uint8_t *r_codes, const uint8_t *r_scales,
+                                  const uint8_t *w_codes, const uint8_t *w_scales,
+                                  int64_t M, int64_t N, int64_t K,
+                                  void *z, rfq_dtype z_dtype, void *hip_stream);
+
+/*
  * Workspace rfq_gemm_split uses for this shape: parts * M * N * 4 bytes for
  * the fp32 partials (at most 32 MiB), or 0 where it does not split (few
  * rows, K not a multiple of 512, many tiles, K < 8192, or sizes that

@@ -8,5 +8,5 @@ from .rfq import (  # noqa: F401
     interleave_gate_up, load, rfq_abi_version, rfq_dequant, rfq_fallback_map, rfq_gemm,
     rfq_gemm_phi, rfq_gemm_stream, rfq_gemm_swiglu_quantize, rfq_quantize_act, rfq_quantize_weight,
     rfq_hif4_dequant, rfq_hif4_gemm, rfq_hif4_gemm_wbf16, rfq_hif4_quantize, rfq_status_str,
-    rfq_gemm_split, rfq_gemm_workspace_bytes, rfq_mfma_fp4_loop, rfq_swiglu_quantize_act,
+    rfq_gemm_split, rfq_gemm_split_noalloc, rfq_gemm_workspace_bytes, rfq_mfma_fp4_loop, rfq_swiglu_quantize_act,
 )

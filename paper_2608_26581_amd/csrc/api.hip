@@ -182,6 +182,28 @@ rfq_status rfq_gemm_split(const uint8_t *q_codes, const uint8_t *q_scales,
                                    static_cast<float *>(workspace), workspace_bytes));
 }
 
+rfq_status rfq_gemm_split_noalloc(const uint8_t *q_codes, const uint8_t *q_scales,
+                                  const uint8_t *r_codes, const uint8_t *r_scales,
+                                  const uint8_t *w_codes, const uint8_t *w_scales, int64_t M,
+                                  int64_t N, int64_t K, void *z, rfq_dtype z_dtype,
+                                  void *hip_stream) {
+  if (!valid_dtype(z_dtype)) return RFQ_ERR_DTYPE;
+  rfq_status s = check_k(M, K);
+  if (s != RFQ_OK) return s;
+  if (N < 0 || !product_fits(M, N)) return RFQ_ERR_SHAPE;
+  if (rfq::gemm_split_bytes(M, N, K) > rfq::static_scratch_bytes()) return RFQ_ERR_SHAPE;
+  if (M == 0 || N == 0) return RFQ_OK;
+  if (!q_codes || !q_scales || !w_codes || !w_scales || !z) return RFQ_ERR_NULL;
+  if ((r_codes == nullptr) != (r_scales == nullptr)) return RFQ_ERR_NULL;
+  if (!aligned(q_codes, 16) || !aligned(w_codes, 16) || (r_codes && !aligned(r_codes, 16)) ||
+      !aligned(z, 16))
+    return RFQ_ERR_ALIGN;
+  if ((s = check_device()) != RFQ_OK) return s;
+  return launched(rfq::launch_gemm_static_scratch(q_codes, q_scales, r_codes, r_scales, w_codes,
+                                                  w_scales, M, N, K, z, z_dtype == RFQ_BF16,
+                                                  static_cast<hipStream_t>(hip_stream)));
+}
+
 rfq_status rfq_dequant(const uint8_t *codes, const uint8_t *scales, int64_t rows,
                        int64_t K, float *out, void *hip_stream) {
   rfq_status s = check_k(rows, K);

@@ -91,6 +91,15 @@ hipError_t launch_gemm_large_split(const uint8_t *q_codes, const uint8_t *q_scal
                                    int64_t N, int64_t K, void *z, bool z_bf16,
                                    const SplitPlan &plan, float *work, hipStream_t stream);
 
+// launch_gemm with the library's static device scratch array as the split
+// product's workspace (no allocation); static_scratch_bytes() is its size.
+int64_t static_scratch_bytes();
+hipError_t launch_gemm_static_scratch(const uint8_t *q_codes, const uint8_t *q_scales,
+                                      const uint8_t *r_codes, const uint8_t *r_scales,
+                                      const uint8_t *w_codes, const uint8_t *w_scales,
+                                      int64_t M, int64_t N, int64_t K, void *z, bool z_bf16,
+                                      hipStream_t stream);
+
 // Between 65 and kSkinnyMaxRows rows the large-tile kernel's 128-wide tiles
 // are faster than the few-row kernel once there are at least 96 column tiles
 // (N > 12160): measured 0.45-0.77 of its time at 80-128 rows and N = 12288,

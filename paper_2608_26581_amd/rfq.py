@@ -31,6 +31,7 @@ EXPORTS = (
     "rfq_swiglu_quantize_act", "rfq_gemm_phi", "rfq_fallback_map", "rfq_gemm_swiglu_quantize",
     "rfq_gemm_stream", "rfq_hif4_quantize", "rfq_hif4_dequant", "rfq_hif4_gemm",
     "rfq_hif4_gemm_wbf16", "rfq_mfma_fp4_loop", "rfq_gemm_split", "rfq_gemm_workspace_bytes",
+    "rfq_gemm_split_noalloc",
     "rfq_status_str", "rfq_abi_version",
 )
 
@@ -79,12 +80,14 @@ def load():
     lib.rfq_hif4_gemm_wbf16.argtypes = [P, P, P, P, P, I64, I64, I64, P, I32, P]
     lib.rfq_mfma_fp4_loop.argtypes = [I64, I32, P, P]
     lib.rfq_gemm_split.argtypes = [P, P, P, P, P, P, I64, I64, I64, P, I32, P, I64, P]
+    lib.rfq_gemm_split_noalloc.argtypes = [P, P, P, P, P, P, I64, I64, I64, P, I32, P]
     lib.rfq_gemm_workspace_bytes.argtypes = [I64, I64, I64]
     lib.rfq_gemm_workspace_bytes.restype = I64
     for f in ("rfq_quantize_act", "rfq_quantize_weight", "rfq_gemm", "rfq_dequant",
               "rfq_swiglu_quantize_act", "rfq_gemm_swiglu_quantize", "rfq_gemm_phi",
               "rfq_fallback_map", "rfq_gemm_stream", "rfq_hif4_quantize", "rfq_hif4_dequant",
-              "rfq_hif4_gemm", "rfq_hif4_gemm_wbf16", "rfq_mfma_fp4_loop", "rfq_gemm_split"):
+              "rfq_hif4_gemm", "rfq_hif4_gemm_wbf16", "rfq_mfma_fp4_loop", "rfq_gemm_split",
+              "rfq_gemm_split_noalloc"):
         getattr(lib, f).restype = I32
     lib.rfq_status_str.argtypes = [I32]
     lib.rfq_status_str.restype = ctypes.c_char_p
@@ -291,6 +294,28 @@ def rfq_gemm(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales,
                          _ptr(w_codes), _ptr(w_scales), M, N, K, _ptr(z), _dtype_code(z),
                          _stream(stream, dev))
     _check("rfq_gemm", st)
+    return z
+
+
+def rfq_gemm_split_noalloc(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales,
+                           out=None, out_dtype=torch.float32, stream=None):
+    """rfq_gemm_split on the library's static device scratch array (no
+    device allocation in the library; pass `out` to allocate nothing here
+    either)."""
+    M, K = _shape_of_codes(q_codes, "q codes")
+    N, Kw = _shape_of_codes(w_codes, "w codes")
+    if Kw != K:
+        raise ValueError("K mismatch between activation and weight codes")
+    _need(q_codes, "q codes", _U8, (M, K // 2))
+    dev = q_codes.get_device()
+    _need_codes(q_codes, q_scales, M, K, "q", dev)
+    _need_pair(r_codes, r_scales, M, K, "r", dev)
+    _need_codes(w_codes, w_scales, N, K, "w", dev)
+    z = _z_out(out, out_dtype, M, N, q_codes.device, dev)
+    st = load().rfq_gemm_split_noalloc(_ptr(q_codes), _ptr(q_scales), _ptr(r_codes),
+                                       _ptr(r_scales), _ptr(w_codes), _ptr(w_scales), M, N, K,
+                                       _ptr(z), _dtype_code(z), _stream(stream, dev))
+    _check("rfq_gemm_split_noalloc", st)
     return z
 
 

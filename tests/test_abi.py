@@ -340,6 +340,18 @@ def test_gemm_split_validation_and_workspace_sizes():
     assert w(-1, 4096, 12288) == 0 and w(129, 4096, 100) == 0
 
 
+def test_gemm_split_noalloc_validation():
+    """The allocation-free split product checks what rfq_gemm checks."""
+    f = _lib().rfq_gemm_split_noalloc
+    assert f(A, A, A, A, A, A, 8, 8, 512, A, 7, None) == EDTYPE
+    assert f(A, A, A, A, A, A, 8, 8, 100, A, 0, None) == ESHAPE
+    assert f(A, A, A, A, A, A, 1 << 21, 1 << 21, 64, A, 0, None) == ESHAPE
+    assert f(A, A, A, A, A, A, 0, 8, 512, None, 0, None) == OK
+    assert f(None, A, A, A, A, A, 8, 8, 512, A, 0, None) == ENULL
+    assert f(A, A, A, None, A, A, 8, 8, 512, A, 0, None) == ENULL
+    assert f(A, A, A, A, A, A, 8, 8, 512, MIS, 0, None) == EALIGN
+
+
 def test_mfma_loop_validation():
     """The measurement loop: iteration count 1 .. 2^24, a 16-byte aligned
     sink."""
@@ -376,6 +388,7 @@ def test_binding_rejects_host_tensors():
         lambda: binding.rfq_hif4_gemm_wbf16(c, m, None, None, xb),
         lambda: binding.rfq_mfma_fp4_loop(4, sink=torch.zeros(binding.MFMA_LOOP_ITEMS)),
         lambda: binding.rfq_gemm_split(c, s, None, None, c, s, None),
+        lambda: binding.rfq_gemm_split_noalloc(c, s, None, None, c, s),
     ]
     for call in calls:
         with pytest.raises(ValueError, match="device tensor"):
@@ -393,6 +406,7 @@ def test_valid_arguments_without_a_gpu_report_device_error():
     assert _lib().rfq_hif4_gemm(A, A, A, A, A, A, 8, 8, 64, A, 0, None) == EDEVICE
     assert _lib().rfq_mfma_fp4_loop(4, 1, A, None) == EDEVICE
     assert _lib().rfq_gemm_split(A, A, A, A, A, A, 8, 8, 512, A, 0, A, 64, None) == EDEVICE
+    assert _lib().rfq_gemm_split_noalloc(A, A, A, A, A, A, 8, 8, 512, A, 0, None) == EDEVICE
     # The HiF4 product's launch-size limit sits at the largest grid it may
     # launch: 128-row tiles of 256 weight rows with 768 work items or of 128
     # weight rows with 640, whichever the dispatch picks (N = 256: two

@@ -1,0 +1,55 @@
+"""The allocation-free split product (rfq_gemm_split_noalloc), called through
+the C ABI, against rfq_gemm_split with a caller-owned workspace: the same
+split plan on the same codes must give the same bits.  Two calls in a row on
+the shared static scratch array, the second with a smaller input (its
+partials overwrite only part of what the first left there)."""
+import ctypes
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2608_26581_amd as rfq
+from paper_2608_26581_amd import workloads as wl
+from gpu_util import dev, x_device
+
+pytestmark = pytest.mark.gpu
+
+P, I64, I32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
+
+
+def _lib():
+    lib = ctypes.CDLL(rfq.LIB_PATH)
+    lib.rfq_gemm_split_noalloc.argtypes = [P, P, P, P, P, P, I64, I64, I64, P, I32, P]
+    lib.rfq_gemm_split_noalloc.restype = I32
+    return lib
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+@pytest.mark.parametrize("residual", [True, False])
+def test_noalloc_split_matches_workspace_split(residual):
+    lib = _lib()
+    # 16 MiB of partials (4 parts), then 0.6 MiB (4 parts).
+    for (M, N, K) in [(256, 4096, 12288), (129, 300, 8192)]:
+        print("noalloc split M=%d N=%d K=%d residual=%s" % (M, N, K, residual), flush=True)
+        w = wl.WORKLOADS["qwen"].scaled(M=M, K=K, weights=(("w", K, N),))
+        data = wl.generate(w, seed=M + K)
+        q = rfq.rfq_quantize_act(x_device(data), residual=residual)
+        wq = rfq.rfq_quantize_weight(dev(data["w"]))
+        nbytes = rfq.rfq_gemm_workspace_bytes(M, N, K)
+        assert 0 < nbytes <= 32 << 20
+        ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        for dt, code in ((torch.float32, 0), (torch.bfloat16, 1)):
+            ref = rfq.rfq_gemm_split(*q, *wq, ws, out_dtype=dt)
+            z = torch.full((M, N), float("nan"), dtype=dt, device="cuda")
+            st = lib.rfq_gemm_split_noalloc(_ptr(q[0]), _ptr(q[1]), _ptr(q[2]), _ptr(q[3]),
+                                            _ptr(wq[0]), _ptr(wq[1]), M, N, K, _ptr(z), code,
+                                            torch.cuda.current_stream().cuda_stream)
+            assert st == 0, rfq.rfq_status_str(st)
+            torch.cuda.synchronize()
+            a = z.view(torch.int16 if dt == torch.bfloat16 else torch.int32)
+            b = ref.view(torch.int16 if dt == torch.bfloat16 else torch.int32)
+            assert torch.equal(a, b), (M, N, K, dt)
