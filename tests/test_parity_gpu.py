@@ -951,6 +951,48 @@ def test_path_replays_from_a_hip_graph(M, N, K):
         assert torch.equal(a, b), "replay with new inputs differs from the eager result"
 
 
+def test_split_products_replay_from_a_hip_graph():
+    """The split product with a caller-owned workspace and the allocation-free
+    one on the static scratch array capture into one HIP graph (two kernels
+    each, nothing allocated or cleared inside the calls); every replay
+    reproduces the eager results, and both give the same bits."""
+    M, N, K = 130, 300, 8192
+    gen = torch.Generator(device="cuda").manual_seed(5)
+    x = torch.randn((M, K), generator=gen, device="cuda").to(torch.bfloat16)
+    w = rfq.rfq_quantize_weight(torch.randn((N, K), generator=gen, device="cuda") * 0.02)
+    q = rfq.rfq_quantize_act(x)
+    ws = torch.empty(rfq.rfq_gemm_workspace_bytes(M, N, K), dtype=torch.uint8, device="cuda")
+    assert ws.numel() > 0
+    za = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    zb = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+
+    def path():
+        rfq.rfq_quantize_act(x, out=q)
+        rfq.rfq_gemm_split(*q, *w, ws, out=za)
+        rfq.rfq_gemm_split_noalloc(*q, *w, out=zb)
+
+    path()
+    torch.cuda.synchronize()
+    want = [za.clone(), zb.clone()]
+    assert torch.equal(want[0].view(torch.int16), want[1].view(torch.int16))
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        path()
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        path()
+    _say("graph replay split M=%d N=%d K=%d" % (M, N, K))
+    for i in range(4):
+        za.zero_()
+        zb.zero_()
+        rfq.rfq_gemm(*q, *w, out=torch.empty_like(za))     # eager work between replays
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(za, want[0]) and torch.equal(zb, want[1]), "replay %d" % i
+
+
 def test_hif4_path_replays_from_a_hip_graph():
     """The HiF4 quantizer, product and bf16-weight product capture into a HIP
     graph; every replay (eager work between) reproduces the eager results."""
