@@ -520,132 +520,169 @@ __global__ __launch_bounds__((HSmem<RES, BN>::kThreads)) void hif4_gemm_kernel(
 // ---------------------------------------------------------------- few rows
 //
 // Product for at most 16 activation rows (decode): one workgroup per 16 or
-// 32 weight rows; its 4 waves take interleaved K blocks (wave w: blocks w, w+4,
-// ...), decode the block's weight rows and activation rows into a
-// wave-private LDS area (no workgroup barrier in the loop: LDS serves one
-// wave's accesses in order) and run v_mfma_f32_16x16x32_bf16 with the weights
-// as the first operand; the four partial sums are added in wave order at the
-// end.  Lane l of a 16x16x32 operand holds row l mod 16 and 8 consecutive K
-// values (chunk l / 16 of the 32-value half); the result in lane l is Z[m = l
-// mod 16][n = 4 (l / 16) .. +3] of the fragment.  Only activation rows below
-// M are decoded; the other rows of the area are never written and only feed
-// result columns m >= M, which are not stored.
+// 32 weight rows (F = 1 or 2 fragments of 16) and up to MAXM activation
+// rows; its WAVES waves take interleaved chunks of 128 K values (wave w:
+// chunks w, w + WAVES, ...) and run v_mfma_f32_16x16x32_bf16 with the
+// weights as the first operand; the partial sums are added in wave order at
+// the end.
+//
+// Weights go straight from memory into operand registers: lane l (row
+// l mod 16 of a fragment, quarter g = l / 16) loads the 16 code bytes of
+// elements 32 g .. 32 g + 31 of its row's chunk (half g mod 2 of block
+// 2 c + g / 2, one metadata word) and decodes them into four 8-element
+// operand pieces; MFMA jj of the chunk takes piece jj from every lane, so
+// it contracts elements 32 g + 8 jj + (0..7) over the four quarters - a
+// fixed permutation of the chunk's K values inside the instruction, which
+// the activation operand follows.  The activation rows below M (primary and
+// residual) are decoded, one code word per work item, into a wave-private
+// LDS area in the same order (16-byte pieces XOR-swizzled by row), from
+// which lane l reads row l mod 16; rows at or above M are never written and
+// only feed result columns m >= M, which are not stored.  Loads use buffer
+// descriptors based at the workgroup's first weight row (32-bit offsets);
+// K values past K (a final half chunk) load as zeros, without memory access.
 constexpr int kFewRows = 16;
 constexpr int kFewN = 32;                   // weight rows per workgroup (at most)
-constexpr int kFewWaves = 4;
+constexpr int kFewChunk = 128;              // K values per chunk
+constexpr uint32_t kFewSkip = 0x80000000u;  // load offset past every buffer: zeros
+// Per wave: 16 primary and 16 residual activation rows of one chunk, bf16.
+constexpr int kFewXRow = kFewChunk * 2;     // bytes of one decoded row chunk
 
-struct alignas(16) FewArea {
-  uint8_t w[kFewN * kRowBytes];             // up to 32 weight rows of one K block
-  uint8_t x[2 * kFewRows * kRowBytes];      // primary rows 0..15, residual 16..31
-};
+__device__ __forceinline__ int few_xoff(int row, int piece) {
+  return row * kFewXRow + 16 * (piece ^ (row & 15));
+}
 
-// NR weight rows per workgroup: 16 for up to 4 activation rows (twice the
-// workgroups, for latency hiding, where activation decoding costs little),
-// else 32.
-template <bool RES, bool ZBF16, bool WBF16, int NR>
-__global__ __launch_bounds__(kFewWaves * 64) void hif4_gemm_few_kernel(
+// The largest K the few-row kernel takes: its buffer ranges and offsets,
+// for 32 weight rows of bf16 values (2^30 bytes), stay below the skip offset.
+constexpr int64_t kFewMaxK = int64_t(1) << 24;
+
+template <bool RES, bool ZBF16, bool WBF16, int NR, int MAXM, int WAVES>
+__global__ __launch_bounds__(WAVES * 64) void hif4_gemm_few_kernel(
     const uint8_t *__restrict__ qc, const uint32_t *__restrict__ qm,
     const uint8_t *__restrict__ rc, const uint32_t *__restrict__ rm,
     const uint8_t *__restrict__ wc, const uint32_t *__restrict__ wm,
     const uint16_t *__restrict__ wv, int64_t M, int64_t N, int64_t K, void *__restrict__ z) {
-  __shared__ FewArea area[kFewWaves];
-  __shared__ v4f part[kFewWaves][2][64];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   static_assert(NR == 16 || NR == 32, "weight rows per workgroup");
+  constexpr int F = NR / 16, kFewWaves = WAVES;
+  __shared__ __attribute__((aligned(16))) uint8_t xarea[kFewWaves][2 * kFewRows * kFewXRow];
+  __shared__ v4f part[kFewWaves][F][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r = lane & 15, g = lane >> 4;
   const int64_t n0 = (int64_t)blockIdx.x * NR;
   const int64_t kbytes = K / 2, kblocks = K / kH;
-
-  // Work items are code words (8 elements, one LDS chunk): 256 per K block
-  // for the NR weight rows (lane l takes words l + 64 i, i < NR / 8: row
-  // (l + 64 i) / 8, word l mod 8), and 8 per activation row for the
-  // 2M activation rows (words l + 64 i below 16 M), so a lane decodes NR / 8
-  // weight words and at most four activation words, and with few rows most
-  // lanes decode no activation word at all.
-  constexpr int kWI = NR / 8, kXI = 4;
-  const int dw = lane & 7;
-  const uint8_t *wsrc[kWI];
-  const uint32_t *wmsrc[kWI];
-  const u32x4 *wvsrc[kWI];
-  int wlrow[kWI];
-#pragma unroll
-  for (int i = 0; i < kWI; ++i) {
-    const int r = (lane >> 3) + 8 * i;
-    wlrow[i] = r;
-    const int64_t g = min(n0 + r, N - 1);
-    wsrc[i] = WBF16 ? nullptr : wc + g * kbytes + 4 * dw;
-    wmsrc[i] = WBF16 ? nullptr : wm + g * kblocks;
-    wvsrc[i] = WBF16 ? reinterpret_cast<const u32x4 *>(wv + g * K + 8 * dw) : nullptr;
-  }
-  const int nx = (RES ? 2 : 1) * (int)M * 8;              // activation words per block
-  const uint8_t *xsrc[kXI];
-  const uint32_t *xmsrc[kXI];
-  int xlrow[kXI];
-#pragma unroll
-  for (int i = 0; i < kXI; ++i) {
-    const int t = lane + 64 * i;
-    const int j = t >> 3;                                   // activation row index
-    const bool on = t < nx;
-    const bool is_r = RES && j >= M;
-    const int64_t g = on ? (is_r ? j - M : j) : 0;
-    xlrow[i] = is_r ? kFewRows + (j - (int)M) : j;
-    xsrc[i] = (is_r ? rc : qc) + g * kbytes + 4 * dw;
-    xmsrc[i] = (is_r ? rm : qm) + g * kblocks;
-  }
-
-  FewArea &A = area[wave];
-  const int frow = lane & 15, fch = lane >> 4;
-  v4f acc[2] = {v4f{0.f, 0.f, 0.f, 0.f}, v4f{0.f, 0.f, 0.f, 0.f}};
-  // The words of a wave's next K block are loaded while the current one is
-  // decoded and multiplied.
-  struct Words {
-    u32x4 v[WBF16 ? kWI : 1];
-    uint32_t c[kWI], m[kWI], xc[kXI], xm[kXI];
+  const int nchunks = (int)((K + kFewChunk - 1) / kFewChunk);
+  // Rows of this workgroup's buffers: NR weight rows from n0 (clamped to N).
+  const int64_t nrows = min<int64_t>(NR, N - n0);
+  auto rsrc = [](const void *p, int64_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)bytes,
+                                             0x00020000);
   };
-  Words cur, nxt;
-  auto load = [&](int64_t b, Words &o) {
+  const __amdgpu_buffer_rsrc_t bw =
+      WBF16 ? rsrc(wv + n0 * K, nrows * K * 2) : rsrc(wc + n0 * kbytes, nrows * kbytes);
+  const __amdgpu_buffer_rsrc_t bwm = rsrc(WBF16 ? nullptr : wm + n0 * kblocks, nrows * kblocks * 4);
+  uint32_t w_off[F], wm_off[F];
 #pragma unroll
-    for (int i = 0; i < kWI; ++i) {
+  for (int f = 0; f < F; ++f) {
+    const int64_t lr = min<int64_t>(16 * f + r, nrows - 1);
+    w_off[f] = WBF16 ? (uint32_t)(lr * K * 2 + 64 * g) : (uint32_t)(lr * kbytes + 16 * g);
+    wm_off[f] = (uint32_t)(lr * kblocks + (g >> 1)) * 4u;
+  }
+
+  // Activation work items: code word w (0..15) of row j of the chunk, j <
+  // M primary rows then M residual rows (M <= MAXM); lane l takes items
+  // l + 64 i.
+  constexpr int kXI = (RES ? 2 : 1) * MAXM * 16 / 64;
+  const int nx = (RES ? 2 : 1) * (int)M * 16;
+  const __amdgpu_buffer_rsrc_t bq = rsrc(qc, M * kbytes), br = rsrc(RES ? rc : qc, M * kbytes);
+  const __amdgpu_buffer_rsrc_t bqm = rsrc(qm, M * kblocks * 4),
+                               brm = rsrc(RES ? rm : qm, M * kblocks * 4);
+  // Item i of this lane: residual or primary, its activation row and word.
+  struct XItem {
+    bool res;
+    int row, w;
+  };
+  auto xitem = [&](int i) {
+    const int t = lane + 64 * i, j = t >> 4;
+    const bool is_r = RES && j >= (int)M;
+    return XItem{is_r, is_r ? j - (int)M : j, t & 15};
+  };
+
+  struct Chunk {
+    u32x4 w[F][WBF16 ? 4 : 1];
+    uint32_t m[F], xc[kXI], xm[kXI];
+  };
+  auto load = [&](int c, Chunk &o) {
+    // Quarter g of chunk c exists when 128 c + 32 g < K (K is a multiple of 64).
+    const bool live = (int64_t)kFewChunk * c + 32 * g < K;
+#pragma unroll
+    for (int f = 0; f < F; ++f) {
       if constexpr (WBF16) {
-        o.v[i] = wvsrc[i][b * 8];
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj)
+          o.w[f][jj] = __builtin_amdgcn_raw_buffer_load_b128(
+              bw, live ? w_off[f] + 16 * jj : kFewSkip, kFewChunk * 2 * c, 0);
       } else {
-        o.c[i] = *reinterpret_cast<const uint32_t *>(wsrc[i] + b * 32);
-        o.m[i] = wmsrc[i][b];
+        o.w[f][0] = __builtin_amdgcn_raw_buffer_load_b128(bw, live ? w_off[f] : kFewSkip,
+                                                          (kFewChunk / 2) * c, 0);
+        o.m[f] = __builtin_amdgcn_raw_buffer_load_b32(bwm, live ? wm_off[f] : kFewSkip, 8 * c, 0);
       }
     }
 #pragma unroll
     for (int i = 0; i < kXI; ++i) {
       if (lane + 64 * i < nx) {
-        o.xc[i] = *reinterpret_cast<const uint32_t *>(xsrc[i] + b * 32);
-        o.xm[i] = xmsrc[i][b];
+        const XItem it = xitem(i);
+        const bool xl = (int64_t)kFewChunk * c + 8 * it.w < K;
+        const uint32_t off = (uint32_t)it.row * (uint32_t)kbytes + 4 * it.w;
+        const uint32_t moff = ((uint32_t)it.row * (uint32_t)kblocks + (it.w >> 3)) * 4u;
+        o.xc[i] = __builtin_amdgcn_raw_buffer_load_b32(it.res ? br : bq, xl ? off : kFewSkip,
+                                                       (kFewChunk / 2) * c, 0);
+        o.xm[i] = __builtin_amdgcn_raw_buffer_load_b32(it.res ? brm : bqm, xl ? moff : kFewSkip,
+                                                       8 * c, 0);
       }
     }
   };
-  if (wave < kblocks) load(wave, cur);
-  for (int64_t b = wave; b < kblocks; b += kFewWaves) {
-    if (b + kFewWaves < kblocks) load(b + kFewWaves, nxt);
+
+  uint8_t *X = xarea[wave];
+  v4f acc[F];
 #pragma unroll
-    for (int i = 0; i < kWI; ++i) {
-      u32x4 v;
-      if constexpr (WBF16) v = cur.v[i];
-      else v = decode8_bf16(cur.c[i], cur.m[i], dw);
-      *reinterpret_cast<u32x4 *>(A.w + hswz(wlrow[i], dw)) = v;
+  for (int f = 0; f < F; ++f) acc[f] = v4f{0.f, 0.f, 0.f, 0.f};
+  Chunk cur, nxt;
+  if (wave < nchunks) load(wave, cur);
+  for (int c = wave; c < nchunks; c += kFewWaves) {
+    if (c + kFewWaves < nchunks) load(c + kFewWaves, nxt);
+    // Activation rows into the wave's LDS area.
+#pragma unroll
+    for (int i = 0; i < kXI; ++i) {
+      if (lane + 64 * i < nx) {
+        const XItem it = xitem(i);
+        *reinterpret_cast<u32x4 *>(X + few_xoff(it.res ? kFewRows + it.row : it.row, it.w)) =
+            decode8_bf16(cur.xc[i], cur.xm[i], it.w & 7);
+      }
     }
+    // Weight pieces in registers.
+    u32x4 wp[F][4];
 #pragma unroll
-    for (int i = 0; i < kXI; ++i)
-      if (lane + 64 * i < nx)
-        *reinterpret_cast<u32x4 *>(A.x + hswz(xlrow[i], dw)) = decode8_bf16(cur.xc[i], cur.xm[i], dw);
+    for (int f = 0; f < F; ++f) {
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        if constexpr (WBF16) {
+          wp[f][jj] = cur.w[f][jj];
+        } else {
+          const uint32_t words[4] = {cur.w[f][0].x, cur.w[f][0].y, cur.w[f][0].z, cur.w[f][0].w};
+          wp[f][jj] = decode8_bf16(words[jj], cur.m[f], 4 * (g & 1) + jj);
+        }
+      }
+    }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #pragma unroll
-    for (int sub = 0; sub < 2; ++sub) {
-      const int ch = 4 * sub + fch;
-      const v8bf xq = *reinterpret_cast<const v8bf *>(A.x + hswz(frow, ch));
+    for (int jj = 0; jj < 4; ++jj) {
+      const v8bf xq = *reinterpret_cast<const v8bf *>(X + few_xoff(r, 4 * g + jj));
       v8bf xr = xq;
-      if constexpr (RES) xr = *reinterpret_cast<const v8bf *>(A.x + hswz(kFewRows + frow, ch));
+      if constexpr (RES) xr = *reinterpret_cast<const v8bf *>(X + few_xoff(kFewRows + r, 4 * g + jj));
 #pragma unroll
-      for (int f = 0; f < NR / 16; ++f) {
-        const v8bf wf = *reinterpret_cast<const v8bf *>(A.w + hswz(16 * f + frow, ch));
+      for (int f = 0; f < F; ++f) {
+        const v8bf wf = __builtin_bit_cast(v8bf, wp[f][jj]);
         acc[f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, xq, acc[f], 0, 0, 0);
         if constexpr (RES) acc[f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, xr, acc[f], 0, 0, 0);
       }
@@ -655,19 +692,19 @@ __global__ __launch_bounds__(kFewWaves * 64) void hif4_gemm_few_kernel(
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     cur = nxt;
   }
-  part[wave][0][lane] = acc[0];
-  part[wave][1][lane] = acc[1];
+#pragma unroll
+  for (int f = 0; f < F; ++f) part[wave][f][lane] = acc[f];
   __syncthreads();
   if (wave != 0) return;
-  const int64_t m = frow;
+  const int64_t m = r;
   if (m >= M) return;
   const bool vec_ok = (N & 3) == 0;
 #pragma unroll
-  for (int f = 0; f < NR / 16; ++f) {
+  for (int f = 0; f < F; ++f) {
     v4f t = part[0][f][lane];
 #pragma unroll
     for (int w = 1; w < kFewWaves; ++w) t += part[w][f][lane];
-    const int64_t n = n0 + 16 * f + 4 * fch;
+    const int64_t n = n0 + 16 * f + 4 * g;
     if constexpr (ZBF16) {
       uint16_t *zp = reinterpret_cast<uint16_t *>(z) + m * N + n;
       if (vec_ok && n + 3 < N) {
@@ -717,15 +754,24 @@ hipError_t launch_hg(const uint8_t *qc, const uint32_t *qm, const uint8_t *rc,
                      const uint32_t *rm, const uint8_t *wc, const uint32_t *wm,
                      const uint16_t *wv, int64_t M, int64_t N, int64_t K, void *z,
                      hipStream_t stream) {
-  if (M <= kFewRows && (N + 15) / 16 <= int64_t(UINT32_MAX / (kFewWaves * 64))) {
+  if (M <= kFewRows && K <= kFewMaxK && (N + 15) / 16 <= int64_t(UINT32_MAX / 512)) {
+#define RFQ_FEW(NR, MAXM, W)                                                                  \
+  hif4_gemm_few_kernel<RES, ZBF16, WBF16, NR, MAXM, W>                                        \
+      <<<dim3((unsigned)((N + NR - 1) / NR)), dim3(W * 64), 0, stream>>>(qc, qm, rc, rm, wc, wm, \
+                                                                        wv, M, N, K, z)
+    // Up to 8 activation rows: 16 weight rows and 8 waves per workgroup.
+    // Above: 32 weight rows (the activation decode, repeated by every
+    // workgroup, is then spread over twice the weight rows), 8 waves while
+    // that leaves fewer than 1536 waves in the grid, else 4.
     if (M <= 4)
-      hif4_gemm_few_kernel<RES, ZBF16, WBF16, 16>
-          <<<dim3((unsigned)((N + 15) / 16)), dim3(kFewWaves * 64), 0, stream>>>(
-              qc, qm, rc, rm, wc, wm, wv, M, N, K, z);
+      RFQ_FEW(16, 4, 8);
+    else if (M <= 8)
+      RFQ_FEW(16, 8, 8);
+    else if ((N + 31) / 32 < 384)
+      RFQ_FEW(32, 16, 8);
     else
-      hif4_gemm_few_kernel<RES, ZBF16, WBF16, kFewN>
-          <<<dim3((unsigned)((N + kFewN - 1) / kFewN)), dim3(kFewWaves * 64), 0, stream>>>(
-              qc, qm, rc, rm, wc, wm, wv, M, N, K, z);
+      RFQ_FEW(32, 16, 4);
+#undef RFQ_FEW
     return hipGetLastError();
   }
   if (((M + kBM - 1) / kBM) * ((N + 255) / 256) < kFillTiles)

@@ -266,7 +266,11 @@ def test_gemm_wbf16_any_bf16_weight(orc):
     assert_gemm_close(z, zr, bound, False, "hif4 wbf16")
 
 
-FEW_SHAPES = [(1, 1, 64), (2, 33, 192), (5, 300, 640), (16, 700, 1024), (3, 64, 128)]
+# Up to 4 and up to 8 rows (16 weight rows and 8 waves per workgroup), 9-16
+# rows with 8 waves (few workgroups) and with 4 (N above 12256); K ending in
+# half a chunk of 128 (64, 192, 576, 4160) and fewer chunks than waves.
+FEW_SHAPES = [(1, 1, 64), (2, 33, 192), (5, 300, 640), (16, 700, 1024), (3, 64, 128),
+              (8, 257, 4160), (9, 12300, 576)]
 
 
 @pytest.mark.parametrize("M,N,K", FEW_SHAPES)
@@ -274,8 +278,8 @@ FEW_SHAPES = [(1, 1, 64), (2, 33, 192), (5, 300, 640), (16, 700, 1024), (3, 64, 
 @pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
 def test_gemm_few_rows_matches_oracle(orc, M, N, K, residual, out_dtype):
     """At most 16 activation rows run the few-row kernel (K split over four
-    waves, partial sums added in wave order); fewer K blocks than waves
-    included.  The bf16-weight form is bit-identical to it."""
+    or eight waves, partial sums added in wave order); fewer K chunks than
+    waves included.  The bf16-weight form is bit-identical to it."""
     _say("hif4 few rows %dx%dx%d residual=%s %s" % (M, N, K, residual, out_dtype))
     w = wl.WORKLOADS["tiny"].scaled(M=M, K=K, weights=(("w", K, N),))
     data = wl.generate(w, seed=M * 13 + N + K)
