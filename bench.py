@@ -60,7 +60,7 @@ def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: the RFQ path is data parallel over "
-              "tokens and this build runs and reports a single MI355X "
+              "tokens and this benchmark runs and reports a single MI355X "
               "(got --gpus %d)." % args.gpus, file=sys.stderr)
         sys.exit(2)
 

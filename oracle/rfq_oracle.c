@@ -25,7 +25,7 @@
  *     indicator phi fixed to 1 (every block carries a residual), 0 (plain
  *     MXFP4), or given per activation tile of ORACLE_PHI_ROWS rows by
  *     ORACLE_PHI_K reduction columns (Algorithm 1 takes phi(p, r) as an input
- *     over blocks of P_s x R_s; these are the tile sizes of this build).
+ *     over blocks of P_s x R_s; these are the library's tile sizes).
  *   - Two rules that produce such a phi map (the paper states none): phi = 1
  *     where a tile's residual codes are not all zero (the residual term of
  *     the other tiles is exactly zero), or where a tile holds a primary scale

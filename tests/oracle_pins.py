@@ -16,7 +16,7 @@ Sources of truth used here:
     half-error bound of the second stage);
   * closed forms for the SwiGLU intermediate and bf16 rounding;
   * HiF4 (Sec. 3.3): the decode of Eq. 6 worked by hand and implemented
-    here independently; the encoder is this build's reading (parity
+    here independently; the encoder is the library's reading (parity
     unpinned) and is pinned by its defining properties (smallest macro scale
     with no saturation, smallest non-saturating micro-exponents under the
     shared 8-element bit, nearest element with ties to even) checked by
@@ -574,7 +574,7 @@ def pin_hif4_golden_decode(o):
 
 
 def pin_hif4_golden_encode(o):
-    """H7: one block encoded by hand under this build's reading."""
+    """H7: one block encoded by hand under the library's reading."""
     g, meta, codes, want = _hif4_golden(o, "h7_hif4_encode.txt")
     x = padded_floats(g["x"], 64).reshape(1, 64)
     qc, qm, _, _ = o.hif4_quantize(x, residual=False)
