@@ -539,11 +539,12 @@ def secondary(torch, rfq, wl, x, w, stream):
         "stages": "quantize X; RFQ gate/up product (N=24576) with SwiGLU + RFQ quantize "
                   "in its epilogue; RFQ down product; bf16 output"}
 
-    # Prefill-sized token counts through the block's products: the gate
-    # product (12288 x 4096 weights; 128-wide tiles) and the down product
-    # (4096 x 12288 weights), the latter with K unsplit (rfq_gemm) and split
-    # over workgroups (rfq_gemm_split).
-    for mp in (256, 512):
+    # Batched-decode and prefill-sized token counts through the block's
+    # products: the gate product (12288 x 4096 weights; few-row kernel at 64
+    # rows, 128-wide tiles above) and the down product (4096 x 12288
+    # weights), the latter with K unsplit (rfq_gemm) and split over
+    # workgroups (rfq_gemm_split).
+    for mp in (64, 256, 512):
         qp = [t[:mp] for t in q]
         hp = [t[:mp] for t in h]
         gp = torch.empty((mp, Nh), dtype=torch.bfloat16, device=dev)

@@ -764,19 +764,21 @@ hipError_t launch_split(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc,
   return hipGetLastError();
 }
 
-// Parts of K for the split product (1: no split): only for K >= 8192 and at
-// most 192 tiles of 128 x 128, 256 / tiles parts up to 128 tiles and
-// 512 / tiles above, at most 4 (parts x tiles <= 512, so the partials take
-// at most 32 MiB).  Measured against the unsplit 128-wide tiles (random
-// codes, bf16 Z): 129 rows x 4096 x 12288 60.3 -> 23.9 us (4 parts); 256
-// rows 61.9 -> 28.5 (4); 512 rows 63.2 -> 44.3 (2); 768 rows 64.2 -> 63.5
-// (2); 129 and 256 rows x 5120 x 13824 69.6 -> 30.3 and 71.8 -> 34.2 (3);
-// 512 rows 72.5 -> 57.5 (3).  With K = 4096 at 12288 columns the partial
-// sums cost more than the split saves (21.3 -> 25.5 us with 2 parts).
+// Parts of K for the split product (1: no split), so that the parts x tiles
+// workgroups fill the 256 CUs about once: 256 / tiles parts (at most 8) up to
+// 128 tiles of 128 x 128, and for K >= 8192 512 / tiles (at most 4) up to
+// 192 tiles; parts x tiles <= 512, so the partials take at most 32 MiB.
+// Measured against the unsplit 128-wide tiles (random codes, bf16 Z): 64
+// rows x 4096 x 12288 64.7 -> 18.5 us (8 parts); 129 rows 60.3 -> 23.9 (4);
+// 256 rows 61.9 -> 28.5 (4); 512 rows 63.2 -> 44.3 (2); 64 rows x 5120 x
+// 13824 80.9 -> 24.6 (6); 512 rows 72.5 -> 57.5 (3); 128 rows x 12288 x
+// 4096 25.7 -> 22.1 (2).  With K = 4096 and 192 tiles (129 rows x 12288)
+// two parts cost more than they save (21.3 -> 25.5 us).
 int splitk_default_parts(int64_t M, int64_t N, int64_t K) {
   const int64_t tiles = ((M + Mid::kBM - 1) / Mid::kBM) * ((N + Mid::kBN - 1) / Mid::kBN);
-  if (K < 8192 || tiles > 192) return 1;
-  return (int)std::min<int64_t>(4, (tiles <= 128 ? 256 : 512) / tiles);
+  if (tiles <= 128) return (int)std::min<int64_t>(8, 256 / tiles);
+  if (tiles <= 192 && K >= 8192) return (int)std::min<int64_t>(4, 512 / tiles);
+  return 1;
 }
 
 // 128 x 128 tiles while they number fewer than two per CU of the 256 (up to

@@ -332,10 +332,12 @@ def test_gemm_split_validation_and_workspace_sizes():
     w = _lib().rfq_gemm_workspace_bytes
     assert w(129, 4096, 12288) == 4 * 129 * 4096 * 4       # 64 tiles: 4 parts
     assert w(512, 4096, 12288) == 2 * 512 * 4096 * 4       # 128 tiles: 2 parts
-    assert w(512, 5120, 13824) == 3 * 512 * 5120 * 4       # 160 tiles: 3 parts
+    assert w(512, 5120, 13824) == 3 * 512 * 5120 * 4       # 160 tiles, K >= 8192: 3 parts
+    assert w(64, 4096, 12288) == 8 * 64 * 4096 * 4         # 32 tiles: 8 parts
+    assert w(100, 12288, 4096) == 2 * 100 * 12288 * 4      # 96 tiles: 2 parts
     assert w(1024, 4096, 12288) == 0                       # 256 tiles
-    assert w(129, 12288, 4096) == 0                        # K below 8192
-    assert w(64, 4096, 12288) == 0                         # few-row kernel
+    assert w(129, 12288, 4096) == 0                        # 192 tiles, K below 8192
+    assert w(32, 4096, 12288) == 0                         # few-row kernel
     assert w(129, 4096, 12300) == 0                        # K not a multiple of 512
     assert w(-1, 4096, 12288) == 0 and w(129, 4096, 100) == 0
 

@@ -421,9 +421,11 @@ def test_gemm_mid_rows_full_width(orc, M, N, K):
     assert_gemm_close(zbf[rows, cols], zr, bound, True, "mid rows bf16")
 
 
-# K = 8192 (4 parts of 2048), 8704 (parts of 2560 and a last one of 1024),
-# 9216 at a ragged shape; M x N not a multiple of 4 for the scalar sum.
-SPLIT = [(130, 300, 8192), (131, 301, 8704), (200, 257, 9216)]
+# 6 tiles of 128 x 128 or fewer: 8 parts; K = 8192 (8 parts of 1024), 8704
+# (parts of 1536 and a last one of 1024), 9216 at a ragged shape, 2560 (5
+# parts of 512) with 40 rows (past the few-row kernel's range in the split
+# product); M x N not a multiple of 4 for the scalar sum.
+SPLIT = [(130, 300, 8192), (131, 301, 8704), (200, 257, 9216), (40, 300, 2560)]
 
 
 @pytest.mark.parametrize("M,N,K", SPLIT)
@@ -449,11 +451,12 @@ def test_gemm_split_matches_oracle(orc, M, N, K, residual, out_dtype):
     assert torch.equal(_gemm_bits(short), _gemm_bits(rfq.rfq_gemm(*q, *w, out_dtype=out_dtype)))
 
 
-@pytest.mark.parametrize("M,N,K", [(256, 4096, 12288), (129, 5120, 13824), (100, 12288, 12288)])
+@pytest.mark.parametrize("M,N,K", [(256, 4096, 12288), (129, 5120, 13824), (100, 12288, 12288),
+                                   (64, 4096, 12288), (100, 12288, 4096)])
 def test_gemm_split_full_width(orc, M, N, K):
-    """Down-projection shapes with few activation rows (K split in 4, 3 and
-    2 parts), sampled in every 64 x 64 output tile plus the last row and
-    column in full."""
+    """Down-projection and wide shapes with few activation rows (K split in
+    4, 3, 2, 8 and 2 parts), sampled in every 64 x 64 output tile plus the
+    last row and column in full."""
     data = _gemm_case("qwen", M, N, K, seed=M + 5)
     _say("gemm split full M=%d N=%d K=%d" % (M, N, K))
     q = rfq.rfq_quantize_act(x_device(data))
