@@ -874,6 +874,27 @@ def test_codes_beyond_4gib(orc):
     assert_gemm_close(zr_rows, zr, bound, False, "beyond 4 GiB product")
 
 
+def test_gemm_split_long_k(orc):
+    """The split product over a long reduction: K = 2^20 in 8 parts of 2^17
+    (1024 stages each), every output against the oracle, and against the
+    unsplit product within the same tolerance."""
+    M, N, K = 33, 40, 1 << 20
+    gen = torch.Generator(device="cuda").manual_seed(21)
+    x = torch.randn((M, K), generator=gen, device="cuda").to(torch.bfloat16)
+    wt = torch.randn((N, K), generator=gen, device="cuda") * 0.02
+    q = rfq.rfq_quantize_act(x)
+    w = rfq.rfq_quantize_weight(wt)
+    nbytes = rfq.rfq_gemm_workspace_bytes(M, N, K)
+    assert nbytes == 8 * M * N * 4
+    _say("gemm split long K: M=%d N=%d K=%d" % (M, N, K))
+    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    z = host(rfq.rfq_gemm_split(*q, *w, ws))
+    zu = host(rfq.rfq_gemm(*q, *w))
+    zr, bound = orc.gemm(*[host(t) for t in q], host(w[0]), host(w[1]))
+    assert_gemm_close(z, zr, bound, False, "split long K")
+    assert_gemm_close(zu, zr, bound, False, "unsplit long K")
+
+
 def test_empty_inputs_are_noops():
     x = torch.empty((0, 64), dtype=torch.bfloat16, device="cuda")
     q = rfq.rfq_quantize_act(x)
