@@ -541,7 +541,6 @@ __global__ __launch_bounds__((HSmem<RES, BN>::kThreads)) void hif4_gemm_kernel(
 // descriptors based at the workgroup's first weight row (32-bit offsets);
 // K values past K (a final half chunk) load as zeros, without memory access.
 constexpr int kFewRows = 16;
-constexpr int kFewN = 32;                   // weight rows per workgroup (at most)
 constexpr int kFewChunk = 128;              // K values per chunk
 constexpr uint32_t kFewSkip = 0x80000000u;  // load offset past every buffer: zeros
 // Per wave: 16 primary and 16 residual activation rows of one chunk, bf16.
@@ -552,7 +551,8 @@ __device__ __forceinline__ int few_xoff(int row, int piece) {
 }
 
 // The largest K the few-row kernel takes: its buffer ranges and offsets,
-// for 32 weight rows of bf16 values (2^30 bytes), stay below the skip offset.
+// for 32 weight rows of bf16 values (2^30 bytes) or 64 of codes (2^29),
+// stay below the skip offset.
 constexpr int64_t kFewMaxK = int64_t(1) << 24;
 
 template <bool RES, bool ZBF16, bool WBF16, int NR, int MAXM, int WAVES>
@@ -561,7 +561,7 @@ __global__ __launch_bounds__(WAVES * 64) void hif4_gemm_few_kernel(
     const uint8_t *__restrict__ rc, const uint32_t *__restrict__ rm,
     const uint8_t *__restrict__ wc, const uint32_t *__restrict__ wm,
     const uint16_t *__restrict__ wv, int64_t M, int64_t N, int64_t K, void *__restrict__ z) {
-  static_assert(NR == 16 || NR == 32, "weight rows per workgroup");
+  static_assert(NR == 16 || NR == 32 || NR == 64, "weight rows per workgroup");
   constexpr int F = NR / 16, kFewWaves = WAVES;
   __shared__ __attribute__((aligned(16))) uint8_t xarea[kFewWaves][2 * kFewRows * kFewXRow];
   __shared__ v4f part[kFewWaves][F][64];
@@ -759,18 +759,29 @@ hipError_t launch_hg(const uint8_t *qc, const uint32_t *qm, const uint8_t *rc,
   hif4_gemm_few_kernel<RES, ZBF16, WBF16, NR, MAXM, W>                                        \
       <<<dim3((unsigned)((N + NR - 1) / NR)), dim3(W * 64), 0, stream>>>(qc, qm, rc, rm, wc, wm, \
                                                                         wv, M, N, K, z)
-    // Up to 8 activation rows: 16 weight rows and 8 waves per workgroup.
-    // Above: 32 weight rows (the activation decode, repeated by every
-    // workgroup, is then spread over twice the weight rows), 8 waves while
-    // that leaves fewer than 1536 waves in the grid, else 4.
-    if (M <= 4)
+    // Eight waves per workgroup throughout, so that both weight forms add
+    // every output's partial sums in the same order.  Weight rows per
+    // workgroup: 16 up to 4 activation rows.  Above, every workgroup
+    // decodes all activation rows again, so more weight rows per workgroup
+    // spread that decode, as long as the grid keeps about one workgroup per
+    // CU (one fits per CU at these register counts): 64 from N = 11264
+    // (176 or more workgroups; 32 for the bf16-weight form, whose 64-row
+    // variant spills), 32 above N = 4096, 16 up to it (256 workgroups at
+    // most).  Measured at 16 rows: 12288 x 4096 weights 35.4 -> 27.5 us
+    // against 32 rows and four waves, 4096 x 12288 52.2 -> 43.9 us against 32
+    // rows.
+    const bool wide = !WBF16 && N >= 11264, narrow = N <= 4096;
+    if (M <= 4) {
       RFQ_FEW(16, 4, 8);
-    else if (M <= 8)
-      RFQ_FEW(16, 8, 8);
-    else if ((N + 31) / 32 < 384)
-      RFQ_FEW(32, 16, 8);
-    else
-      RFQ_FEW(32, 16, 4);
+    } else if (M <= 8) {
+      if (narrow) RFQ_FEW(16, 8, 8);
+      else if (!wide) RFQ_FEW(32, 8, 8);
+      else if constexpr (!WBF16) RFQ_FEW(64, 8, 8);
+    } else {
+      if (narrow) RFQ_FEW(16, 16, 8);
+      else if (!wide) RFQ_FEW(32, 16, 8);
+      else if constexpr (!WBF16) RFQ_FEW(64, 16, 8);
+    }
 #undef RFQ_FEW
     return hipGetLastError();
   }
