@@ -179,7 +179,7 @@ template <int F>
 struct WPair { WGroup f[F]; };
 
 template <bool RES, bool ZBF16, int S, int F>
-__global__ __launch_bounds__(kSkThreads, F == 1 ? 3 : 2) void rfq_gemm_skinny_kernel(
+__global__ __launch_bounds__(kSkThreads, F == 1 ? 3 : (F == 2 ? 2 : 1)) void rfq_gemm_skinny_kernel(
     const uint8_t *__restrict__ qc, const uint8_t *__restrict__ qs,
     const uint8_t *__restrict__ rc, const uint8_t *__restrict__ rs,
     const uint8_t *__restrict__ wc, const uint8_t *__restrict__ ws, int64_t M, int64_t N,
@@ -515,6 +515,10 @@ hipError_t launch_sk_s(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc, 
 // leave CUs without a workgroup; else two (the activation codes are then
 // loaded once per 32 weight rows).  Measured on MI355X at 12288 x 4096 and
 // 4096 x 12288 weights: 8 - 26% faster where chosen, slower elsewhere.
+// Single slices also take four (64 weight rows, one workgroup per CU at 274
+// registers) for 5-16 rows where that gives 176-256 workgroups (11264 <= N
+// < 16384; 16 rows x 12288 x 4096: 11.8 -> 9.8 us), and two from N = 16384
+// at any row count (1 row x 24576 x 4096: 14.5 -> 12.7 us).
 constexpr int64_t kFillWorkgroups = 256;    // one per CU on MI355X
 template <bool RES, bool ZBF16>
 hipError_t launch_sk(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc, const uint8_t *rs,
@@ -525,7 +529,11 @@ hipError_t launch_sk(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc, co
     return M <= 4 || wgs < kFillWorkgroups;
   };
 #define RFQ_SK(S, F) launch_sk_s<RES, ZBF16, S, F>(qc, qs, rc, rs, wc, ws, M, N, K, z, stream)
-  if (M <= kSkRows) return narrow(1) ? RFQ_SK(1, 1) : RFQ_SK(1, 2);
+  if (M <= kSkRows) {
+    if (M > 4 && N >= 11264 && N < 16384) return RFQ_SK(1, 4);
+    if (N >= 16384) return RFQ_SK(1, 2);
+    return narrow(1) ? RFQ_SK(1, 1) : RFQ_SK(1, 2);
+  }
   if (M <= 2 * kSkRows) return narrow(2) ? RFQ_SK(2, 1) : RFQ_SK(2, 2);
   return narrow(4) ? RFQ_SK(4, 1) : RFQ_SK(4, 2);
 #undef RFQ_SK
