@@ -130,7 +130,8 @@ rfq_status rfq_gemm(const uint8_t *q_codes, const uint8_t *q_scales,
  * several workgroups per output tile where that is faster: products with few
  * output tiles (at most 128 tiles of 128 x 128, or at most 192 with
  * K >= 8192) and at least 33 activation rows, e.g. an MLP down projection
- * for a few dozen to a few hundred tokens.
+ * for a few dozen to a few hundred tokens; not for 33-64 rows with
+ * 11264 <= N < 16384, where rfq_gemm's few-row product is faster.
  * Each part of K writes its fp32 partial sums to the workspace; one pass then
  * adds the parts in a fixed order and rounds to z_dtype, so the result is
  * deterministic but its fp32 summation order differs from rfq_gemm's (both
@@ -172,8 +173,9 @@ rfq_status rfq_gemm_split_noalloc(const uint8_t *q_codes, const uint8_t *q_scale
 /*
  * Workspace rfq_gemm_split uses for this shape: parts * M * N * 4 bytes for
  * the fp32 partials (at most 32 MiB), or 0 where it does not split (up to
- * 32 rows, K not a multiple of 512, more than 128 tiles of 128 x 128 with
- * K < 8192 or more than 192, or sizes that rfq_gemm rejects).  Assumes 16-byte aligned scale tensors (with others the
+ * 32 rows, 33-64 rows with 11264 <= N < 16384, K not a multiple of 512,
+ * more than 128 tiles of 128 x 128 with K < 8192 or more than 192, or sizes
+ * that rfq_gemm rejects).  Assumes 16-byte aligned scale tensors (with others the
  * product runs unsplit).  Host-only; no device call.
  */
 int64_t rfq_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K);

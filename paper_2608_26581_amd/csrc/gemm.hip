@@ -322,12 +322,17 @@ static bool few_rows_chosen(int64_t M, int64_t N, int64_t K) {
 // With a workspace, from this many rows on the split product replaces the
 // few-row kernel where it splits (measured, bf16 Z: 64 rows x 4096 x 12288
 // 32.2 us few-row against 18.5 us split, 32 rows 19.5 against 16.6, 16 rows
-// 13.2 against 16.1; 48 rows x 12288 x 4096 21.5 against 18.3).
+// 13.2 against 16.1), except where the few-row kernel runs 64 weight rows per
+// workgroup below N = 16384 (48 rows x 12288 x 4096: 15.3 us few-row
+// against 17.1 split, 64 rows 17.0 against 17.8).
 constexpr int64_t kSplitMinRows = 33;
+static bool few_rows_beat_split(int64_t M, int64_t N) {
+  return M < kSplitMinRows || (skinny_four_fragments(M, N) && N < 16384);
+}
 
 int64_t gemm_split_bytes(int64_t M, int64_t N, int64_t K) {
   if (M <= 0 || N <= 0 || (K % 512) != 0) return 0;
-  if (few_rows_chosen(M, N, K) && M < kSplitMinRows) return 0;
+  if (few_rows_chosen(M, N, K) && few_rows_beat_split(M, N)) return 0;
   const SplitPlan p = splitk_plan(M, N, K);
   return p.parts > 1 ? p.work_bytes : 0;
 }
@@ -343,7 +348,7 @@ hipError_t launch_gemm(const uint8_t *q_codes, const uint8_t *q_scales,
     plan = splitk_plan(M, N, K);
     if (plan.work_bytes > work_bytes) plan = SplitPlan{1, K, 0};
   }
-  const bool split = plan.parts > 1 && M >= kSplitMinRows;
+  const bool split = plan.parts > 1 && !(few_rows_chosen(M, N, K) && few_rows_beat_split(M, N));
   if (gemm_skinny_applies(q_scales, r_scales, w_scales, M, N, K) && !split &&
       !(large && large_tiles_beat_few_rows(M, N)))
     return launch_gemm_skinny(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K,

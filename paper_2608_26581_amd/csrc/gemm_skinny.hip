@@ -515,10 +515,12 @@ hipError_t launch_sk_s(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc, 
 // leave CUs without a workgroup; else two (the activation codes are then
 // loaded once per 32 weight rows).  Measured on MI355X at 12288 x 4096 and
 // 4096 x 12288 weights: 8 - 26% faster where chosen, slower elsewhere.
-// Single slices also take four (64 weight rows, one workgroup per CU at 274
-// registers) for 5-16 rows where that gives 176-256 workgroups (11264 <= N
-// < 16384; 16 rows x 12288 x 4096: 11.8 -> 9.8 us), and two from N = 16384
-// at any row count (1 row x 24576 x 4096: 14.5 -> 12.7 us).
+// Four fragments (64 weight rows, one workgroup per CU at 274-392
+// registers) serve 5-64 rows where that gives 176-256 workgroups per row of
+// workgroups (11264 <= N < 16384; at 12288 x 4096 weights 16 rows 11.8 ->
+// 9.7 us, 32 rows 16.6 -> 12.1, 64 rows 25.4 -> 17.0) and 33-64 rows from
+// N = 16384 (64 rows x 24576 x 4096: 37.2 -> 32.8 us); single slices take
+// two from N = 16384 at any row count (1 row x 24576 x 4096: 14.5 -> 12.9 us).
 constexpr int64_t kFillWorkgroups = 256;    // one per CU on MI355X
 template <bool RES, bool ZBF16>
 hipError_t launch_sk(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc, const uint8_t *rs,
@@ -529,13 +531,14 @@ hipError_t launch_sk(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc, co
     return M <= 4 || wgs < kFillWorkgroups;
   };
 #define RFQ_SK(S, F) launch_sk_s<RES, ZBF16, S, F>(qc, qs, rc, rs, wc, ws, M, N, K, z, stream)
+  const bool four = skinny_four_fragments(M, N);
   if (M <= kSkRows) {
-    if (M > 4 && N >= 11264 && N < 16384) return RFQ_SK(1, 4);
+    if (four) return RFQ_SK(1, 4);
     if (N >= 16384) return RFQ_SK(1, 2);
     return narrow(1) ? RFQ_SK(1, 1) : RFQ_SK(1, 2);
   }
-  if (M <= 2 * kSkRows) return narrow(2) ? RFQ_SK(2, 1) : RFQ_SK(2, 2);
-  return narrow(4) ? RFQ_SK(4, 1) : RFQ_SK(4, 2);
+  if (M <= 2 * kSkRows) return four ? RFQ_SK(2, 4) : (narrow(2) ? RFQ_SK(2, 1) : RFQ_SK(2, 2));
+  return four ? RFQ_SK(4, 4) : (narrow(4) ? RFQ_SK(4, 1) : RFQ_SK(4, 2));
 #undef RFQ_SK
 }
 
@@ -558,6 +561,12 @@ hipError_t launch_st(const void *x, const uint8_t *wc, const uint8_t *ws, int64_
 }
 
 }  // namespace
+
+bool skinny_four_fragments(int64_t M, int64_t N) {
+  if (M <= 4 || M > 4 * kSkRows) return false;
+  if (N >= 11264 && N < 16384) return true;
+  return N >= 16384 && M > 2 * kSkRows;
+}
 
 bool gemm_skinny_applies(const uint8_t *q_scales, const uint8_t *r_scales,
                          const uint8_t *w_scales, int64_t M, int64_t N, int64_t K) {

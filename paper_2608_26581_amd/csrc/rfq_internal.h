@@ -109,8 +109,11 @@ bool large_tiles_beat_few_rows(int64_t M, int64_t N);
 
 // Product for few activation rows (M <= kSkinnyMaxRows, K a multiple of 512,
 // 16-byte aligned scale tensors, code tensors below 2 GiB): one workgroup per
-// 32 weight rows and up to 64 activation rows.
+// 16, 32 or 64 weight rows and up to 64 activation rows.
 constexpr int64_t kSkinnyMaxRows = 128;
+// Where it runs 64 weight rows per workgroup (5-64 activation rows at
+// 11264 <= N < 16384, 33-64 rows from N = 16384).
+bool skinny_four_fragments(int64_t M, int64_t N);
 bool gemm_skinny_applies(const uint8_t *q_scales, const uint8_t *r_scales,
                          const uint8_t *w_scales, int64_t M, int64_t N, int64_t K);
 hipError_t launch_gemm_skinny(const uint8_t *q_codes, const uint8_t *q_scales,

@@ -338,6 +338,9 @@ def test_gemm_split_validation_and_workspace_sizes():
     assert w(1024, 4096, 12288) == 0                       # 256 tiles
     assert w(129, 12288, 4096) == 0                        # 192 tiles, K below 8192
     assert w(32, 4096, 12288) == 0                         # few-row kernel
+    assert w(64, 12288, 4096) == 0                         # few-row kernel, 64 weight rows
+    assert w(48, 13824, 5120) == 0                         # the same
+    assert w(64, 16384, 12288) == 2 * 64 * 16384 * 4       # 128 tiles, from N = 16384: split
     assert w(129, 4096, 12300) == 0                        # K not a multiple of 512
     assert w(-1, 4096, 12288) == 0 and w(129, 4096, 100) == 0
 

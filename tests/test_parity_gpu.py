@@ -306,8 +306,12 @@ GEMM_SMALL = [
     # enough weight rows for 32 per workgroup (16 elsewhere), ragged
     ("qwen", 16, 8200, 512),
     ("qwen", 40, 8200, 512),
-    # 64 weight rows per workgroup (5-16 rows, 11264 <= N < 16384), ragged
+    # 64 weight rows per workgroup (5-64 rows at 11264 <= N < 16384, 33-64
+    # from N = 16384), one, two and four row slices, ragged
     ("qwen", 9, 12300, 1024),
+    ("qwen", 24, 12300, 512),
+    ("qwen", 50, 11300, 1024),
+    ("qwen", 40, 16400, 512),
     # 32 weight rows per workgroup at up to 4 rows from N = 16384, ragged
     ("qwen", 3, 16400, 512),
     # 65-128 rows with 96 or more 128-wide column tiles: the large-tile kernel
@@ -510,7 +514,7 @@ def test_gemm_stream_matches_oracle(orc, name, M, N, K, xdt, residual, out_dtype
 
 @pytest.mark.parametrize("M,N,K", [(1, 300, 512), (16, 256, 1024), (64, 200, 5120), (23, 515, 2048),
                                    (65, 97, 1536), (128, 300, 512), (100, 33, 2048),
-                                   (12, 12300, 1024), (2, 16400, 512)])
+                                   (12, 12300, 1024), (2, 16400, 512), (40, 12300, 1024)])
 @pytest.mark.parametrize("residual", [True, False])
 def test_gemm_stream_bit_identical_to_quantize_then_gemm(M, N, K, residual):
     """Where rfq_gemm runs its few-row kernel (up to 64 rows, and up to 128
