@@ -11,11 +11,12 @@
 // With few rows the product is bound by streaming W's codes from memory, and
 // the large-tile kernels (256 activation rows per tile) would leave most of the
 // chip idle.  Here a workgroup owns 32 rows of W (two fragments; one where
-// that gives too few workgroups or for up to 4 activation rows, and one in
-// the streaming form) and up to four 16-row activation slices, and its four waves
-// split K into four contiguous ranges; the partial 16 x 16 results of the
-// waves are summed in a fixed order through LDS.  W is read once per 64
-// activation rows.
+// that gives too few workgroups or for up to 4 activation rows, four where
+// 64 rows still give about one workgroup per CU, and one in the streaming
+// form) and up to four 16-row activation slices, and its four waves split K
+// into four contiguous ranges; the partial 16 x 16 results of the waves are
+// summed in a fixed order through LDS.  W is read once per 64 activation
+// rows.
 //
 // Instruction: v_mfma_scale_f32_16x16x128_f8f6f4 with E2M1 operands (format
 // 4).  In k-step ks (128 K values, 4 MX blocks) lane l holds row l mod 16 and
