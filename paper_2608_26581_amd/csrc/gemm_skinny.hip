@@ -318,14 +318,18 @@ struct alignas(16) StreamArea {
   uint8_t rs[kSkRows * kGroupBlocks];
 };
 
-// The streaming form holds one W fragment per workgroup (16 rows): with the
-// quantizer's registers a second fragment would spill.
-constexpr int kStFrags = 1;
-struct StW { WGroup f[kStFrags]; };
+// The streaming form holds one W fragment per workgroup (16 rows), or four
+// (64 rows) where that still gives about one workgroup per CU: the
+// quantization of the activation slice, which every workgroup repeats, is
+// then shared by four times the weight rows.  With the quantizer's registers
+// a second fragment no longer fits two waves per SIMD, so four take one
+// (406-480 registers).
+template <int F>
+struct StW { WGroup f[F]; };
 
 // (fp32 input: one wave per SIMD; its registers do not fit two without spilling.)
-template <bool RES, bool ZBF16, bool XF32, int S>
-__global__ __launch_bounds__(kSkThreads, XF32 ? 1 : 2) void rfq_gemm_stream_kernel(
+template <bool RES, bool ZBF16, bool XF32, int S, int kStFrags>
+__global__ __launch_bounds__(kSkThreads, (XF32 || kStFrags > 1) ? 1 : 2) void rfq_gemm_stream_kernel(
     const void *__restrict__ x, const uint8_t *__restrict__ wc, const uint8_t *__restrict__ ws,
     int64_t M, int64_t N, int64_t K, void *__restrict__ z) {
   __shared__ v4f partial[kSkThreads / 64][kStFrags * S][64];
@@ -351,7 +355,7 @@ __global__ __launch_bounds__(kSkThreads, XF32 ? 1 : 2) void rfq_gemm_stream_kern
     w_off[f] = (uint32_t)wn * (uint32_t)kbytes + 16 * g;
     ws_off[f] = (uint32_t)wn * (uint32_t)kblocks;
   }
-  auto load_w = [&](StW &w, int gi) {
+  auto load_w = [&](StW<kStFrags> &w, int gi) {
 #pragma unroll
     for (int f = 0; f < kStFrags; ++f) {
 #pragma unroll
@@ -423,7 +427,7 @@ __global__ __launch_bounds__(kSkThreads, XF32 ? 1 : 2) void rfq_gemm_stream_kern
   // Units run slice by slice, so only one slice's accumulators are live (the
   // slices' passes over the wave's W range re-read it from L2).
   XRound xn, xa, xb;
-  auto unit = [&](const StW &w, int gi, int sl, v4f (&a)[kStFrags]) {
+  auto unit = [&](const StW<kStFrags> &w, int gi, int sl, v4f (&a)[kStFrags]) {
     const int live = live_rows(sl);
     const int rounds = (live * kGroupBlocks + 63) / 64;
     xa = xn;
@@ -468,7 +472,7 @@ __global__ __launch_bounds__(kSkThreads, XF32 ? 1 : 2) void rfq_gemm_stream_kern
 #pragma unroll
     for (int f = 0; f < kStFrags; ++f) a[f] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
     if (gb < ge) {
-      StW w0, w1;
+      StW<kStFrags> w0, w1;
       load_w(w0, gb);
       int gi = gb;
       for (; gi + 1 < ge; gi += 2) {
@@ -543,22 +547,34 @@ hipError_t launch_sk(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc, co
 #undef RFQ_SK
 }
 
-template <bool RES, bool ZBF16, bool XF32, int S>
+template <bool RES, bool ZBF16, bool XF32, int S, int F>
 hipError_t launch_st_s(const void *x, const uint8_t *wc, const uint8_t *ws, int64_t M, int64_t N,
                        int64_t K, void *z, hipStream_t stream) {
-  const dim3 grid((unsigned)((N + kStFrags * kSkRows - 1) / (kStFrags * kSkRows)),
+  const dim3 grid((unsigned)((N + F * kSkRows - 1) / (F * kSkRows)),
                   (unsigned)((M + S * kSkRows - 1) / (S * kSkRows)));
-  rfq_gemm_stream_kernel<RES, ZBF16, XF32, S><<<grid, dim3(kSkThreads), 0, stream>>>(
+  rfq_gemm_stream_kernel<RES, ZBF16, XF32, S, F><<<grid, dim3(kSkThreads), 0, stream>>>(
       x, wc, ws, M, N, K, z);
   return hipGetLastError();
+}
+
+// Four fragments from N = 11264 for 5 or more rows (bf16 activations:
+// 16 rows x 12288 x 4096 16.6 -> 12.1 us, 64 rows 51.7 -> 41.0 us; 16 rows
+// x 24576 x 4096 30.9 -> 23.9 us); one elsewhere (4096 x 12288 weights: 19.1
+// against 30.6 us at 16 rows).
+template <bool RES, bool ZBF16, bool XF32, int S>
+hipError_t launch_st_f(const void *x, const uint8_t *wc, const uint8_t *ws, int64_t M, int64_t N,
+                       int64_t K, void *z, hipStream_t stream) {
+  if (M > 4 && N >= 11264)
+    return launch_st_s<RES, ZBF16, XF32, S, 4>(x, wc, ws, M, N, K, z, stream);
+  return launch_st_s<RES, ZBF16, XF32, S, 1>(x, wc, ws, M, N, K, z, stream);
 }
 
 template <bool RES, bool ZBF16, bool XF32>
 hipError_t launch_st(const void *x, const uint8_t *wc, const uint8_t *ws, int64_t M, int64_t N,
                      int64_t K, void *z, hipStream_t stream) {
-  if (M <= kSkRows) return launch_st_s<RES, ZBF16, XF32, 1>(x, wc, ws, M, N, K, z, stream);
-  if (M <= 2 * kSkRows) return launch_st_s<RES, ZBF16, XF32, 2>(x, wc, ws, M, N, K, z, stream);
-  return launch_st_s<RES, ZBF16, XF32, 4>(x, wc, ws, M, N, K, z, stream);
+  if (M <= kSkRows) return launch_st_f<RES, ZBF16, XF32, 1>(x, wc, ws, M, N, K, z, stream);
+  if (M <= 2 * kSkRows) return launch_st_f<RES, ZBF16, XF32, 2>(x, wc, ws, M, N, K, z, stream);
+  return launch_st_f<RES, ZBF16, XF32, 4>(x, wc, ws, M, N, K, z, stream);
 }
 
 }  // namespace

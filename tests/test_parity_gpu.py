@@ -489,6 +489,7 @@ STREAM = [
     ("wan", 64, 200, 5120),
     ("qwen", 100, 97, 512),           # two workgroup rows, the second ragged
     ("qwen", 150, 97, 1024),          # more rows than the codes path's few-row kernel
+    ("qwen", 24, 12300, 512),         # 64 weight rows per workgroup, ragged
 ]
 
 
