@@ -759,9 +759,11 @@ hipError_t launch_hg(const uint8_t *qc, const uint32_t *qm, const uint8_t *rc,
   hif4_gemm_few_kernel<RES, ZBF16, WBF16, NR, MAXM, W>                                        \
       <<<dim3((unsigned)((N + NR - 1) / NR)), dim3(W * 64), 0, stream>>>(qc, qm, rc, rm, wc, wm, \
                                                                         wv, M, N, K, z)
-    // Eight waves per workgroup throughout, so that both weight forms add
-    // every output's partial sums in the same order.  Weight rows per
-    // workgroup: 16 up to 4 activation rows.  Above, every workgroup
+    // Eight waves per workgroup (sixteen up to 8 rows where N <= 4096: the
+    // grid then holds at most 256 workgroups, and K splits further: 1 row
+    // x 4096 x 12288 20.9 -> 17.3 us, 8 rows 29.6 -> 25.1 us), the same in
+    // both weight forms, so that both add every output's partial sums in the
+    // same order.  Weight rows per workgroup: 16 up to 4 activation rows.  Above, every workgroup
     // decodes all activation rows again, so more weight rows per workgroup
     // spread that decode, as long as the grid keeps about one workgroup per
     // CU (one fits per CU at these register counts): 64 from N = 11264
@@ -772,9 +774,10 @@ hipError_t launch_hg(const uint8_t *qc, const uint32_t *qm, const uint8_t *rc,
     // rows.
     const bool wide = !WBF16 && N >= 11264, narrow = N <= 4096;
     if (M <= 4) {
-      RFQ_FEW(16, 4, 8);
+      if (narrow) RFQ_FEW(16, 4, 16);
+      else RFQ_FEW(16, 4, 8);
     } else if (M <= 8) {
-      if (narrow) RFQ_FEW(16, 8, 8);
+      if (narrow) RFQ_FEW(16, 8, 16);
       else if (!wide) RFQ_FEW(32, 8, 8);
       else if constexpr (!WBF16) RFQ_FEW(64, 8, 8);
     } else {

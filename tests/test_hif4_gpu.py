@@ -269,13 +269,14 @@ def test_gemm_wbf16_any_bf16_weight(orc):
 # Up to 4 and up to 8 rows (16 weight rows and 8 waves per workgroup), 9-16
 # rows with 8 waves (few workgroups) and with 4 (N above 12256); K ending in
 # half a chunk of 128 (64, 192, 576, 4160) and fewer chunks than waves.
-# Workgroup shapes of the few-row kernel (weight rows, activation rows):
-# 16 x 4 up to 4 rows; 16 x 8, 32 x 8 or 64 x 8 up to 8 and 16 x 16, 32 x 16
-# or 64 x 16 up to 16, by N (at most 4096, below 11264, from 11264; the
-# bf16-weight form stays at 32 rows there), each with a ragged last workgroup.
+# Workgroup shapes of the few-row kernel (weight rows, activation rows,
+# waves): 16 x 4 up to 4 rows; 16 x 8, 32 x 8 or 64 x 8 up to 8 and 16 x 16,
+# 32 x 16 or 64 x 16 up to 16, by N (at most 4096, below 11264, from 11264;
+# the bf16-weight form stays at 32 rows there); sixteen waves up to 8 rows
+# where N <= 4096, eight elsewhere; each with a ragged last workgroup.
 FEW_SHAPES = [(1, 1, 64), (2, 33, 192), (5, 300, 640), (16, 700, 1024), (3, 64, 128),
               (8, 257, 4160), (9, 12300, 576), (6, 5000, 320), (7, 11300, 192),
-              (12, 4200, 256)]
+              (12, 4200, 256), (3, 16400, 256), (4, 4096, 8192)]
 
 
 @pytest.mark.parametrize("M,N,K", FEW_SHAPES)
