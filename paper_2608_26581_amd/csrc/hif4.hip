@@ -541,6 +541,7 @@ __global__ __launch_bounds__((HSmem<RES, BN>::kThreads)) void hif4_gemm_kernel(
 // descriptors based at the workgroup's first weight row (32-bit offsets);
 // K values past K (a final half chunk) load as zeros, without memory access.
 constexpr int kFewRows = 16;
+constexpr int kFewMaxRows = 64;             // four slices of 16 activation rows
 constexpr int kFewChunk = 128;              // K values per chunk
 constexpr uint32_t kFewSkip = 0x80000000u;  // load offset past every buffer: zeros
 // Per wave: 16 primary and 16 residual activation rows of one chunk, bf16.
@@ -555,21 +556,27 @@ __device__ __forceinline__ int few_xoff(int row, int piece) {
 // stay below the skip offset.
 constexpr int64_t kFewMaxK = int64_t(1) << 24;
 
-template <bool RES, bool ZBF16, bool WBF16, int NR, int MAXM, int WAVES>
+// S > 1: the activation rows come in slices of 16 (MAXM = 16), each
+// decoded into the wave's LDS area in turn and multiplied with the weight
+// pieces of the chunk, which are decoded once for all slices.
+template <bool RES, bool ZBF16, bool WBF16, int NR, int MAXM, int WAVES, int S = 1>
 __global__ __launch_bounds__(WAVES * 64) void hif4_gemm_few_kernel(
     const uint8_t *__restrict__ qc, const uint32_t *__restrict__ qm,
     const uint8_t *__restrict__ rc, const uint32_t *__restrict__ rm,
     const uint8_t *__restrict__ wc, const uint32_t *__restrict__ wm,
     const uint16_t *__restrict__ wv, int64_t M, int64_t N, int64_t K, void *__restrict__ z) {
   static_assert(NR == 16 || NR == 32 || NR == 64, "weight rows per workgroup");
+  static_assert(S == 1 || MAXM == kFewRows, "slices of 16 activation rows");
   constexpr int F = NR / 16, kFewWaves = WAVES;
+  static_assert(F * S <= 8, "partial sums of at most 8 output tiles per wave");
   __shared__ __attribute__((aligned(16))) uint8_t xarea[kFewWaves][2 * kFewRows * kFewXRow];
-  __shared__ v4f part[kFewWaves][F][64];
+  __shared__ v4f part[kFewWaves][F * S][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r = lane & 15, g = lane >> 4;
   const int64_t n0 = (int64_t)blockIdx.x * NR;
   const int64_t kbytes = K / 2, kblocks = K / kH;
   const int nchunks = (int)((K + kFewChunk - 1) / kFewChunk);
+  const int slices = S == 1 ? 1 : (int)min<int64_t>(S, (M + kFewRows - 1) / kFewRows);
   // Rows of this workgroup's buffers: NR weight rows from n0 (clamped to N).
   const int64_t nrows = min<int64_t>(NR, N - n0);
   auto rsrc = [](const void *p, int64_t bytes) {
@@ -587,11 +594,10 @@ __global__ __launch_bounds__(WAVES * 64) void hif4_gemm_few_kernel(
     wm_off[f] = (uint32_t)(lr * kblocks + (g >> 1)) * 4u;
   }
 
-  // Activation work items: code word w (0..15) of row j of the chunk, j <
-  // M primary rows then M residual rows (M <= MAXM); lane l takes items
-  // l + 64 i.
+  // Activation work items (one slice): code word w (0..15) of row j of the
+  // chunk, j < M primary rows then M residual rows (M <= MAXM); lane l
+  // takes items l + 64 i.
   constexpr int kXI = (RES ? 2 : 1) * MAXM * 16 / 64;
-  const int nx = (RES ? 2 : 1) * (int)M * 16;
   const __amdgpu_buffer_rsrc_t bq = rsrc(qc, M * kbytes), br = rsrc(RES ? rc : qc, M * kbytes);
   const __amdgpu_buffer_rsrc_t bqm = rsrc(qm, M * kblocks * 4),
                                brm = rsrc(RES ? rm : qm, M * kblocks * 4);
@@ -600,17 +606,20 @@ __global__ __launch_bounds__(WAVES * 64) void hif4_gemm_few_kernel(
     bool res;
     int row, w;
   };
-  auto xitem = [&](int i) {
+  auto xitem = [&](int i, int ms) {
     const int t = lane + 64 * i, j = t >> 4;
-    const bool is_r = RES && j >= (int)M;
-    return XItem{is_r, is_r ? j - (int)M : j, t & 15};
+    const bool is_r = RES && j >= ms;
+    return XItem{is_r, is_r ? j - ms : j, t & 15};
   };
 
-  struct Chunk {
+  struct WChunk {
     u32x4 w[F][WBF16 ? 4 : 1];
-    uint32_t m[F], xc[kXI], xm[kXI];
+    uint32_t m[F];
   };
-  auto load = [&](int c, Chunk &o) {
+  struct XChunk {
+    uint32_t c[kXI], m[kXI];
+  };
+  auto load_w = [&](int c, WChunk &o) {
     // Quarter g of chunk c exists when 128 c + 32 g < K (K is a multiple of 64).
     const bool live = (int64_t)kFewChunk * c + 32 * g < K;
 #pragma unroll
@@ -626,84 +635,145 @@ __global__ __launch_bounds__(WAVES * 64) void hif4_gemm_few_kernel(
         o.m[f] = __builtin_amdgcn_raw_buffer_load_b32(bwm, live ? wm_off[f] : kFewSkip, 8 * c, 0);
       }
     }
+  };
+  auto load_x = [&](int c, int s, XChunk &o) {
+    if constexpr (S == 1) {
+      const int ms = (int)M;
 #pragma unroll
-    for (int i = 0; i < kXI; ++i) {
-      if (lane + 64 * i < nx) {
-        const XItem it = xitem(i);
-        const bool xl = (int64_t)kFewChunk * c + 8 * it.w < K;
-        const uint32_t off = (uint32_t)it.row * (uint32_t)kbytes + 4 * it.w;
-        const uint32_t moff = ((uint32_t)it.row * (uint32_t)kblocks + (it.w >> 3)) * 4u;
-        o.xc[i] = __builtin_amdgcn_raw_buffer_load_b32(it.res ? br : bq, xl ? off : kFewSkip,
-                                                       (kFewChunk / 2) * c, 0);
-        o.xm[i] = __builtin_amdgcn_raw_buffer_load_b32(it.res ? brm : bqm, xl ? moff : kFewSkip,
-                                                       8 * c, 0);
+      for (int i = 0; i < kXI; ++i) {
+        if (lane + 64 * i < (RES ? 2 : 1) * ms * 16) {
+          const XItem it = xitem(i, ms);
+          const bool xl = (int64_t)kFewChunk * c + 8 * it.w < K;
+          const uint32_t off = (uint32_t)it.row * (uint32_t)kbytes + 4 * it.w;
+          const uint32_t moff = ((uint32_t)it.row * (uint32_t)kblocks + (it.w >> 3)) * 4u;
+          o.c[i] = __builtin_amdgcn_raw_buffer_load_b32(it.res ? br : bq, xl ? off : kFewSkip,
+                                                        (kFewChunk / 2) * c, 0);
+          o.m[i] = __builtin_amdgcn_raw_buffer_load_b32(it.res ? brm : bqm, xl ? moff : kFewSkip,
+                                                        8 * c, 0);
+        }
+      }
+    } else {
+      // Whole 16-row slices: item i is word t mod 16 of row (t / 16) mod 16
+      // of the slice, residual for t >= 256 (t = lane + 64 i); rows at or
+      // past M load zeros without memory access.  The slice's row offset
+      // goes into the scalar offset, so the per-item offsets are the same
+      // for every slice.
+      const uint32_t sc = (uint32_t)(kFewRows * s) * (uint32_t)kbytes + (kFewChunk / 2) * c;
+      const uint32_t sm = (uint32_t)(kFewRows * s) * (uint32_t)kblocks * 4u + 8 * c;
+#pragma unroll
+      for (int i = 0; i < kXI; ++i) {
+        const int t = lane + 64 * i, row = (t >> 4) & 15, w = t & 15;
+        const bool res = RES && t >= 256;
+        const bool xl = kFewRows * s + row < M && (int64_t)kFewChunk * c + 8 * w < K;
+        const uint32_t off = (uint32_t)row * (uint32_t)kbytes + 4 * w;
+        const uint32_t moff = ((uint32_t)row * (uint32_t)kblocks + (w >> 3)) * 4u;
+        o.c[i] = __builtin_amdgcn_raw_buffer_load_b32(res ? br : bq, xl ? off : kFewSkip, sc, 0);
+        o.m[i] = __builtin_amdgcn_raw_buffer_load_b32(res ? brm : bqm, xl ? moff : kFewSkip, sm, 0);
       }
     }
   };
 
   uint8_t *X = xarea[wave];
-  v4f acc[F];
+  v4f acc[S][F];
 #pragma unroll
-  for (int f = 0; f < F; ++f) acc[f] = v4f{0.f, 0.f, 0.f, 0.f};
-  Chunk cur, nxt;
-  if (wave < nchunks) load(wave, cur);
+  for (int s = 0; s < S; ++s)
+#pragma unroll
+    for (int f = 0; f < F; ++f) acc[s][f] = v4f{0.f, 0.f, 0.f, 0.f};
+  WChunk wcur, wnxt;
+  XChunk xcur, xnxt;
+  if (wave < nchunks) {
+    load_w(wave, wcur);
+    load_x(wave, 0, xcur);
+  }
+  // The next unit's activation codes (the next slice, or the next chunk's
+  // first) are requested before a unit is decoded.
+  auto load_next_x = [&](int c, int s) {
+    if (s + 1 < slices) load_x(c, s + 1, xnxt);
+    else if (c + kFewWaves < nchunks) load_x(c + kFewWaves, 0, xnxt);
+  };
   for (int c = wave; c < nchunks; c += kFewWaves) {
-    if (c + kFewWaves < nchunks) load(c + kFewWaves, nxt);
-    // Activation rows into the wave's LDS area.
-#pragma unroll
-    for (int i = 0; i < kXI; ++i) {
-      if (lane + 64 * i < nx) {
-        const XItem it = xitem(i);
-        *reinterpret_cast<u32x4 *>(X + few_xoff(it.res ? kFewRows + it.row : it.row, it.w)) =
-            decode8_bf16(cur.xc[i], cur.xm[i], it.w & 7);
-      }
-    }
-    // Weight pieces in registers.
+    if (c + kFewWaves < nchunks) load_w(c + kFewWaves, wnxt);
     u32x4 wp[F][4];
 #pragma unroll
-    for (int f = 0; f < F; ++f) {
+    for (int s = 0; s < S; ++s) {
+      if (s < slices) {
+        load_next_x(c, s);
+        // Activation rows of the slice into the wave's LDS area.
+        if constexpr (S == 1) {
+          const int ms = (int)M;
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
-        if constexpr (WBF16) {
-          wp[f][jj] = cur.w[f][jj];
+          for (int i = 0; i < kXI; ++i) {
+            if (lane + 64 * i < (RES ? 2 : 1) * ms * 16) {
+              const XItem it = xitem(i, ms);
+              *reinterpret_cast<u32x4 *>(X + few_xoff(it.res ? kFewRows + it.row : it.row, it.w)) =
+                  decode8_bf16(xcur.c[i], xcur.m[i], it.w & 7);
+            }
+          }
         } else {
-          const uint32_t words[4] = {cur.w[f][0].x, cur.w[f][0].y, cur.w[f][0].z, cur.w[f][0].w};
-          wp[f][jj] = decode8_bf16(words[jj], cur.m[f], 4 * (g & 1) + jj);
+#pragma unroll
+          for (int i = 0; i < kXI; ++i) {
+            const int t = lane + 64 * i, row = (t >> 4) & 15, w = t & 15;
+            const bool res = RES && t >= 256;
+            *reinterpret_cast<u32x4 *>(X + few_xoff(res ? kFewRows + row : row, w)) =
+                decode8_bf16(xcur.c[i], xcur.m[i], w & 7);
+          }
         }
+        // Weight pieces in registers, once per chunk for all its slices.
+        if (s == 0) {
+#pragma unroll
+          for (int f = 0; f < F; ++f) {
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+              if constexpr (WBF16) {
+                wp[f][jj] = wcur.w[f][jj];
+              } else {
+                const uint32_t words[4] = {wcur.w[f][0].x, wcur.w[f][0].y, wcur.w[f][0].z,
+                                           wcur.w[f][0].w};
+                wp[f][jj] = decode8_bf16(words[jj], wcur.m[f], 4 * (g & 1) + jj);
+              }
+            }
+          }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          const v8bf xq = *reinterpret_cast<const v8bf *>(X + few_xoff(r, 4 * g + jj));
+          v8bf xr = xq;
+          if constexpr (RES)
+            xr = *reinterpret_cast<const v8bf *>(X + few_xoff(kFewRows + r, 4 * g + jj));
+#pragma unroll
+          for (int f = 0; f < F; ++f) {
+            const v8bf wf = __builtin_bit_cast(v8bf, wp[f][jj]);
+            acc[s][f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, xq, acc[s][f], 0, 0, 0);
+            if constexpr (RES)
+              acc[s][f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, xr, acc[s][f], 0, 0, 0);
+          }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        xcur = xnxt;
       }
     }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-#pragma unroll
-    for (int jj = 0; jj < 4; ++jj) {
-      const v8bf xq = *reinterpret_cast<const v8bf *>(X + few_xoff(r, 4 * g + jj));
-      v8bf xr = xq;
-      if constexpr (RES) xr = *reinterpret_cast<const v8bf *>(X + few_xoff(kFewRows + r, 4 * g + jj));
-#pragma unroll
-      for (int f = 0; f < F; ++f) {
-        const v8bf wf = __builtin_bit_cast(v8bf, wp[f][jj]);
-        acc[f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, xq, acc[f], 0, 0, 0);
-        if constexpr (RES) acc[f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, xr, acc[f], 0, 0, 0);
-      }
-    }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    cur = nxt;
+    wcur = wnxt;
   }
 #pragma unroll
-  for (int f = 0; f < F; ++f) part[wave][f][lane] = acc[f];
+  for (int s = 0; s < S; ++s)
+#pragma unroll
+    for (int f = 0; f < F; ++f) part[wave][f * S + s][lane] = acc[s][f];
   __syncthreads();
-  if (wave != 0) return;
-  const int64_t m = r;
-  if (m >= M) return;
+  // Output tile p (weight fragment p / S, slice p mod S), summed in wave
+  // order and stored by wave p mod WAVES.
   const bool vec_ok = (N & 3) == 0;
+  for (int p = wave; p < F * S; p += kFewWaves) {
+    const int f = p / S, s = p % S;
+    const int64_t m = (int64_t)kFewRows * s + r;
+    if (s >= slices || m >= M) continue;
+    v4f t = part[0][p][lane];
 #pragma unroll
-  for (int f = 0; f < F; ++f) {
-    v4f t = part[0][f][lane];
-#pragma unroll
-    for (int w = 1; w < kFewWaves; ++w) t += part[w][f][lane];
+    for (int w = 1; w < kFewWaves; ++w) t += part[w][p][lane];
     const int64_t n = n0 + 16 * f + 4 * g;
     if constexpr (ZBF16) {
       uint16_t *zp = reinterpret_cast<uint16_t *>(z) + m * N + n;
@@ -754,11 +824,12 @@ hipError_t launch_hg(const uint8_t *qc, const uint32_t *qm, const uint8_t *rc,
                      const uint32_t *rm, const uint8_t *wc, const uint32_t *wm,
                      const uint16_t *wv, int64_t M, int64_t N, int64_t K, void *z,
                      hipStream_t stream) {
-  if (M <= kFewRows && K <= kFewMaxK && (N + 15) / 16 <= int64_t(UINT32_MAX / 512)) {
-#define RFQ_FEW(NR, MAXM, W)                                                                  \
-  hif4_gemm_few_kernel<RES, ZBF16, WBF16, NR, MAXM, W>                                        \
+  if (M <= kFewMaxRows && K <= kFewMaxK && (N + 15) / 16 <= int64_t(UINT32_MAX / 1024)) {
+#define RFQ_FEW_S(NR, MAXM, W, S)                                                              \
+  hif4_gemm_few_kernel<RES, ZBF16, WBF16, NR, MAXM, W, S>                                      \
       <<<dim3((unsigned)((N + NR - 1) / NR)), dim3(W * 64), 0, stream>>>(qc, qm, rc, rm, wc, wm, \
                                                                         wv, M, N, K, z)
+#define RFQ_FEW(NR, MAXM, W) RFQ_FEW_S(NR, MAXM, W, 1)
     // Eight waves per workgroup (sixteen up to 8 rows where N <= 4096: the
     // grid then holds at most 256 workgroups, and K splits further: 1 row
     // x 4096 x 12288 20.9 -> 17.3 us, 8 rows 29.6 -> 25.1 us), the same in
@@ -780,12 +851,20 @@ hipError_t launch_hg(const uint8_t *qc, const uint32_t *qm, const uint8_t *rc,
       if (narrow) RFQ_FEW(16, 8, 16);
       else if (!wide) RFQ_FEW(32, 8, 8);
       else if constexpr (!WBF16) RFQ_FEW(64, 8, 8);
-    } else {
+    } else if (M <= kFewRows) {
       if (narrow) RFQ_FEW(16, 16, 8);
       else if (!wide) RFQ_FEW(32, 16, 8);
       else if constexpr (!WBF16) RFQ_FEW(64, 16, 8);
+    } else if (M <= 2 * kFewRows) {
+      if (narrow) RFQ_FEW_S(16, 16, 8, 2);
+      else if (!wide) RFQ_FEW_S(32, 16, 8, 2);
+      else if constexpr (!WBF16) RFQ_FEW_S(64, 16, 8, 2);
+    } else {
+      if (narrow) RFQ_FEW_S(16, 16, 8, 4);
+      else RFQ_FEW_S(32, 16, 8, 4);
     }
 #undef RFQ_FEW
+#undef RFQ_FEW_S
     return hipGetLastError();
   }
   if (((M + kBM - 1) / kBM) * ((N + 255) / 256) < kFillTiles)

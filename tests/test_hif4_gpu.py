@@ -273,19 +273,24 @@ def test_gemm_wbf16_any_bf16_weight(orc):
 # waves): 16 x 4 up to 4 rows; 16 x 8, 32 x 8 or 64 x 8 up to 8 and 16 x 16,
 # 32 x 16 or 64 x 16 up to 16, by N (at most 4096, below 11264, from 11264;
 # the bf16-weight form stays at 32 rows there); sixteen waves up to 8 rows
-# where N <= 4096, eight elsewhere; each with a ragged last workgroup.
+# where N <= 4096, eight elsewhere; 17-64 rows in two or four slices of 16
+# rows per workgroup; each with a ragged last workgroup.
 FEW_SHAPES = [(1, 1, 64), (2, 33, 192), (5, 300, 640), (16, 700, 1024), (3, 64, 128),
               (8, 257, 4160), (9, 12300, 576), (6, 5000, 320), (7, 11300, 192),
-              (12, 4200, 256), (3, 16400, 256), (4, 4096, 8192)]
+              (12, 4200, 256), (3, 16400, 256), (4, 4096, 8192),
+              # 17-64 rows: two or four slices of 16 rows per workgroup
+              (17, 300, 640), (24, 12300, 320), (33, 5000, 256), (50, 4096, 1024),
+              (64, 11300, 128)]
 
 
 @pytest.mark.parametrize("M,N,K", FEW_SHAPES)
 @pytest.mark.parametrize("residual", [True, False])
 @pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
 def test_gemm_few_rows_matches_oracle(orc, M, N, K, residual, out_dtype):
-    """At most 16 activation rows run the few-row kernel (K split over four
-    or eight waves, partial sums added in wave order); fewer K chunks than
-    waves included.  The bf16-weight form is bit-identical to it."""
+    """At most 64 activation rows run the few-row kernel (K split over eight
+    or sixteen waves, partial sums added in wave order; above 16 rows in
+    slices of 16); fewer K chunks than waves included.  The bf16-weight form
+    is bit-identical to it."""
     _say("hif4 few rows %dx%dx%d residual=%s %s" % (M, N, K, residual, out_dtype))
     w = wl.WORKLOADS["tiny"].scaled(M=M, K=K, weights=(("w", K, N),))
     data = wl.generate(w, seed=M * 13 + N + K)
