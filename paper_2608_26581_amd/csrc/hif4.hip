@@ -519,9 +519,10 @@ __global__ __launch_bounds__((HSmem<RES, BN>::kThreads)) void hif4_gemm_kernel(
 
 // ---------------------------------------------------------------- few rows
 //
-// Product for at most 16 activation rows (decode): one workgroup per 16 or
-// 32 weight rows (F = 1 or 2 fragments of 16) and up to MAXM activation
-// rows; its WAVES waves take interleaved chunks of 128 K values (wave w:
+// Product for at most 64 activation rows (decode, short prefill): one
+// workgroup per 16, 32 or 64 weight rows (F = 1, 2 or 4 fragments of 16) and
+// up to MAXM activation rows, or S slices of 16; its WAVES waves take
+// interleaved chunks of 128 K values (wave w:
 // chunks w, w + WAVES, ...) and run v_mfma_f32_16x16x32_bf16 with the
 // weights as the first operand; the partial sums are added in wave order at
 // the end.
