@@ -839,23 +839,49 @@ bool gemm_large_applies(const uint8_t *q_scales, const uint8_t *r_scales,
          N * (K / 2) < limit;
 }
 
+// 256-row tile rows that run 256 x 256 tiles where those do not fill their
+// last round of 256 well: a last round of at most 64 tiles would run at a
+// quarter of the chip for a whole tile time, so the tile rows of that round
+// run 128 x 128 tiles in a second launch instead (1536 rows x 12288 x 4096:
+// 101 -> 85 us; 4096 rows x 5120 x 13824: 330 -> 308 us).  Returns the
+// number of tile rows of the 256 x 256 launch (all of them where nothing is
+// peeled).
+static int64_t big_tile_rows(int64_t M, int64_t N) {
+  const int64_t ntm = (M + Big::kBM - 1) / Big::kBM, ntn = (N + Big::kBN - 1) / Big::kBN;
+  const int64_t tiles = ntm * ntn, tail = tiles % 256;
+  if (tail == 0 || tail > 64) return ntm;
+  const int64_t rows = (tiles - tail) / ntn;
+  return rows > 0 ? rows : ntm;
+}
+
 hipError_t launch_gemm_large(const uint8_t *q_codes, const uint8_t *q_scales,
                              const uint8_t *r_codes, const uint8_t *r_scales,
                              const uint8_t *w_codes, const uint8_t *w_scales,
                              int64_t M, int64_t N, int64_t K, void *z, bool z_bf16,
                              hipStream_t stream) {
-  auto go = [&](auto tile) {
+  auto go = [&](auto tile, int64_t row0, int64_t rows) {
     using C = decltype(tile);
+    // Activation rows [row0, row0 + rows) and the same rows of Z.
+    const uint8_t *qc = q_codes + row0 * (K / 2), *qs = q_scales + row0 * (K / 32);
+    const uint8_t *rc = r_codes ? r_codes + row0 * (K / 2) : nullptr;
+    const uint8_t *rs = r_codes ? r_scales + row0 * (K / 32) : nullptr;
+    void *zr = static_cast<uint8_t *>(z) + row0 * N * (z_bf16 ? 2 : 4);
     if (r_codes) {
       if (z_bf16)
-        return launch<C, true, true>(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K, z, stream);
-      return launch<C, true, false>(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K, z, stream);
+        return launch<C, true, true>(qc, qs, rc, rs, w_codes, w_scales, rows, N, K, zr, stream);
+      return launch<C, true, false>(qc, qs, rc, rs, w_codes, w_scales, rows, N, K, zr, stream);
     }
     if (z_bf16)
-      return launch<C, false, true>(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K, z, stream);
-    return launch<C, false, false>(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K, z, stream);
+      return launch<C, false, true>(qc, qs, rc, rs, w_codes, w_scales, rows, N, K, zr, stream);
+    return launch<C, false, false>(qc, qs, rc, rs, w_codes, w_scales, rows, N, K, zr, stream);
   };
-  return use_mid_tiles(M, N) ? go(Mid{}) : go(Big{});
+  if (use_mid_tiles(M, N)) return go(Mid{}, 0, M);
+  const int64_t big_rows = std::min<int64_t>(big_tile_rows(M, N) * Big::kBM, M);
+  const hipError_t e = go(Big{}, 0, big_rows);
+  if (e != hipSuccess || big_rows == M) return e;
+  // Both tile shapes accumulate every output in the same order, so the
+  // peeled rows carry the bits the 256 x 256 tiles would give them.
+  return go(Mid{}, big_rows, M - big_rows);
 }
 
 hipError_t launch_gemm_large_phi(const uint8_t *q_codes, const uint8_t *q_scales,

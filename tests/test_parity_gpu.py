@@ -409,6 +409,35 @@ def test_gemm_tile_shapes_agree(orc, residual, out_dtype):
         assert torch.equal(_gemm_bits(zs), _gemm_bits(z[:, a:b].contiguous())), "cols %d:%d" % (a, b)
 
 
+@pytest.mark.parametrize("residual", [True, False])
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
+def test_gemm_last_round_peeled(orc, residual, out_dtype):
+    """1400 x 11000 has 6 x 43 = 258 tiles of 256 x 256, two past a round of
+    256: the tile rows of that last round (rows 1280-1399) run 128 x 128
+    tiles in a second launch.  Sampled against the oracle in every 64 x 64
+    tile, the last row and the last column; the 256-wide rows and the peeled
+    rows give the bits of products of those rows alone (256-wide tiles for
+    rows 0-1279, 128-wide ones for rows 1152-1399)."""
+    M, N, K = 1400, 11000, 512
+    data = _gemm_case("qwen", M, N, K, seed=78)
+    _say("gemm peeled last round M=%d N=%d K=%d residual=%s out=%s" % (M, N, K, residual, out_dtype))
+    q = rfq.rfq_quantize_act(x_device(data), residual=residual)
+    w = rfq.rfq_quantize_weight(dev(data["w"]))
+    z = rfq.rfq_gemm(*q, *w, out_dtype=out_dtype)
+    zh = host(z) if out_dtype == torch.float32 else host_bf16_as_f32(z)
+    rng = np.random.default_rng(6)
+    tr, tc = _tile_samples(M, N, 64, rng)
+    rows = np.concatenate([tr, np.full(N, M - 1), np.arange(M)])
+    cols = np.concatenate([tc, np.arange(N), np.full(M, N - 1)])
+    hq = [None if t is None else host(t) for t in q]
+    zr, bound = orc.gemm_sampled(*hq, host(w[0]), host(w[1]), rows, cols)
+    assert_gemm_close(zh[rows, cols], zr, bound, out_dtype == torch.bfloat16, "peeled product")
+    for a, b in ((0, 1280), (1152, 1400)):
+        qs = [None if t is None else t[a:b] for t in q]
+        zs = rfq.rfq_gemm(*qs, *w, out_dtype=out_dtype)
+        assert torch.equal(_gemm_bits(zs), _gemm_bits(z[a:b])), "rows %d:%d" % (a, b)
+
+
 @pytest.mark.parametrize("M,N,K", [(256, 12288, 4096), (300, 4096, 12288), (129, 12288, 4096)])
 def test_gemm_mid_rows_full_width(orc, M, N, K):
     """Between 129 and a few hundred activation rows at the workloads' weight
