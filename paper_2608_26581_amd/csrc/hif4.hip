@@ -825,7 +825,23 @@ hipError_t launch_hg(const uint8_t *qc, const uint32_t *qm, const uint8_t *rc,
                      const uint32_t *rm, const uint8_t *wc, const uint32_t *wm,
                      const uint16_t *wv, int64_t M, int64_t N, int64_t K, void *z,
                      hipStream_t stream) {
-  if (M <= kFewMaxRows && K <= kFewMaxK && (N + 15) / 16 <= int64_t(UINT32_MAX / 1024)) {
+  const bool few_fits = K <= kFewMaxK && (N + 15) / 16 <= int64_t(UINT32_MAX / 1024);
+  // 65-128 rows at N <= 4096: the tile kernel has at most 32 tiles there,
+  // each with the whole reduction; the few-row kernel on each 64-row half is
+  // faster (96 rows x 4096 x 12288: 314 -> ~175 us; every row's result is
+  // the few-row kernel's for that row).
+  if (few_fits && M > kFewMaxRows && M <= 2 * kFewMaxRows && N <= 4096) {
+    const int64_t kb = K / 2, km = K / kH;
+    hipError_t e = launch_hg<RES, ZBF16, WBF16>(qc, qm, rc, rm, wc, wm, wv, kFewMaxRows, N, K, z,
+                                                stream);
+    if (e != hipSuccess) return e;
+    const int64_t r0 = kFewMaxRows;
+    return launch_hg<RES, ZBF16, WBF16>(qc + r0 * kb, qm + r0 * km, RES ? rc + r0 * kb : rc,
+                                        RES ? rm + r0 * km : rm, wc, wm, wv, M - r0, N, K,
+                                        static_cast<uint8_t *>(z) + r0 * N * (ZBF16 ? 2 : 4),
+                                        stream);
+  }
+  if (M <= kFewMaxRows && few_fits) {
 #define RFQ_FEW_S(NR, MAXM, W, S)                                                              \
   hif4_gemm_few_kernel<RES, ZBF16, WBF16, NR, MAXM, W, S>                                      \
       <<<dim3((unsigned)((N + NR - 1) / NR)), dim3(W * 64), 0, stream>>>(qc, qm, rc, rm, wc, wm, \

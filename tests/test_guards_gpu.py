@@ -166,7 +166,7 @@ def test_binding_rejects_bad_tensors():
 
 
 @pytest.mark.parametrize("M,N,K", [(131, 97, 192), (1, 1, 64), (257, 300, 640), (37, 515, 128),
-                                   (12, 11301, 128), (6, 4999, 64)])
+                                   (12, 11301, 128), (6, 4999, 64), (70, 400, 128)])
 def test_hif4_outputs_stay_in_bounds(M, N, K):
     w = wl.WORKLOADS["qwen"].scaled(M=M, K=K, weights=(("w", K, N),))
     data = wl.generate(w, seed=37)

@@ -280,7 +280,9 @@ FEW_SHAPES = [(1, 1, 64), (2, 33, 192), (5, 300, 640), (16, 700, 1024), (3, 64, 
               (12, 4200, 256), (3, 16400, 256), (4, 4096, 8192),
               # 17-64 rows: two or four slices of 16 rows per workgroup
               (17, 300, 640), (24, 12300, 320), (33, 5000, 256), (50, 4096, 1024),
-              (64, 11300, 128)]
+              (64, 11300, 128),
+              # 65-128 rows at N <= 4096: two launches on 64-row halves
+              (100, 300, 640)]
 
 
 @pytest.mark.parametrize("M,N,K", FEW_SHAPES)
