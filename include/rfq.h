@@ -395,6 +395,39 @@ rfq_status rfq_hif4_gemm_wbf16(const uint8_t *q_codes, const uint32_t *q_meta,
                                void *z, rfq_dtype z_dtype, void *hip_stream);
 
 /*
+ * rfq_hif4_gemm with the reduction over K split across several workgroups per
+ * output tile where that is faster: products whose 128 x 256 tiles number
+ * fewer than 256 and whose 128 x 128 tiles number at most 128 (a few hundred
+ * activation rows against a narrow weight, e.g. an MLP down projection, and
+ * more rows than the few-row form takes: above 64, or above 128 where
+ * N <= 4096), with K at least 512.  Each part of K writes its fp32 partial
+ * sums to the workspace; one pass then adds the parts in a fixed order and
+ * rounds to z_dtype, so the result is deterministic but its fp32 summation
+ * order differs from rfq_hif4_gemm's (both agree within the product's
+ * rounding).  Where the shape does not split, or workspace_bytes is below
+ * rfq_hif4_gemm_workspace_bytes(M, N, K), it is rfq_hif4_gemm.
+ *   workspace: device memory owned by the caller, 16-byte aligned, not read
+ *            before it is written; NULL only with workspace_bytes == 0.
+ *   workspace_bytes: its size, >= 0.
+ * Other arguments, shape limits and errors as rfq_hif4_gemm.  Calls that
+ * share a workspace must be ordered (one stream, or events).  Asynchronous
+ * on hip_stream.
+ */
+rfq_status rfq_hif4_gemm_split(const uint8_t *q_codes, const uint32_t *q_meta,
+                               const uint8_t *r_codes, const uint32_t *r_meta,
+                               const uint8_t *w_codes, const uint32_t *w_meta,
+                               int64_t M, int64_t N, int64_t K,
+                               void *z, rfq_dtype z_dtype, void *workspace,
+                               int64_t workspace_bytes, void *hip_stream);
+
+/*
+ * Workspace rfq_hif4_gemm_split uses for this shape: parts * M * N * 4 bytes
+ * for the fp32 partials (at most 16 MiB), or 0 where it does not split.
+ * Host-only; no device call.
+ */
+int64_t rfq_hif4_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K);
+
+/*
  * Measurement support, not a step of the method: the sustained rate of the
  * FP4 matrix cores that the product (Eq. 11) runs on, without memory
  * traffic.  256 workgroups of 8 waves (one per CU of the MI355X, two waves

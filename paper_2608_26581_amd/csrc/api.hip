@@ -388,6 +388,37 @@ rfq_status rfq_hif4_gemm(const uint8_t *q_codes, const uint32_t *q_meta,
                                         static_cast<hipStream_t>(hip_stream)));
 }
 
+int64_t rfq_hif4_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) {
+  if (check_k64(M, K) != RFQ_OK || N < 0 || !hif4_product_fits(M, N)) return 0;
+  const rfq::SplitPlan p = rfq::hif4_split_plan(M, N, K);
+  return p.parts > 1 ? p.work_bytes : 0;
+}
+
+rfq_status rfq_hif4_gemm_split(const uint8_t *q_codes, const uint32_t *q_meta,
+                               const uint8_t *r_codes, const uint32_t *r_meta,
+                               const uint8_t *w_codes, const uint32_t *w_meta,
+                               int64_t M, int64_t N, int64_t K,
+                               void *z, rfq_dtype z_dtype, void *workspace,
+                               int64_t workspace_bytes, void *hip_stream) {
+  if (!valid_dtype(z_dtype)) return RFQ_ERR_DTYPE;
+  rfq_status s = check_k64(M, K);
+  if (s != RFQ_OK) return s;
+  if (N < 0 || !hif4_product_fits(M, N) || workspace_bytes < 0) return RFQ_ERR_SHAPE;
+  if (M == 0 || N == 0) return RFQ_OK;
+  if (!q_codes || !q_meta || !w_codes || !w_meta || !z) return RFQ_ERR_NULL;
+  if ((r_codes == nullptr) != (r_meta == nullptr)) return RFQ_ERR_NULL;
+  if (!workspace && workspace_bytes > 0) return RFQ_ERR_NULL;
+  if (!aligned(q_codes, 16) || !aligned(w_codes, 16) || !aligned(q_meta, 4) ||
+      !aligned(w_meta, 4) || (r_codes && (!aligned(r_codes, 16) || !aligned(r_meta, 4))) ||
+      !aligned(z, 16) || !aligned(workspace, 16))
+    return RFQ_ERR_ALIGN;
+  if ((s = check_device()) != RFQ_OK) return s;
+  return launched(rfq::launch_hif4_gemm_split(q_codes, q_meta, r_codes, r_meta, w_codes, w_meta,
+                                              M, N, K, z, z_dtype == RFQ_BF16,
+                                              static_cast<float *>(workspace), workspace_bytes,
+                                              static_cast<hipStream_t>(hip_stream)));
+}
+
 rfq_status rfq_hif4_gemm_wbf16(const uint8_t *q_codes, const uint32_t *q_meta,
                                const uint8_t *r_codes, const uint32_t *r_meta,
                                const void *w_bf16, int64_t M, int64_t N, int64_t K,

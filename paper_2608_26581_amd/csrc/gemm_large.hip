@@ -750,18 +750,7 @@ hipError_t launch_split(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc,
   kern<<<dim3((unsigned)(ntiles * parts)), dim3(Mid::kThreads), L::kBytes, stream>>>(
       qc, qs, rc, rs, wc, ws, M, N, K, work, SwigluOut{}, nullptr, ksplit);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  const int64_t mn = M * N;
-  const bool v4 = (mn % 4) == 0;
-  const int64_t items = v4 ? mn / 4 : mn;
-  const unsigned blocks = (unsigned)std::min<int64_t>((items + 255) / 256, 4096);
-  if (z_bf16) {
-    if (v4) splitk_sum_kernel<true, true><<<blocks, 256, 0, stream>>>(work, parts, mn, z);
-    else splitk_sum_kernel<true, false><<<blocks, 256, 0, stream>>>(work, parts, mn, z);
-  } else {
-    if (v4) splitk_sum_kernel<false, true><<<blocks, 256, 0, stream>>>(work, parts, mn, z);
-    else splitk_sum_kernel<false, false><<<blocks, 256, 0, stream>>>(work, parts, mn, z);
-  }
-  return hipGetLastError();
+  return launch_splitk_sum(work, parts, M * N, z, z_bf16, stream);
 }
 
 // Parts of K for the split product (1: no split), so that the parts x tiles
@@ -793,6 +782,21 @@ bool use_mid_tiles(int64_t M, int64_t N) {
 }
 
 }  // namespace
+
+hipError_t launch_splitk_sum(const float *work, int parts, int64_t mn, void *z, bool z_bf16,
+                             hipStream_t stream) {
+  const bool v4 = (mn % 4) == 0;
+  const int64_t items = v4 ? mn / 4 : mn;
+  const unsigned blocks = (unsigned)std::min<int64_t>((items + 255) / 256, 4096);
+  if (z_bf16) {
+    if (v4) splitk_sum_kernel<true, true><<<blocks, 256, 0, stream>>>(work, parts, mn, z);
+    else splitk_sum_kernel<true, false><<<blocks, 256, 0, stream>>>(work, parts, mn, z);
+  } else {
+    if (v4) splitk_sum_kernel<false, true><<<blocks, 256, 0, stream>>>(work, parts, mn, z);
+    else splitk_sum_kernel<false, false><<<blocks, 256, 0, stream>>>(work, parts, mn, z);
+  }
+  return hipGetLastError();
+}
 
 SplitPlan splitk_plan(int64_t M, int64_t N, int64_t K, int parts_wanted) {
   SplitPlan p{1, K, 0};

@@ -61,6 +61,7 @@
 // are free of bank conflicts.  Rows past M or N are clamped to the last row
 // for loading; their results are not stored.
 #include <hip/hip_runtime.h>
+#include <algorithm>
 #include <stdint.h>
 
 #include <atomic>
@@ -330,21 +331,35 @@ __device__ __forceinline__ u32x4 decode8_bf16(uint32_t w, uint32_t meta, int g) 
 // WBF16: the weights come as bf16 values wv[N][K] (for example HiF4 weights
 // decoded once) and are copied into LDS as they are; only the activation
 // codes are decoded.
-template <bool RES, bool ZBF16, bool WBF16, int BN>
+// SPLIT: the grid holds ceil(K / ksplit) copies of the tile grid, copy s
+// multiplying K columns [s ksplit, (s + 1) ksplit) (ksplit a multiple of 64)
+// and writing its fp32 partial product to z + s M N.
+template <bool RES, bool ZBF16, bool WBF16, int BN, bool SPLIT = false>
 __global__ __launch_bounds__((HSmem<RES, BN>::kThreads)) void hif4_gemm_kernel(
     const uint8_t *__restrict__ qc, const uint32_t *__restrict__ qm,
     const uint8_t *__restrict__ rc, const uint32_t *__restrict__ rm,
     const uint8_t *__restrict__ wc, const uint32_t *__restrict__ wm,
-    const uint16_t *__restrict__ wv, int64_t M, int64_t N, int64_t K, void *__restrict__ z) {
+    const uint16_t *__restrict__ wv, int64_t M, int64_t N, int64_t K, void *__restrict__ z,
+    int64_t ksplit) {
+  static_assert(!SPLIT || !ZBF16, "split partials are fp32");
   using S = HSmem<RES, BN>;
   constexpr int kTN = S::kTN, kFN = S::kFN;
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
 
+  const int ntm = (int)((M + kBM - 1) / kBM), ntn = (int)((N + BN - 1) / BN);
+  int bid = blockIdx.x, split = 0;
+  if constexpr (SPLIT) {
+    split = bid / (ntm * ntn);
+    bid -= split * ntm * ntn;
+    z = reinterpret_cast<float *>(z) + (int64_t)split * M * N;
+  }
   int tm, tn;
-  tile_coords<8>(blockIdx.x, (int)((M + kBM - 1) / kBM), (int)((N + BN - 1) / BN), tm, tn);
+  tile_coords<8>(bid, ntm, ntn, tm, tn);
   const int64_t m0 = (int64_t)tm * kBM, n0 = (int64_t)tn * BN;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int nsteps = (int)(K / kH);
+  // This workgroup's K blocks: [kb0, kb0 + nsteps).
+  const int64_t kb0 = SPLIT ? (int64_t)split * (ksplit / kH) : 0;
+  const int nsteps = (int)((SPLIT ? min(ksplit, K - kb0 * kH) : K) / kH);
   const int64_t kbytes = K / 2, kblocks = K / kH;
 
   if (wave < S::kProducers) {
@@ -368,18 +383,18 @@ __global__ __launch_bounds__((HSmem<RES, BN>::kThreads)) void hif4_gemm_kernel(
       if (r >= S::kWRow0) {
         grow = min(n0 + (r - S::kWRow0), N - 1);
         if constexpr (WBF16) {
-          vsrc[i] = reinterpret_cast<const u32x4 *>(wv + grow * K + 32 * (pt & 1));
+          vsrc[i] = reinterpret_cast<const u32x4 *>(wv + grow * K + kb0 * kH + 32 * (pt & 1));
           src[i] = nullptr;
           msrc[i] = nullptr;
         } else {
-          src[i] = wc + grow * kbytes + 16 * (pt & 1);
-          msrc[i] = wm + grow * kblocks;
+          src[i] = wc + grow * kbytes + kb0 * (kH / 2) + 16 * (pt & 1);
+          msrc[i] = wm + grow * kblocks + kb0;
         }
       } else {
         const bool is_r = RES && r >= kBM;
         grow = min(m0 + (is_r ? r - kBM : r), M - 1);
-        src[i] = (is_r ? rc : qc) + grow * kbytes + 16 * (pt & 1);
-        msrc[i] = (is_r ? rm : qm) + grow * kblocks;
+        src[i] = (is_r ? rc : qc) + grow * kbytes + kb0 * (kH / 2) + 16 * (pt & 1);
+        msrc[i] = (is_r ? rm : qm) + grow * kblocks + kb0;
       }
     }
     const int h = pt & 1;
@@ -801,19 +816,19 @@ __global__ __launch_bounds__(WAVES * 64) void hif4_gemm_few_kernel(
   }
 }
 
-template <bool RES, bool ZBF16, bool WBF16, int BN>
+template <bool RES, bool ZBF16, bool WBF16, int BN, bool SPLIT = false>
 hipError_t launch_tiles(const uint8_t *qc, const uint32_t *qm, const uint8_t *rc,
                         const uint32_t *rm, const uint8_t *wc, const uint32_t *wm,
                         const uint16_t *wv, int64_t M, int64_t N, int64_t K, void *z,
-                        hipStream_t stream) {
+                        hipStream_t stream, int parts = 1, int64_t ksplit = 0) {
   using S = HSmem<RES, BN>;
-  auto kern = hif4_gemm_kernel<RES, ZBF16, WBF16, BN>;
+  auto kern = hif4_gemm_kernel<RES, ZBF16, WBF16, BN, SPLIT>;
   static std::atomic<bool> attr_done[kMaxDevices];
   const hipError_t e = set_lds_limit(attr_done, reinterpret_cast<const void *>(kern), S::kBytes);
   if (e != hipSuccess) return e;
   const int64_t tiles = ((M + kBM - 1) / kBM) * ((N + BN - 1) / BN);
-  kern<<<dim3((unsigned)tiles), dim3(S::kThreads), S::kBytes, stream>>>(qc, qm, rc, rm, wc, wm,
-                                                                         wv, M, N, K, z);
+  kern<<<dim3((unsigned)(tiles * parts)), dim3(S::kThreads), S::kBytes, stream>>>(
+      qc, qm, rc, rm, wc, wm, wv, M, N, K, z, SPLIT ? ksplit : K);
   return hipGetLastError();
 }
 
@@ -951,6 +966,51 @@ hipError_t launch_hif4_gemm(const uint8_t *q_codes, const uint32_t *q_meta,
   RFQ_HG(false, true, true) RFQ_HG(false, false, true)
 #undef RFQ_HG
   return hipErrorInvalidValue;
+}
+
+// Split of K: where the product runs 128-wide tiles that number at most 128
+// (a few hundred activation rows against a narrow weight, the down
+// projection of an MLP), 256 / tiles parts (at most 8) of at least 4 blocks
+// each, so that parts x tiles workgroups fill the 256 CUs about once; the
+// partials take parts x M x N x 4 <= 16 MiB.
+SplitPlan hif4_split_plan(int64_t M, int64_t N, int64_t K) {
+  SplitPlan p{1, K, 0};
+  if (M <= 0 || N <= 0 || K < kH || K % kH) return p;
+  const bool few_fits = K <= kFewMaxK && (N + 15) / 16 <= int64_t(UINT32_MAX / 1024);
+  if (few_fits && (M <= kFewMaxRows || (M <= 2 * kFewMaxRows && N <= 4096))) return p;
+  if (((M + kBM - 1) / kBM) * ((N + 255) / 256) >= kFillTiles) return p;
+  const int64_t tiles = ((M + kBM - 1) / kBM) * ((N + 127) / 128);
+  if (tiles > 128) return p;
+  constexpr int64_t kMinBlocks = 4;
+  const int64_t blocks = K / kH;
+  const int64_t want = std::min<int64_t>(std::min<int64_t>(8, 256 / tiles), blocks / kMinBlocks);
+  if (want < 2) return p;
+  const int64_t per = (blocks + want - 1) / want;
+  p.parts = (int)((blocks + per - 1) / per);
+  if (p.parts < 2) return SplitPlan{1, K, 0};
+  p.ksplit = per * kH;
+  p.work_bytes = (int64_t)p.parts * M * N * 4;
+  return p;
+}
+
+hipError_t launch_hif4_gemm_split(const uint8_t *q_codes, const uint32_t *q_meta,
+                                  const uint8_t *r_codes, const uint32_t *r_meta,
+                                  const uint8_t *w_codes, const uint32_t *w_meta, int64_t M,
+                                  int64_t N, int64_t K, void *z, bool z_bf16, float *work,
+                                  int64_t work_bytes, hipStream_t stream) {
+  const SplitPlan p = hif4_split_plan(M, N, K);
+  if (p.parts < 2 || work == nullptr || work_bytes < p.work_bytes)
+    return launch_hif4_gemm(q_codes, q_meta, r_codes, r_meta, w_codes, w_meta, nullptr, M, N, K,
+                            z, z_bf16, stream);
+  const hipError_t e =
+      r_codes ? launch_tiles<true, false, false, 128, true>(q_codes, q_meta, r_codes, r_meta,
+                                                             w_codes, w_meta, nullptr, M, N, K,
+                                                             work, stream, p.parts, p.ksplit)
+              : launch_tiles<false, false, false, 128, true>(q_codes, q_meta, nullptr, nullptr,
+                                                              w_codes, w_meta, nullptr, M, N, K,
+                                                              work, stream, p.parts, p.ksplit);
+  if (e != hipSuccess) return e;
+  return launch_splitk_sum(work, p.parts, M * N, z, z_bf16, stream);
 }
 
 }  // namespace rfq

@@ -91,6 +91,11 @@ hipError_t launch_gemm_large_split(const uint8_t *q_codes, const uint8_t *q_scal
                                    int64_t N, int64_t K, void *z, bool z_bf16,
                                    const SplitPlan &plan, float *work, hipStream_t stream);
 
+// Z = the sum of parts fp32 partial products work[parts][mn], added in the
+// order 0, 1, ..., rounded to bf16 or kept in fp32.
+hipError_t launch_splitk_sum(const float *work, int parts, int64_t mn, void *z, bool z_bf16,
+                             hipStream_t stream);
+
 // launch_gemm with the library's static device scratch array as the split
 // product's workspace (no allocation); static_scratch_bytes() is its size.
 int64_t static_scratch_bytes();
@@ -172,6 +177,17 @@ hipError_t launch_hif4_gemm(const uint8_t *q_codes, const uint32_t *q_meta,
                             const uint8_t *w_codes, const uint32_t *w_meta,
                             const uint16_t *w_bf16, int64_t M, int64_t N, int64_t K, void *z,
                             bool z_bf16, hipStream_t stream);
+// Split of K for the HiF4 tile product's 128-wide tiles (ksplit a multiple
+// of 64); parts == 1: no split (the shape runs the few-row kernel, or its
+// tiles fill the chip, or K is short).
+SplitPlan hif4_split_plan(int64_t M, int64_t N, int64_t K);
+// launch_hif4_gemm (codes form) with the plan's split where work_bytes
+// covers it (work: 16-byte aligned device memory), else unsplit.
+hipError_t launch_hif4_gemm_split(const uint8_t *q_codes, const uint32_t *q_meta,
+                                  const uint8_t *r_codes, const uint32_t *r_meta,
+                                  const uint8_t *w_codes, const uint32_t *w_meta, int64_t M,
+                                  int64_t N, int64_t K, void *z, bool z_bf16, float *work,
+                                  int64_t work_bytes, hipStream_t stream);
 
 // Register-only loop of FP4 scaled MFMAs (measurement support):
 // kMfmaLoopWorkgroups workgroups of 512 work items, each wave issuing

@@ -31,7 +31,7 @@ EXPORTS = (
     "rfq_swiglu_quantize_act", "rfq_gemm_phi", "rfq_fallback_map", "rfq_gemm_swiglu_quantize",
     "rfq_gemm_stream", "rfq_hif4_quantize", "rfq_hif4_dequant", "rfq_hif4_gemm",
     "rfq_hif4_gemm_wbf16", "rfq_mfma_fp4_loop", "rfq_gemm_split", "rfq_gemm_workspace_bytes",
-    "rfq_gemm_split_noalloc",
+    "rfq_gemm_split_noalloc", "rfq_hif4_gemm_split", "rfq_hif4_gemm_workspace_bytes",
     "rfq_status_str", "rfq_abi_version",
 )
 
@@ -83,10 +83,14 @@ def load():
     lib.rfq_gemm_split_noalloc.argtypes = [P, P, P, P, P, P, I64, I64, I64, P, I32, P]
     lib.rfq_gemm_workspace_bytes.argtypes = [I64, I64, I64]
     lib.rfq_gemm_workspace_bytes.restype = I64
+    lib.rfq_hif4_gemm_split.argtypes = [P, P, P, P, P, P, I64, I64, I64, P, I32, P, I64, P]
+    lib.rfq_hif4_gemm_workspace_bytes.argtypes = [I64, I64, I64]
+    lib.rfq_hif4_gemm_workspace_bytes.restype = I64
     for f in ("rfq_quantize_act", "rfq_quantize_weight", "rfq_gemm", "rfq_dequant",
               "rfq_swiglu_quantize_act", "rfq_gemm_swiglu_quantize", "rfq_gemm_phi",
               "rfq_fallback_map", "rfq_gemm_stream", "rfq_hif4_quantize", "rfq_hif4_dequant",
               "rfq_hif4_gemm", "rfq_hif4_gemm_wbf16", "rfq_mfma_fp4_loop", "rfq_gemm_split",
+              "rfq_hif4_gemm_split",
               "rfq_gemm_split_noalloc"):
         getattr(lib, f).restype = I32
     lib.rfq_status_str.argtypes = [I32]
@@ -542,9 +546,8 @@ def rfq_hif4_dequant(codes, meta, out_dtype=torch.float32, out=None, stream=None
     return o
 
 
-def rfq_hif4_gemm(q_codes, q_meta, r_codes, r_meta, w_codes, w_meta,
-                  out_dtype=torch.float32, out=None, stream=None):
-    """HiF4 RFQ product Z[M][N] = (V_q + V_r) V_w^T; r_* None: primary only."""
+def _hif4_operands(q_codes, q_meta, r_codes, r_meta, w_codes, w_meta):
+    """(M, N, K, device) of a HiF4 product's checked operands."""
     M, K = _shape_of_codes(q_codes, "q codes")
     N, Kw = _shape_of_codes(w_codes, "w codes")
     if Kw != K:
@@ -557,11 +560,54 @@ def rfq_hif4_gemm(q_codes, q_meta, r_codes, r_meta, w_codes, w_meta,
     if r_codes is not None:
         _need_hif4(r_codes, r_meta, M, K, "r", dev)
     _need_hif4(w_codes, w_meta, N, K, "w", dev)
+    return M, N, K, dev
+
+
+def rfq_hif4_gemm(q_codes, q_meta, r_codes, r_meta, w_codes, w_meta,
+                  out_dtype=torch.float32, out=None, stream=None, split=False):
+    """HiF4 RFQ product Z[M][N] = (V_q + V_r) V_w^T; r_* None: primary only.
+    split=True: rfq_hif4_gemm_split with a workspace from torch's allocator
+    where the shape splits K (a different fp32 summation order)."""
+    M, N, K, dev = _hif4_operands(q_codes, q_meta, r_codes, r_meta, w_codes, w_meta)
     z = _z_out(out, out_dtype, M, N, q_codes.device, dev)
+    if split:
+        nbytes = load().rfq_hif4_gemm_workspace_bytes(M, N, K)
+        if nbytes > 0:
+            ws = torch.empty(nbytes, dtype=torch.uint8, device=q_codes.device)
+            st = load().rfq_hif4_gemm_split(_ptr(q_codes), _ptr(q_meta), _ptr(r_codes),
+                                            _ptr(r_meta), _ptr(w_codes), _ptr(w_meta), M, N, K,
+                                            _ptr(z), _dtype_code(z), _ptr(ws), nbytes,
+                                            _stream(stream, dev))
+            _check("rfq_hif4_gemm_split", st)
+            return z
     st = load().rfq_hif4_gemm(_ptr(q_codes), _ptr(q_meta), _ptr(r_codes), _ptr(r_meta),
                               _ptr(w_codes), _ptr(w_meta), M, N, K, _ptr(z), _dtype_code(z),
                               _stream(stream, dev))
     _check("rfq_hif4_gemm", st)
+    return z
+
+
+def rfq_hif4_gemm_workspace_bytes(M, N, K):
+    """Workspace rfq_hif4_gemm_split splits K with for this shape (0: no split)."""
+    return int(load().rfq_hif4_gemm_workspace_bytes(int(M), int(N), int(K)))
+
+
+def rfq_hif4_gemm_split(q_codes, q_meta, r_codes, r_meta, w_codes, w_meta, workspace,
+                        out_dtype=torch.float32, out=None, stream=None):
+    """rfq_hif4_gemm with K split over workgroups where the shape calls for
+    it; workspace: a contiguous device uint8 tensor
+    (rfq_hif4_gemm_workspace_bytes long, or shorter to run unsplit) or None."""
+    M, N, K, dev = _hif4_operands(q_codes, q_meta, r_codes, r_meta, w_codes, w_meta)
+    nbytes = 0
+    if workspace is not None:
+        _need(workspace, "workspace", _U8, None, dev)
+        nbytes = workspace.numel()
+    z = _z_out(out, out_dtype, M, N, q_codes.device, dev)
+    st = load().rfq_hif4_gemm_split(_ptr(q_codes), _ptr(q_meta), _ptr(r_codes), _ptr(r_meta),
+                                    _ptr(w_codes), _ptr(w_meta), M, N, K, _ptr(z),
+                                    _dtype_code(z), _ptr(workspace), nbytes,
+                                    _stream(stream, dev))
+    _check("rfq_hif4_gemm_split", st)
     return z
 
 

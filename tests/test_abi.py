@@ -345,6 +345,32 @@ def test_gemm_split_validation_and_workspace_sizes():
     assert w(-1, 4096, 12288) == 0 and w(129, 4096, 100) == 0
 
 
+def test_hif4_gemm_split_validation_and_workspace_sizes():
+    """rfq_hif4_gemm_split checks what rfq_hif4_gemm checks plus its
+    workspace; the workspace query is host-only: parts x M x N x 4 bytes where
+    K splits (128-wide tiles, at most 128 of them, more rows than the
+    few-row form takes)."""
+    f = _lib().rfq_hif4_gemm_split
+    assert f(A, A, A, A, A, A, 8, 8, 512, A, 7, A, 64, None) == EDTYPE
+    assert f(A, A, A, A, A, A, 8, 8, 96, A, 0, A, 64, None) == ESHAPE
+    assert f(A, A, A, A, A, A, 8, 8, 512, A, 0, A, -1, None) == ESHAPE
+    assert f(A, A, A, A, A, A, 8, 8, 512, A, 0, None, 64, None) == ENULL
+    assert f(None, A, A, A, A, A, 8, 8, 512, A, 0, A, 64, None) == ENULL
+    assert f(A, A, A, None, A, A, 8, 8, 512, A, 0, A, 64, None) == ENULL
+    assert f(A, A, A, A, A, A, 8, 8, 512, A, 0, MIS, 64, None) == EALIGN
+    assert f(A, A, A, A, A, A, 0, 8, 512, None, 0, None, 0, None) == OK
+    w = _lib().rfq_hif4_gemm_workspace_bytes
+    assert w(256, 4096, 12288) == 4 * 256 * 4096 * 4       # 64 tiles: 4 parts
+    assert w(512, 4096, 12288) == 2 * 512 * 4096 * 4       # 128 tiles: 2 parts
+    assert w(200, 300, 2560) == 8 * 200 * 300 * 4          # 6 tiles: 8 parts of 5 blocks
+    assert w(129, 12288, 4096) == 0                        # 192 tiles
+    assert w(1024, 4096, 12288) == 0                       # 256 tiles
+    assert w(64, 4096, 12288) == 0                         # few-row form
+    assert w(128, 4096, 12288) == 0                        # few-row form, two halves
+    assert w(200, 300, 448) == 0                           # 7 blocks: under 2 parts of 4
+    assert w(200, 300, 100) == 0 and w(-1, 300, 2560) == 0
+
+
 def test_gemm_split_noalloc_validation():
     """The allocation-free split product checks what rfq_gemm checks."""
     f = _lib().rfq_gemm_split_noalloc

@@ -200,3 +200,13 @@ def test_hif4_outputs_stay_in_bounds(M, N, K):
             rfq.rfq_hif4_gemm_wbf16(q[0], q[1], q[2] if res else None, q[3] if res else None,
                                     wv, out=z.t)
             z.check("hif4_gemm_wbf16 res=%s %s" % (res, dt))
+    # The split product (where the shape splits): Z and the workspace.
+    nb = rfq.rfq_hif4_gemm_workspace_bytes(M, N, K)
+    if nb:
+        for res in (True, False):
+            for dt in (torch.float32, torch.bfloat16):
+                z, wsb = Guarded((M, N), dt), Guarded((nb,), torch.uint8)
+                rfq.rfq_hif4_gemm_split(q[0], q[1], q[2] if res else None, q[3] if res else None,
+                                        wb[0].t, wb[1].t, wsb.t, out=z.t)
+                z.check("hif4_gemm_split res=%s %s" % (res, dt))
+                wsb.check("hif4_gemm_split workspace res=%s %s" % (res, dt))

@@ -345,6 +345,58 @@ def test_gemm_full_size_k12288_sampled(orc):
     assert_gemm_close(z[np.ix_(rows, cols)], zr, bound, False, "hif4 K=12288")
 
 
+# K split over workgroups: 6 tiles of 128 x 128 -> 8 parts of 5 blocks; 9
+# tiles, 16 blocks -> 4 parts of 4; 10 tiles, 64 blocks -> 8 parts of 8.
+HIF4_SPLIT = [(200, 300, 2560), (300, 257, 1024), (150, 640, 4096)]
+
+
+@pytest.mark.parametrize("M,N,K", HIF4_SPLIT)
+@pytest.mark.parametrize("residual", [True, False])
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
+def test_gemm_split_matches_oracle(orc, M, N, K, residual, out_dtype):
+    """rfq_hif4_gemm_split (fp32 partials per part of K, added in order)
+    against the oracle, every output; a workspace below the plan's size runs
+    the unsplit product, bit for bit."""
+    _say("hif4 gemm split %dx%dx%d residual=%s %s" % (M, N, K, residual, out_dtype))
+    nbytes = rfq.rfq_hif4_gemm_workspace_bytes(M, N, K)
+    assert nbytes > 0
+    w = wl.WORKLOADS["tiny"].scaled(M=M, K=K, weights=(("w", K, N),))
+    data = wl.generate(w, seed=M + 5 * N + K)
+    _, q = _gpu_quant(data["x"], False, residual)
+    _, wq = _gpu_quant(data["w"], False, residual=False)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    z = rfq.rfq_hif4_gemm_split(*q, wq[0], wq[1], ws, out_dtype=out_dtype)
+    oq = orc.hif4_quantize(data["x"].astype(np.float64), residual)
+    ow = orc.hif4_quantize(data["w"].astype(np.float64), residual=False)
+    zr, bound = orc.hif4_gemm(oq[0], oq[1], oq[2], oq[3], ow[0], ow[1])
+    assert_gemm_close(host(z.float()), zr, bound, out_dtype == torch.bfloat16, "hif4 split")
+    small = torch.empty(nbytes - 16, dtype=torch.uint8, device="cuda")
+    z1 = rfq.rfq_hif4_gemm_split(*q, wq[0], wq[1], small, out_dtype=out_dtype)
+    z2 = rfq.rfq_hif4_gemm(*q, wq[0], wq[1], out_dtype=out_dtype)
+    iv = torch.int32 if out_dtype == torch.float32 else torch.int16
+    assert torch.equal(z1.view(iv), z2.view(iv)), "short workspace: not the unsplit product"
+
+
+def test_gemm_split_down_projection_sampled(orc):
+    """The down-projection shape at 256 activation rows (4096 x 12288
+    weights, 64 tiles, 4 parts of 48 blocks), split: 24 sampled rows against
+    the oracle in every column."""
+    M, N, K = 256, 4096, 12288
+    _say("hif4 gemm split %dx%dx%d sampled" % (M, N, K))
+    w = wl.WORKLOADS["qwen"].scaled(M=M, K=K, weights=(("w", K, N),))
+    data = wl.generate(w, seed=9)
+    x, wt = data["x"], data["w"]
+    _, q = _gpu_quant(x, True)
+    _, wq = _gpu_quant(wt, False, residual=False)
+    z = host(rfq.rfq_hif4_gemm(*q, wq[0], wq[1], split=True))
+    rng = np.random.default_rng(13)
+    rows = np.sort(np.concatenate([[0, M - 1], rng.choice(M, 22, replace=False)]))
+    oq = orc.hif4_quantize(x[rows].astype(np.float64))
+    ow = orc.hif4_quantize(wt.astype(np.float64), residual=False)
+    zr, bound = orc.hif4_gemm(oq[0], oq[1], oq[2], oq[3], ow[0], ow[1])
+    assert_gemm_close(z[rows], zr, bound, False, "hif4 split K=12288")
+
+
 @pytest.mark.parametrize("residual", [True, False])
 @pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
 def test_gemm_wide_tiles_ragged(orc, residual, out_dtype):
