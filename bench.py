@@ -494,7 +494,8 @@ def secondary(torch, rfq, wl, x, w, stream):
     xs = torch.from_numpy(d["x_bf16"].view(np.int16)).to(dev).view(torch.bfloat16)
     wg = rfq.rfq_quantize_weight(torch.from_numpy(d["w_gate"]).to(dev))
     wu = rfq.rfq_quantize_weight(torch.from_numpy(d["w_up"]).to(dev))
-    wd = rfq.rfq_quantize_weight(torch.from_numpy(d["w_down"]).to(dev))
+    wd32 = torch.from_numpy(d["w_down"]).to(dev)
+    wd = rfq.rfq_quantize_weight(wd32)
     del d
     Ms, Ks = xs.shape
     Nh = wg[0].shape[0]
@@ -563,6 +564,25 @@ def secondary(torch, rfq, wl, x, w, stream):
             "down_ms": round(ms_d, 5), "down_exec_tflops": round(fl / ms_d / 1e9, 1),
             "down_split_ms": round(ms_s, 5), "down_split_exec_tflops": round(fl / ms_s / 1e9, 1),
             "down_split_workspace_bytes": nb}
+
+    # The down product in HiF4 at 256 rows (activations N(0,1) in bf16; the
+    # tile product with K unsplit and split over workgroups).
+    hwd = rfq.rfq_hif4_quantize(wd32, residual=False)
+    del wd32
+    mp = 256
+    hx = rfq.rfq_hif4_quantize(torch.randn((mp, Nh), device=dev).to(torch.bfloat16))
+    yp = torch.empty((mp, Ks), dtype=torch.bfloat16, device=dev)
+    ms_d = _per_launch_ms(torch, stream, lambda i: rfq.rfq_hif4_gemm(
+        *hx, hwd[0], hwd[1], out=yp, stream=stream), 20)
+    nb = rfq.rfq_hif4_gemm_workspace_bytes(mp, Ks, Nh)
+    ws = torch.empty(max(nb, 16), dtype=torch.uint8, device=dev)
+    ms_s = _per_launch_ms(torch, stream, lambda i: rfq.rfq_hif4_gemm_split(
+        *hx, hwd[0], hwd[1], ws, out=yp, stream=stream), 20)
+    fl = 4.0 * mp * Ks * Nh
+    out["hif4_prefill_%d_rows" % mp] = {
+        "down_ms": round(ms_d, 5), "down_exec_tflops": round(fl / ms_d / 1e9, 1),
+        "down_split_ms": round(ms_s, 5), "down_split_exec_tflops": round(fl / ms_s / 1e9, 1),
+        "down_split_workspace_bytes": nb}
     return out
 
 
