@@ -835,17 +835,27 @@ hipError_t launch_tiles(const uint8_t *qc, const uint32_t *qm, const uint8_t *rc
 // Workgroups that fill the chip once (256 CUs on MI355X).
 constexpr int64_t kFillTiles = 256;
 
+// The few-row kernel's sizes (K and its grid) and row counts: up to 64 rows,
+// and 65-128 rows at N <= 4096, there as two launches on 64-row halves (the
+// tile kernel has at most 32 tiles there, each with the whole reduction:
+// 96 rows x 4096 x 12288 314 -> 175 us; every row's result is the few-row
+// kernel's for that row).
+bool few_fits(int64_t N, int64_t K) {
+  return K <= kFewMaxK && (N + 15) / 16 <= int64_t(UINT32_MAX / 1024);
+}
+bool few_halves(int64_t M, int64_t N, int64_t K) {
+  return few_fits(N, K) && M > kFewMaxRows && M <= 2 * kFewMaxRows && N <= 4096;
+}
+bool few_rows_product(int64_t M, int64_t N, int64_t K) {
+  return (M <= kFewMaxRows && few_fits(N, K)) || few_halves(M, N, K);
+}
+
 template <bool RES, bool ZBF16, bool WBF16>
 hipError_t launch_hg(const uint8_t *qc, const uint32_t *qm, const uint8_t *rc,
                      const uint32_t *rm, const uint8_t *wc, const uint32_t *wm,
                      const uint16_t *wv, int64_t M, int64_t N, int64_t K, void *z,
                      hipStream_t stream) {
-  const bool few_fits = K <= kFewMaxK && (N + 15) / 16 <= int64_t(UINT32_MAX / 1024);
-  // 65-128 rows at N <= 4096: the tile kernel has at most 32 tiles there,
-  // each with the whole reduction; the few-row kernel on each 64-row half is
-  // faster (96 rows x 4096 x 12288: 314 -> ~175 us; every row's result is
-  // the few-row kernel's for that row).
-  if (few_fits && M > kFewMaxRows && M <= 2 * kFewMaxRows && N <= 4096) {
+  if (few_halves(M, N, K)) {
     const int64_t kb = K / 2, km = K / kH;
     hipError_t e = launch_hg<RES, ZBF16, WBF16>(qc, qm, rc, rm, wc, wm, wv, kFewMaxRows, N, K, z,
                                                 stream);
@@ -856,7 +866,7 @@ hipError_t launch_hg(const uint8_t *qc, const uint32_t *qm, const uint8_t *rc,
                                         static_cast<uint8_t *>(z) + r0 * N * (ZBF16 ? 2 : 4),
                                         stream);
   }
-  if (M <= kFewMaxRows && few_fits) {
+  if (M <= kFewMaxRows && few_fits(N, K)) {
 #define RFQ_FEW_S(NR, MAXM, W, S)                                                              \
   hif4_gemm_few_kernel<RES, ZBF16, WBF16, NR, MAXM, W, S>                                      \
       <<<dim3((unsigned)((N + NR - 1) / NR)), dim3(W * 64), 0, stream>>>(qc, qm, rc, rm, wc, wm, \
@@ -976,8 +986,7 @@ hipError_t launch_hif4_gemm(const uint8_t *q_codes, const uint32_t *q_meta,
 SplitPlan hif4_split_plan(int64_t M, int64_t N, int64_t K) {
   SplitPlan p{1, K, 0};
   if (M <= 0 || N <= 0 || K < kH || K % kH) return p;
-  const bool few_fits = K <= kFewMaxK && (N + 15) / 16 <= int64_t(UINT32_MAX / 1024);
-  if (few_fits && (M <= kFewMaxRows || (M <= 2 * kFewMaxRows && N <= 4096))) return p;
+  if (few_rows_product(M, N, K)) return p;
   if (((M + kBM - 1) / kBM) * ((N + 255) / 256) >= kFillTiles) return p;
   const int64_t tiles = ((M + kBM - 1) / kBM) * ((N + 127) / 128);
   if (tiles > 128) return p;
