@@ -319,20 +319,28 @@ static bool few_rows_chosen(int64_t M, int64_t N, int64_t K) {
   return M <= kSkinnyMaxRows && (K % 512) == 0 && !large_tiles_beat_few_rows(M, N);
 }
 
-// With a workspace, from this many rows on the split product replaces the
-// few-row kernel where it splits (measured, bf16 Z: 64 rows x 4096 x 12288
-// 32.2 us few-row against 18.5 us split, 32 rows 19.5 against 16.6, 16 rows
-// 13.2 against 16.1), except where the few-row kernel runs 64 weight rows per
-// workgroup below N = 16384 (48 rows x 12288 x 4096: 15.3 us few-row
-// against 17.1 split, 64 rows 17.0 against 17.8).
-constexpr int64_t kSplitMinRows = 33;
-static bool few_rows_beat_split(int64_t M, int64_t N) {
-  return M < kSplitMinRows || (skinny_four_fragments(M, N) && N < 16384);
+// With a workspace the split product replaces the few-row kernel where it
+// splits, from 33 rows; from 24 where K >= 12288, and from 17 where the
+// few-row grid is uneven (between one and two workgroups per CU).  Measured,
+// bf16 Z, few-row against split: 64 rows x 4096 x 12288 32.5 against 18.1
+// us, 32 rows 19.3 against 16.5, 24 rows 16.8 against 16.0, 16 rows 13.0
+// against 15.8; 24 rows x 5120 x 13824 31.4 against 21.0, 16 rows (the
+// few-row kernel split over K) 19.3 against 20.5; 32 rows x 4096 x 8192 13.7
+// against 13.6, 24 rows 11.9 against 13.2.  Not where the few-row kernel runs
+// 64 weight rows per workgroup below N = 16384 (48 rows x 12288 x 4096: 15.4
+// us few-row against 18.4 split, 64 rows 17.1 against 19.5).
+static bool few_rows_beat_split(int64_t M, int64_t N, int64_t K) {
+  if (skinny_four_fragments(M, N) && N < 16384) return true;
+  const int64_t min_rows = skinny_grid_uneven(M, N) ? 17 : (K >= 12288 ? 24 : 33);
+  return M < min_rows;
 }
 
 int64_t gemm_split_bytes(int64_t M, int64_t N, int64_t K) {
   if (M <= 0 || N <= 0 || (K % 512) != 0) return 0;
-  if (few_rows_chosen(M, N, K) && few_rows_beat_split(M, N)) return 0;
+  if (few_rows_chosen(M, N, K) && few_rows_beat_split(M, N, K)) {
+    const int parts = skinny_split_parts(M, N, K);
+    return parts > 1 ? int64_t(parts) * M * N * 4 : 0;
+  }
   const SplitPlan p = splitk_plan(M, N, K);
   return p.parts > 1 ? p.work_bytes : 0;
 }
@@ -348,11 +356,16 @@ hipError_t launch_gemm(const uint8_t *q_codes, const uint8_t *q_scales,
     plan = splitk_plan(M, N, K);
     if (plan.work_bytes > work_bytes) plan = SplitPlan{1, K, 0};
   }
-  const bool split = plan.parts > 1 && !(few_rows_chosen(M, N, K) && few_rows_beat_split(M, N));
+  const bool split = plan.parts > 1 && !(few_rows_chosen(M, N, K) && few_rows_beat_split(M, N, K));
   if (gemm_skinny_applies(q_scales, r_scales, w_scales, M, N, K) && !split &&
-      !(large && large_tiles_beat_few_rows(M, N)))
+      !(large && large_tiles_beat_few_rows(M, N))) {
+    const int parts = work ? skinny_split_parts(M, N, K) : 1;
+    if (parts > 1 && int64_t(parts) * M * N * 4 <= work_bytes)
+      return launch_gemm_skinny_split(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M,
+                                      N, K, z, z_bf16, parts, work, stream);
     return launch_gemm_skinny(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M, N, K,
                               z, z_bf16, stream);
+  }
   if (large) {
     if (plan.parts > 1)
       return launch_gemm_large_split(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M,

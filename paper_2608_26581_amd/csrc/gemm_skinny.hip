@@ -176,6 +176,13 @@ __device__ __forceinline__ void reduce_store(v4f (&partial)[kSkThreads / 64][64]
 // current one is multiplied.  Per output the accumulation order is that of
 // a single slice: groups, k-steps, primary then residual, then the
 // fixed-order sum over the four waves.
+//
+// Split K (gridDim.z = parts > 1, fp32 output only): workgroup z covers the
+// groups [ngroups z / parts, ngroups (z + 1) / parts) of K / 512, which its
+// waves divide as they would the whole K, and writes its partial products to
+// the z-th M x N fp32 slab of the output; a second kernel adds the slabs in
+// the order z = 0, 1, ...  With one part the ranges and the output are those
+// of the unsplit product.
 template <int F>
 struct WPair { WGroup f[F]; };
 
@@ -195,9 +202,12 @@ __global__ __launch_bounds__(kSkThreads, F == 1 ? 3 : (F == 2 ? 2 : 1)) void rfq
   const int slices = (int)min<int64_t>(S, (M - m0 + kSkRows - 1) / kSkRows);
   const int64_t kbytes = K / 2, kblocks = K / 32;
 
-  // This wave's groups of 4 k-steps: [gb, ge) of K / 512.
+  // This wave's groups of 4 k-steps: [gb, ge) of K / 512, within this
+  // workgroup's part [pb, pe).
   const int ngroups = (int)(K / kSkGroupK);
-  const int gb = (ngroups * wave) / 4, ge = (ngroups * (wave + 1)) / 4;
+  const int part = (int)blockIdx.z, parts = (int)gridDim.z;
+  const int pb = (ngroups * part) / parts, pe = (ngroups * (part + 1)) / parts;
+  const int gb = pb + ((pe - pb) * wave) / 4, ge = pb + ((pe - pb) * (wave + 1)) / 4;
 
   const __amdgpu_buffer_rsrc_t rwc = rsrc(wc, N * kbytes), rws = rsrc(ws, N * kblocks);
   uint32_t w_off[F], ws_off[F];
@@ -288,6 +298,7 @@ __global__ __launch_bounds__(kSkThreads, F == 1 ? 3 : (F == 2 ? 2 : 1)) void rfq
 
   // Fixed-order sum over the four waves; output (fragment f, slice sl) is
   // summed and stored by wave (f S + sl) mod 4.
+  void *const zpart = ZBF16 ? z : static_cast<void *>(static_cast<float *>(z) + part * M * N);
 #pragma unroll
   for (int f = 0; f < F; ++f)
 #pragma unroll
@@ -302,7 +313,7 @@ __global__ __launch_bounds__(kSkThreads, F == 1 ? 3 : (F == 2 ? 2 : 1)) void rfq
       const v4f q = partial[w][p][lane];
       s = v4f{s[0] + q[0], s[1] + q[1], s[2] + q[2], s[3] + q[3]};
     }
-    store_tile<ZBF16>(s, lane, m0 + kSkRows * sl, n0 + kSkRows * f, M, N, z);
+    store_tile<ZBF16>(s, lane, m0 + kSkRows * sl, n0 + kSkRows * f, M, N, zpart);
   }
 }
 
@@ -505,9 +516,9 @@ __global__ __launch_bounds__(kSkThreads, (XF32 || kStFrags > 1) ? 1 : 2) void rf
 template <bool RES, bool ZBF16, int S, int F = 2>
 hipError_t launch_sk_s(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc, const uint8_t *rs,
                        const uint8_t *wc, const uint8_t *ws, int64_t M, int64_t N, int64_t K,
-                       void *z, hipStream_t stream) {
+                       void *z, int parts, hipStream_t stream) {
   const dim3 grid((unsigned)((N + F * kSkRows - 1) / (F * kSkRows)),
-                  (unsigned)((M + S * kSkRows - 1) / (S * kSkRows)));
+                  (unsigned)((M + S * kSkRows - 1) / (S * kSkRows)), (unsigned)parts);
   rfq_gemm_skinny_kernel<RES, ZBF16, S, F><<<grid, dim3(kSkThreads), 0, stream>>>(
       qc, qs, rc, rs, wc, ws, M, N, K, z);
   return hipGetLastError();
@@ -527,23 +538,28 @@ hipError_t launch_sk_s(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc, 
 // N = 16384 (64 rows x 24576 x 4096: 37.2 -> 32.8 us); single slices take
 // two from N = 16384 at any row count (1 row x 24576 x 4096: 14.5 -> 12.9 us).
 constexpr int64_t kFillWorkgroups = 256;    // one per CU on MI355X
+int sk_slices(int64_t M) { return M <= kSkRows ? 1 : (M <= 2 * kSkRows ? 2 : 4); }
+int sk_fragments(int64_t M, int64_t N) {
+  if (skinny_four_fragments(M, N)) return 4;
+  const int S = sk_slices(M);
+  if (S == 1 && N >= 16384) return 2;
+  const int64_t wgs = ((N + 2 * kSkRows - 1) / (2 * kSkRows)) * ((M + S * kSkRows - 1) / (S * kSkRows));
+  return (M <= 4 || wgs < kFillWorkgroups) ? 1 : 2;
+}
+int64_t sk_workgroups(int64_t M, int64_t N) {
+  const int64_t S = sk_slices(M), F = sk_fragments(M, N);
+  return ((N + F * kSkRows - 1) / (F * kSkRows)) * ((M + S * kSkRows - 1) / (S * kSkRows));
+}
+
 template <bool RES, bool ZBF16>
 hipError_t launch_sk(const uint8_t *qc, const uint8_t *qs, const uint8_t *rc, const uint8_t *rs,
                      const uint8_t *wc, const uint8_t *ws, int64_t M, int64_t N, int64_t K,
-                     void *z, hipStream_t stream) {
-  auto narrow = [&](int64_t S) {
-    const int64_t wgs = ((N + 2 * kSkRows - 1) / (2 * kSkRows)) * ((M + S * kSkRows - 1) / (S * kSkRows));
-    return M <= 4 || wgs < kFillWorkgroups;
-  };
-#define RFQ_SK(S, F) launch_sk_s<RES, ZBF16, S, F>(qc, qs, rc, rs, wc, ws, M, N, K, z, stream)
-  const bool four = skinny_four_fragments(M, N);
-  if (M <= kSkRows) {
-    if (four) return RFQ_SK(1, 4);
-    if (N >= 16384) return RFQ_SK(1, 2);
-    return narrow(1) ? RFQ_SK(1, 1) : RFQ_SK(1, 2);
-  }
-  if (M <= 2 * kSkRows) return four ? RFQ_SK(2, 4) : (narrow(2) ? RFQ_SK(2, 1) : RFQ_SK(2, 2));
-  return four ? RFQ_SK(4, 4) : (narrow(4) ? RFQ_SK(4, 1) : RFQ_SK(4, 2));
+                     void *z, hipStream_t stream, int parts = 1) {
+#define RFQ_SK(S, F) launch_sk_s<RES, ZBF16, S, F>(qc, qs, rc, rs, wc, ws, M, N, K, z, parts, stream)
+  const int S = sk_slices(M), F = sk_fragments(M, N);
+  if (S == 1) return F == 4 ? RFQ_SK(1, 4) : (F == 2 ? RFQ_SK(1, 2) : RFQ_SK(1, 1));
+  if (S == 2) return F == 4 ? RFQ_SK(2, 4) : (F == 2 ? RFQ_SK(2, 2) : RFQ_SK(2, 1));
+  return F == 4 ? RFQ_SK(4, 4) : (F == 2 ? RFQ_SK(4, 2) : RFQ_SK(4, 1));
 #undef RFQ_SK
 }
 
@@ -579,6 +595,24 @@ hipError_t launch_st(const void *x, const uint8_t *wc, const uint8_t *ws, int64_
 
 }  // namespace
 
+bool skinny_grid_uneven(int64_t M, int64_t N) {
+  const int64_t wgs = sk_workgroups(M, N);
+  return wgs > kFillWorkgroups && wgs < 2 * kFillWorkgroups;
+}
+
+// Where the grid holds between one and two workgroups per CU (one weight
+// fragment per workgroup at 4096 < N < 8192), the CUs that run two finish
+// last; three parts of K even that out, at the cost of the sum.  Each part
+// keeps at least 8 groups of 512 (two per wave).  Measured at 5120 x 13824
+// weights, bf16 Z, sum included: 1 row 15.0 -> 12.8 us, 8 rows 17.9 -> 15.2,
+// 16 rows 23.7 -> 19.3; at 4096 x 12288 (256 workgroups) and N >= 12288
+// every split was slower (1 row x 4096 x 12288: 8.2 -> 9.5 us).
+int skinny_split_parts(int64_t M, int64_t N, int64_t K) {
+  constexpr int kParts = 3;
+  if (M > kSkRows || K / kSkGroupK < 8 * kParts || !skinny_grid_uneven(M, N)) return 1;
+  return kParts;
+}
+
 bool skinny_four_fragments(int64_t M, int64_t N) {
   if (M <= 4 || M > 4 * kSkRows) return false;
   if (N >= 11264 && N < 16384) return true;
@@ -607,6 +641,20 @@ hipError_t launch_gemm_skinny(const uint8_t *q_codes, const uint8_t *q_scales,
   if (z_bf16)
     return launch_sk<false, true>(q_codes, q_scales, nullptr, nullptr, w_codes, w_scales, M, N, K, z, stream);
   return launch_sk<false, false>(q_codes, q_scales, nullptr, nullptr, w_codes, w_scales, M, N, K, z, stream);
+}
+
+hipError_t launch_gemm_skinny_split(const uint8_t *q_codes, const uint8_t *q_scales,
+                                    const uint8_t *r_codes, const uint8_t *r_scales,
+                                    const uint8_t *w_codes, const uint8_t *w_scales, int64_t M,
+                                    int64_t N, int64_t K, void *z, bool z_bf16, int parts,
+                                    float *work, hipStream_t stream) {
+  const hipError_t e =
+      r_codes ? launch_sk<true, false>(q_codes, q_scales, r_codes, r_scales, w_codes, w_scales, M,
+                                       N, K, work, stream, parts)
+              : launch_sk<false, false>(q_codes, q_scales, nullptr, nullptr, w_codes, w_scales, M,
+                                        N, K, work, stream, parts);
+  if (e != hipSuccess) return e;
+  return launch_splitk_sum(work, parts, M * N, z, z_bf16, stream);
 }
 
 hipError_t launch_gemm_stream(const void *x, bool x_bf16, bool residual, const uint8_t *w_codes,

@@ -125,6 +125,18 @@ hipError_t launch_gemm_skinny(const uint8_t *q_codes, const uint8_t *q_scales,
                               const uint8_t *r_codes, const uint8_t *r_scales,
                               const uint8_t *w_codes, const uint8_t *w_scales, int64_t M,
                               int64_t N, int64_t K, void *z, bool z_bf16, hipStream_t stream);
+// Whether the few-row kernel's grid for this shape holds between one and two
+// workgroups per CU (so some CUs run two and the rest one).
+bool skinny_grid_uneven(int64_t M, int64_t N);
+// Parts of K the few-row kernel splits into when given a workspace of
+// parts * M * N fp32 partials (1: no split), and that split product: the
+// kernel writes the partials to work, launch_splitk_sum adds them.
+int skinny_split_parts(int64_t M, int64_t N, int64_t K);
+hipError_t launch_gemm_skinny_split(const uint8_t *q_codes, const uint8_t *q_scales,
+                                    const uint8_t *r_codes, const uint8_t *r_scales,
+                                    const uint8_t *w_codes, const uint8_t *w_scales, int64_t M,
+                                    int64_t N, int64_t K, void *z, bool z_bf16, int parts,
+                                    float *work, hipStream_t stream);
 
 // Streaming form of the product: X[M][K] (bf16 or fp32) is quantized inside
 // the product's K loop (primary and, with residual, the quantized residual);

@@ -337,7 +337,14 @@ def test_gemm_split_validation_and_workspace_sizes():
     assert w(100, 12288, 4096) == 2 * 100 * 12288 * 4      # 96 tiles: 2 parts
     assert w(1024, 4096, 12288) == 0                       # 256 tiles
     assert w(129, 12288, 4096) == 0                        # 192 tiles, K below 8192
-    assert w(32, 4096, 12288) == 0                         # few-row kernel
+    assert w(20, 4096, 12288) == 0                         # few-row kernel
+    assert w(24, 4096, 12288) == 8 * 24 * 4096 * 4         # from 24 rows at K >= 12288: split
+    assert w(32, 4096, 8192) == 0                          # few-row kernel up to 32 rows
+    assert w(16, 5120, 13824) == 3 * 16 * 5120 * 4         # uneven few-row grid: K in 3 parts
+    assert w(1, 6000, 12288) == 3 * 1 * 6000 * 4           # the same
+    assert w(16, 5120, 8192) == 0                          # too short for 3 parts of 8 groups
+    assert w(16, 4096, 13824) == 0                         # 256 workgroups: even
+    assert w(17, 5120, 13824) == 6 * 17 * 5120 * 4         # uneven few-row grid: split from 17
     assert w(64, 12288, 4096) == 0                         # few-row kernel, 64 weight rows
     assert w(48, 13824, 5120) == 0                         # the same
     assert w(64, 16384, 12288) == 2 * 64 * 16384 * 4       # 128 tiles, from N = 16384: split

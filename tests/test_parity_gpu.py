@@ -462,7 +462,8 @@ def test_gemm_mid_rows_full_width(orc, M, N, K):
 # (parts of 1536 and a last one of 1024), 9216 at a ragged shape, 2560 (5
 # parts of 512) with 40 rows (past the few-row kernel's range in the split
 # product); M x N not a multiple of 4 for the scalar sum.
-SPLIT = [(130, 300, 8192), (131, 301, 8704), (200, 257, 9216), (40, 300, 2560)]
+SPLIT = [(130, 300, 8192), (131, 301, 8704), (200, 257, 9216), (40, 300, 2560),
+         (5, 5000, 12288), (16, 6000, 12800)]    # few-row kernel, K in 3 parts
 
 
 @pytest.mark.parametrize("M,N,K", SPLIT)
@@ -489,11 +490,13 @@ def test_gemm_split_matches_oracle(orc, M, N, K, residual, out_dtype):
 
 
 @pytest.mark.parametrize("M,N,K", [(256, 4096, 12288), (129, 5120, 13824), (100, 12288, 12288),
-                                   (64, 4096, 12288), (100, 12288, 4096)])
+                                   (64, 4096, 12288), (100, 12288, 4096), (24, 4096, 12288),
+                                   (20, 5120, 13824), (16, 5120, 13824), (1, 5120, 13824)])
 def test_gemm_split_full_width(orc, M, N, K):
     """Down-projection and wide shapes with few activation rows (K split in
-    4, 3, 2, 8 and 2 parts), sampled in every 64 x 64 output tile plus the
-    last row and column in full."""
+    4, 3, 2, 8, 2, 8 and 6 parts over 128-wide tiles, and in 3 parts by the
+    few-row kernel at 16 and 1 rows x 5120), sampled in every 64 x 64 output
+    tile plus the last row and column in full."""
     data = _gemm_case("qwen", M, N, K, seed=M + 5)
     _say("gemm split full M=%d N=%d K=%d" % (M, N, K))
     q = rfq.rfq_quantize_act(x_device(data))
