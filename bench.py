@@ -34,6 +34,7 @@ PEAK_FP4_TFLOPS = 10100.0     # MI355X dense MXFP4 matrix cores
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 matrix cores
 N_SETS = 3
+EV_EVERY = 4                  # product events on every 4th timed step (all input sets alike)
 Q_SETS = 9                    # 9 x 64 MiB quantizer inputs: over twice the 256 MB last-level cache
 PHI_MARGINS = (2, 4, 6)       # scale-threshold phi: median primary scale byte + margin
 MFMA_LOOP_ITERS = 512         # register-only MFMA loop: iterations per launch (2.1 GFLOP each)
@@ -111,20 +112,25 @@ def main():
         step(i)
     torch.cuda.synchronize()
 
-    # Timed region: the K steps, with events only around each product (an
-    # event recorded between two kernels adds a few microseconds of its own).
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    # Timed region: the K steps.  A pair of events around the product of every
+    # step adds about 5 us to each step (measured on one MI355X: 239.4 against
+    # 234.4 us without events); around every EV_EVERY-th product it adds
+    # nothing measurable and gives the same average product time (185.0
+    # against 185.1 us), so the product is timed on that uniform sample of
+    # the timed launches.
+    sampled = [i for i in range(args.steps) if i % EV_EVERY == 0]
+    evs = {i: [torch.cuda.Event(enable_timing=True) for _ in range(2)] for i in sampled}
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0.record(stream)
     for i in range(args.steps):
-        step(i, evs[i])
+        step(i, evs.get(i))
     t1.record(stream)
     torch.cuda.synchronize()
     total_ms = t0.elapsed_time(t1)
     ms_step = total_ms / args.steps
-    gm_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    gm_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs.values()]))
 
     # The two quantizers of the step, each timed over back-to-back launches
     # on the same rotated inputs (outside the timed region).
