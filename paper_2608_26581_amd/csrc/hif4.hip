@@ -575,6 +575,12 @@ constexpr int64_t kFewMaxK = int64_t(1) << 24;
 // S > 1: the activation rows come in slices of 16 (MAXM = 16), each
 // decoded into the wave's LDS area in turn and multiplied with the weight
 // pieces of the chunk, which are decoded once for all slices.
+//
+// Split K (gridDim.y = parts > 1, fp32 output only): workgroup row y takes
+// the chunks [C y / parts, C (y + 1) / parts) of the C chunks, which its
+// waves interleave as they would all of them, and writes its partial
+// products to the y-th M x N fp32 slab of the output; a second kernel adds
+// the slabs in order.  With one part this is the unsplit product.
 template <bool RES, bool ZBF16, bool WBF16, int NR, int MAXM, int WAVES, int S = 1>
 __global__ __launch_bounds__(WAVES * 64) void hif4_gemm_few_kernel(
     const uint8_t *__restrict__ qc, const uint32_t *__restrict__ qm,
@@ -587,11 +593,13 @@ __global__ __launch_bounds__(WAVES * 64) void hif4_gemm_few_kernel(
   static_assert(F * S <= 8, "partial sums of at most 8 output tiles per wave");
   __shared__ __attribute__((aligned(16))) uint8_t xarea[kFewWaves][2 * kFewRows * kFewXRow];
   __shared__ v4f part[kFewWaves][F * S][64];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane & 15, g = lane >> 4;
   const int64_t n0 = (int64_t)blockIdx.x * NR;
   const int64_t kbytes = K / 2, kblocks = K / kH;
   const int nchunks = (int)((K + kFewChunk - 1) / kFewChunk);
+  const int kpart = (int)blockIdx.y, kparts = (int)gridDim.y;
+  const int cb = (nchunks * kpart) / kparts, ce = (nchunks * (kpart + 1)) / kparts;
   const int slices = S == 1 ? 1 : (int)min<int64_t>(S, (M + kFewRows - 1) / kFewRows);
   // Rows of this workgroup's buffers: NR weight rows from n0 (clamped to N).
   const int64_t nrows = min<int64_t>(NR, N - n0);
@@ -697,18 +705,18 @@ __global__ __launch_bounds__(WAVES * 64) void hif4_gemm_few_kernel(
     for (int f = 0; f < F; ++f) acc[s][f] = v4f{0.f, 0.f, 0.f, 0.f};
   WChunk wcur, wnxt;
   XChunk xcur, xnxt;
-  if (wave < nchunks) {
-    load_w(wave, wcur);
-    load_x(wave, 0, xcur);
+  if (cb + wave < ce) {
+    load_w(cb + wave, wcur);
+    load_x(cb + wave, 0, xcur);
   }
   // The next unit's activation codes (the next slice, or the next chunk's
   // first) are requested before a unit is decoded.
   auto load_next_x = [&](int c, int s) {
     if (s + 1 < slices) load_x(c, s + 1, xnxt);
-    else if (c + kFewWaves < nchunks) load_x(c + kFewWaves, 0, xnxt);
+    else if (c + kFewWaves < ce) load_x(c + kFewWaves, 0, xnxt);
   };
-  for (int c = wave; c < nchunks; c += kFewWaves) {
-    if (c + kFewWaves < nchunks) load_w(c + kFewWaves, wnxt);
+  for (int c = cb + wave; c < ce; c += kFewWaves) {
+    if (c + kFewWaves < ce) load_w(c + kFewWaves, wnxt);
     u32x4 wp[F][4];
 #pragma unroll
     for (int s = 0; s < S; ++s) {
@@ -804,7 +812,7 @@ __global__ __launch_bounds__(WAVES * 64) void hif4_gemm_few_kernel(
           if (n + e < N) zp[e] = (uint16_t)bf16_rne(t[e]);
       }
     } else {
-      float *zp = reinterpret_cast<float *>(z) + m * N + n;
+      float *zp = reinterpret_cast<float *>(z) + kpart * M * N + m * N + n;
       if (vec_ok && n + 3 < N) {
         *reinterpret_cast<float4 *>(zp) = make_float4(t[0], t[1], t[2], t[3]);
       } else {
@@ -850,11 +858,73 @@ bool few_rows_product(int64_t M, int64_t N, int64_t K) {
   return (M <= kFewMaxRows && few_fits(N, K)) || few_halves(M, N, K);
 }
 
+// Workgroup shape of the few-row kernel for M activation rows against N
+// weight rows: weight rows per workgroup, activation rows per slice, waves,
+// slices.  Eight waves per workgroup (sixteen up to 8 rows where N <= 4096:
+// the grid then holds at most 256 workgroups, and K splits further: 1 row
+// x 4096 x 12288 20.9 -> 17.3 us, 8 rows 29.6 -> 25.1 us), the same in both
+// weight forms, so that both add every output's partial sums in the same
+// order.  Weight rows per workgroup: 16 up to 4 activation rows.  Above,
+// every workgroup decodes all activation rows again, so more weight rows per
+// workgroup spread that decode, as long as the grid keeps about one
+// workgroup per CU (one fits per CU at these register counts): 64 from N =
+// 11264 (176 or more workgroups; 32 for the bf16-weight form, whose 64-row
+// variant spills), 32 above N = 4096, 16 up to it (256 workgroups at most).
+// Measured at 16 rows: 12288 x 4096 weights 35.4 -> 27.5 us against 32 rows
+// and four waves, 4096 x 12288 52.2 -> 43.9 us against 32 rows.
+struct FewShape {
+  int nr, maxm, waves, slices;
+};
+FewShape few_shape(int64_t M, int64_t N, bool wbf16) {
+  const bool wide = !wbf16 && N >= 11264, narrow = N <= 4096;
+  const int nr = narrow ? 16 : (wide ? 64 : 32);
+  if (M <= 4) return FewShape{16, 4, narrow ? 16 : 8, 1};
+  if (M <= 8) return FewShape{nr, 8, narrow ? 16 : 8, 1};
+  if (M <= kFewRows) return FewShape{nr, 16, 8, 1};
+  if (M <= 2 * kFewRows) return FewShape{nr, 16, 8, 2};
+  return FewShape{narrow ? 16 : 32, 16, 8, 4};
+}
+
+// Parts of K for the few-row kernel given a workspace (1: unsplit; never
+// with the two launches on row halves).  The grid's g workgroups run in
+// rounds of 256 (one per CU); where the last round is partly empty, p parts
+// (g p workgroups, each a p-th of K) fill it better.  Parts are taken where
+// they raise the filled fraction of the last round, (g p / 256) /
+// ceil(g p / 256), by at least 0.15 (the sum kernel and the shorter K loops
+// cost the rest), and every wave keeps at least two chunks of 128.  Measured
+// (bf16 Z, sum included): 5120 x 13824 weights (160 workgroups; 320 up to 4
+// rows), 1 row 29.7 -> 23.2 us (4 parts), 8 rows 39.4 -> 29.2, 16 rows
+// 52.3 -> 40.4, 64 rows 114.0 -> 80.3 (3 parts); 64 rows x 12288 x 4096 (384
+// workgroups) 71.9 -> 61.1 (2 parts); where the grid fills its rounds (4096
+// x 12288: 256 workgroups) or a wave would keep one chunk (12288 x 4096 up
+// to 32 rows), every split was slower.
+int few_split_parts(int64_t M, int64_t N, int64_t K) {
+  if (M > kFewMaxRows || !few_fits(N, K)) return 1;
+  const FewShape f = few_shape(M, N, false);
+  const int64_t g = (N + f.nr - 1) / f.nr;
+  const int64_t nchunks = (K + kFewChunk - 1) / kFewChunk;
+  auto filled = [&](int64_t p) {
+    const int64_t wgs = g * p, rounds = (wgs + kFillTiles - 1) / kFillTiles;
+    return double(wgs) / double(rounds * kFillTiles);
+  };
+  int best = 1;
+  double fb = filled(1);
+  for (int p = 2; p <= 4; ++p) {
+    if (nchunks < int64_t(2) * p * f.waves) break;
+    const double fp = filled(p);
+    if (fp >= filled(1) + 0.15 && fp > fb) {
+      best = p;
+      fb = fp;
+    }
+  }
+  return best;
+}
+
 template <bool RES, bool ZBF16, bool WBF16>
 hipError_t launch_hg(const uint8_t *qc, const uint32_t *qm, const uint8_t *rc,
                      const uint32_t *rm, const uint8_t *wc, const uint32_t *wm,
                      const uint16_t *wv, int64_t M, int64_t N, int64_t K, void *z,
-                     hipStream_t stream) {
+                     hipStream_t stream, int parts = 1) {
   if (few_halves(M, N, K)) {
     const int64_t kb = K / 2, km = K / kH;
     hipError_t e = launch_hg<RES, ZBF16, WBF16>(qc, qm, rc, rm, wc, wm, wv, kFewMaxRows, N, K, z,
@@ -868,46 +938,23 @@ hipError_t launch_hg(const uint8_t *qc, const uint32_t *qm, const uint8_t *rc,
   }
   if (M <= kFewMaxRows && few_fits(N, K)) {
 #define RFQ_FEW_S(NR, MAXM, W, S)                                                              \
-  hif4_gemm_few_kernel<RES, ZBF16, WBF16, NR, MAXM, W, S>                                      \
-      <<<dim3((unsigned)((N + NR - 1) / NR)), dim3(W * 64), 0, stream>>>(qc, qm, rc, rm, wc, wm, \
-                                                                        wv, M, N, K, z)
-#define RFQ_FEW(NR, MAXM, W) RFQ_FEW_S(NR, MAXM, W, 1)
-    // Eight waves per workgroup (sixteen up to 8 rows where N <= 4096: the
-    // grid then holds at most 256 workgroups, and K splits further: 1 row
-    // x 4096 x 12288 20.9 -> 17.3 us, 8 rows 29.6 -> 25.1 us), the same in
-    // both weight forms, so that both add every output's partial sums in the
-    // same order.  Weight rows per workgroup: 16 up to 4 activation rows.  Above, every workgroup
-    // decodes all activation rows again, so more weight rows per workgroup
-    // spread that decode, as long as the grid keeps about one workgroup per
-    // CU (one fits per CU at these register counts): 64 from N = 11264
-    // (176 or more workgroups; 32 for the bf16-weight form, whose 64-row
-    // variant spills), 32 above N = 4096, 16 up to it (256 workgroups at
-    // most).  Measured at 16 rows: 12288 x 4096 weights 35.4 -> 27.5 us
-    // against 32 rows and four waves, 4096 x 12288 52.2 -> 43.9 us against 32
-    // rows.
-    const bool wide = !WBF16 && N >= 11264, narrow = N <= 4096;
-    if (M <= 4) {
-      if (narrow) RFQ_FEW(16, 4, 16);
-      else RFQ_FEW(16, 4, 8);
-    } else if (M <= 8) {
-      if (narrow) RFQ_FEW(16, 8, 16);
-      else if (!wide) RFQ_FEW(32, 8, 8);
-      else if constexpr (!WBF16) RFQ_FEW(64, 8, 8);
-    } else if (M <= kFewRows) {
-      if (narrow) RFQ_FEW(16, 16, 8);
-      else if (!wide) RFQ_FEW(32, 16, 8);
-      else if constexpr (!WBF16) RFQ_FEW(64, 16, 8);
-    } else if (M <= 2 * kFewRows) {
-      if (narrow) RFQ_FEW_S(16, 16, 8, 2);
-      else if (!wide) RFQ_FEW_S(32, 16, 8, 2);
-      else if constexpr (!WBF16) RFQ_FEW_S(64, 16, 8, 2);
-    } else {
-      if (narrow) RFQ_FEW_S(16, 16, 8, 4);
-      else RFQ_FEW_S(32, 16, 8, 4);
+  if (f.nr == NR && f.maxm == MAXM && f.waves == W && f.slices == S) {                         \
+    hif4_gemm_few_kernel<RES, ZBF16, WBF16, NR, MAXM, W, S>                                    \
+        <<<dim3((unsigned)((N + NR - 1) / NR), (unsigned)parts), dim3(W * 64), 0, stream>>>(    \
+            qc, qm, rc, rm, wc, wm, wv, M, N, K, z);                                           \
+    return hipGetLastError();                                                                  \
+  }
+    const FewShape f = few_shape(M, N, WBF16);
+    RFQ_FEW_S(16, 4, 16, 1) RFQ_FEW_S(16, 4, 8, 1)
+    RFQ_FEW_S(16, 8, 16, 1) RFQ_FEW_S(32, 8, 8, 1)
+    RFQ_FEW_S(16, 16, 8, 1) RFQ_FEW_S(32, 16, 8, 1)
+    RFQ_FEW_S(16, 16, 8, 2) RFQ_FEW_S(32, 16, 8, 2)
+    RFQ_FEW_S(16, 16, 8, 4) RFQ_FEW_S(32, 16, 8, 4)
+    if constexpr (!WBF16) {
+      RFQ_FEW_S(64, 8, 8, 1) RFQ_FEW_S(64, 16, 8, 1) RFQ_FEW_S(64, 16, 8, 2)
     }
-#undef RFQ_FEW
 #undef RFQ_FEW_S
-    return hipGetLastError();
+    return hipErrorInvalidValue;
   }
   if (((M + kBM - 1) / kBM) * ((N + 255) / 256) < kFillTiles)
     return launch_tiles<RES, ZBF16, WBF16, 128>(qc, qm, rc, rm, wc, wm, wv, M, N, K, z, stream);
@@ -986,7 +1033,11 @@ hipError_t launch_hif4_gemm(const uint8_t *q_codes, const uint32_t *q_meta,
 SplitPlan hif4_split_plan(int64_t M, int64_t N, int64_t K) {
   SplitPlan p{1, K, 0};
   if (M <= 0 || N <= 0 || K < kH || K % kH) return p;
-  if (few_rows_product(M, N, K)) return p;
+  if (few_rows_product(M, N, K)) {
+    p.parts = few_split_parts(M, N, K);
+    if (p.parts > 1) p.work_bytes = (int64_t)p.parts * M * N * 4;
+    return p;
+  }
   if (((M + kBM - 1) / kBM) * ((N + 255) / 256) >= kFillTiles) return p;
   const int64_t tiles = ((M + kBM - 1) / kBM) * ((N + 127) / 128);
   if (tiles > 128) return p;
@@ -1011,6 +1062,15 @@ hipError_t launch_hif4_gemm_split(const uint8_t *q_codes, const uint32_t *q_meta
   if (p.parts < 2 || work == nullptr || work_bytes < p.work_bytes)
     return launch_hif4_gemm(q_codes, q_meta, r_codes, r_meta, w_codes, w_meta, nullptr, M, N, K,
                             z, z_bf16, stream);
+  if (few_rows_product(M, N, K)) {
+    const hipError_t e =
+        r_codes ? launch_hg<true, false, false>(q_codes, q_meta, r_codes, r_meta, w_codes, w_meta,
+                                                nullptr, M, N, K, work, stream, p.parts)
+                : launch_hg<false, false, false>(q_codes, q_meta, nullptr, nullptr, w_codes,
+                                                 w_meta, nullptr, M, N, K, work, stream, p.parts);
+    if (e != hipSuccess) return e;
+    return launch_splitk_sum(work, p.parts, M * N, z, z_bf16, stream);
+  }
   const hipError_t e =
       r_codes ? launch_tiles<true, false, false, 128, true>(q_codes, q_meta, r_codes, r_meta,
                                                              w_codes, w_meta, nullptr, M, N, K,

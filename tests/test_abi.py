@@ -372,8 +372,15 @@ def test_hif4_gemm_split_validation_and_workspace_sizes():
     assert w(200, 300, 2560) == 8 * 200 * 300 * 4          # 6 tiles: 8 parts of 5 blocks
     assert w(129, 12288, 4096) == 0                        # 192 tiles
     assert w(1024, 4096, 12288) == 0                       # 256 tiles
-    assert w(64, 4096, 12288) == 0                         # few-row form
+    assert w(64, 4096, 12288) == 0                         # few-row form, 256 workgroups
     assert w(128, 4096, 12288) == 0                        # few-row form, two halves
+    assert w(1, 5120, 13824) == 4 * 1 * 5120 * 4           # few-row form, 320 workgroups: 4 parts
+    assert w(16, 5120, 13824) == 3 * 16 * 5120 * 4         # 160 workgroups: 3 parts
+    assert w(64, 5120, 13824) == 3 * 64 * 5120 * 4         # the same
+    assert w(64, 12288, 4096) == 2 * 64 * 12288 * 4        # 384 workgroups: 2 parts
+    assert w(16, 12288, 4096) == 0                         # 192 workgroups, one chunk a wave at 4
+    assert w(1, 13824, 5120) == 0                          # 864 workgroups: filled enough
+    assert w(16, 5120, 1024) == 0                          # 8 chunks: under two a wave
     assert w(200, 300, 448) == 0                           # 7 blocks: under 2 parts of 4
     assert w(200, 300, 100) == 0 and w(-1, 300, 2560) == 0
 

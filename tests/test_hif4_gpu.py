@@ -347,7 +347,9 @@ def test_gemm_full_size_k12288_sampled(orc):
 
 # K split over workgroups: 6 tiles of 128 x 128 -> 8 parts of 5 blocks; 9
 # tiles, 16 blocks -> 4 parts of 4; 10 tiles, 64 blocks -> 8 parts of 8.
-HIF4_SPLIT = [(200, 300, 2560), (300, 257, 1024), (150, 640, 4096)]
+HIF4_SPLIT = [(200, 300, 2560), (300, 257, 1024), (150, 640, 4096),
+              (3, 5000, 8192),      # few-row form, 313 workgroups: K in 4 parts
+              (20, 5000, 6208)]     # 157 workgroups: 3 parts, the last chunk half
 
 
 @pytest.mark.parametrize("M,N,K", HIF4_SPLIT)
@@ -377,11 +379,15 @@ def test_gemm_split_matches_oracle(orc, M, N, K, residual, out_dtype):
     assert torch.equal(z1.view(iv), z2.view(iv)), "short workspace: not the unsplit product"
 
 
-def test_gemm_split_down_projection_sampled(orc):
-    """The down-projection shape at 256 activation rows (4096 x 12288
-    weights, 64 tiles, 4 parts of 48 blocks), split: 24 sampled rows against
-    the oracle in every column."""
-    M, N, K = 256, 4096, 12288
+@pytest.mark.parametrize("M,N,K,nrows", [(256, 4096, 12288, 24), (64, 5120, 13824, 8),
+                                         (1, 5120, 13824, 1), (50, 12288, 4096, 8)])
+def test_gemm_split_down_projection_sampled(orc, M, N, K, nrows):
+    """Split products at full width, sampled rows against the oracle in
+    every column: the down-projection shape at 256 activation rows (4096 x
+    12288 weights, 64 tiles, 4 parts of 48 blocks), and the few-row form at
+    64 and 1 rows x 5120 x 13824 (3 and 4 parts) and 50 rows x 12288 x 4096
+    (2 parts)."""
+    assert rfq.rfq_hif4_gemm_workspace_bytes(M, N, K) > 0
     _say("hif4 gemm split %dx%dx%d sampled" % (M, N, K))
     w = wl.WORKLOADS["qwen"].scaled(M=M, K=K, weights=(("w", K, N),))
     data = wl.generate(w, seed=9)
@@ -390,11 +396,12 @@ def test_gemm_split_down_projection_sampled(orc):
     _, wq = _gpu_quant(wt, False, residual=False)
     z = host(rfq.rfq_hif4_gemm(*q, wq[0], wq[1], split=True))
     rng = np.random.default_rng(13)
-    rows = np.sort(np.concatenate([[0, M - 1], rng.choice(M, 22, replace=False)]))
+    inner = rng.choice(np.arange(1, M - 1), max(0, nrows - 2), replace=False) if M > 2 else []
+    rows = np.unique(np.concatenate([[0, M - 1], inner]).astype(np.int64))
     oq = orc.hif4_quantize(x[rows].astype(np.float64))
     ow = orc.hif4_quantize(wt.astype(np.float64), residual=False)
     zr, bound = orc.hif4_gemm(oq[0], oq[1], oq[2], oq[3], ow[0], ow[1])
-    assert_gemm_close(z[rows], zr, bound, False, "hif4 split K=12288")
+    assert_gemm_close(z[rows], zr, bound, False, "hif4 split sampled")
 
 
 @pytest.mark.parametrize("residual", [True, False])
