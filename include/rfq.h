@@ -402,10 +402,13 @@ rfq_status rfq_hif4_gemm_wbf16(const uint8_t *q_codes, const uint32_t *q_meta,
 /*
  * rfq_hif4_gemm with the reduction over K split across several workgroups per
  * output tile where that is faster: products whose 128 x 256 tiles number
- * fewer than 256 and whose 128 x 128 tiles number at most 128 (a few hundred
- * activation rows against a narrow weight, e.g. an MLP down projection, and
- * more rows than the few-row form takes: above 64, or above 128 where
- * N <= 4096), with K at least 512.  Each part of K writes its fp32 partial
+ * fewer than 256 and whose 128 x 128 tiles number at most 128 (up to a few
+ * hundred activation rows against a narrow weight, e.g. an MLP down
+ * projection), with K at least 512, from 49 activation rows (where
+ * N <= 4096 from 24 with K >= 12288, from 40 below); with fewer rows, where
+ * the few-row product's grid leaves its last round of workgroups partly
+ * empty (e.g. N = 5120), that product split over K in 2 to 4 parts.
+ * Each part of K writes its fp32 partial
  * sums to the workspace; one pass then adds the parts in a fixed order and
  * rounds to z_dtype, so the result is deterministic but its fp32 summation
  * order differs from rfq_hif4_gemm's (both agree within the product's

@@ -1025,19 +1025,13 @@ hipError_t launch_hif4_gemm(const uint8_t *q_codes, const uint32_t *q_meta,
   return hipErrorInvalidValue;
 }
 
-// Split of K: where the product runs 128-wide tiles that number at most 128
-// (a few hundred activation rows against a narrow weight, the down
-// projection of an MLP), 256 / tiles parts (at most 8) of at least 4 blocks
-// each, so that parts x tiles workgroups fill the 256 CUs about once; the
-// partials take parts x M x N x 4 <= 16 MiB.
-SplitPlan hif4_split_plan(int64_t M, int64_t N, int64_t K) {
+// Split of K over 128-wide tiles: where those number at most 128 (a few
+// hundred activation rows against a narrow weight, the down projection of an
+// MLP), 256 / tiles parts (at most 8) of at least 4 blocks each, so that
+// parts x tiles workgroups fill the 256 CUs about once; the partials take
+// parts x M x N x 4 <= 16 MiB.
+static SplitPlan tile_split_plan(int64_t M, int64_t N, int64_t K) {
   SplitPlan p{1, K, 0};
-  if (M <= 0 || N <= 0 || K < kH || K % kH) return p;
-  if (few_rows_product(M, N, K)) {
-    p.parts = few_split_parts(M, N, K);
-    if (p.parts > 1) p.work_bytes = (int64_t)p.parts * M * N * 4;
-    return p;
-  }
   if (((M + kBM - 1) / kBM) * ((N + 255) / 256) >= kFillTiles) return p;
   const int64_t tiles = ((M + kBM - 1) / kBM) * ((N + 127) / 128);
   if (tiles > 128) return p;
@@ -1053,6 +1047,33 @@ SplitPlan hif4_split_plan(int64_t M, int64_t N, int64_t K) {
   return p;
 }
 
+// With a workspace the tile split also replaces the few-row kernel where it
+// splits, from 49 activation rows; where N <= 4096, from 24 rows with K >=
+// 12288 and from 40 below.  Measured (bf16 Z, the few-row kernel split or
+// not by its own rule): 64 rows x 4096 x 12288 91.2 -> 47.7 us, 128 rows
+// (two launches on halves) 183.4 -> 54.2, 24 rows 50.5 -> 45.3, 16 rows
+// 40.6 against 44.6; 64 rows x 5120 x 13824 80.1 -> 65.1, 48 rows 64.2
+// against 63.9; 64 rows x 13824 x 5120 88.5 -> 72.9; 64 rows x 12288 x 4096
+// 61.6 -> 59.6, 48 rows 50.4 against 58.0; 4096 x 4096 weights 48 rows 25.9
+// -> 22.4, 96 rows 50.8 -> 26.9, 32 rows 18.7 against 21.1.
+static bool split_on_tiles(int64_t M, int64_t N, int64_t K, const SplitPlan &tiles) {
+  if (!few_rows_product(M, N, K)) return true;
+  if (tiles.parts < 2) return false;
+  const int64_t from = N <= 4096 ? (K >= 12288 ? 24 : 40) : 49;
+  return M >= from;
+}
+
+SplitPlan hif4_split_plan(int64_t M, int64_t N, int64_t K) {
+  SplitPlan p{1, K, 0};
+  if (M <= 0 || N <= 0 || K < kH || K % kH) return p;
+  const SplitPlan tiles = tile_split_plan(M, N, K);
+  if (split_on_tiles(M, N, K, tiles)) return tiles;
+  p.few_rows = true;
+  p.parts = few_split_parts(M, N, K);
+  if (p.parts > 1) p.work_bytes = (int64_t)p.parts * M * N * 4;
+  return p;
+}
+
 hipError_t launch_hif4_gemm_split(const uint8_t *q_codes, const uint32_t *q_meta,
                                   const uint8_t *r_codes, const uint32_t *r_meta,
                                   const uint8_t *w_codes, const uint32_t *w_meta, int64_t M,
@@ -1062,7 +1083,7 @@ hipError_t launch_hif4_gemm_split(const uint8_t *q_codes, const uint32_t *q_meta
   if (p.parts < 2 || work == nullptr || work_bytes < p.work_bytes)
     return launch_hif4_gemm(q_codes, q_meta, r_codes, r_meta, w_codes, w_meta, nullptr, M, N, K,
                             z, z_bf16, stream);
-  if (few_rows_product(M, N, K)) {
+  if (p.few_rows) {
     const hipError_t e =
         r_codes ? launch_hg<true, false, false>(q_codes, q_meta, r_codes, r_meta, w_codes, w_meta,
                                                 nullptr, M, N, K, work, stream, p.parts)

@@ -372,12 +372,18 @@ def test_hif4_gemm_split_validation_and_workspace_sizes():
     assert w(200, 300, 2560) == 8 * 200 * 300 * 4          # 6 tiles: 8 parts of 5 blocks
     assert w(129, 12288, 4096) == 0                        # 192 tiles
     assert w(1024, 4096, 12288) == 0                       # 256 tiles
-    assert w(64, 4096, 12288) == 0                         # few-row form, 256 workgroups
-    assert w(128, 4096, 12288) == 0                        # few-row form, two halves
+    assert w(20, 4096, 12288) == 0                         # few-row form, 256 workgroups
+    assert w(24, 4096, 12288) == 8 * 24 * 4096 * 4         # tiles from 24 rows (N <= 4096, long K)
+    assert w(64, 4096, 12288) == 8 * 64 * 4096 * 4         # the same
+    assert w(128, 4096, 12288) == 8 * 128 * 4096 * 4       # instead of two few-row halves
+    assert w(39, 4096, 4096) == 0                          # few-row form up to 39 rows at K = 4096
+    assert w(40, 4096, 4096) == 8 * 40 * 4096 * 4          # then tiles
     assert w(1, 5120, 13824) == 4 * 1 * 5120 * 4           # few-row form, 320 workgroups: 4 parts
     assert w(16, 5120, 13824) == 3 * 16 * 5120 * 4         # 160 workgroups: 3 parts
-    assert w(64, 5120, 13824) == 3 * 64 * 5120 * 4         # the same
-    assert w(64, 12288, 4096) == 2 * 64 * 12288 * 4        # 384 workgroups: 2 parts
+    assert w(48, 5120, 13824) == 3 * 48 * 5120 * 4         # the same up to 48 rows
+    assert w(49, 5120, 13824) == 6 * 49 * 5120 * 4         # then tiles (40 of them: 6 parts)
+    assert w(40, 12288, 4096) == 2 * 40 * 12288 * 4        # few-row form, 384 workgroups: 2 parts
+    assert w(64, 12288, 4096) == 2 * 64 * 12288 * 4        # tiles (96: 2 parts)
     assert w(16, 12288, 4096) == 0                         # 192 workgroups, one chunk a wave at 4
     assert w(1, 13824, 5120) == 0                          # 864 workgroups: filled enough
     assert w(16, 5120, 1024) == 0                          # 8 chunks: under two a wave

@@ -379,14 +379,15 @@ def test_gemm_split_matches_oracle(orc, M, N, K, residual, out_dtype):
     assert torch.equal(z1.view(iv), z2.view(iv)), "short workspace: not the unsplit product"
 
 
-@pytest.mark.parametrize("M,N,K,nrows", [(256, 4096, 12288, 24), (64, 5120, 13824, 8),
-                                         (1, 5120, 13824, 1), (50, 12288, 4096, 8)])
+@pytest.mark.parametrize("M,N,K,nrows", [(256, 4096, 12288, 24), (64, 4096, 12288, 8),
+                                         (30, 4000, 12288, 8), (40, 5120, 13824, 8),
+                                         (1, 5120, 13824, 1), (40, 12288, 4096, 8)])
 def test_gemm_split_down_projection_sampled(orc, M, N, K, nrows):
     """Split products at full width, sampled rows against the oracle in
-    every column: the down-projection shape at 256 activation rows (4096 x
-    12288 weights, 64 tiles, 4 parts of 48 blocks), and the few-row form at
-    64 and 1 rows x 5120 x 13824 (3 and 4 parts) and 50 rows x 12288 x 4096
-    (2 parts)."""
+    every column: 128-wide tiles at the down-projection shape (4096 x 12288
+    weights) for 256 rows (64 tiles, 4 parts of 48 blocks), 64 rows and 30
+    rows (ragged N; 32 tiles, 8 parts), and the few-row form at 40 and 1 rows
+    x 5120 x 13824 (3 and 4 parts) and 40 rows x 12288 x 4096 (2 parts)."""
     assert rfq.rfq_hif4_gemm_workspace_bytes(M, N, K) > 0
     _say("hif4 gemm split %dx%dx%d sampled" % (M, N, K))
     w = wl.WORKLOADS["qwen"].scaled(M=M, K=K, weights=(("w", K, N),))
