@@ -177,7 +177,7 @@ __device__ __forceinline__ void reads_first() {
 // that lane; the lower lane stores the primary codes, the upper the residual.
 template <class C, bool HRES>
 __device__ __forceinline__ void swiglu_epilogue(const v16f (&acc)[C::kFM][C::kFN],
-                                                const SwigluOut &so, int64_t M, int64_t m_base,
+                                                const SwigluOut so, int64_t M, int64_t m_base,
                                                 int64_t n_base, int h) {
   const int64_t nblk = so.nh / 32;
 #pragma unroll
@@ -187,15 +187,20 @@ __device__ __forceinline__ void swiglu_epilogue(const v16f (&acc)[C::kFM][C::kFN
       const v16f &ag = acc[i][2 * p], &au = acc[i][2 * p + 1];
       const int64_t m = m_base + 32 * i;
       const int64_t blk = (n_base + 64 * p) / 64;
+      // g, u and h rounded to bf16 in pairs by the hardware conversion (the
+      // bits of the integer rounding the standalone SwiGLU quantizer uses).
       float hv[16];
-      uint32_t hbits[16];
+      uint32_t hpair[8];
       float am = 0.0f;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        hbits[e] = swiglu_bits(__uint_as_float(bf16_rne_bits(ag[e])),
-                               __uint_as_float(bf16_rne_bits(au[e])));
-        hv[e] = __uint_as_float(hbits[e]);
-        am = fmaxf(am, fabsf(hv[e]));
+      for (int e = 0; e < 16; e += 2) {
+        const uint32_t gp = bf16x2_rne(ag[e], ag[e + 1]), up = bf16x2_rne(au[e], au[e + 1]);
+        hpair[e / 2] = bf16x2_rne(
+            swiglu_f32(__uint_as_float(gp << 16), __uint_as_float(up << 16)),
+            swiglu_f32(__uint_as_float(gp & 0xFFFF0000u), __uint_as_float(up & 0xFFFF0000u)));
+        hv[e] = __uint_as_float(hpair[e / 2] << 16);
+        hv[e + 1] = __uint_as_float(hpair[e / 2] & 0xFFFF0000u);
+        am = fmaxf(am, fmaxf(fabsf(hv[e]), fabsf(hv[e + 1])));
       }
       am = fmaxf(am, __shfl_xor(am, 32));
       const uint32_t qb = scale_byte(am);
@@ -246,8 +251,8 @@ __device__ __forceinline__ void swiglu_epilogue(const v16f (&acc)[C::kFM][C::kFN
 #pragma unroll
           for (int a = 0; a < 4; ++a) {
             uint2 w;
-            w.x = (hbits[4 * a] >> 16) | (hbits[4 * a + 1] & 0xFFFF0000u);
-            w.y = (hbits[4 * a + 2] >> 16) | (hbits[4 * a + 3] & 0xFFFF0000u);
+            w.x = hpair[2 * a];
+            w.y = hpair[2 * a + 1];
             *reinterpret_cast<uint2 *>(hp + 8 * a) = w;
           }
         }
@@ -272,7 +277,7 @@ __device__ __forceinline__ void gemm_tile(
     const uint8_t *__restrict__ qc, const uint8_t *__restrict__ qs,
     const uint8_t *__restrict__ rc, const uint8_t *__restrict__ rs,
     const uint8_t *__restrict__ wc, const uint8_t *__restrict__ ws,
-    int64_t M, int64_t N, int64_t K, void *__restrict__ z, const SwigluOut &so,
+    int64_t M, int64_t N, int64_t K, void *__restrict__ z, const SwigluOut so,
     const uint8_t *__restrict__ phi, int64_t ksplit) {
   static_assert(!PHI || std::is_same<C, Big>::value, "fallback-indicator maps use 256 x 256 tiles");
   static_assert(!SPLIT || (!ZBF16 && !SWIGLU && !PHI), "split partials are fp32 products");

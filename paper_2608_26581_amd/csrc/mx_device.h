@@ -67,11 +67,16 @@ __device__ __forceinline__ uint32_t bf16_rne_bits(float f) {
   return (u + 0x7FFFu + ((u >> 16) & 1u)) & 0xFFFF0000u;
 }
 
-// SwiGLU intermediate of one element: bf16(silu(g) * u), silu(g) = g / (1 +
-// exp(-g)), fp32 arithmetic; g and u are bf16 values.  Returned as fp32 bits.
-__device__ __forceinline__ uint32_t swiglu_bits(float g, float u) {
+// SwiGLU intermediate of one element before its bf16 rounding: silu(g) * u,
+// silu(g) = g / (1 + exp(-g)), fp32 arithmetic; g and u are bf16 values.
+__device__ __forceinline__ float swiglu_f32(float g, float u) {
   const float silu = g * __builtin_amdgcn_rcpf(1.0f + __expf(-g));
-  return bf16_rne_bits(silu * u);
+  return silu * u;
+}
+
+// bf16(silu(g) * u), returned as fp32 bits.
+__device__ __forceinline__ uint32_t swiglu_bits(float g, float u) {
+  return bf16_rne_bits(swiglu_f32(g, u));
 }
 
 }  // namespace rfq

@@ -32,8 +32,9 @@ def _ptr(t):
 @pytest.mark.parametrize("residual", [True, False])
 def test_noalloc_split_matches_workspace_split(residual):
     lib = _lib()
-    # 16 MiB of partials (4 parts), then 0.6 MiB (4 parts).
-    for (M, N, K) in [(256, 4096, 12288), (129, 300, 8192)]:
+    # 16 MiB of partials (4 parts), then 0.6 MiB (4 parts), then the few-row
+    # kernel's own split (3 parts, 0.9 MiB).
+    for (M, N, K) in [(256, 4096, 12288), (129, 300, 8192), (16, 5120, 13824)]:
         print("noalloc split M=%d N=%d K=%d residual=%s" % (M, N, K, residual), flush=True)
         w = wl.WORKLOADS["qwen"].scaled(M=M, K=K, weights=(("w", K, N),))
         data = wl.generate(w, seed=M + K)
