@@ -1017,12 +1017,13 @@ def test_path_replays_from_a_hip_graph(M, N, K):
         assert torch.equal(a, b), "replay with new inputs differs from the eager result"
 
 
-def test_split_products_replay_from_a_hip_graph():
+@pytest.mark.parametrize("M,N,K", [(130, 300, 8192), (16, 5120, 13824)])
+def test_split_products_replay_from_a_hip_graph(M, N, K):
     """The split product with a caller-owned workspace and the allocation-free
     one on the static scratch array capture into one HIP graph (two kernels
-    each, nothing allocated or cleared inside the calls); every replay
+    each, nothing allocated or cleared inside the calls; 128-wide tiles, and
+    the few-row kernel's own split at 16 rows x 5120); every replay
     reproduces the eager results, and both give the same bits."""
-    M, N, K = 130, 300, 8192
     gen = torch.Generator(device="cuda").manual_seed(5)
     x = torch.randn((M, K), generator=gen, device="cuda").to(torch.bfloat16)
     w = rfq.rfq_quantize_weight(torch.randn((N, K), generator=gen, device="cuda") * 0.02)
@@ -1059,10 +1060,12 @@ def test_split_products_replay_from_a_hip_graph():
         assert torch.equal(za, want[0]) and torch.equal(zb, want[1]), "replay %d" % i
 
 
-def test_hif4_path_replays_from_a_hip_graph():
-    """The HiF4 quantizer, product and bf16-weight product capture into a HIP
-    graph; every replay (eager work between) reproduces the eager results."""
-    M, N, K = 300, 700, 640
+@pytest.mark.parametrize("M,N,K", [(300, 700, 640), (3, 5000, 8192)])
+def test_hif4_path_replays_from_a_hip_graph(M, N, K):
+    """The HiF4 quantizer, product, bf16-weight product and split product
+    (128-wide tiles in 2 parts; the few-row kernel in 4 at 3 rows x 5000)
+    capture into a HIP graph; every replay (eager work between) reproduces
+    the eager results."""
     gen = torch.Generator(device="cuda").manual_seed(5)
     x = torch.randn((M, K), generator=gen, device="cuda").to(torch.bfloat16)
     hw = rfq.rfq_hif4_quantize(torch.randn((N, K), generator=gen, device="cuda") * 0.02,
@@ -1074,15 +1077,20 @@ def test_hif4_path_replays_from_a_hip_graph():
          torch.empty((M, K // 64), dtype=torch.int32, device="cuda")]
     z = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
     z2 = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    z3 = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(rfq.rfq_hif4_gemm_workspace_bytes(M, N, K), dtype=torch.uint8,
+                     device="cuda")
+    assert ws.numel() > 0
 
     def path():
         rfq.rfq_hif4_quantize(x, out=q)
         rfq.rfq_hif4_gemm(*q, hw[0], hw[1], out=z)
         rfq.rfq_hif4_gemm_wbf16(*q, wv, out=z2)
+        rfq.rfq_hif4_gemm_split(*q, hw[0], hw[1], ws, out=z3)
 
     path()
     torch.cuda.synchronize()
-    want = [t.clone() for t in q + [z, z2]]
+    want = [t.clone() for t in q + [z, z2, z3]]
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):
@@ -1093,10 +1101,10 @@ def test_hif4_path_replays_from_a_hip_graph():
         path()
     _say("hif4 graph replay M=%d N=%d K=%d" % (M, N, K))
     for i in range(4):
-        for t in q + [z, z2]:
+        for t in q + [z, z2, z3]:
             t.zero_()
         torch.randn((1024, 1024), generator=gen, device="cuda").sum()
         graph.replay()
         torch.cuda.synchronize()
-        for a, b in zip(q + [z, z2], want):
+        for a, b in zip(q + [z, z2, z3], want):
             assert torch.equal(a, b), "replay %d differs from the eager result" % i
