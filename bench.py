@@ -380,6 +380,14 @@ def secondary(torch, rfq, wl, x, w, stream):
         loop[mode] = {"ms": round(ms, 5), "tflops": round(
             MFMA_LOOP_ITERS * rfq.MFMA_LOOP_FLOPS_PER_ITER / ms / 1e9, 1)}
     out["mfma_fp4_register_loop"] = loop
+    # The same loop on the bf16 matrix cores the HiF4 product runs on.
+    loop = {}
+    for mode, rnd in (("random_operands", True), ("constant_operands", False)):
+        ms = _per_launch_ms(torch, stream, lambda i: rfq.rfq_mfma_bf16_loop(
+            MFMA_LOOP_ITERS, random_operands=rnd, sink=sink, stream=stream), 20)
+        loop[mode] = {"ms": round(ms, 5), "tflops": round(
+            MFMA_LOOP_ITERS * rfq.MFMA_BF16_LOOP_FLOPS_PER_ITER / ms / 1e9, 1)}
+    out["mfma_bf16_register_loop"] = loop
     # Fallback indicator by the scale-threshold rule (phi = 1 on tiles holding
     # a primary scale byte >= the median + margin): residual work only where
     # outliers are, at three thresholds; exec_tflops counts the MFMA work
@@ -402,6 +410,7 @@ def secondary(torch, rfq, wl, x, w, stream):
     # quantizer (primary + residual of the bf16 activations) and the product,
     # which decodes to bf16 and runs the bf16 matrix cores (no HiF4 format
     # there), so its rate is set against the 2.5 PFLOP/s dense bf16 peak.
+    bf16_loop = out["mfma_bf16_register_loop"]["random_operands"]["tflops"]
     hq = rfq.rfq_hif4_quantize(x)
     hw = rfq.rfq_hif4_quantize(w, residual=False)
     ms = _per_launch_ms(torch, stream, lambda i: rfq.rfq_hif4_quantize(x, out=hq, stream=stream),
@@ -416,7 +425,8 @@ def secondary(torch, rfq, wl, x, w, stream):
         tf = (4.0 if res else 2.0) * M * N * K / ms / 1e9
         out["hif4_gemm" if res else "hif4_gemm_plain"] = {
             "ms": round(ms, 5), "exec_tflops": round(tf, 1),
-            "frac_of_bf16_peak": round(tf / (PEAK_BF16_TFLOPS), 4)}
+            "frac_of_bf16_peak": round(tf / (PEAK_BF16_TFLOPS), 4),
+            "frac_of_bf16_loop_random": round(tf / bf16_loop, 4)}
     # The same product with the weights decoded to bf16 once (exact; constant
     # weights, or weights re-quantized once per training step).
     wv = rfq.rfq_hif4_dequant(hw[0], hw[1], out_dtype=torch.bfloat16)
@@ -424,7 +434,8 @@ def secondary(torch, rfq, wl, x, w, stream):
         *hq, wv, out=z, stream=stream), 10)
     tf = 4.0 * M * N * K / ms / 1e9
     out["hif4_gemm_bf16_weights"] = {"ms": round(ms, 5), "exec_tflops": round(tf, 1),
-                                     "frac_of_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4)}
+                                     "frac_of_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4),
+                                     "frac_of_bf16_loop_random": round(tf / bf16_loop, 4)}
     del hq, hw, z, wv
 
     # Decode-sized products on the same weight: few activation rows, codes in

@@ -456,6 +456,18 @@ int64_t rfq_hif4_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K);
  */
 rfq_status rfq_mfma_fp4_loop(int64_t iters, int random_operands, float *sink, void *hip_stream);
 
+/*
+ * Measurement support, not a step of the method: rfq_mfma_fp4_loop on the
+ * bf16 matrix cores that the HiF4 product (Sec. 3.3) runs on.  Same grid,
+ * wave layout, accumulator pattern, arguments, sink and errors; each wave
+ * issues 8 * iters v_mfma_f32_32x32x16_bf16 (2 * 32 * 32 * 16 flops each),
+ * so one launch is 256 * 8 * 8 * iters * 32768 flops.  Random operands are
+ * finite bf16 values in [0.5, 2) of either sign (random sign and mantissa,
+ * fixed per work item); constant operands are 1.0, which gives
+ * sink[t] = 2048 * iters (exact up to iters = 8192).
+ */
+rfq_status rfq_mfma_bf16_loop(int64_t iters, int random_operands, float *sink, void *hip_stream);
+
 /* Static, never-NULL description of a status code. */
 const char *rfq_status_str(rfq_status s);
 

@@ -451,6 +451,17 @@ rfq_status rfq_mfma_fp4_loop(int64_t iters, int random_operands, float *sink,
                                             static_cast<hipStream_t>(hip_stream)));
 }
 
+rfq_status rfq_mfma_bf16_loop(int64_t iters, int random_operands, float *sink,
+                              void *hip_stream) {
+  if (iters < 1 || iters > (int64_t(1) << 24)) return RFQ_ERR_SHAPE;
+  if (!sink) return RFQ_ERR_NULL;
+  if (!aligned(sink, 16)) return RFQ_ERR_ALIGN;
+  rfq_status s = check_device();
+  if (s != RFQ_OK) return s;
+  return launched(rfq::launch_mfma_bf16_loop(iters, random_operands != 0, sink,
+                                             static_cast<hipStream_t>(hip_stream)));
+}
+
 const char *rfq_status_str(rfq_status s) {
   switch (s) {
     case RFQ_OK: return "ok";

@@ -66,7 +66,61 @@ __global__ __launch_bounds__(kLoopThreads, 2) void mfma_fp4_loop_kernel(int64_t 
   sink[gid] = s;
 }
 
+// The same loop on the bf16 matrix cores that the HiF4 product runs on
+// (v_mfma_f32_32x32x16_bf16, 2 x 4 accumulators of 32 x 32 per wave).  Random
+// operands are finite bf16 values: random sign and 7 mantissa bits, exponent
+// 0x7E or 0x7F (magnitudes in [0.5, 2)); constant operands are 1.0.
+typedef __bf16 v8bf_t __attribute__((ext_vector_type(8)));
+
+__global__ __launch_bounds__(kLoopThreads, 2) void mfma_bf16_loop_kernel(int64_t iters, int random,
+                                                                        float *__restrict__ sink) {
+  const uint32_t gid = blockIdx.x * kLoopThreads + threadIdx.x;
+  auto operand = [&](uint32_t salt) {
+    uint32_t v[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const uint32_t h = mix(gid * 97u + salt * 8u + e + 1u);
+      // Two bf16 halves: sign, the exponent's lowest bit and the mantissa
+      // from h, the exponent's upper bits 0111111 (exponent 0x7E or 0x7F).
+      v[e] = random ? (h & 0x80FF80FFu) | 0x3F003F00u : 0x3F803F80u;
+    }
+    return __builtin_bit_cast(v8bf_t, u32x4{v[0], v[1], v[2], v[3]});
+  };
+  v8bf_t w[4], a[2];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) w[j] = operand(j);
+#pragma unroll
+  for (int i = 0; i < 2; ++i) a[i] = operand(4 + i);
+  v16f acc[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = v16f{};
+  for (int64_t it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w[j], a[i], acc[i][j], 0, 0, 0);
+  }
+  float s = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) s += acc[i][j][e];
+  sink[gid] = s;
+}
+
 }  // namespace
+
+hipError_t launch_mfma_bf16_loop(int64_t iters, bool random_operands, float *sink,
+                                 hipStream_t stream) {
+  mfma_bf16_loop_kernel<<<dim3(kMfmaLoopWorkgroups), dim3(kLoopThreads), 0, stream>>>(
+      iters, random_operands ? 1 : 0, sink);
+  return hipGetLastError();
+}
 
 hipError_t launch_mfma_fp4_loop(int64_t iters, bool random_operands, float *sink,
                                 hipStream_t stream) {

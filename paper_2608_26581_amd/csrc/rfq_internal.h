@@ -208,5 +208,8 @@ hipError_t launch_hif4_gemm_split(const uint8_t *q_codes, const uint32_t *q_meta
 constexpr int kMfmaLoopWorkgroups = 256;
 hipError_t launch_mfma_fp4_loop(int64_t iters, bool random_operands, float *sink,
                                 hipStream_t stream);
+// The same loop of bf16 MFMAs (32x32x16), same grid and sink.
+hipError_t launch_mfma_bf16_loop(int64_t iters, bool random_operands, float *sink,
+                                 hipStream_t stream);
 
 }  // namespace rfq

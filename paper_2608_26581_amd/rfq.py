@@ -30,7 +30,8 @@ EXPORTS = (
     "rfq_quantize_act", "rfq_quantize_weight", "rfq_gemm", "rfq_dequant",
     "rfq_swiglu_quantize_act", "rfq_gemm_phi", "rfq_fallback_map", "rfq_gemm_swiglu_quantize",
     "rfq_gemm_stream", "rfq_hif4_quantize", "rfq_hif4_dequant", "rfq_hif4_gemm",
-    "rfq_hif4_gemm_wbf16", "rfq_mfma_fp4_loop", "rfq_gemm_split", "rfq_gemm_workspace_bytes",
+    "rfq_hif4_gemm_wbf16", "rfq_mfma_fp4_loop", "rfq_mfma_bf16_loop", "rfq_gemm_split",
+    "rfq_gemm_workspace_bytes",
     "rfq_gemm_split_noalloc", "rfq_hif4_gemm_split", "rfq_hif4_gemm_workspace_bytes",
     "rfq_status_str", "rfq_abi_version",
 )
@@ -39,6 +40,8 @@ EXPORTS = (
 # iteration (each of the 2048 waves issues 8 MFMAs of 32 x 32 x 64).
 MFMA_LOOP_ITEMS = 256 * 512
 MFMA_LOOP_FLOPS_PER_ITER = 256 * 8 * 8 * 2 * 32 * 32 * 64
+# rfq_mfma_bf16_loop: the same grid, 8 MFMAs of 32 x 32 x 16 per wave and iteration.
+MFMA_BF16_LOOP_FLOPS_PER_ITER = 256 * 8 * 8 * 2 * 32 * 32 * 16
 
 RFQ_PHI_RESIDUAL_NONZERO = 0
 RFQ_PHI_SCALE_AT_LEAST = 1
@@ -79,6 +82,7 @@ def load():
     lib.rfq_hif4_gemm.argtypes = [P, P, P, P, P, P, I64, I64, I64, P, I32, P]
     lib.rfq_hif4_gemm_wbf16.argtypes = [P, P, P, P, P, I64, I64, I64, P, I32, P]
     lib.rfq_mfma_fp4_loop.argtypes = [I64, I32, P, P]
+    lib.rfq_mfma_bf16_loop.argtypes = [I64, I32, P, P]
     lib.rfq_gemm_split.argtypes = [P, P, P, P, P, P, I64, I64, I64, P, I32, P, I64, P]
     lib.rfq_gemm_split_noalloc.argtypes = [P, P, P, P, P, P, I64, I64, I64, P, I32, P]
     lib.rfq_gemm_workspace_bytes.argtypes = [I64, I64, I64]
@@ -89,8 +93,8 @@ def load():
     for f in ("rfq_quantize_act", "rfq_quantize_weight", "rfq_gemm", "rfq_dequant",
               "rfq_swiglu_quantize_act", "rfq_gemm_swiglu_quantize", "rfq_gemm_phi",
               "rfq_fallback_map", "rfq_gemm_stream", "rfq_hif4_quantize", "rfq_hif4_dequant",
-              "rfq_hif4_gemm", "rfq_hif4_gemm_wbf16", "rfq_mfma_fp4_loop", "rfq_gemm_split",
-              "rfq_hif4_gemm_split",
+              "rfq_hif4_gemm", "rfq_hif4_gemm_wbf16", "rfq_mfma_fp4_loop", "rfq_mfma_bf16_loop",
+              "rfq_gemm_split", "rfq_hif4_gemm_split",
               "rfq_gemm_split_noalloc"):
         getattr(lib, f).restype = I32
     lib.rfq_status_str.argtypes = [I32]
@@ -425,6 +429,19 @@ def rfq_mfma_fp4_loop(iters, random_operands=True, sink=None, stream=None):
     st = load().rfq_mfma_fp4_loop(int(iters), 1 if random_operands else 0, _ptr(sink),
                                   _stream(stream, sink.get_device()))
     _check("rfq_mfma_fp4_loop", st)
+    return sink
+
+
+def rfq_mfma_bf16_loop(iters, random_operands=True, sink=None, stream=None):
+    """Measurement support: rfq_mfma_fp4_loop on the bf16 matrix cores
+    (MFMA_BF16_LOOP_FLOPS_PER_ITER flops per iteration)."""
+    if sink is None:
+        sink = torch.empty(MFMA_LOOP_ITEMS, dtype=torch.float32, device="cuda")
+    else:
+        _need(sink, "sink", (torch.float32,), (MFMA_LOOP_ITEMS,))
+    st = load().rfq_mfma_bf16_loop(int(iters), 1 if random_operands else 0, _ptr(sink),
+                                   _stream(stream, sink.get_device()))
+    _check("rfq_mfma_bf16_loop", st)
     return sink
 
 

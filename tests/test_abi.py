@@ -406,12 +406,12 @@ def test_gemm_split_noalloc_validation():
 def test_mfma_loop_validation():
     """The measurement loop: iteration count 1 .. 2^24, a 16-byte aligned
     sink."""
-    f = _lib().rfq_mfma_fp4_loop
-    assert f(0, 1, A, None) == ESHAPE
-    assert f(-5, 1, A, None) == ESHAPE
-    assert f((1 << 24) + 1, 0, A, None) == ESHAPE
-    assert f(4, 1, None, None) == ENULL
-    assert f(4, 1, MIS, None) == EALIGN
+    for f in (_lib().rfq_mfma_fp4_loop, _lib().rfq_mfma_bf16_loop):
+        assert f(0, 1, A, None) == ESHAPE
+        assert f(-5, 1, A, None) == ESHAPE
+        assert f((1 << 24) + 1, 0, A, None) == ESHAPE
+        assert f(4, 1, None, None) == ENULL
+        assert f(4, 1, MIS, None) == EALIGN
 
 
 def test_binding_rejects_host_tensors():
@@ -438,6 +438,7 @@ def test_binding_rejects_host_tensors():
         lambda: binding.rfq_hif4_gemm(c, m, None, None, c, m),
         lambda: binding.rfq_hif4_gemm_wbf16(c, m, None, None, xb),
         lambda: binding.rfq_mfma_fp4_loop(4, sink=torch.zeros(binding.MFMA_LOOP_ITEMS)),
+        lambda: binding.rfq_mfma_bf16_loop(4, sink=torch.zeros(binding.MFMA_LOOP_ITEMS)),
         lambda: binding.rfq_gemm_split(c, s, None, None, c, s, None),
         lambda: binding.rfq_gemm_split_noalloc(c, s, None, None, c, s),
     ]
@@ -456,6 +457,7 @@ def test_valid_arguments_without_a_gpu_report_device_error():
     assert _lib().rfq_hif4_quantize(A, 1, 4, 64, A, A, A, A, None) == EDEVICE
     assert _lib().rfq_hif4_gemm(A, A, A, A, A, A, 8, 8, 64, A, 0, None) == EDEVICE
     assert _lib().rfq_mfma_fp4_loop(4, 1, A, None) == EDEVICE
+    assert _lib().rfq_mfma_bf16_loop(4, 1, A, None) == EDEVICE
     assert _lib().rfq_gemm_split(A, A, A, A, A, A, 8, 8, 512, A, 0, A, 64, None) == EDEVICE
     assert _lib().rfq_gemm_split_noalloc(A, A, A, A, A, A, 8, 8, 512, A, 0, None) == EDEVICE
     # The HiF4 product's launch-size limit sits at the largest grid it may
