@@ -54,7 +54,10 @@ def parse():
                    help="skip the secondary workloads and the accuracy diagnostics")
     p.add_argument("--cpu-rows", type=int, default=8,
                    help="activation rows in the oracle's sample of the step")
-    return p.parse_args()
+    args = p.parse_args()
+    if args.steps < 1 or args.warmup < 0:
+        p.error("--steps must be at least 1 and --warmup at least 0")
+    return args
 
 
 def main():
