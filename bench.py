@@ -430,6 +430,15 @@ def secondary(torch, rfq, wl, x, w, stream):
             "ms": round(ms, 5), "exec_tflops": round(tf, 1),
             "frac_of_bf16_peak": round(tf / (PEAK_BF16_TFLOPS), 4),
             "frac_of_bf16_loop_random": round(tf / bf16_loop, 4)}
+    # The product given a workspace (rfq_hif4_gemm_split): at this size the
+    # weights are decoded to bf16 into it on every call, then multiplied.
+    ms = _per_launch_ms(torch, stream, lambda i: rfq.rfq_hif4_gemm(
+        *hq, hw[0], hw[1], out=z, stream=stream, split=True), 10)
+    tf = 4.0 * M * N * K / ms / 1e9
+    out["hif4_gemm_workspace"] = {"ms": round(ms, 5), "exec_tflops": round(tf, 1),
+                                  "frac_of_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4),
+                                  "frac_of_bf16_loop_random": round(tf / bf16_loop, 4),
+                                  "workspace_bytes": rfq.rfq_hif4_gemm_workspace_bytes(M, N, K)}
     # The same product with the weights decoded to bf16 once (exact; constant
     # weights, or weights re-quantized once per training step).
     wv = rfq.rfq_hif4_dequant(hw[0], hw[1], out_dtype=torch.bfloat16)

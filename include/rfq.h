@@ -407,7 +407,11 @@ rfq_status rfq_hif4_gemm_wbf16(const uint8_t *q_codes, const uint32_t *q_meta,
  * projection), with K at least 512, from 49 activation rows (where
  * N <= 4096 from 24 with K >= 12288, from 40 below); with fewer rows, where
  * the few-row product's grid leaves its last round of workgroups partly
- * empty (e.g. N = 5120), that product split over K in 2 to 4 parts.
+ * empty (e.g. N = 5120), that product split over K in 2 to 4 parts.  From
+ * 1024 rows, where K is not split, the workspace instead receives the
+ * weights decoded to bf16 (N * K * 2 bytes, at most 1 GiB) and the product
+ * of rfq_hif4_gemm_wbf16 runs on them: the bits of rfq_hif4_gemm, without
+ * decoding W again for every 128 rows.
  * Each part of K writes its fp32 partial
  * sums to the workspace; one pass then adds the parts in a fixed order and
  * rounds to z_dtype, so the result is deterministic but its fp32 summation
@@ -430,7 +434,8 @@ rfq_status rfq_hif4_gemm_split(const uint8_t *q_codes, const uint32_t *q_meta,
 
 /*
  * Workspace rfq_hif4_gemm_split uses for this shape: parts * M * N * 4 bytes
- * for the fp32 partials (at most 16 MiB), or 0 where it does not split.
+ * for the fp32 partials (at most 16 MiB), N * K * 2 bytes where it decodes
+ * the weights into it (at most 1 GiB), or 0 where it does neither.
  * Host-only; no device call.
  */
 int64_t rfq_hif4_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K);

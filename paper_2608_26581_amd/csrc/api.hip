@@ -391,7 +391,7 @@ rfq_status rfq_hif4_gemm(const uint8_t *q_codes, const uint32_t *q_meta,
 int64_t rfq_hif4_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) {
   if (check_k64(M, K) != RFQ_OK || N < 0 || !hif4_product_fits(M, N)) return 0;
   const rfq::SplitPlan p = rfq::hif4_split_plan(M, N, K);
-  return p.parts > 1 ? p.work_bytes : 0;
+  return (p.parts > 1 || p.decode_w) ? p.work_bytes : 0;
 }
 
 rfq_status rfq_hif4_gemm_split(const uint8_t *q_codes, const uint32_t *q_meta,

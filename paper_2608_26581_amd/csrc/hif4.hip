@@ -1063,10 +1063,25 @@ static bool split_on_tiles(int64_t M, int64_t N, int64_t K, const SplitPlan &til
   return M >= from;
 }
 
+// Without a split, from this many rows the weights are decoded to bf16 once
+// into the workspace and the bf16-weight product runs on them (the same bits
+// as the codes form, whose tile rows each decode all of W again).  Measured
+// (bf16 Z, decode included): 4096 rows x 4096 x 12288 832 -> 740 us, 4096 x
+// 12288 x 4096 847 -> 754-780, 4096 x 13824 x 5120 1218 -> 1084-1100, 1024
+// rows x 12288 x 4096 268 -> 249; at 512 rows no gain (220 against 228).
+constexpr int64_t kDecodeMinRows = 1024;
+constexpr int64_t kDecodeMaxBytes = int64_t(1) << 30;
+
 SplitPlan hif4_split_plan(int64_t M, int64_t N, int64_t K) {
   SplitPlan p{1, K, 0};
   if (M <= 0 || N <= 0 || K < kH || K % kH) return p;
   const SplitPlan tiles = tile_split_plan(M, N, K);
+  if (tiles.parts < 2 && !few_rows_product(M, N, K) && M >= kDecodeMinRows &&
+      N * K * 2 <= kDecodeMaxBytes) {
+    p.decode_w = true;
+    p.work_bytes = N * K * 2;
+    return p;
+  }
   if (split_on_tiles(M, N, K, tiles)) return tiles;
   p.few_rows = true;
   p.parts = few_split_parts(M, N, K);
@@ -1080,6 +1095,13 @@ hipError_t launch_hif4_gemm_split(const uint8_t *q_codes, const uint32_t *q_meta
                                   int64_t N, int64_t K, void *z, bool z_bf16, float *work,
                                   int64_t work_bytes, hipStream_t stream) {
   const SplitPlan p = hif4_split_plan(M, N, K);
+  if (p.decode_w && work != nullptr && work_bytes >= p.work_bytes) {
+    uint16_t *wv = reinterpret_cast<uint16_t *>(work);
+    const hipError_t e = launch_hif4_dequant(w_codes, w_meta, N * K, wv, true, stream);
+    if (e != hipSuccess) return e;
+    return launch_hif4_gemm(q_codes, q_meta, r_codes, r_meta, nullptr, nullptr, wv, M, N, K, z,
+                            z_bf16, stream);
+  }
   if (p.parts < 2 || work == nullptr || work_bytes < p.work_bytes)
     return launch_hif4_gemm(q_codes, q_meta, r_codes, r_meta, w_codes, w_meta, nullptr, M, N, K,
                             z, z_bf16, stream);

@@ -82,6 +82,7 @@ struct SplitPlan {
   int64_t ksplit;
   int64_t work_bytes;
   bool few_rows = false;  // HiF4: the split runs the few-row kernel
+  bool decode_w = false;  // HiF4: no split; W decoded to bf16 in the workspace
 };
 SplitPlan splitk_plan(int64_t M, int64_t N, int64_t K, int parts_wanted = 0);
 // The product with the plan's split (work: plan.work_bytes of device memory,

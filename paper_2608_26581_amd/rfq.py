@@ -584,7 +584,8 @@ def rfq_hif4_gemm(q_codes, q_meta, r_codes, r_meta, w_codes, w_meta,
                   out_dtype=torch.float32, out=None, stream=None, split=False):
     """HiF4 RFQ product Z[M][N] = (V_q + V_r) V_w^T; r_* None: primary only.
     split=True: rfq_hif4_gemm_split with a workspace from torch's allocator
-    where the shape splits K (a different fp32 summation order)."""
+    where the shape splits K (a different fp32 summation order) or decodes
+    the weights into it (the same bits)."""
     M, N, K, dev = _hif4_operands(q_codes, q_meta, r_codes, r_meta, w_codes, w_meta)
     z = _z_out(out, out_dtype, M, N, q_codes.device, dev)
     if split:
@@ -612,8 +613,10 @@ def rfq_hif4_gemm_workspace_bytes(M, N, K):
 def rfq_hif4_gemm_split(q_codes, q_meta, r_codes, r_meta, w_codes, w_meta, workspace,
                         out_dtype=torch.float32, out=None, stream=None):
     """rfq_hif4_gemm with K split over workgroups where the shape calls for
-    it; workspace: a contiguous device uint8 tensor
-    (rfq_hif4_gemm_workspace_bytes long, or shorter to run unsplit) or None."""
+    it, or (from 1024 rows) with the weights decoded to bf16 in the workspace
+    first (the same bits); workspace: a contiguous device uint8 tensor
+    (rfq_hif4_gemm_workspace_bytes long, or shorter to run rfq_hif4_gemm) or
+    None."""
     M, N, K, dev = _hif4_operands(q_codes, q_meta, r_codes, r_meta, w_codes, w_meta)
     nbytes = 0
     if workspace is not None:

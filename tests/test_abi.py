@@ -371,7 +371,10 @@ def test_hif4_gemm_split_validation_and_workspace_sizes():
     assert w(512, 4096, 12288) == 2 * 512 * 4096 * 4       # 128 tiles: 2 parts
     assert w(200, 300, 2560) == 8 * 200 * 300 * 4          # 6 tiles: 8 parts of 5 blocks
     assert w(129, 12288, 4096) == 0                        # 192 tiles
-    assert w(1024, 4096, 12288) == 0                       # 256 tiles
+    assert w(1023, 4096, 12288) == 0                       # 256 tiles: no split
+    assert w(1024, 4096, 12288) == 4096 * 12288 * 2        # from 1024 rows: W decoded into it
+    assert w(4096, 12288, 4096) == 12288 * 4096 * 2
+    assert w(1024, 32768, 32768) == 0                      # the decoded W would pass 1 GiB
     assert w(20, 4096, 12288) == 0                         # few-row form, 256 workgroups
     assert w(24, 4096, 12288) == 8 * 24 * 4096 * 4         # tiles from 24 rows (N <= 4096, long K)
     assert w(64, 4096, 12288) == 8 * 64 * 4096 * 4         # the same

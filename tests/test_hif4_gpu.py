@@ -379,6 +379,29 @@ def test_gemm_split_matches_oracle(orc, M, N, K, residual, out_dtype):
     assert torch.equal(z1.view(iv), z2.view(iv)), "short workspace: not the unsplit product"
 
 
+@pytest.mark.parametrize("M,N,K", [(1024, 2560, 640), (1100, 4100, 256)])
+@pytest.mark.parametrize("residual", [True, False])
+def test_gemm_split_decoding_weights_is_the_unsplit_product(M, N, K, residual):
+    """From 1024 rows without a split of K, rfq_hif4_gemm_split decodes the
+    weights to bf16 in the workspace and runs the bf16-weight product: the
+    bits of rfq_hif4_gemm, in both output types (ragged N included); with a
+    workspace one byte short it runs rfq_hif4_gemm itself."""
+    nbytes = rfq.rfq_hif4_gemm_workspace_bytes(M, N, K)
+    assert nbytes == N * K * 2
+    _say("hif4 gemm split, W decoded: %dx%dx%d residual=%s" % (M, N, K, residual))
+    w = wl.WORKLOADS["tiny"].scaled(M=M, K=K, weights=(("w", K, N),))
+    data = wl.generate(w, seed=M + N + K)
+    _, q = _gpu_quant(data["x"], False, residual)
+    _, wq = _gpu_quant(data["w"], False, residual=False)
+    ws = torch.full((nbytes,), 0xFF, dtype=torch.uint8, device="cuda")
+    for dt, iv in ((torch.float32, torch.int32), (torch.bfloat16, torch.int16)):
+        want = rfq.rfq_hif4_gemm(*q, wq[0], wq[1], out_dtype=dt)
+        got = rfq.rfq_hif4_gemm_split(*q, wq[0], wq[1], ws, out_dtype=dt)
+        assert torch.equal(got.view(iv), want.view(iv)), dt
+        short = rfq.rfq_hif4_gemm_split(*q, wq[0], wq[1], ws[:nbytes - 1], out_dtype=dt)
+        assert torch.equal(short.view(iv), want.view(iv)), dt
+
+
 @pytest.mark.parametrize("M,N,K,nrows", [(256, 4096, 12288, 24), (64, 4096, 12288, 8),
                                          (30, 4000, 12288, 8), (40, 5120, 13824, 8),
                                          (1, 5120, 13824, 1), (40, 12288, 4096, 8)])
