@@ -129,13 +129,14 @@ rfq_status rfq_gemm(const uint8_t *q_codes, const uint8_t *q_scales,
  * The RFQ product of rfq_gemm with the reduction over K split across
  * several workgroups per output tile where that is faster: products with few
  * output tiles (at most 128 tiles of 128 x 128, or at most 192 with
- * K >= 8192) and at least 33 activation rows (24 with K >= 12288, 17 where
- * the few-row product's grid holds between one and two workgroups per CU,
- * e.g. N = 5120), e.g. an MLP down projection for a few dozen to a few
- * hundred tokens; not for 33-64 rows with 11264 <= N < 16384, where
- * rfq_gemm's few-row product is faster.  Where that uneven few-row grid
- * meets up to 16 rows and K >= 12288, the few-row product itself splits K
- * in three parts.
+ * K >= 8192) and at least 33 activation rows (24 with K >= 12288, 17 with
+ * K >= 8192 where the few-row product's grid holds between one and two
+ * workgroups per CU, e.g. N = 5120), e.g. an MLP down projection for a few
+ * dozen to a few hundred tokens; not for 33-64 rows with 11264 <= N < 16384,
+ * where rfq_gemm's few-row product is faster.  Where the few-row grid's last
+ * round of workgroups is at most a quarter full (e.g. N = 5120) with up to
+ * 16 rows and K >= 12288, the few-row product itself splits K in three
+ * parts.
  * Each part of K writes its fp32 partial sums to the workspace; one pass then
  * adds the parts in a fixed order and rounds to z_dtype, so the result is
  * deterministic but its fp32 summation order differs from rfq_gemm's (both

@@ -321,7 +321,9 @@ static bool few_rows_chosen(int64_t M, int64_t N, int64_t K) {
 
 // With a workspace the split product replaces the few-row kernel where it
 // splits, from 33 rows; from 24 where K >= 12288, and from 17 where the
-// few-row grid is uneven (between one and two workgroups per CU).  Measured,
+// few-row grid is uneven (between one and two workgroups per CU) and K >=
+// 8192 (20 rows x 9216 x 4096: 13.6 us few-row against 14.9 split; x 4608 x
+// 8192 19.6 against 14.6).  Measured,
 // bf16 Z, few-row against split: 64 rows x 4096 x 12288 32.5 against 18.1
 // us, 32 rows 19.3 against 16.5, 24 rows 16.8 against 16.0, 16 rows 13.0
 // against 15.8; 24 rows x 5120 x 13824 31.4 against 21.0, 16 rows (the
@@ -331,7 +333,7 @@ static bool few_rows_chosen(int64_t M, int64_t N, int64_t K) {
 // us few-row against 18.4 split, 64 rows 17.1 against 19.5).
 static bool few_rows_beat_split(int64_t M, int64_t N, int64_t K) {
   if (skinny_four_fragments(M, N) && N < 16384) return true;
-  const int64_t min_rows = skinny_grid_uneven(M, N) ? 17 : (K >= 12288 ? 24 : 33);
+  const int64_t min_rows = (skinny_grid_uneven(M, N) && K >= 8192) ? 17 : (K >= 12288 ? 24 : 33);
   return M < min_rows;
 }
 

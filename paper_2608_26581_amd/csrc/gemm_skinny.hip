@@ -600,17 +600,20 @@ bool skinny_grid_uneven(int64_t M, int64_t N) {
   return wgs > kFillWorkgroups && wgs < 2 * kFillWorkgroups;
 }
 
-// Where the grid holds between one and two workgroups per CU (one weight
-// fragment per workgroup at 4096 < N < 8192), the CUs that run two finish
-// last; three parts of K even that out, at the cost of the sum.  Each part
-// keeps at least 8 groups of 512 (two per wave).  Measured at 5120 x 13824
-// weights, bf16 Z, sum included: 1 row 15.0 -> 12.8 us, 8 rows 17.9 -> 15.2,
-// 16 rows 23.7 -> 19.3; at 4096 x 12288 (256 workgroups) and N >= 12288
-// every split was slower (1 row x 4096 x 12288: 8.2 -> 9.5 us).
+// Where the grid's last round of workgroups is at most a quarter full (257
+// to 320 workgroups: one weight fragment per workgroup at 4096 < N <= 5120),
+// the CUs that run two finish last; three parts of K even that out, at the
+// cost of the sum.  Each part keeps at least 8 groups of 512 (two per wave).
+// Measured at 5120 x 13824 weights, bf16 Z, sum included: 1 row 15.0 -> 12.8
+// us, 8 rows 17.9 -> 15.2, 16 rows 23.7 -> 19.3; at 6144 x 12288 (384
+// workgroups) 1 row 13.1 -> 14.6 and 8 rows 17.7 -> 17.5; at 4096 x 12288
+// (256 workgroups) and N >= 12288 every split was slower (1 row x 4096 x
+// 12288: 8.2 -> 9.5 us).
 int skinny_split_parts(int64_t M, int64_t N, int64_t K) {
   constexpr int kParts = 3;
-  if (M > kSkRows || K / kSkGroupK < 8 * kParts || !skinny_grid_uneven(M, N)) return 1;
-  return kParts;
+  if (M > kSkRows || K / kSkGroupK < 8 * kParts) return 1;
+  const int64_t wgs = sk_workgroups(M, N);
+  return (wgs > kFillWorkgroups && 4 * wgs <= 5 * kFillWorkgroups) ? kParts : 1;
 }
 
 bool skinny_four_fragments(int64_t M, int64_t N) {

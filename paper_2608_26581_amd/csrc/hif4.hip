@@ -890,8 +890,11 @@ FewShape few_shape(int64_t M, int64_t N, bool wbf16) {
 // rounds of 256 (one per CU); where the last round is partly empty, p parts
 // (g p workgroups, each a p-th of K) fill it better.  Parts are taken where
 // they raise the filled fraction of the last round, (g p / 256) /
-// ceil(g p / 256), by at least 0.15 (the sum kernel and the shorter K loops
-// cost the rest), and every wave keeps at least two chunks of 128.  Measured
+// ceil(g p / 256), by at least 0.2 (the sum kernel and the shorter K loops
+// cost the rest: a gain of 0.15 at 1 row x 9216 x 4096 measured 16.2 ->
+// 17.0 us), every wave keeps at least two chunks of 128, and the workgroups
+// have 8 waves (the 16-wave shapes up to 8 rows at N <= 4096 already split
+// K finely: 1 row x 3072 x 16384 20.0 -> 21.7 us with 4 parts).  Measured
 // (bf16 Z, sum included): 5120 x 13824 weights (160 workgroups; 320 up to 4
 // rows), 1 row 29.7 -> 23.2 us (4 parts), 8 rows 39.4 -> 29.2, 16 rows
 // 52.3 -> 40.4, 64 rows 114.0 -> 80.3 (3 parts); 64 rows x 12288 x 4096 (384
@@ -901,6 +904,7 @@ FewShape few_shape(int64_t M, int64_t N, bool wbf16) {
 int few_split_parts(int64_t M, int64_t N, int64_t K) {
   if (M > kFewMaxRows || !few_fits(N, K)) return 1;
   const FewShape f = few_shape(M, N, false);
+  if (f.waves != 8) return 1;
   const int64_t g = (N + f.nr - 1) / f.nr;
   const int64_t nchunks = (K + kFewChunk - 1) / kFewChunk;
   auto filled = [&](int64_t p) {
@@ -912,7 +916,7 @@ int few_split_parts(int64_t M, int64_t N, int64_t K) {
   for (int p = 2; p <= 4; ++p) {
     if (nchunks < int64_t(2) * p * f.waves) break;
     const double fp = filled(p);
-    if (fp >= filled(1) + 0.15 && fp > fb) {
+    if (fp >= filled(1) + 0.2 && fp > fb) {
       best = p;
       fb = fp;
     }

@@ -341,7 +341,9 @@ def test_gemm_split_validation_and_workspace_sizes():
     assert w(24, 4096, 12288) == 8 * 24 * 4096 * 4         # from 24 rows at K >= 12288: split
     assert w(32, 4096, 8192) == 0                          # few-row kernel up to 32 rows
     assert w(16, 5120, 13824) == 3 * 16 * 5120 * 4         # uneven few-row grid: K in 3 parts
-    assert w(1, 6000, 12288) == 3 * 1 * 6000 * 4           # the same
+    assert w(1, 5000, 12288) == 3 * 1 * 5000 * 4           # the same (313 workgroups)
+    assert w(1, 6000, 12288) == 0                          # 375: last round over a quarter full
+    assert w(20, 9216, 4096) == 0                          # uneven, but K below 8192: from 33 rows
     assert w(16, 5120, 8192) == 0                          # too short for 3 parts of 8 groups
     assert w(16, 4096, 13824) == 0                         # 256 workgroups: even
     assert w(17, 5120, 13824) == 6 * 17 * 5120 * 4         # uneven few-row grid: split from 17
@@ -388,6 +390,8 @@ def test_hif4_gemm_split_validation_and_workspace_sizes():
     assert w(40, 12288, 4096) == 2 * 40 * 12288 * 4        # few-row form, 384 workgroups: 2 parts
     assert w(64, 12288, 4096) == 2 * 64 * 12288 * 4        # tiles (96: 2 parts)
     assert w(16, 12288, 4096) == 0                         # 192 workgroups, one chunk a wave at 4
+    assert w(1, 9216, 4096) == 0                           # 576 workgroups: a gain of 0.15 only
+    assert w(8, 3072, 16384) == 0                          # 16 waves a workgroup: no split
     assert w(1, 13824, 5120) == 0                          # 864 workgroups: filled enough
     assert w(16, 5120, 1024) == 0                          # 8 chunks: under two a wave
     assert w(200, 300, 448) == 0                           # 7 blocks: under 2 parts of 4

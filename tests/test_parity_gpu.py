@@ -463,7 +463,7 @@ def test_gemm_mid_rows_full_width(orc, M, N, K):
 # parts of 512) with 40 rows (past the few-row kernel's range in the split
 # product); M x N not a multiple of 4 for the scalar sum.
 SPLIT = [(130, 300, 8192), (131, 301, 8704), (200, 257, 9216), (40, 300, 2560),
-         (5, 5000, 12288), (16, 6000, 12800)]    # few-row kernel, K in 3 parts
+         (5, 5000, 12288), (16, 4900, 12800)]    # few-row kernel, K in 3 parts
 
 
 @pytest.mark.parametrize("M,N,K", SPLIT)
