@@ -316,6 +316,10 @@ GEMM_SMALL = [
     ("qwen", 3, 16400, 512),
     # 65-128 rows with 96 or more 128-wide column tiles: the large-tile kernel
     ("qwen", 100, 12300, 512),
+    # long K at a narrow grid (at most one workgroup per CU), ragged N; 4-5
+    # groups of 512 per wave at K = 9216
+    ("qwen", 3, 1000, 8192),
+    ("qwen", 16, 4000, 9216),
 ]
 
 
@@ -547,7 +551,8 @@ def test_gemm_stream_matches_oracle(orc, name, M, N, K, xdt, residual, out_dtype
 
 @pytest.mark.parametrize("M,N,K", [(1, 300, 512), (16, 256, 1024), (64, 200, 5120), (23, 515, 2048),
                                    (65, 97, 1536), (128, 300, 512), (100, 33, 2048),
-                                   (12, 12300, 1024), (2, 16400, 512), (40, 12300, 1024)])
+                                   (12, 12300, 1024), (2, 16400, 512), (40, 12300, 1024),
+                                   (3, 1000, 8192), (16, 4000, 9216)])
 @pytest.mark.parametrize("residual", [True, False])
 def test_gemm_stream_bit_identical_to_quantize_then_gemm(M, N, K, residual):
     """Where rfq_gemm runs its few-row kernel (up to 64 rows, and up to 128
