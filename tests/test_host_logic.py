@@ -1,6 +1,7 @@
 """Host-side logic checked on the CPU: the product path never reaches the
-oracle, and bench.py's traffic record is honoured only while the kernel
-sources it was measured on are unchanged."""
+oracle, bench.py's traffic record is honoured only while the kernel sources
+it was measured on are unchanged, and bench.py refuses step counts it
+cannot time."""
 import json
 import os
 import re
@@ -55,3 +56,16 @@ def test_traffic_record_follows_the_sources(tmp_path, monkeypatch):
     with open(root / first, "a") as f:
         f.write("\n// changed\n")
     assert bench.recorded_traffic(path) is None
+
+
+@pytest.mark.parametrize("args", [["--steps", "0"], ["--steps", "-3"], ["--warmup", "-1"]])
+def test_bench_rejects_step_counts_it_cannot_time(args):
+    """bench.py times at least one step (its product events bracket every
+    fourth timed step, starting with the first) and needs a warm-up count of
+    zero or more; it says so and exits before touching a GPU."""
+    import subprocess
+    import sys
+    res = subprocess.run([sys.executable, os.path.join(REPO, "bench.py"), *args],
+                         capture_output=True, text=True, timeout=60)
+    assert res.returncode == 2
+    assert "--steps must be at least 1" in res.stderr
